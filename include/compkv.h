@@ -1,0 +1,164 @@
+/*
+ * compkv.h -- C ABI of the MI355X (gfx950) CompKV decode-step attention library (libcompkv.so).
+ *
+ * CompKV (compensation-aware KV selection) decodes one token per sequence. Each KV head of each
+ * sequence (a "unit") is shared by G = n_q_heads / n_kv_heads query heads (Section 3.1). The cache is
+ * split into contiguous blocks of block_size tokens from the first token; the last block may be
+ * partial (Section 3.1). For every block the library keeps a summary: mean key, mean value and r
+ * grouped key variances (Sections 4.1 and 4.2). A decode step scores every block from the summaries
+ * (Eqs. grouped-variance-metadata, compkv-mass-estimate, compkv-score), selects the mandatory blocks
+ * plus the best-scoring others up to the budget (Eq. compkv-selected-set), then attends exactly over
+ * the selected blocks and through one mean pseudo-token per omitted block (Eq. compkv-output).
+ *
+ * Conventions shared by every call:
+ *  - Every pointer argument is a DEVICE pointer allocated and owned by the caller. The library never
+ *    allocates, frees or synchronizes, and never reads device memory from the host. Every call only
+ *    validates its host-side arguments and enqueues work on `stream` (a hipStream_t; NULL means the
+ *    default stream). Results are ready when the stream reaches that point.
+ *  - Layouts (row-major, innermost last). d = head_dim, Xcap = ceil(capacity_tokens / block_size):
+ *      k_cache, v_cache  bf16 [batch][n_kv_heads][capacity_tokens][d]
+ *      q                 bf16 [batch][n_q_heads][d]; query head hq uses KV head hq / G
+ *      kmean, vmean      fp32 [batch][n_kv_heads][Xcap][d]
+ *      dvar              fp32 [batch][n_kv_heads][Xcap][n_var_groups]
+ *      seq_lens          int32 [batch]: tokens present per sequence (device memory). Values above
+ *                        max_seq_len are treated as max_seq_len and values below 0 as 0, so a bad
+ *                        length can never address memory outside the buffers described here
+ *      sel               int32 [batch][n_kv_heads][budget_blocks], n_sel int32 [batch][n_kv_heads]
+ *      blk_logit         fp32 [batch][n_kv_heads][G][Xcap]: block-mean logits s q_g . kmean_b
+ *      scores            fp32 [batch][n_kv_heads][Xcap]
+ *      out               fp32 [batch][n_q_heads][d]; lse fp32 [batch][n_q_heads] (natural log)
+ *  - bf16 values are passed as their 16-bit patterns. Inputs must be finite.
+ *  - workspace: device scratch of at least compkv_workspace_bytes(...) bytes, 256-byte aligned.
+ *    Its first bytes hold arrival counters that must be ZERO before the first call that uses the
+ *    buffer (e.g. allocate it zeroed); every call leaves them zero again when it completes. Calls
+ *    that may run concurrently need distinct workspaces.
+ *  - Return value: COMPKV_OK (0) or a negative status; compkv_status_string() names it. On error
+ *    nothing has been enqueued, except for COMPKV_EHIP (a launch failed).
+ *
+ * Supported shapes: head_dim in {64, 128}; G in {1, 2, 4, 8}; 1 <= block_size <= 1024; n_var_groups
+ * r dividing head_dim / 2, or r == head_dim.
+ */
+#ifndef COMPKV_H
+#define COMPKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define COMPKV_OK 0
+#define COMPKV_EINVAL (-1)      /* null required pointer, inconsistent dims or sizes */
+#define COMPKV_EUNSUPPORTED (-2) /* head_dim, G, block_size or n_var_groups outside the supported set */
+#define COMPKV_EBUDGET (-3)     /* budget smaller than the mandatory set n_sink + n_recent */
+#define COMPKV_EWORKSPACE (-4)  /* workspace null, misaligned or too small */
+#define COMPKV_EHIP (-5)        /* a kernel launch failed */
+
+/* Coordinate groups of the grouped key variance (Appendix A.4): the d coordinates form d/2 RoPE
+ * frequency pairs, cut into r equal consecutive groups with both coordinates of a pair together.
+ * ROTATE_HALF pairs coordinate f with f + d/2 (the layout of the paper's models); INTERLEAVED pairs
+ * 2f with 2f + 1. With r == d every coordinate is its own group t = {t}. */
+#define COMPKV_GROUPS_ROTATE_HALF 0
+#define COMPKV_GROUPS_INTERLEAVED 1
+
+typedef struct compkv_dims {
+    int32_t batch;           /* sequences */
+    int32_t n_q_heads;       /* query heads per sequence */
+    int32_t n_kv_heads;      /* KV heads per sequence; must divide n_q_heads */
+    int32_t head_dim;        /* d */
+    int32_t block_size;      /* B, tokens per block (Section 3.1) */
+    int32_t n_var_groups;    /* r, grouped variances per block (Section 4.1) */
+    int32_t group_layout;    /* COMPKV_GROUPS_* */
+    int32_t capacity_tokens; /* cache rows per unit (row stride of k_cache / v_cache) */
+    int32_t max_seq_len;     /* host-side upper bound of seq_lens, 1..capacity_tokens; sizes grids */
+} compkv_dims;
+
+typedef struct compkv_select_params {
+    int32_t budget_blocks; /* K: blocks read exactly per unit, mandatory blocks included (Eq. compkv-selected-set) */
+    int32_t n_sink;        /* leading blocks always selected (the paper uses 1; Section 4.2) */
+    int32_t n_recent;      /* most recent blocks always selected (the paper uses 2; Section 4.2) */
+    float scale;           /* logit scale s; the paper's 1/sqrt(d) (Section 3.1) */
+} compkv_select_params;
+
+/* Which call a workspace is sized for (compkv_workspace_bytes). */
+#define COMPKV_WS_ALL 0
+#define COMPKV_WS_SCORE_SELECT 1
+#define COMPKV_WS_SPARSE_DECODE 2
+#define COMPKV_WS_DENSE_DECODE 3
+
+/*
+ * Block summaries of the first seq_lens[b] tokens of every unit (prefill). Section 4.1, Eq.
+ * grouped-variance-metadata, and Section 4.2: for block b with |b| tokens,
+ *   kmean[b] = mean key, vmean[b] = mean value,
+ *   dvar[b][t] = (1 / (|b| |G_t|)) sum_{j in b} sum_{i in G_t} (k_{j,i} - kmean[b][i])^2
+ * (population variances, Appendix E.1). Blocks at or past ceil(seq_lens[b] / B) are not written.
+ */
+int compkv_build_stats(const compkv_dims* dims, const void* k_cache, const void* v_cache,
+                       const int32_t* seq_lens, float* kmean, float* dvar, float* vmean, void* stream);
+
+/*
+ * Streaming append (Section 4.2, Appendix E.1): writes the new token's key and value (bf16
+ * [batch][n_kv_heads][d] each) into cache row n = seq_lens[b] -- the length BEFORE the append;
+ * seq_lens is not modified -- and refreshes the summary of the active block n / B only (completed
+ * blocks never change). The refreshed summary is bit-identical to what compkv_build_stats computes
+ * for n + 1 tokens. Units whose n is not below capacity_tokens are left untouched.
+ */
+int compkv_append_stats(const compkv_dims* dims, void* k_cache, void* v_cache, const void* k_new,
+                        const void* v_new, const int32_t* seq_lens, float* kmean, float* dvar,
+                        float* vmean, void* stream);
+
+/*
+ * Scoring and selection (Sections 4.1 and 4.2). Per unit and block b, with s = params->scale:
+ *   zbar[g][b] = s q_g . kmean_b,   sig2[g][b] = s^2 sum_t (sum_{i in G_t} q_{g,i}^2) dvar[b][t],
+ *   phat[g][b] = |b| exp(zbar + sig2/2) / sum_c |c| exp(zbar_c + sig2_c/2)   (per query head, all blocks)
+ *   S_b = sum_g phat[g][b] sig2[g][b]
+ * then S = F u TopK_{K-|F|}{S_b : b not in F}, F = first n_sink and last n_recent blocks (overlap
+ * counted once). Ties rank the lower block id first; sel lists the ids in ascending order and
+ * n_sel[u] = min(K, X); slots past n_sel are set to -1. If K >= X every block is selected.
+ * blk_logit receives zbar (needed by compkv_sparse_decode); scores (nullable) receives S_b for every
+ * block. q is bf16 [batch][n_q_heads][d]. Returns COMPKV_EBUDGET if K < n_sink + n_recent.
+ */
+int compkv_score_select(const compkv_dims* dims, const compkv_select_params* params, const void* q,
+                        const float* kmean, const float* dvar, const int32_t* seq_lens, int32_t* sel,
+                        int32_t* n_sel, float* blk_logit, float* scores, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
+ * Compensated sparse decode (Eq. compkv-output). For every unit and query head g:
+ *   out_g = [ sum_{b in S} sum_{j in b} e^{z_{g,j}} v_j + sum_{b not in S} |b| e^{zbar_{g,b}} vmean_b ]
+ *         / [ sum_{b in S} sum_{j in b} e^{z_{g,j}}     + sum_{b not in S} |b| e^{zbar_{g,b}} ]
+ * with z_{g,j} = scale q_g . k_j, S = sel[u][0 .. n_sel[u]) (ascending, unique ids below X; entries
+ * outside [0, X) are ignored) and zbar read from blk_logit as written by compkv_score_select.
+ * sel_stride is the row stride of sel (the budget K). lse (nullable) receives the log of the
+ * denominator, i.e. of the compensated normalizer.
+ */
+int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
+                         const void* v_cache, const float* vmean, const float* blk_logit,
+                         const int32_t* seq_lens, const int32_t* sel, const int32_t* n_sel,
+                         int32_t sel_stride, float* out, float* lse, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/*
+ * Dense decode over every cached token (full attention of Section 3.1, the speedup baseline):
+ * out_g = softmax_j(scale q_g . k_j) V, lse_g = log sum_j e^{z_{g,j}} (lse nullable).
+ */
+int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* seq_lens, float* out, float* lse,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by `which` (COMPKV_WS_*; COMPKV_WS_ALL = enough for every call) for these
+ * dims and budget. Returns 0 if dims are invalid. */
+size_t compkv_workspace_bytes(const compkv_dims* dims, int32_t budget_blocks, int32_t which);
+
+/* Static string naming a status code. */
+const char* compkv_status_string(int status);
+
+/* Library ABI version (major * 100 + minor). */
+int compkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COMPKV_H */

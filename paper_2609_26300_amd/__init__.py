@@ -1,0 +1,33 @@
+"""MI355X-native CompKV decode-step attention.
+
+The compute lives in ``libcompkv.so`` (hand-written HIP for gfx950, C ABI in ``include/compkv.h``).
+This package is a thin ctypes binding with the same function names: it checks tensor dtypes, shapes
+and devices, passes raw device pointers and the current HIP stream, and raises on a non-zero status.
+PyTorch only provides device memory and streams. There is no fallback: if the library is not built,
+every call raises.
+"""
+from .binding import (  # noqa: F401
+    COMPKV_GROUPS_INTERLEAVED,
+    COMPKV_GROUPS_ROTATE_HALF,
+    COMPKV_WS_ALL,
+    COMPKV_WS_DENSE_DECODE,
+    COMPKV_WS_SCORE_SELECT,
+    COMPKV_WS_SPARSE_DECODE,
+    CompkvDims,
+    CompkvError,
+    CompkvSelectParams,
+    Summaries,
+    alloc_summaries,
+    alloc_workspace,
+    compkv_append_stats,
+    compkv_build_stats,
+    compkv_dense_decode,
+    compkv_score_select,
+    compkv_sparse_decode,
+    compkv_status_string,
+    compkv_version,
+    compkv_workspace_bytes,
+    exported_symbols,
+    library,
+    make_dims,
+)

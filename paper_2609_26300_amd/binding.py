@@ -1,0 +1,239 @@
+"""ctypes binding of libcompkv.so: argument marshalling only (see include/compkv.h for semantics)."""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcompkv.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "compkv.h")
+
+COMPKV_GROUPS_ROTATE_HALF = 0
+COMPKV_GROUPS_INTERLEAVED = 1
+COMPKV_WS_ALL = 0
+COMPKV_WS_SCORE_SELECT = 1
+COMPKV_WS_SPARSE_DECODE = 2
+COMPKV_WS_DENSE_DECODE = 3
+
+
+class CompkvError(RuntimeError):
+    pass
+
+
+class CompkvDims(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "batch", "n_q_heads", "n_kv_heads", "head_dim", "block_size", "n_var_groups", "group_layout",
+        "capacity_tokens", "max_seq_len")]
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+    @property
+    def xcap(self) -> int:
+        return -(-self.capacity_tokens // self.block_size)
+
+
+class CompkvSelectParams(ctypes.Structure):
+    _fields_ = [("budget_blocks", ctypes.c_int32), ("n_sink", ctypes.c_int32),
+                ("n_recent", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+def make_dims(batch, n_q_heads, n_kv_heads, head_dim, block_size, n_var_groups, capacity_tokens,
+              max_seq_len=None, group_layout=COMPKV_GROUPS_ROTATE_HALF) -> CompkvDims:
+    return CompkvDims(batch, n_q_heads, n_kv_heads, head_dim, block_size, n_var_groups, group_layout,
+                      capacity_tokens, capacity_tokens if max_seq_len is None else max_seq_len)
+
+
+_lib = None
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+
+
+def library():
+    """The loaded libcompkv.so; raises if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise CompkvError(f"{LIB_PATH} is not built; run __graft_entry__.build() or "
+                              "python -m paper_2609_26300_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        dp = ctypes.POINTER(CompkvDims)
+        L.compkv_build_stats.argtypes = [dp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+        L.compkv_append_stats.argtypes = [dp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+        L.compkv_score_select.argtypes = [dp, ctypes.POINTER(CompkvSelectParams), _vp, _vp, _vp, _vp, _vp,
+                                          _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+        L.compkv_sparse_decode.argtypes = [dp, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                           _i32, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+        L.compkv_dense_decode.argtypes = [dp, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                          ctypes.c_size_t, _vp]
+        L.compkv_workspace_bytes.argtypes = [dp, _i32, _i32]
+        L.compkv_workspace_bytes.restype = ctypes.c_size_t
+        L.compkv_status_string.argtypes = [ctypes.c_int]
+        L.compkv_status_string.restype = ctypes.c_char_p
+        L.compkv_version.argtypes = []
+        for name in ("compkv_build_stats", "compkv_append_stats", "compkv_score_select",
+                     "compkv_sparse_decode", "compkv_dense_decode", "compkv_version"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def exported_symbols() -> list[str]:
+    """Function names declared in include/compkv.h."""
+    text = open(HEADER_PATH).read()
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\*)\s+(compkv_\w+)\s*\(", text, re.M)))
+
+
+def compkv_status_string(status: int) -> str:
+    return library().compkv_status_string(int(status)).decode()
+
+
+def compkv_version() -> int:
+    return library().compkv_version()
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        raise CompkvError(f"{what}: {compkv_status_string(status)}")
+
+
+def _ptr(t, dtype, shape, name, nullable=False):
+    if t is None:
+        if nullable:
+            return None
+        raise CompkvError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise CompkvError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise CompkvError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise CompkvError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise CompkvError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if isinstance(stream, torch.cuda.Stream) else stream
+
+
+def _ws(workspace):
+    if workspace is None or workspace.device.type != "cuda" or not workspace.is_contiguous():
+        raise CompkvError("workspace must be a contiguous CUDA tensor")
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def compkv_workspace_bytes(dims: CompkvDims, budget_blocks: int, which: int = COMPKV_WS_ALL) -> int:
+    return int(library().compkv_workspace_bytes(ctypes.byref(dims), int(budget_blocks), int(which)))
+
+
+def alloc_workspace(dims: CompkvDims, budget_blocks: int, device="cuda") -> torch.Tensor:
+    """Zeroed workspace large enough for every call (its arrival counters start at zero)."""
+    nbytes = compkv_workspace_bytes(dims, budget_blocks, COMPKV_WS_ALL)
+    if nbytes == 0:
+        raise CompkvError("invalid dims for workspace sizing")
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+
+
+@dataclass
+class Summaries:
+    kmean: torch.Tensor  # fp32 [batch][n_kv_heads][Xcap][d]
+    dvar: torch.Tensor   # fp32 [batch][n_kv_heads][Xcap][r]
+    vmean: torch.Tensor  # fp32 [batch][n_kv_heads][Xcap][d]
+
+
+def alloc_summaries(dims: CompkvDims, device="cuda") -> Summaries:
+    shp = (dims.batch, dims.n_kv_heads, dims.xcap)
+    return Summaries(
+        kmean=torch.zeros(*shp, dims.head_dim, dtype=torch.float32, device=device),
+        dvar=torch.zeros(*shp, dims.n_var_groups, dtype=torch.float32, device=device),
+        vmean=torch.zeros(*shp, dims.head_dim, dtype=torch.float32, device=device),
+    )
+
+
+def _shapes(d: CompkvDims):
+    cache = (d.batch, d.n_kv_heads, d.capacity_tokens, d.head_dim)
+    summ = (d.batch, d.n_kv_heads, d.xcap, d.head_dim)
+    dvar = (d.batch, d.n_kv_heads, d.xcap, d.n_var_groups)
+    q = (d.batch, d.n_q_heads, d.head_dim)
+    return cache, summ, dvar, q
+
+
+def compkv_build_stats(dims, k_cache, v_cache, seq_lens, kmean, dvar, vmean, stream=None):
+    cache, summ, dv, _ = _shapes(dims)
+    bf, f32 = torch.bfloat16, torch.float32
+    st = library().compkv_build_stats(
+        ctypes.byref(dims), _ptr(k_cache, bf, cache, "k_cache"), _ptr(v_cache, bf, cache, "v_cache"),
+        _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _ptr(kmean, f32, summ, "kmean"),
+        _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"), _stream(stream))
+    _check(st, "compkv_build_stats")
+
+
+def compkv_append_stats(dims, k_cache, v_cache, k_new, v_new, seq_lens, kmean, dvar, vmean, stream=None):
+    cache, summ, dv, _ = _shapes(dims)
+    bf, f32 = torch.bfloat16, torch.float32
+    new = (dims.batch, dims.n_kv_heads, dims.head_dim)
+    st = library().compkv_append_stats(
+        ctypes.byref(dims), _ptr(k_cache, bf, cache, "k_cache"), _ptr(v_cache, bf, cache, "v_cache"),
+        _ptr(k_new, bf, new, "k_new"), _ptr(v_new, bf, new, "v_new"),
+        _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _ptr(kmean, f32, summ, "kmean"),
+        _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"), _stream(stream))
+    _check(st, "compkv_append_stats")
+
+
+def compkv_score_select(dims, params: CompkvSelectParams, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit,
+                        scores, workspace, stream=None):
+    _, summ, dv, qs = _shapes(dims)
+    f32, i32 = torch.float32, torch.int32
+    units = (dims.batch, dims.n_kv_heads)
+    ws, ws_bytes = _ws(workspace)
+    st = library().compkv_score_select(
+        ctypes.byref(dims), ctypes.byref(params), _ptr(q, torch.bfloat16, qs, "q"),
+        _ptr(kmean, f32, summ, "kmean"), _ptr(dvar, f32, dv, "dvar"),
+        _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, params.budget_blocks), "sel"),
+        _ptr(n_sel, i32, units, "n_sel"),
+        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
+        _ptr(scores, f32, (*units, dims.xcap), "scores", nullable=True), ws, ws_bytes, _stream(stream))
+    _check(st, "compkv_score_select")
+
+
+def compkv_sparse_decode(dims, scale, q, k_cache, v_cache, vmean, blk_logit, seq_lens, sel, n_sel, out,
+                         lse=None, workspace=None, stream=None):
+    cache, summ, _, qs = _shapes(dims)
+    bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+    units = (dims.batch, dims.n_kv_heads)
+    if sel is None or sel.dim() != 3:
+        raise CompkvError("sel must be int32 [batch][n_kv_heads][budget]")
+    ws, ws_bytes = _ws(workspace)
+    st = library().compkv_sparse_decode(
+        ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _ptr(k_cache, bf, cache, "k_cache"),
+        _ptr(v_cache, bf, cache, "v_cache"), _ptr(vmean, f32, summ, "vmean"),
+        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
+        _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, sel.shape[2]), "sel"),
+        _ptr(n_sel, i32, units, "n_sel"), int(sel.shape[2]), _ptr(out, f32, qs, "out"),
+        _ptr(lse, f32, qs[:2], "lse", nullable=True), ws, ws_bytes, _stream(stream))
+    _check(st, "compkv_sparse_decode")
+
+
+def compkv_dense_decode(dims, scale, q, k_cache, v_cache, seq_lens, out, lse=None, workspace=None, stream=None):
+    cache, _, _, qs = _shapes(dims)
+    bf, f32 = torch.bfloat16, torch.float32
+    ws, ws_bytes = _ws(workspace)
+    st = library().compkv_dense_decode(
+        ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _ptr(k_cache, bf, cache, "k_cache"),
+        _ptr(v_cache, bf, cache, "v_cache"), _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"),
+        _ptr(out, f32, qs, "out"), _ptr(lse, f32, qs[:2], "lse", nullable=True), ws, ws_bytes,
+        _stream(stream))
+    _check(st, "compkv_dense_decode")
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

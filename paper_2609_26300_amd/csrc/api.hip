@@ -1,0 +1,298 @@
+// api.hip -- host side of the C ABI declared in include/compkv.h: argument validation, workspace
+// layout and launch shapes. Never touches device memory from the host.
+#include "compkv.h"
+#include "internal.h"
+
+#include <algorithm>
+
+using compkv::Geom;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+bool valid_r(int d, int r) { return r >= 1 && (r == d || (d % 2 == 0 && (d / 2) % r == 0)); }
+
+// Validate dims; fill geom. Returns COMPKV_OK or a status.
+int check_dims(const compkv_dims* dm, Geom* g) {
+    if (!dm) return COMPKV_EINVAL;
+    if (dm->batch < 1 || dm->n_q_heads < 1 || dm->n_kv_heads < 1 || dm->n_q_heads % dm->n_kv_heads != 0)
+        return COMPKV_EINVAL;
+    if (dm->capacity_tokens < 1 || dm->max_seq_len < 1 || dm->max_seq_len > dm->capacity_tokens)
+        return COMPKV_EINVAL;
+    const int G = dm->n_q_heads / dm->n_kv_heads;
+    if (dm->head_dim != 64 && dm->head_dim != 128) return COMPKV_EUNSUPPORTED;
+    if (G != 1 && G != 2 && G != 4 && G != 8) return COMPKV_EUNSUPPORTED;
+    if (dm->block_size < 1 || dm->block_size > 1024) return COMPKV_EUNSUPPORTED;
+    if (!valid_r(dm->head_dim, dm->n_var_groups)) return COMPKV_EUNSUPPORTED;
+    if (dm->group_layout != COMPKV_GROUPS_ROTATE_HALF && dm->group_layout != COMPKV_GROUPS_INTERLEAVED)
+        return COMPKV_EUNSUPPORTED;
+    const long long units = (long long)dm->batch * dm->n_kv_heads;
+    if (units > 65535) return COMPKV_EUNSUPPORTED;  // grid.y limit
+    g->batch = dm->batch;
+    g->hq = dm->n_q_heads;
+    g->hkv = dm->n_kv_heads;
+    g->G = G;
+    g->D = dm->head_dim;
+    g->B = dm->block_size;
+    g->r = dm->n_var_groups;
+    g->layout = dm->group_layout;
+    g->cap = dm->capacity_tokens;
+    g->xcap = ceil_div(dm->capacity_tokens, dm->block_size);
+    g->max_seq = dm->max_seq_len;
+    return COMPKV_OK;
+}
+
+// ---------------------------------------------------------------- launch shapes
+
+struct ScoreShape {
+    int bpc, nchunks;
+};
+
+ScoreShape score_shape(const Geom& g) {
+    const int xmax = g.xmax();
+    int bpc = 32;
+    // widen chunks while the grid stays >= 1024 workgroups (fewer partials to merge)
+    while (bpc < 256 && (long long)g.units() * ceil_div(xmax, bpc * 2) >= 1024) bpc *= 2;
+    return {bpc, ceil_div(xmax, bpc)};
+}
+
+struct SparseShape {
+    int eb, n_exact, cb, n_comp;
+};
+
+SparseShape sparse_shape(const Geom& g, int K) {
+    const int xmax = g.xmax();
+    const int keff = std::max(1, std::min(K, xmax));
+    int eb = std::max(1, 128 / g.B);                // about 128 exact tokens per item
+    eb = std::max(eb, ceil_div(keff, 160));         // at most 160 exact items
+    const int n_exact = ceil_div(keff, eb);
+    int cb = std::max(32, ceil_div(xmax, 32));      // at most 32 compensation items
+    cb = ceil_div(cb, 32) * 32;
+    cb = std::max(cb, ceil_div(xmax, 256 - n_exact));
+    const int n_comp = ceil_div(xmax, cb);
+    return {eb, n_exact, cb, n_comp};
+}
+
+struct DenseShape {
+    int te, items;
+};
+
+DenseShape dense_shape(const Geom& g) {
+    int te = std::max(256, ceil_div(g.max_seq, 128));
+    te = ceil_div(te, 64) * 64;
+    return {te, ceil_div(g.max_seq, te)};
+}
+
+// ---------------------------------------------------------------- workspace layout
+
+size_t counters_bytes(const Geom& g) { return align_up((size_t)g.units() * sizeof(uint32_t)); }
+
+size_t score_ws(const Geom& g) {
+    const ScoreShape sh = score_shape(g);
+    const size_t units = g.units(), xmax = g.xmax();
+    return align_up(units * sh.nchunks * g.G * 2 * sizeof(float)) +
+           2 * align_up(units * g.G * xmax * sizeof(float)) + align_up(units * xmax * sizeof(uint32_t));
+}
+
+size_t sparse_ws(const Geom& g, int K) {
+    const SparseShape sh = sparse_shape(g, K);
+    return align_up((size_t)g.units() * (sh.n_exact + sh.n_comp) * g.G * (g.D + 2) * sizeof(float));
+}
+
+size_t dense_ws(const Geom& g) {
+    const DenseShape sh = dense_shape(g);
+    return align_up((size_t)g.units() * sh.items * g.G * (g.D + 2) * sizeof(float));
+}
+
+size_t ws_bytes(const Geom& g, int K, int which) {
+    size_t body = 0;
+    if (which == COMPKV_WS_ALL || which == COMPKV_WS_SCORE_SELECT) body = std::max(body, score_ws(g));
+    if (which == COMPKV_WS_ALL || which == COMPKV_WS_SPARSE_DECODE) body = std::max(body, sparse_ws(g, K));
+    if (which == COMPKV_WS_ALL || which == COMPKV_WS_DENSE_DECODE) body = std::max(body, dense_ws(g));
+    return counters_bytes(g) + body;
+}
+
+int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
+    if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || bytes < need) return COMPKV_EWORKSPACE;
+    (void)g;
+    return COMPKV_OK;
+}
+
+int launch_status(hipError_t e) { return e == hipSuccess ? COMPKV_OK : COMPKV_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+int compkv_version(void) { return 100; }
+
+const char* compkv_status_string(int status) {
+    switch (status) {
+        case COMPKV_OK: return "COMPKV_OK";
+        case COMPKV_EINVAL: return "COMPKV_EINVAL: null pointer or inconsistent dims";
+        case COMPKV_EUNSUPPORTED: return "COMPKV_EUNSUPPORTED: head_dim, group size, block size or r not supported";
+        case COMPKV_EBUDGET: return "COMPKV_EBUDGET: budget smaller than the mandatory set";
+        case COMPKV_EWORKSPACE: return "COMPKV_EWORKSPACE: workspace null, misaligned or too small";
+        case COMPKV_EHIP: return "COMPKV_EHIP: kernel launch failed";
+        default: return "unknown compkv status";
+    }
+}
+
+size_t compkv_workspace_bytes(const compkv_dims* dims, int32_t budget_blocks, int32_t which) {
+    Geom g;
+    if (check_dims(dims, &g) != COMPKV_OK || budget_blocks < 1 || which < 0 || which > 3) return 0;
+    return ws_bytes(g, budget_blocks, which);
+}
+
+int compkv_build_stats(const compkv_dims* dims, const void* k_cache, const void* v_cache,
+                       const int32_t* seq_lens, float* kmean, float* dvar, float* vmean, void* stream) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!k_cache || !v_cache || !seq_lens || !kmean || !dvar || !vmean) return COMPKV_EINVAL;
+    compkv::StatsArgs a{};
+    a.K = static_cast<const uint16_t*>(k_cache);
+    a.V = static_cast<const uint16_t*>(v_cache);
+    a.seq_lens = seq_lens;
+    a.kmean = kmean;
+    a.dvar = dvar;
+    a.vmean = vmean;
+    return launch_status(compkv::launch_build_stats(g, a, static_cast<hipStream_t>(stream)));
+}
+
+int compkv_append_stats(const compkv_dims* dims, void* k_cache, void* v_cache, const void* k_new,
+                        const void* v_new, const int32_t* seq_lens, float* kmean, float* dvar,
+                        float* vmean, void* stream) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!k_cache || !v_cache || !k_new || !v_new || !seq_lens || !kmean || !dvar || !vmean) return COMPKV_EINVAL;
+    compkv::StatsArgs a{};
+    a.K = static_cast<const uint16_t*>(k_cache);
+    a.V = static_cast<const uint16_t*>(v_cache);
+    a.K_out = static_cast<uint16_t*>(k_cache);
+    a.V_out = static_cast<uint16_t*>(v_cache);
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
+    a.seq_lens = seq_lens;
+    a.kmean = kmean;
+    a.dvar = dvar;
+    a.vmean = vmean;
+    return launch_status(compkv::launch_append_stats(g, a, static_cast<hipStream_t>(stream)));
+}
+
+int compkv_score_select(const compkv_dims* dims, const compkv_select_params* params, const void* q,
+                        const float* kmean, const float* dvar, const int32_t* seq_lens, int32_t* sel,
+                        int32_t* n_sel, float* blk_logit, float* scores, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel || !blk_logit) return COMPKV_EINVAL;
+    if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
+    if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
+    const size_t need = ws_bytes(g, params->budget_blocks, COMPKV_WS_SCORE_SELECT);
+    st = check_ws(g, workspace, workspace_bytes, need);
+    if (st != COMPKV_OK) return st;
+    const ScoreShape sh = score_shape(g);
+    const size_t units = g.units(), xmax = g.xmax();
+    char* base = static_cast<char*>(workspace);
+    compkv::ScoreArgs a{};
+    a.counters = reinterpret_cast<uint32_t*>(base);
+    char* p = base + counters_bytes(g);
+    a.ws_part = reinterpret_cast<float*>(p);
+    p += align_up(units * sh.nchunks * g.G * 2 * sizeof(float));
+    a.ws_a = reinterpret_cast<float*>(p);
+    p += align_up(units * g.G * xmax * sizeof(float));
+    a.ws_v = reinterpret_cast<float*>(p);
+    p += align_up(units * g.G * xmax * sizeof(float));
+    a.ws_key = reinterpret_cast<uint32_t*>(p);
+    a.q = static_cast<const uint16_t*>(q);
+    a.kmean = kmean;
+    a.dvar = dvar;
+    a.seq_lens = seq_lens;
+    a.sel = sel;
+    a.n_sel = n_sel;
+    a.blk_logit = blk_logit;
+    a.scores = scores;
+    a.bpc = sh.bpc;
+    a.nchunks = sh.nchunks;
+    a.K = params->budget_blocks;
+    a.n_sink = params->n_sink;
+    a.n_recent = params->n_recent;
+    a.scale = params->scale;
+    return launch_status(compkv::launch_score_select(g, a, static_cast<hipStream_t>(stream)));
+}
+
+int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
+                         const void* v_cache, const float* vmean, const float* blk_logit,
+                         const int32_t* seq_lens, const int32_t* sel, const int32_t* n_sel,
+                         int32_t sel_stride, float* out, float* lse, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!q || !k_cache || !v_cache || !vmean || !blk_logit || !seq_lens || !sel || !n_sel || !out)
+        return COMPKV_EINVAL;
+    if (sel_stride < 1) return COMPKV_EINVAL;
+    const size_t need = ws_bytes(g, sel_stride, COMPKV_WS_SPARSE_DECODE);
+    st = check_ws(g, workspace, workspace_bytes, need);
+    if (st != COMPKV_OK) return st;
+    const SparseShape sh = sparse_shape(g, sel_stride);
+    char* base = static_cast<char*>(workspace);
+    compkv::DecodeArgs a{};
+    a.counters = reinterpret_cast<uint32_t*>(base);
+    a.ws_part = reinterpret_cast<float*>(base + counters_bytes(g));
+    a.q = static_cast<const uint16_t*>(q);
+    a.K = static_cast<const uint16_t*>(k_cache);
+    a.V = static_cast<const uint16_t*>(v_cache);
+    a.vmean = vmean;
+    a.blk_logit = blk_logit;
+    a.seq_lens = seq_lens;
+    a.sel = sel;
+    a.n_sel = n_sel;
+    a.out = out;
+    a.lse = lse;
+    a.sel_stride = sel_stride;
+    a.n_exact = sh.n_exact;
+    a.eb = sh.eb;
+    a.n_comp = sh.n_comp;
+    a.cb = sh.cb;
+    a.dense = 0;
+    a.scale = scale;
+    return launch_status(compkv::launch_decode(g, a, static_cast<hipStream_t>(stream)));
+}
+
+int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
+                        const void* v_cache, const int32_t* seq_lens, float* out, float* lse,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!q || !k_cache || !v_cache || !seq_lens || !out) return COMPKV_EINVAL;
+    const size_t need = ws_bytes(g, 1, COMPKV_WS_DENSE_DECODE);
+    st = check_ws(g, workspace, workspace_bytes, need);
+    if (st != COMPKV_OK) return st;
+    const DenseShape sh = dense_shape(g);
+    char* base = static_cast<char*>(workspace);
+    compkv::DecodeArgs a{};
+    a.counters = reinterpret_cast<uint32_t*>(base);
+    a.ws_part = reinterpret_cast<float*>(base + counters_bytes(g));
+    a.q = static_cast<const uint16_t*>(q);
+    a.K = static_cast<const uint16_t*>(k_cache);
+    a.V = static_cast<const uint16_t*>(v_cache);
+    a.seq_lens = seq_lens;
+    a.out = out;
+    a.lse = lse;
+    a.n_exact = sh.items;
+    a.eb = sh.te;
+    a.dense = 1;
+    a.scale = scale;
+    return launch_status(compkv::launch_decode(g, a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+// internal.h -- private declarations shared by libcompkv's translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace compkv {
+
+constexpr int kThreads = 256;  // every kernel runs 256-thread workgroups (4 wave64)
+
+// Shape of one call after host validation.
+struct Geom {
+    int batch, hq, hkv, G, D, B, r, layout, cap, xcap, max_seq;
+    __host__ __device__ int units() const { return batch * hkv; }
+    __host__ __device__ int xmax() const { return (max_seq + B - 1) / B; }
+};
+
+// ------------------------------------------------------------------ launch parameter blocks
+
+struct StatsArgs {
+    const uint16_t* K;
+    const uint16_t* V;
+    const uint16_t* k_new;  // append only
+    const uint16_t* v_new;  // append only
+    uint16_t* K_out;        // append only: cache rows written
+    uint16_t* V_out;
+    const int32_t* seq_lens;
+    float* kmean;
+    float* dvar;
+    float* vmean;
+};
+
+struct ScoreArgs {
+    const uint16_t* q;
+    const float* kmean;
+    const float* dvar;
+    const int32_t* seq_lens;
+    int32_t* sel;
+    int32_t* n_sel;
+    float* blk_logit;
+    float* scores;     // nullable
+    float* ws_part;    // [units][nchunks][G][2]  (chunk max, chunk sum of exp)
+    float* ws_a;       // [units][G][xmax]       log block weight estimate
+    float* ws_v;       // [units][G][xmax]       projected variance
+    uint32_t* ws_key;  // [units][xmax]          score bits
+    uint32_t* counters;
+    int bpc;      // blocks per chunk (multiple of 32)
+    int nchunks;  // grid.x
+    int K, n_sink, n_recent;
+    float scale;
+};
+
+struct DecodeArgs {
+    const uint16_t* q;
+    const uint16_t* K;
+    const uint16_t* V;
+    const float* vmean;
+    const float* blk_logit;
+    const int32_t* seq_lens;
+    const int32_t* sel;
+    const int32_t* n_sel;
+    float* out;
+    float* lse;      // nullable
+    float* ws_part;  // [units][items][G][D + 2]
+    uint32_t* counters;
+    int sel_stride;
+    int n_exact;  // exact items per unit
+    int eb;       // selected blocks per exact item (sparse) / tokens per item (dense)
+    int n_comp;   // compensation items per unit (sparse)
+    int cb;       // blocks per compensation item
+    int dense;    // 1: every item is a token range of the dense decode
+    float scale;
+};
+
+// ------------------------------------------------------------------ launchers (one per kernel family)
+
+hipError_t launch_build_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
+hipError_t launch_append_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
+hipError_t launch_score_select(const Geom& g, const ScoreArgs& a, hipStream_t s);
+hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
+
+// ------------------------------------------------------------------ device helpers
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_at(const uint16_t* p) { return __uint_as_float(uint32_t(*p) << 16); }
+
+__device__ __forceinline__ void unpack_bf16x8(const uint4 w, float f[8]) {
+    f[0] = bf16_lo(w.x);
+    f[1] = bf16_hi(w.x);
+    f[2] = bf16_lo(w.y);
+    f[3] = bf16_hi(w.y);
+    f[4] = bf16_lo(w.z);
+    f[5] = bf16_hi(w.z);
+    f[6] = bf16_lo(w.w);
+    f[7] = bf16_hi(w.w);
+}
+
+__device__ __forceinline__ int clamp_len(int n, int cap) { return n < 0 ? 0 : (n > cap ? cap : n); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Merge two softmax partials (max m, sum l, accumulators) into the first.
+__device__ __forceinline__ void merge_scales(float m_a, float m_b, float& m, float& ca, float& cb) {
+    m = fmaxf(m_a, m_b);
+    ca = (m_a == -INFINITY) ? 0.0f : __expf(m_a - m);
+    cb = (m_b == -INFINITY) ? 0.0f : __expf(m_b - m);
+}
+
+}  // namespace compkv

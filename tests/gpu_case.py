@@ -1,0 +1,153 @@
+"""Helpers for GPU parity tests: upload a seeded workload, run the library through the C ABI, and
+compare with the CPU oracle under the parity rules.
+
+Parity rules (bf16 inputs, fp32 accumulation on the GPU, fp64 in the oracle):
+  * floating-point results: max_i |x_i - y_i| / max(|y_i|, tau) <= 2e-3 with tau = 1e-3 * RMS(y)
+    over the compared row (an output row, a mean-key / mean-value row) or tensor (grouped
+    variances, scores);
+  * selected ids: same count, ascending, mandatory blocks present, and identical outside the band
+    of blocks whose oracle score is within 1e-5 (relative) of the oracle's (K-|F|)-th candidate
+    score -- several selections are correct when scores tie up to rounding.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2609_26300_amd as P
+from workloads import Workload, gen_layer
+
+TOL = 2e-3
+BAND = 1e-5
+
+
+def dev_bf16(bits: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to("cuda")
+
+
+def bits_of(t: torch.Tensor) -> np.ndarray:
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def rel_err(x, y, axis=None) -> float:
+    """Max relative error with the RMS floor, rows along ``axis`` (None: whole tensor)."""
+    x = np.asarray(x, np.float64)
+    y = np.asarray(y, np.float64)
+    if axis is None:
+        rms = math.sqrt(float(np.mean(y * y))) if y.size else 0.0
+        tau = 1e-3 * rms if rms > 0 else 1e-12
+        return float(np.max(np.abs(x - y) / np.maximum(np.abs(y), tau))) if y.size else 0.0
+    rms = np.sqrt(np.mean(y * y, axis=axis, keepdims=True))
+    tau = np.where(rms > 0, 1e-3 * rms, 1e-12)
+    return float(np.max(np.abs(x - y) / np.maximum(np.abs(y), tau))) if y.size else 0.0
+
+
+def mandatory(X, n_sink=1, n_recent=2):
+    return {b for b in range(X) if b < n_sink or b >= X - n_recent}
+
+
+def check_selection(sel_gpu, score_oracle, K, n_sink=1, n_recent=2, band=BAND):
+    """Selection parity under the tie band; returns the oracle's selection."""
+    sel_gpu = [int(s) for s in sel_gpu]
+    X = len(score_oracle)
+    sel_or = oracle.select(score_oracle, K, n_sink, n_recent).tolist()
+    assert len(sel_gpu) == len(sel_or) == min(K, X), (len(sel_gpu), len(sel_or))
+    assert sel_gpu == sorted(set(sel_gpu)), "selection not ascending/unique"
+    F = mandatory(X, n_sink, n_recent)
+    assert F <= set(sel_gpu)
+    if K >= X:
+        assert sel_gpu == sel_or
+        return sel_or
+    cand = sorted((b for b in range(X) if b not in F), key=lambda b: (-score_oracle[b], b))
+    kk = K - len(F)
+    if kk == 0:
+        assert sel_gpu == sel_or
+        return sel_or
+    s_k = score_oracle[cand[kk - 1]]
+    A = {b for b in range(X) if abs(score_oracle[b] - s_k) <= band * abs(s_k)}
+    assert set(sel_gpu) - A == set(sel_or) - A, (sorted(set(sel_gpu) ^ set(sel_or)), sorted(A))
+    return sel_or
+
+
+class Case:
+    """One seeded workload resident on the GPU (layer 0) plus its library outputs."""
+
+    def __init__(self, w: Workload, seq_lens=None, r=None, layout=0, budget=None, n_sink=1, n_recent=2,
+                 capacity=None, max_seq_len=None):
+        self.w = w
+        self.K_bits, self.V_bits, self.q_bits = gen_layer(w, 0)
+        self.seq_lens = np.array(seq_lens if seq_lens is not None else [w.context] * w.batch, np.int32)
+        self.r = w.n_var_groups if r is None else r
+        self.layout = layout
+        self.budget = w.budget_blocks if budget is None else budget
+        self.n_sink, self.n_recent = n_sink, n_recent
+        self.scale = 1.0 / math.sqrt(w.head_dim)
+        cap = w.capacity if capacity is None else capacity
+        self.dims = P.make_dims(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size, self.r, cap,
+                                max_seq_len=int(max_seq_len or max(1, self.seq_lens.max())),
+                                group_layout=layout)
+        self.K = dev_bf16(self.K_bits[:, :, :cap])
+        self.V = dev_bf16(self.V_bits[:, :, :cap])
+        self.q = dev_bf16(self.q_bits)
+        self.sl = torch.from_numpy(self.seq_lens).to("cuda")
+        self.ws = P.alloc_workspace(self.dims, self.budget)
+        self.G = w.group
+
+    # ---------------------------------------------------------------- library calls
+    def build_stats(self):
+        self.summ = P.alloc_summaries(self.dims)
+        P.compkv_build_stats(self.dims, self.K, self.V, self.sl, self.summ.kmean, self.summ.dvar, self.summ.vmean)
+        return self.summ
+
+    def score_select(self, q=None):
+        d = self.dims
+        units = (d.batch, d.n_kv_heads)
+        self.sel = torch.full((*units, self.budget), -7, dtype=torch.int32, device="cuda")
+        self.n_sel = torch.zeros(units, dtype=torch.int32, device="cuda")
+        self.blk_logit = torch.zeros((*units, self.G, d.xcap), dtype=torch.float32, device="cuda")
+        self.scores = torch.zeros((*units, d.xcap), dtype=torch.float32, device="cuda")
+        params = P.CompkvSelectParams(self.budget, self.n_sink, self.n_recent, self.scale)
+        P.compkv_score_select(d, params, self.q if q is None else q, self.summ.kmean, self.summ.dvar, self.sl,
+                              self.sel, self.n_sel, self.blk_logit, self.scores, self.ws)
+
+    def sparse_decode(self, sel=None, n_sel=None):
+        d = self.dims
+        self.out = torch.zeros((d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device="cuda")
+        self.lse = torch.zeros((d.batch, d.n_q_heads), dtype=torch.float32, device="cuda")
+        P.compkv_sparse_decode(d, self.scale, self.q, self.K, self.V, self.summ.vmean, self.blk_logit, self.sl,
+                               self.sel if sel is None else sel, self.n_sel if n_sel is None else n_sel,
+                               self.out, self.lse, self.ws)
+        return self.out, self.lse
+
+    def dense_decode(self):
+        d = self.dims
+        out = torch.zeros((d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device="cuda")
+        lse = torch.zeros((d.batch, d.n_q_heads), dtype=torch.float32, device="cuda")
+        P.compkv_dense_decode(d, self.scale, self.q, self.K, self.V, self.sl, out, lse, self.ws)
+        return out, lse
+
+    def run_all(self):
+        self.build_stats()
+        self.score_select()
+        self.sparse_decode()
+        torch.cuda.synchronize()
+
+    # ---------------------------------------------------------------- oracle side
+    def unit_inputs(self, b, h):
+        G = self.G
+        return self.q_bits[b, h * G:(h + 1) * G], self.K_bits[b, h], self.V_bits[b, h], int(self.seq_lens[b])
+
+    def oracle_stats(self, b, h):
+        q, K, V, n = self.unit_inputs(b, h)
+        return oracle.block_stats(K, V, n, self.w.block_size, self.r, self.layout)
+
+    def oracle_scores(self, b, h, stats=None):
+        q, K, V, n = self.unit_inputs(b, h)
+        km, dv, vm = stats if stats is not None else self.oracle_stats(b, h)
+        return oracle.block_scores(q, km, dv, n, self.w.block_size, self.r, self.scale, self.layout)
+
+    def units(self):
+        return [(b, h) for b in range(self.w.batch) for h in range(self.w.n_kv_heads)]

@@ -1,0 +1,129 @@
+"""C ABI contract checks that need no GPU: the library loads, exports every function the header
+declares, sizes workspaces, and rejects invalid arguments on the host before enqueuing anything
+(every call below returns from host-side validation; no kernel is launched)."""
+import ctypes
+import json
+import os
+
+import pytest
+
+import paper_2609_26300_amd as P
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+EINVAL, EUNSUP, EBUDGET, EWS = -1, -2, -3, -4
+FAKE = ctypes.c_void_p(4096)  # never dereferenced: validation fails before any device access
+
+
+def dims(**kw):
+    base = dict(batch=1, n_q_heads=8, n_kv_heads=2, head_dim=128, block_size=16, n_var_groups=4,
+                capacity_tokens=4096, max_seq_len=4096)
+    base.update(kw)
+    layout = base.pop("group_layout", 0)
+    return P.make_dims(group_layout=layout, **base)
+
+
+def test_library_exports_every_declared_function():
+    L = P.library()
+    names = P.exported_symbols()
+    assert {"compkv_build_stats", "compkv_append_stats", "compkv_score_select", "compkv_sparse_decode",
+            "compkv_dense_decode", "compkv_workspace_bytes", "compkv_status_string",
+            "compkv_version"} <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings_and_version():
+    assert P.compkv_version() >= 100
+    for code in (0, EINVAL, EUNSUP, EBUDGET, EWS, -5):
+        assert P.compkv_status_string(code).startswith("COMPKV_")
+    assert "unknown" in P.compkv_status_string(-99)
+
+
+def test_workspace_sizing():
+    d = dims()
+    for which in range(4):
+        assert P.compkv_workspace_bytes(d, 16, which) > 0
+    all_ = P.compkv_workspace_bytes(d, 16, 0)
+    assert all(all_ >= P.compkv_workspace_bytes(d, 16, w) for w in (1, 2, 3))
+    assert P.compkv_workspace_bytes(d, 0, 0) == 0
+    assert P.compkv_workspace_bytes(dims(head_dim=96), 16, 0) == 0
+    # grows with context
+    assert P.compkv_workspace_bytes(dims(capacity_tokens=131072, max_seq_len=131072), 64, 0) > all_
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(n_q_heads=6, n_kv_heads=4), EINVAL),
+    (dict(batch=0), EINVAL),
+    (dict(max_seq_len=5000), EINVAL),
+    (dict(max_seq_len=0), EINVAL),
+    (dict(head_dim=96), EUNSUP),
+    (dict(n_q_heads=24, n_kv_heads=2), EUNSUP),  # G = 12
+    (dict(block_size=0), EUNSUP),
+    (dict(n_var_groups=3), EUNSUP),
+    (dict(n_var_groups=128, head_dim=64), EUNSUP),
+    (dict(group_layout=2), EUNSUP),
+])
+def test_invalid_dims_rejected(bad, code):
+    d = dims(**bad)
+    L = P.library()
+    assert L.compkv_build_stats(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == code
+    assert L.compkv_dense_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30,
+                                 None) == code
+
+
+def test_null_pointers_rejected():
+    d = dims()
+    L = P.library()
+    assert L.compkv_build_stats(ctypes.byref(d), None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == EINVAL
+    assert L.compkv_append_stats(ctypes.byref(d), FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == EINVAL
+    p = P.CompkvSelectParams(16, 1, 2, 0.088)
+    assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                 None, FAKE, 1 << 30, None) == EINVAL  # blk_logit required
+    assert L.compkv_sparse_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 16,
+                                  FAKE, None, FAKE, 1 << 30, None) == EINVAL
+
+
+def test_budget_below_mandatory_set_rejected():
+    """Section 4.2: the sink and recent blocks count inside the budget, so K < n_sink + n_recent
+    cannot be honoured."""
+    d = dims()
+    L = P.library()
+    for K, ns, nr in ((2, 1, 2), (0, 0, 0), (4, 3, 2)):
+        p = P.CompkvSelectParams(K, ns, nr, 0.088)
+        rc = L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                   None, FAKE, 1 << 30, None)
+        assert rc == (EINVAL if K < 1 else EBUDGET)
+
+
+def test_workspace_checks():
+    d = dims()
+    L = P.library()
+    p = P.CompkvSelectParams(16, 1, 2, 0.088)
+    need = P.compkv_workspace_bytes(d, 16, P.COMPKV_WS_SCORE_SELECT)
+    args = [FAKE] * 6 + [FAKE, None]
+    assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), *args, FAKE, need - 1, None) == EWS
+    assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), *args, None, need, None) == EWS
+    assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), *args, ctypes.c_void_p(4100), need,
+                                 None) == EWS  # misaligned
+    need = P.compkv_workspace_bytes(d, 1, P.COMPKV_WS_DENSE_DECODE)
+    assert L.compkv_dense_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, need - 1,
+                                 None) == EWS
+
+
+def test_summary_layout_matches_paper():
+    """Section 4.2: a block summary holds 2d + r + 1 scalars; the library stores the mean key (d),
+    grouped variances (r) and mean value (d) per block, and derives |b| from the sequence length."""
+    fx = json.load(open(os.path.join(GOLDEN, "summary_size.json")))
+    for case in fx["cases"]:
+        d = dims(head_dim=fx["head_dim"], n_var_groups=case["r"])
+        per_block = d.head_dim + d.n_var_groups + d.head_dim + 1
+        assert per_block == case["scalars_per_block"]
+
+
+def test_product_path_fails_loudly_without_library(monkeypatch, tmp_path):
+    """No CPU fallback: a missing library makes every call raise."""
+    from paper_2609_26300_amd import binding
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(binding.CompkvError):
+        binding.library()

@@ -1,0 +1,197 @@
+"""GPU parity: every call of the C ABI against the CPU oracle on seeded inputs (needs an MI355X).
+
+Cases span the tiny 4K workload, the Llama-3-8B-shaped 32K layer at full size, and edge cases:
+partial last blocks, block size 1, per-coordinate groups (r = d), the interleaved group layout,
+head_dim 64, group sizes 1/2/8, variable sequence lengths, contexts of 1-3 blocks (mandatory set
+overlap) and budgets at or above the block count.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_case import TOL, Case, check_selection, dev_bf16, rel_err
+from workloads import WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+TINY = WORKLOADS["tiny_4k"]
+LLAMA = WORKLOADS["llama8b_32k"]
+
+CASES = {
+    "tiny_4k": lambda: Case(TINY),
+    "llama8b_32k": lambda: Case(LLAMA),
+    "partial_tail": lambda: Case(TINY.with_(context=4001, seed=7)),
+    "block1": lambda: Case(TINY.with_(context=300, block_size=1, budget_blocks=40, seed=8)),
+    "r_eq_d": lambda: Case(TINY.with_(n_var_groups=128, seed=9)),
+    "interleaved_r8": lambda: Case(TINY.with_(n_var_groups=8, seed=10), layout=1),
+    "d64": lambda: Case(TINY.with_(head_dim=64, seed=11)),
+    "g1": lambda: Case(TINY.with_(n_q_heads=2, seed=12)),
+    "g2_b32": lambda: Case(TINY.with_(n_q_heads=4, block_size=32, budget_blocks=9, seed=13)),
+    "g8_b64": lambda: Case(TINY.with_(n_q_heads=16, block_size=64, context=8000, budget_blocks=12, seed=14)),
+    "varlen": lambda: Case(TINY.with_(batch=4, seed=15), seq_lens=[4096, 1000, 17, 49]),
+    "short": lambda: Case(TINY.with_(batch=4, seed=16), seq_lens=[1, 10, 16, 40], budget=3),
+    "budget_ge_x": lambda: Case(TINY.with_(context=1000, budget_blocks=80, seed=17)),
+    "wide_gqa_8k": lambda: Case(WORKLOADS["wide_gqa_64k"].with_(batch=2, context=8192, seed=18)),
+    "long_16k_lognormal": lambda: Case(WORKLOADS["long_128k"].with_(batch=1, context=16384, budget_blocks=32,
+                                                                    seed=19)),
+}
+_cache = {}
+
+
+@pytest.fixture(params=sorted(CASES), scope="module")
+def case(request):
+    name = request.param
+    if name not in _cache:
+        print(f"\n[case {name}] generating + running", flush=True)
+        c = CASES[name]()
+        c.run_all()
+        _cache[name] = c
+    return _cache[name]
+
+
+def _gpu(t):
+    return t.cpu().numpy()
+
+
+def test_build_stats_parity(case):
+    km, dv, vm = (_gpu(x) for x in (case.summ.kmean, case.summ.dvar, case.summ.vmean))
+    for b, h in case.units():
+        okm, odv, ovm = case.oracle_stats(b, h)
+        X = okm.shape[0]
+        assert rel_err(km[b, h, :X], okm, axis=1) <= TOL
+        assert rel_err(vm[b, h, :X], ovm, axis=1) <= TOL
+        assert rel_err(dv[b, h, :X], odv) <= TOL
+
+
+def test_score_select_parity(case):
+    sel, nsel = _gpu(case.sel), _gpu(case.n_sel)
+    scores, zbar = _gpu(case.scores), _gpu(case.blk_logit)
+    for b, h in case.units():
+        sc = case.oracle_scores(b, h)
+        X = sc["score"].shape[0]
+        assert rel_err(scores[b, h, :X], sc["score"]) <= TOL
+        assert rel_err(zbar[b, h, :, :X], sc["zbar"]) <= TOL
+        assert nsel[b, h] == min(case.budget, X)
+        check_selection(sel[b, h, :nsel[b, h]], sc["score"], case.budget, case.n_sink, case.n_recent)
+        assert np.all(sel[b, h, nsel[b, h]:] == -1)
+
+
+def test_sparse_decode_with_oracle_selection(case):
+    """Eq. compkv-output on the oracle's own selected set (decode tested apart from selection)."""
+    d = case.dims
+    sel = np.full((d.batch, d.n_kv_heads, case.budget), -1, np.int32)
+    nsel = np.zeros((d.batch, d.n_kv_heads), np.int32)
+    stats = {}
+    for b, h in case.units():
+        stats[b, h] = case.oracle_stats(b, h)
+        s = oracle.select(case.oracle_scores(b, h, stats[b, h])["score"], case.budget, case.n_sink, case.n_recent)
+        sel[b, h, :len(s)] = s
+        nsel[b, h] = len(s)
+    out, lse = case.sparse_decode(torch.from_numpy(sel).cuda(), torch.from_numpy(nsel).cuda())
+    out, lse = _gpu(out), _gpu(lse)
+    G = case.G
+    for b, h in case.units():
+        q, K, V, n = case.unit_inputs(b, h)
+        km, dv, vm = stats[b, h]
+        o, l = oracle.sparse_decode(q, K, V, km, vm, n, case.w.block_size, case.scale, sel[b, h, :nsel[b, h]])
+        assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL
+        assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, np.max(np.abs(l)))
+    case.sparse_decode()  # restore the pipeline's own output
+
+
+def test_end_to_end_parity(case):
+    """Whole step: once the GPU's selection passes the band rule, the oracle output recomputed on
+    that same selection must match the GPU output."""
+    sel, nsel = _gpu(case.sel), _gpu(case.n_sel)
+    out, lse = _gpu(case.out), _gpu(case.lse)
+    G = case.G
+    for b, h in case.units():
+        q, K, V, n = case.unit_inputs(b, h)
+        st = case.oracle_stats(b, h)
+        sc = case.oracle_scores(b, h, st)
+        s = sel[b, h, :nsel[b, h]]
+        check_selection(s, sc["score"], case.budget, case.n_sink, case.n_recent)
+        o, l = oracle.sparse_decode(q, K, V, st[0], st[2], n, case.w.block_size, case.scale, s)
+        assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL
+
+
+def test_dense_decode_parity(case):
+    out, lse = case.dense_decode()
+    out, lse = _gpu(out), _gpu(lse)
+    G = case.G
+    for b, h in case.units():
+        q, K, V, n = case.unit_inputs(b, h)
+        o, l = oracle.dense_decode(q, K, V, n, case.scale)
+        assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL
+        assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, np.max(np.abs(l)))
+
+
+def test_rerun_is_bit_identical(case):
+    """No float atomics: a second run reproduces every output bit."""
+    before = [x.clone() for x in (case.summ.kmean, case.summ.dvar, case.summ.vmean, case.sel, case.n_sel,
+                                  case.scores, case.out, case.lse)]
+    case.run_all()
+    after = (case.summ.kmean, case.summ.dvar, case.summ.vmean, case.sel, case.n_sel, case.scores, case.out, case.lse)
+    for x, y in zip(before, after):
+        assert torch.equal(x, y)
+
+
+# ---------------------------------------------------------------- special cases pinned by the paper
+
+def test_budget_all_blocks_equals_dense_on_gpu():
+    """K >= X: Eq. compkv-output has no omitted block, so sparse decode is dense attention."""
+    c = Case(TINY.with_(context=777, budget_blocks=64, seed=21))
+    c.run_all()
+    o_sp, l_sp = _gpu(c.out), _gpu(c.lse)
+    o_de, l_de = (_gpu(x) for x in c.dense_decode())
+    assert rel_err(o_sp, o_de, axis=-1) <= TOL and np.max(np.abs(l_sp - l_de)) <= 1e-4
+
+
+def test_block_size_one_equals_dense_on_gpu():
+    """B = 1: every pseudo-token is its token, so any budget reproduces dense attention."""
+    c = Case(TINY.with_(context=500, block_size=1, budget_blocks=20, seed=22))
+    c.run_all()
+    assert np.all(_gpu(c.scores)[:, :, :500] == 0.0)
+    # all scores tie at zero: the stable Top-K takes the lowest candidate ids
+    assert np.all(_gpu(c.sel) == np.array(list(range(18)) + [498, 499], np.int32))
+    o_de, l_de = (_gpu(x) for x in c.dense_decode())
+    assert rel_err(_gpu(c.out), o_de, axis=-1) <= TOL and np.max(np.abs(_gpu(c.lse) - l_de)) <= 1e-4
+
+
+def test_append_matches_build_bitwise():
+    """Streaming appends (Appendix E.1) give the same summaries, bit for bit, as a prefill build over
+    the final cache; completed blocks never change; the cache rows hold the appended tokens."""
+    w = TINY.with_(batch=2, context=1000, decode_steps=40, block_size=16, seed=23)
+    c = Case(w, max_seq_len=w.capacity)
+    n0 = 1000
+    torch.cuda.synchronize()
+    # cache holding only the prefix: zero the rows that the appends will write
+    c.K[:, :, n0:] = 0
+    c.V[:, :, n0:] = 0
+    c.build_stats()
+    km0 = c.summ.kmean.clone()
+    Kn = dev_bf16(c.K_bits[:, :, n0:n0 + 40])
+    Vn = dev_bf16(c.V_bits[:, :, n0:n0 + 40])
+    import paper_2609_26300_amd as P
+    for t in range(40):
+        sl = torch.full((w.batch,), n0 + t, dtype=torch.int32, device="cuda")
+        P.compkv_append_stats(c.dims, c.K, c.V, Kn[:, :, t].contiguous(), Vn[:, :, t].contiguous(), sl,
+                              c.summ.kmean, c.summ.dvar, c.summ.vmean)
+    torch.cuda.synchronize()
+    assert np.array_equal(c.K.view(torch.int16).cpu().numpy().view(np.uint16)[:, :, :n0 + 40],
+                          c.K_bits[:, :, :n0 + 40])
+    assert torch.equal(c.summ.kmean[:, :, :n0 // 16], km0[:, :, :n0 // 16])
+    ref = P.alloc_summaries(c.dims)
+    sl = torch.full((w.batch,), n0 + 40, dtype=torch.int32, device="cuda")
+    P.compkv_build_stats(c.dims, c.K, c.V, sl, ref.kmean, ref.dvar, ref.vmean)
+    X = -(-(n0 + 40) // 16)
+    assert torch.equal(ref.kmean[:, :, :X], c.summ.kmean[:, :, :X])
+    assert torch.equal(ref.dvar[:, :, :X], c.summ.dvar[:, :, :X])
+    assert torch.equal(ref.vmean[:, :, :X], c.summ.vmean[:, :, :X])
+    # and against the oracle
+    for b in range(w.batch):
+        for h in range(w.n_kv_heads):
+            okm, odv, ovm = oracle.block_stats(c.K_bits[b, h], c.V_bits[b, h], n0 + 40, 16, w.n_var_groups)
+            assert rel_err(c.summ.kmean[b, h, :X].cpu().numpy(), okm, axis=1) <= TOL
+            assert rel_err(c.summ.dvar[b, h, :X].cpu().numpy(), odv) <= TOL
