@@ -139,64 +139,83 @@ def main():
     params = P.CompkvSelectParams(budget, 1, 2, scale)
     torch.cuda.synchronize()
 
-    names = ["append_stats", "score_select", "sparse_decode"]
-
-    def sparse_step(i, ev=None):
-        L = i % layers
+    def append(L):
         s = summ[L]
-        if ev is not None:
-            ev[0].record()
         P.compkv_append_stats(dims, Ks[L], Vs[L], k_new, v_new, seq_before, s.kmean, s.dvar, s.vmean)
-        if ev is not None:
-            ev[1].record()
-        P.compkv_score_select(dims, params, q, s.kmean, s.dvar, seq_after, sel, n_sel, blk_logit, None, ws)
-        if ev is not None:
-            ev[2].record()
-        P.compkv_sparse_decode(dims, scale, q, Ks[L], Vs[L], s.vmean, blk_logit, seq_after, sel, n_sel, out, lse, ws)
-        if ev is not None:
-            ev[3].record()
 
-    def dense_step(i, ev=None):
-        L = i % layers
-        if ev is not None:
-            ev[0].record()
+    def score(L):
+        s = summ[L]
+        P.compkv_score_select(dims, params, q, s.kmean, s.dvar, seq_after, sel, n_sel, blk_logit, None, ws)
+
+    def decode(L):
+        P.compkv_sparse_decode(dims, scale, q, Ks[L], Vs[L], summ[L].vmean, blk_logit, seq_after, sel, n_sel,
+                               out, lse, ws)
+
+    def row_write(L):
         Ks[L][:, :, n - 1] = k_new
         Vs[L][:, :, n - 1] = v_new
-        if ev is not None:
-            ev[1].record()
-        P.compkv_dense_decode(dims, scale, q, Ks[L], Vs[L], seq_after, out, lse, ws)
-        if ev is not None:
-            ev[2].record()
 
-    def timed(step, nev):
-        for i in range(args.warmup):
-            step(i)
+    def dense(L):
+        P.compkv_dense_decode(dims, scale, q, Ks[L], Vs[L], seq_after, out, lse, ws)
+
+    def capture(fns, layer_ids):
+        """One HIP graph running fns (in order) for each layer in layer_ids."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):  # eager warm-up off the capture
+            for L in layer_ids:
+                for f in fns:
+                    f(L)
+        torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for L in layer_ids:
+                for f in fns:
+                    f(L)
+        torch.cuda.synchronize()
+        return g
+
+    def run_steps(fns, steps, warmup):
+        """Time exactly `steps` steps (one layer each, rotating) as replays of captured graphs."""
+        full = capture(fns, list(range(layers)))
+        tail_n = steps % layers
+        tail = capture(fns, list(range(tail_n))) if tail_n else None
+
+        def replay(k):
+            for _ in range(k // layers):
+                full.replay()
+            if k % layers:
+                (tail if k % layers == tail_n else capture(fns, list(range(k % layers)))).replay()
+
+        replay(warmup)
+        torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
         wall0 = time.perf_counter()
         t0.record()
-        for i in range(args.steps):
-            step(i, evs[i])
+        replay(steps)
         t1.record()
         torch.cuda.synchronize()
-        wall = time.perf_counter() - wall0
-        per_kernel = [float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) * 1e3 for k in range(nev - 1)]
-        return t0.elapsed_time(t1) * 1e3 / args.steps, per_kernel, wall
+        return t0.elapsed_time(t1) * 1e3 / steps, time.perf_counter() - wall0
 
     result = {}
     if args.only in ("all", "sparse"):
-        us, per_k, wall = timed(sparse_step, 4)
-        result["sparse"] = (us, dict(zip(names, per_k)), wall)
+        us, wall = run_steps([append, score, decode], args.steps, args.warmup)
+        per_k = {name: run_steps([f], args.steps, args.warmup)[0]
+                 for name, f in (("append_stats", append), ("score_select", score), ("sparse_decode", decode))}
+        # leave the outputs of a complete step for the checks below
+        append(0), score(0), decode(0)
+        torch.cuda.synchronize()
+        result["sparse"] = (us, per_k, wall)
         sel_host = sel.cpu().numpy().reshape(-1, budget)
         nsel_host = n_sel.cpu().numpy().reshape(-1)
         sel_lists = [list(sel_host[u, :nsel_host[u]]) for u in range(w.units)]
         assert all(len(s) == min(budget, -(-n // w.block_size)) for s in sel_lists), "selection count mismatch"
     if args.only in ("all", "dense"):
-        us_d, per_kd, wall_d = timed(dense_step, 3)
-        result["dense"] = (us_d, dict(zip(["kv_row_write", "dense_decode"], per_kd)), wall_d)
+        us_d, wall_d = run_steps([row_write, dense], args.steps, args.warmup)
+        per_kd = {"dense_decode": run_steps([dense], args.steps, args.warmup)[0]}
+        result["dense"] = (us_d, per_kd, wall_d)
 
     line = {
         "metric": "us/decode-step/layer and HBM GB/s (fraction of peak); speedup vs dense decode",

@@ -28,10 +28,9 @@
  *      scores            fp32 [batch][n_kv_heads][Xcap]
  *      out               fp32 [batch][n_q_heads][d]; lse fp32 [batch][n_q_heads] (natural log)
  *  - bf16 values are passed as their 16-bit patterns. Inputs must be finite.
- *  - workspace: device scratch of at least compkv_workspace_bytes(...) bytes, 256-byte aligned.
- *    Its first bytes hold arrival counters that must be ZERO before the first call that uses the
- *    buffer (e.g. allocate it zeroed); every call leaves them zero again when it completes. Calls
- *    that may run concurrently need distinct workspaces.
+ *  - workspace: device scratch of at least compkv_workspace_bytes(...) bytes, 256-byte aligned, with
+ *    no initial contents required. Each call that takes one enqueues two kernels: the second reads
+ *    what the first wrote there. Calls that may run concurrently need distinct workspaces.
  *  - Return value: COMPKV_OK (0) or a negative status; compkv_status_string() names it. On error
  *    nothing has been enqueued, except for COMPKV_EHIP (a launch failed).
  *

@@ -136,7 +136,7 @@ def compkv_workspace_bytes(dims: CompkvDims, budget_blocks: int, which: int = CO
 
 
 def alloc_workspace(dims: CompkvDims, budget_blocks: int, device="cuda") -> torch.Tensor:
-    """Zeroed workspace large enough for every call (its arrival counters start at zero)."""
+    """Workspace large enough for every call (no initial contents are required)."""
     nbytes = compkv_workspace_bytes(dims, budget_blocks, COMPKV_WS_ALL)
     if nbytes == 0:
         raise CompkvError("invalid dims for workspace sizing")

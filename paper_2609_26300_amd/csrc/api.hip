@@ -55,8 +55,8 @@ struct ScoreShape {
 ScoreShape score_shape(const Geom& g) {
     const int xmax = g.xmax();
     int bpc = 32;
-    // widen chunks while the grid stays >= 1024 workgroups (fewer partials to merge)
-    while (bpc < 256 && (long long)g.units() * ceil_div(xmax, bpc * 2) >= 1024) bpc *= 2;
+    // widen chunks while the grid keeps >= 1024 workgroups (fewer partials to merge)
+    while (bpc < compkv::select_max_bpc() && (long long)g.units() * ceil_div(xmax, bpc * 2) >= 1024) bpc *= 2;
     return {bpc, ceil_div(xmax, bpc)};
 }
 
@@ -67,12 +67,11 @@ struct SparseShape {
 SparseShape sparse_shape(const Geom& g, int K) {
     const int xmax = g.xmax();
     const int keff = std::max(1, std::min(K, xmax));
-    int eb = std::max(1, 128 / g.B);                // about 128 exact tokens per item
-    eb = std::max(eb, ceil_div(keff, 160));         // at most 160 exact items
+    int eb = std::max(1, 128 / g.B);         // one round of 128 exact tokens per item
+    eb = std::max(eb, ceil_div(keff, 128));  // at most 128 exact items
     const int n_exact = ceil_div(keff, eb);
-    int cb = std::max(32, ceil_div(xmax, 32));      // at most 32 compensation items
-    cb = ceil_div(cb, 32) * 32;
-    cb = std::max(cb, ceil_div(xmax, 256 - n_exact));
+    int cb = 128;                            // mean-value rows per compensation item
+    cb = std::max(cb, ceil_div(xmax, compkv::decode_max_items() - n_exact));
     const int n_comp = ceil_div(xmax, cb);
     return {eb, n_exact, cb, n_comp};
 }
@@ -82,14 +81,13 @@ struct DenseShape {
 };
 
 DenseShape dense_shape(const Geom& g) {
-    int te = std::max(256, ceil_div(g.max_seq, 128));
-    te = ceil_div(te, 64) * 64;
+    int te = std::max(128, ceil_div(g.max_seq, 128));  // at most 128 items per unit
+    te = ceil_div(te, 128) * 128;                       // whole rounds of 128 tokens
     return {te, ceil_div(g.max_seq, te)};
 }
 
 // ---------------------------------------------------------------- workspace layout
 
-size_t counters_bytes(const Geom& g) { return align_up((size_t)g.units() * sizeof(uint32_t)); }
 
 size_t score_ws(const Geom& g) {
     const ScoreShape sh = score_shape(g);
@@ -113,7 +111,7 @@ size_t ws_bytes(const Geom& g, int K, int which) {
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SCORE_SELECT) body = std::max(body, score_ws(g));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SPARSE_DECODE) body = std::max(body, sparse_ws(g, K));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_DENSE_DECODE) body = std::max(body, dense_ws(g));
-    return counters_bytes(g) + body;
+    return body;
 }
 
 int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
@@ -202,8 +200,7 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     const size_t units = g.units(), xmax = g.xmax();
     char* base = static_cast<char*>(workspace);
     compkv::ScoreArgs a{};
-    a.counters = reinterpret_cast<uint32_t*>(base);
-    char* p = base + counters_bytes(g);
+    char* p = base;
     a.ws_part = reinterpret_cast<float*>(p);
     p += align_up(units * sh.nchunks * g.G * 2 * sizeof(float));
     a.ws_a = reinterpret_cast<float*>(p);
@@ -243,10 +240,10 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
     const SparseShape sh = sparse_shape(g, sel_stride);
+    if (sh.cb > compkv::decode_max_cb()) return COMPKV_EUNSUPPORTED;
     char* base = static_cast<char*>(workspace);
     compkv::DecodeArgs a{};
-    a.counters = reinterpret_cast<uint32_t*>(base);
-    a.ws_part = reinterpret_cast<float*>(base + counters_bytes(g));
+    a.ws_part = reinterpret_cast<float*>(base);
     a.q = static_cast<const uint16_t*>(q);
     a.K = static_cast<const uint16_t*>(k_cache);
     a.V = static_cast<const uint16_t*>(v_cache);
@@ -280,8 +277,7 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
     const DenseShape sh = dense_shape(g);
     char* base = static_cast<char*>(workspace);
     compkv::DecodeArgs a{};
-    a.counters = reinterpret_cast<uint32_t*>(base);
-    a.ws_part = reinterpret_cast<float*>(base + counters_bytes(g));
+    a.ws_part = reinterpret_cast<float*>(base);
     a.q = static_cast<const uint16_t*>(q);
     a.K = static_cast<const uint16_t*>(k_cache);
     a.V = static_cast<const uint16_t*>(v_cache);

@@ -1,278 +1,462 @@
 // decode.hip -- compensated sparse decode and dense decode (Eq. compkv-output; Section 3.1).
 //
 // grid = (items, units). Every item produces one softmax partial per query head of its unit: the
-// running max m, the sum of weights l and the weighted value sum acc[d] (flash-decoding split-K).
+// max m, the sum of weights l and the weighted value sum acc[d] (flash-decoding split-K).
 //   * exact items (sparse): the tokens of up to `eb` consecutive entries of the selected-id list;
-//   * compensation items (sparse): the unselected blocks of a range of `cb` block ids, each entering
-//     once as a pseudo-token with logit log|b| + zbar_b and value vmean_b;
-//   * dense items: a contiguous range of `eb` tokens.
-// The last item of a unit to arrive (atomic ticket) merges all partials of that unit in item order,
-// so the result does not depend on scheduling. Nothing waits on another workgroup.
+//   * compensation items (sparse): the unselected blocks among `cb` consecutive block ids, each
+//     entering once as a pseudo-token with logit log|b| + zbar_b and value vmean_b;
+//   * dense items: `eb` consecutive tokens.
+// A second launch, grid = (units, G), merges each unit's partials in item order, so the result does
+// not depend on scheduling; the kernel boundary makes the partials visible (no cross-workgroup fences).
 //
-// Exact tokens: d/8 lanes share a token, each holding 8 coordinates (one 16-byte load of the bf16
-// row), so a wave reads 4 rows (d = 128) per load. Logits are reduced across those lanes; every token
-// slot keeps its own online softmax state, and the slots are merged at the end of the item.
-// Compensation: d/4 lanes share a block's fp32 mean-value row (one float4 each).
+// Exact tokens run on the matrix cores, 16 tokens per wave and tile. The logits are formed as
+// S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = 16 key rows, B = the unit's query heads as columns,
+// zero-padded to 16): lane l then holds the logits of head l%16 for tokens 4(l/16)..4(l/16)+3, which is
+// exactly the A-operand layout of v_mfma_f32_16x16x16bf16_1k, so the probabilities feed the P.V product
+// without any data movement. For P.V the value row of each of the lane's 4 tokens is loaded as one
+// contiguous chunk of d/16 coordinates (coordinate (d/16)*(l%16) + j goes to output block j), so every
+// load is a contiguous piece of a row. P.V runs as v_mfma_f32_16x16x32_bf16 over a pair of tiles, with
+// P split into three bf16 terms (three MFMAs), which keeps P within 2^-27 of its fp32 value; products
+// with the bf16 values are exact and accumulate in fp32. The softmax max is taken per pair of tiles.
+//
+// Compensation items are plain fp32 streaming on the vector ALUs: pass 1 forms the pseudo-logits of
+// the item's unselected blocks and their per-head max, pass 2 streams the mean-value rows (d/4 lanes x
+// float4 per row) with all loads of a lane issued before use.
 #include "internal.h"
 
 namespace compkv {
 namespace {
 
-constexpr int kMaxItems = 256;  // partials per unit, upper bound (checked by the host)
-constexpr int kCbMax = 2048;    // blocks per compensation item, upper bound
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf16 __attribute__((ext_vector_type(8)));
+typedef float v4f32 __attribute__((ext_vector_type(4)));
 
-template <int G, int CPL>
-struct SoftmaxState {
-    float m[G], l[G], acc[G][CPL];
-    __device__ void init() {
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            m[g] = -INFINITY;
-            l[g] = 0.0f;
-#pragma unroll
-            for (int e = 0; e < CPL; ++e) acc[g][e] = 0.0f;
-        }
-    }
-    // add one term with logit z[g] and value vals[e] (same value row for every head)
-    __device__ void add(const float (&z)[G], const float (&vals)[CPL]) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const float mn = fmaxf(m[g], z[g]);
-            const float c = (m[g] == -INFINITY) ? 0.0f : __expf(m[g] - mn);
-            const float w = __expf(z[g] - mn);
-            l[g] = l[g] * c + w;
-#pragma unroll
-            for (int e = 0; e < CPL; ++e) acc[g][e] = acc[g][e] * c + w * vals[e];
-            m[g] = mn;
-        }
-    }
-    // merge with the state of the lane `off` away (xor), for lanes holding the same coordinates
-    __device__ void merge_xor(int off) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const float mo = __shfl_xor(m[g], off);
-            const float lo = __shfl_xor(l[g], off);
-            float mn, ca, cb;
-            merge_scales(m[g], mo, mn, ca, cb);
-            l[g] = l[g] * ca + lo * cb;
-#pragma unroll
-            for (int e = 0; e < CPL; ++e) {
-                const float ao = __shfl_xor(acc[g][e], off);
-                acc[g][e] = acc[g][e] * ca + ao * cb;
-            }
-            m[g] = mn;
-        }
-    }
-};
+constexpr int kMaxItems = 256;  // partials per unit, upper bound (checked by the host)
+constexpr int kCbMax = 512;     // blocks per compensation item, upper bound
+constexpr int kTilesPerRound = 2;  // P.V pairs two 16-token tiles into one 32-deep MFMA
 
 template <int D, int G>
 struct DecodeShared {
     float m[4][G], l[4][G];
     float acc[4][G][D];
-    unsigned char flag[kCbMax];
-    float pm[G][kMaxItems], pc[G][kMaxItems];
+    float w[G][kCbMax];  // compensation weights
     float M[G], L[G];
-    int last;
+    unsigned char flag[kCbMax];
 };
 
-// Reduce the per-slot states of the workgroup (LPS lanes per slot, CPL coordinates per lane at
-// coordinate li*CPL) and write the item's partial. Called by all threads.
-template <int D, int G, int CPL, int LPS>
-__device__ void finish_item(SoftmaxState<G, CPL>& st, DecodeShared<D, G>& sh, float* part) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int li = lane % LPS;
+__device__ __forceinline__ short f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    return (short)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+__device__ __forceinline__ float bf16_bits_to_f32(short h) { return __uint_as_float(uint32_t((unsigned short)h) << 16); }
+
+// virtual token v of an item -> cache row, or -1 if v is past the item's tokens / the block's length
+struct TokenMap {
+    const int32_t* sel;  // sparse: the item's selected ids (first entry of the item)
+    int nblk, B, n, X;   // sparse
+    int t0, t1;          // dense: row range
+    bool dense;
+    __device__ int row(int v) const {
+        if (dense) {
+            const int r = t0 + v;
+            return r < t1 ? r : -1;
+        }
+        const int k = v / B;
+        if (k >= nblk) return -1;
+        const int blk = sel[k];
+        const int off = v - k * B;
+        if (blk < 0 || blk >= X || off >= min(B, n - blk * B)) return -1;
+        return blk * B + off;
+    }
+    __device__ int count() const { return dense ? max(0, t1 - t0) : nblk * B; }
+};
+
+// Exact tokens of one item with MFMA. Leaves this wave's (m, l) for head lane%16 (lanes with the same
+// lane%16 agree) and acc[j][i] = sum over the wave's tokens of p * v for head 4(lane/16)+i at
+// coordinate (D/16)*(lane%16) + j.
+template <int D, int G>
+__device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku, const uint16_t* __restrict__ Vu,
+                             const uint16_t* __restrict__ qh, float scale, float& m, float& l, v4f32 (&acc)[D / 16]) {
+    constexpr int KS = D / 32;   // k-steps of the logit MFMA
+    constexpr int CPL = D / 16;  // value coordinates per lane (= output blocks)
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    // B operand of the logit product: query head `col` (zero for padding heads)
+    v8bf16 qb[KS];
 #pragma unroll
-    for (int off = LPS; off < 64; off <<= 1) st.merge_xor(off);
-    if (lane < LPS) {
+    for (int ks = 0; ks < KS; ++ks) {
+        uint4 w = make_uint4(0, 0, 0, 0);
+        if (col < G) w = *reinterpret_cast<const uint4*>(qh + col * D + 32 * ks + 8 * grp);
+        qb[ks] = __builtin_bit_cast(v8bf16, w);
+    }
+    m = -INFINITY;
+    l = 0.0f;
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            if (li == 0) {
-                sh.m[wave][g] = st.m[g];
-                sh.l[wave][g] = st.l[g];
+    for (int j = 0; j < CPL; ++j) acc[j] = v4f32{0.0f, 0.0f, 0.0f, 0.0f};
+    const int ntiles = (tm.count() + 15) / 16;
+    for (int t0 = wave * kTilesPerRound; t0 < ntiles; t0 += 4 * kTilesPerRound) {
+        uint4 kreg[kTilesPerRound][KS];
+        uint4 vreg[kTilesPerRound][4];
+        bool vvalid[kTilesPerRound][4];
+        // issue every load of the round first
+#pragma unroll
+        for (int t = 0; t < kTilesPerRound; ++t) {
+            const int base = (t0 + t) * 16;
+            const int rk = (t0 + t < ntiles) ? tm.row(base + col) : -1;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                kreg[t][ks] = rk >= 0 ? *reinterpret_cast<const uint4*>(Ku + (size_t)rk * D + 32 * ks + 8 * grp)
+                                      : make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int rv = (t0 + t < ntiles) ? tm.row(base + 4 * grp + e) : -1;
+                vvalid[t][e] = rv >= 0;
+                if constexpr (CPL == 8) {
+                    vreg[t][e] = rv >= 0 ? *reinterpret_cast<const uint4*>(Vu + (size_t)rv * D + CPL * col)
+                                         : make_uint4(0, 0, 0, 0);
+                } else {
+                    const uint2 h = rv >= 0 ? *reinterpret_cast<const uint2*>(Vu + (size_t)rv * D + CPL * col)
+                                            : make_uint2(0, 0);
+                    vreg[t][e] = make_uint4(h.x, h.y, 0, 0);
+                }
             }
+        }
+        // logits: lane holds head `col`, tokens 4*grp + i of each tile
+        float z[kTilesPerRound][4];
+        float rmax = -INFINITY;
 #pragma unroll
-            for (int e = 0; e < CPL; ++e) sh.acc[wave][g][li * CPL + e] = st.acc[g][e];
+        for (int t = 0; t < kTilesPerRound; ++t) {
+            v4f32 s = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf16, kreg[t][ks]), qb[ks], s, 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                z[t][i] = vvalid[t][i] ? scale * s[i] : -INFINITY;
+                rmax = fmaxf(rmax, z[t][i]);
+            }
+        }
+        rmax = fmaxf(rmax, __shfl_xor(rmax, 16));
+        rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
+        const float m_new = fmaxf(m, rmax);
+        if (m_new == -INFINITY) continue;  // nothing valid for this head yet (uniform per wave-round)
+        const float c = (m == -INFINITY) ? 0.0f : __expf(m - m_new);
+        m = m_new;
+        l *= c;
+        // rescale accumulator rows: row i holds head 4*grp + i, whose factor lives in lane 4*grp + i
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float ci = __shfl(c, 4 * grp + i);
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) acc[j][i] *= ci;
+        }
+        // P.V over the pair of tiles with v_mfma_f32_16x16x32_bf16: k-index 8*grp + e is token 4*grp + e
+        // of tile 0 for e < 4 and token 4*grp + e - 4 of tile 1 for e >= 4, in both operands. P is split
+        // into three bf16 terms (hi + mid + lo equals p to within 2^-27 relative).
+        v8bf16 pa[3];
+#pragma unroll
+        for (int t = 0; t < kTilesPerRound; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float p = z[t][i] == -INFINITY ? 0.0f : __expf(z[t][i] - m);
+                l += p;
+                const short hi = f32_to_bf16_rne(p);
+                const float r1 = p - bf16_bits_to_f32(hi);
+                const short mid = f32_to_bf16_rne(r1);
+                const short lo = f32_to_bf16_rne(r1 - bf16_bits_to_f32(mid));
+                pa[0][4 * t + i] = __builtin_bit_cast(__bf16, hi);
+                pa[1][4 * t + i] = __builtin_bit_cast(__bf16, mid);
+                pa[2][4 * t + i] = __builtin_bit_cast(__bf16, lo);
+            }
+        const uint32_t* w[2][4];
+#pragma unroll
+        for (int t = 0; t < kTilesPerRound; ++t)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[t][e] = reinterpret_cast<const uint32_t*>(&vreg[t][e]);
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            // B operand for output block j: element 8*grp + e = coordinate CPL*col + j of that token
+            const int wi = j >> 1;
+            uint32_t pk[4];
+#pragma unroll
+            for (int t = 0; t < kTilesPerRound; ++t) {
+                if ((j & 1) == 0) {
+                    pk[2 * t] = (w[t][0][wi] & 0xFFFFu) | (w[t][1][wi] << 16);
+                    pk[2 * t + 1] = (w[t][2][wi] & 0xFFFFu) | (w[t][3][wi] << 16);
+                } else {
+                    pk[2 * t] = (w[t][0][wi] >> 16) | (w[t][1][wi] & 0xFFFF0000u);
+                    pk[2 * t + 1] = (w[t][2][wi] >> 16) | (w[t][3][wi] & 0xFFFF0000u);
+                }
+            }
+            const v8bf16 bv = __builtin_bit_cast(v8bf16, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+#pragma unroll
+            for (int k = 0; k < 3; ++k) acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[k], bv, acc[j], 0, 0, 0);
+        }
+    }
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+}
+
+// Combine the four waves' exact states in LDS and write the item's partial.
+template <int D, int G>
+__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part) {
+    constexpr int CPL = D / 16;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    if (grp == 0 && col < G) {
+        sh.m[wave][col] = m;
+        sh.l[wave][col] = l;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int g = 4 * grp + i;
+        if (g < G) {
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) sh.acc[wave][g][CPL * col + j] = acc[j][i];
         }
     }
     __syncthreads();
     for (int idx = tid; idx < G * D; idx += kThreads) {
         const int g = idx / D, i = idx % D;
-        float m = -INFINITY, l = 0.0f, acc = 0.0f;
+        float mm = -INFINITY, ll = 0.0f, aa = 0.0f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             float mn, ca, cb;
-            merge_scales(m, sh.m[w][g], mn, ca, cb);
-            l = l * ca + sh.l[w][g] * cb;
-            acc = acc * ca + sh.acc[w][g][i] * cb;
-            m = mn;
+            merge_scales(mm, sh.m[w][g], mn, ca, cb);
+            ll = ll * ca + sh.l[w][g] * cb;
+            aa = aa * ca + sh.acc[w][g][i] * cb;
+            mm = mn;
         }
         float* p = part + (size_t)g * (D + 2);
         if (i == 0) {
-            p[0] = m;
-            p[1] = l;
+            p[0] = mm;
+            p[1] = ll;
         }
-        p[2 + i] = acc;
+        p[2 + i] = aa;
+    }
+}
+
+// Pseudo-tokens of the unselected blocks in [c0, c1).
+template <int D, int G>
+__device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n, int X, int c0, int c1,
+                             DecodeShared<D, G>& sh, float* part) {
+    constexpr int LPB = D / 4;          // lanes per mean-value row (one float4 each)
+    constexpr int RPS = kThreads / LPB;  // rows per workgroup step
+    constexpr int UNR = 8;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nb = max(0, c1 - c0);
+    const int nsel = min(a.n_sel[u], a.sel_stride);
+    const int32_t* selu = a.sel + (size_t)u * a.sel_stride;
+    for (int i = tid; i < nb; i += kThreads) sh.flag[i] = 0;
+    __syncthreads();
+    for (int k = tid; k < nsel; k += kThreads) {
+        const int sb = selu[k];
+        if (sb >= c0 && sb < c1) sh.flag[sb - c0] = 1;
+    }
+    __syncthreads();
+    // pass 1: pseudo-logits log|b| + zbar and their per-head max
+    const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
+    for (int idx = tid; idx < G * nb; idx += kThreads) {
+        const int g = idx / nb, lb = idx % nb, b = c0 + lb;
+        sh.w[g][lb] = sh.flag[lb] ? -INFINITY
+                                  : logf((float)min(geo.B, n - b * geo.B)) + lg[(size_t)g * geo.xcap + b];
+    }
+    __syncthreads();
+    for (int g = wave; g < G; g += 4) {
+        float mx = -INFINITY;
+        for (int lb = lane; lb < nb; lb += 64) mx = fmaxf(mx, sh.w[g][lb]);
+        mx = wave_max(mx);
+        float sum = 0.0f;
+        for (int lb = lane; lb < nb; lb += 64) {
+            const float wv = (mx == -INFINITY || sh.w[g][lb] == -INFINITY) ? 0.0f : __expf(sh.w[g][lb] - mx);
+            sh.w[g][lb] = wv;
+            sum += wv;
+        }
+        sum = wave_sum(sum);
+        if (lane == 0) {
+            sh.M[g] = mx;
+            sh.L[g] = sum;
+        }
+    }
+    __syncthreads();
+    // pass 2: weighted mean values; lane li of a row slot holds coordinates 4li..4li+3
+    const int li = tid % LPB, slot = tid / LPB;
+    float acc[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
+    const float4* vm = reinterpret_cast<const float4*>(a.vmean + ((size_t)u * geo.xcap + c0) * D) + li;
+    for (int lb0 = slot; lb0 < nb; lb0 += RPS * UNR) {
+        float4 v[UNR];
+#pragma unroll
+        for (int k = 0; k < UNR; ++k) {
+            const int lb = lb0 + k * RPS;
+            v[k] = (lb < nb && !sh.flag[lb]) ? vm[(size_t)lb * (D / 4)] : make_float4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int k = 0; k < UNR; ++k) {
+            const int lb = lb0 + k * RPS;
+            if (lb >= nb) break;
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float wv = sh.w[g][lb];
+                acc[g][0] += wv * v[k].x;
+                acc[g][1] += wv * v[k].y;
+                acc[g][2] += wv * v[k].z;
+                acc[g][3] += wv * v[k].w;
+            }
+        }
+    }
+    // reduce over row slots: lanes li and li + LPB of a wave, then the four waves
+#pragma unroll
+    for (int off = LPB; off < 64; off <<= 1)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
+    if (lane < LPB) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sh.acc[wave][g][4 * li + e] = acc[g][e];
+    }
+    __syncthreads();
+    for (int idx = tid; idx < G * D; idx += kThreads) {
+        const int g = idx / D, i = idx % D;
+        float* p = part + (size_t)g * (D + 2);
+        if (i == 0) {
+            p[0] = sh.M[g];
+            p[1] = sh.L[g];
+        }
+        p[2 + i] = sh.acc[0][g][i] + sh.acc[1][g][i] + sh.acc[2][g][i] + sh.acc[3][g][i];
     }
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_kernel(Geom geo, DecodeArgs a) {
+__global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, DecodeArgs a) {
     __shared__ DecodeShared<D, G> sh;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x;
     const int u = blockIdx.y, item = blockIdx.x, nitems = gridDim.x;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* part = a.ws_part + ((size_t)u * nitems + item) * G * (D + 2);
-    const bool comp_item = !a.dense && item >= a.n_exact;
 
-    if (!comp_item) {
-        // ---------------- exact tokens
-        constexpr int LPT = D / 8, SPW = 64 / LPT, SLOTS = 4 * SPW;
-        const int li = lane % LPT, slot = wave * SPW + lane / LPT;
-        const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
-        float qreg[G][8];
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            float qf[8];
-            unpack_bf16x8(*reinterpret_cast<const uint4*>(qh + g * D + li * 8), qf);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) qreg[g][e] = a.scale * qf[e];
-        }
-        SoftmaxState<G, 8> st;
-        st.init();
-        const uint16_t* Ku = a.K + (size_t)u * geo.cap * D;
-        const uint16_t* Vu = a.V + (size_t)u * geo.cap * D;
-        int t0, t1;  // virtual token range
-        const int32_t* selu = a.sel + (size_t)u * a.sel_stride;
-        int nsel = 0, e0 = 0;
-        if (a.dense) {
-            t0 = item * a.eb;
-            t1 = min(t0 + a.eb, n);
+    if (a.dense || item < a.n_exact) {
+        TokenMap tm;
+        tm.dense = a.dense != 0;
+        tm.B = geo.B;
+        tm.n = n;
+        tm.X = X;
+        if (tm.dense) {
+            tm.t0 = item * a.eb;
+            tm.t1 = min(tm.t0 + a.eb, n);
+            tm.sel = nullptr;
+            tm.nblk = 0;
         } else {
-            nsel = min(a.n_sel[u], a.sel_stride);
-            e0 = item * a.eb;
-            t0 = 0;
-            t1 = max(0, min(a.eb, nsel - e0)) * geo.B;
+            const int nsel = min(a.n_sel[u], a.sel_stride);
+            const int e0 = item * a.eb;
+            tm.sel = a.sel + (size_t)u * a.sel_stride + e0;
+            tm.nblk = max(0, min(a.eb, nsel - e0));
+            tm.t0 = tm.t1 = 0;
         }
-        for (int t = t0 + slot; t < t1; t += SLOTS) {
-            int row;
-            if (a.dense) {
-                row = t;
-            } else {
-                const int blk = selu[e0 + t / geo.B];
-                const int off = t % geo.B;
-                if (blk < 0 || blk >= X || off >= min(geo.B, n - blk * geo.B)) continue;
-                row = blk * geo.B + off;
-            }
-            float kf[8], vf[8];
-            unpack_bf16x8(*reinterpret_cast<const uint4*>(Ku + (size_t)row * D + li * 8), kf);
-            unpack_bf16x8(*reinterpret_cast<const uint4*>(Vu + (size_t)row * D + li * 8), vf);
-            float z[G];
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                float acc = 0.0f;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc += qreg[g][e] * kf[e];
-                z[g] = acc;
-            }
-#pragma unroll
-            for (int off = 1; off < LPT; off <<= 1)
-#pragma unroll
-                for (int g = 0; g < G; ++g) z[g] += __shfl_xor(z[g], off);
-            st.add(z, vf);
-        }
-        finish_item<D, G, 8, LPT>(st, sh, part);
+        float m, l;
+        v4f32 acc[D / 16];
+        const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+        exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh, a.scale, m, l, acc);
+        finish_exact<D, G>(m, l, acc, sh, part);
     } else {
-        // ---------------- compensation pseudo-tokens of unselected blocks
-        constexpr int LPB = D / 4, BPW = 64 / LPB, CSLOTS = 4 * BPW;
-        const int li = lane % LPB, cslot = wave * BPW + lane / LPB;
         const int c0 = (item - a.n_exact) * a.cb;
-        const int c1 = min(c0 + a.cb, X);
-        const int nsel = min(a.n_sel[u], a.sel_stride);
-        const int32_t* selu = a.sel + (size_t)u * a.sel_stride;
-        for (int i = tid; i < a.cb; i += kThreads) sh.flag[i] = 0;
-        __syncthreads();
-        for (int k = tid; k < nsel; k += kThreads) {
-            const int sb = selu[k];
-            if (sb >= c0 && sb < c1) sh.flag[sb - c0] = 1;
-        }
-        __syncthreads();
-        SoftmaxState<G, 4> st;
-        st.init();
-        const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
-        for (int lb = cslot; lb < c1 - c0; lb += CSLOTS) {
-            if (sh.flag[lb]) continue;
-            const int b = c0 + lb;
-            const float lnb = logf((float)min(geo.B, n - b * geo.B));
-            float z[G];
-#pragma unroll
-            for (int g = 0; g < G; ++g) z[g] = lnb + lg[(size_t)g * geo.xcap + b];
-            const float4 v4 = reinterpret_cast<const float4*>(a.vmean + ((size_t)u * geo.xcap + b) * D)[li];
-            const float vals[4] = {v4.x, v4.y, v4.z, v4.w};
-            st.add(z, vals);
-        }
-        finish_item<D, G, 4, LPB>(st, sh, part);
+        compensation<D, G>(a, geo, u, n, X, c0, min(c0 + a.cb, X), sh, part);
     }
 
-    // ---------------- arrival ticket; the last item of the unit merges
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) sh.last = (atomicAdd(&a.counters[u], 1u) == (unsigned)(nitems - 1));
-    __syncthreads();
-    if (!sh.last) return;
-    __threadfence();
+}
 
-    const float* pu = a.ws_part + (size_t)u * nitems * G * (D + 2);
-    for (int idx = tid; idx < G * nitems; idx += kThreads) {
-        const int g = idx / nitems, it = idx % nitems;
-        const float* p = pu + ((size_t)it * G + g) * (D + 2);
-        sh.pm[g][it] = p[0];
-        sh.pc[g][it] = p[1];
+// Merge of one (unit, query head): the item partials in item order, with every load issued well ahead.
+// grid = (units, G); thread (s, i) sums items s, s + S, ... for coordinate i, then the S partial sums
+// are added in LDS in a fixed order.
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, DecodeArgs a, int nitems) {
+    constexpr int S = kThreads / D;  // item subsets
+    constexpr int UNR = 16;
+    __shared__ float pm[kMaxItems], pc[kMaxItems];
+    __shared__ float part_acc[S][D];
+    __shared__ float sM, sL;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int u = blockIdx.x, g = blockIdx.y;
+    const int bseq = u / geo.hkv, h = u % geo.hkv;
+    const float* pu = a.ws_part + (size_t)u * nitems * G * (D + 2) + (size_t)g * (D + 2);
+    const size_t stride = (size_t)G * (D + 2);
+    for (int it = tid; it < nitems; it += kThreads) {
+        pm[it] = pu[it * stride];
+        pc[it] = pu[it * stride + 1];
     }
     __syncthreads();
-    if (tid < G) {
-        const int g = tid;
+    if (tid < 64) {
         float M = -INFINITY;
-        for (int it = 0; it < nitems; ++it) M = fmaxf(M, sh.pm[g][it]);
+        for (int it = lane; it < nitems; it += 64) M = fmaxf(M, pm[it]);
+        M = wave_max(M);
         float L = 0.0f;
-        for (int it = 0; it < nitems; ++it) {
-            const float c = (sh.pm[g][it] == -INFINITY) ? 0.0f : __expf(sh.pm[g][it] - M);
-            L += c * sh.pc[g][it];
-            sh.pc[g][it] = c;  // reuse as the item's rescale factor
+        for (int it = lane; it < nitems; it += 64) {
+            const float c = (pm[it] == -INFINITY) ? 0.0f : __expf(pm[it] - M);
+            L += c * pc[it];
+            pc[it] = c;  // from here on: the item's rescale factor
         }
-        sh.M[g] = M;
-        sh.L[g] = L;
+        L = wave_sum(L);
+        if (lane == 0) {
+            sM = M;
+            sL = L;
+        }
     }
     __syncthreads();
-    for (int idx = tid; idx < G * D; idx += kThreads) {
-        const int g = idx / D, i = idx % D;
-        float A = 0.0f;
-        for (int it = 0; it < nitems; ++it) {
-            const float c = sh.pc[g][it];
-            if (c != 0.0f) A += c * pu[((size_t)it * G + g) * (D + 2) + 2 + i];
-        }
-        const float L = sh.L[g];
-        const size_t o = (size_t)bseq * geo.hq + (size_t)h * G + g;
-        a.out[o * D + i] = L > 0.0f ? A / L : 0.0f;
-        if (i == 0 && a.lse) a.lse[o] = L > 0.0f ? sh.M[g] + logf(L) : -INFINITY;
+    const int i = tid % D, sub = tid / D;
+    const float* pi = pu + 2 + i;
+    float A = 0.0f;
+    int it = sub;
+    for (; it + (UNR - 1) * S < nitems; it += UNR * S) {
+        float x[UNR];
+#pragma unroll
+        for (int k = 0; k < UNR; ++k) x[k] = pi[(size_t)(it + k * S) * stride];
+#pragma unroll
+        for (int k = 0; k < UNR; ++k) A += pc[it + k * S] * x[k];
     }
-    if (tid == 0) a.counters[u] = 0u;
+    for (; it < nitems; it += S) A += pc[it] * pi[(size_t)it * stride];
+    part_acc[sub][i] = A;
+    __syncthreads();
+    if (sub == 0) {
+        float tot = 0.0f;
+#pragma unroll
+        for (int k = 0; k < S; ++k) tot += part_acc[k][i];
+        const float L = sL;
+        const size_t o = (size_t)bseq * geo.hq + (size_t)h * G + g;
+        a.out[o * D + i] = L > 0.0f ? tot / L : 0.0f;
+        if (i == 0 && a.lse) a.lse[o] = L > 0.0f ? sM + logf(L) : -INFINITY;
+    }
+}
+
+template <int D, int G>
+hipError_t launch_pair(const Geom& g, const DecodeArgs& a, hipStream_t s, dim3 grid) {
+    decode_items_kernel<D, G><<<grid, kThreads, 0, s>>>(g, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    decode_merge_kernel<D, G><<<dim3(g.units(), G), kThreads, 0, s>>>(g, a, (int)grid.x);
+    return hipGetLastError();
 }
 
 template <int D>
 hipError_t dispatch_g(const Geom& g, const DecodeArgs& a, hipStream_t s, dim3 grid) {
     switch (g.G) {
-        case 1: decode_kernel<D, 1><<<grid, kThreads, 0, s>>>(g, a); break;
-        case 2: decode_kernel<D, 2><<<grid, kThreads, 0, s>>>(g, a); break;
-        case 4: decode_kernel<D, 4><<<grid, kThreads, 0, s>>>(g, a); break;
-        case 8: decode_kernel<D, 8><<<grid, kThreads, 0, s>>>(g, a); break;
+        case 1: return launch_pair<D, 1>(g, a, s, grid);
+        case 2: return launch_pair<D, 2>(g, a, s, grid);
+        case 4: return launch_pair<D, 4>(g, a, s, grid);
+        case 8: return launch_pair<D, 8>(g, a, s, grid);
         default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 }  // namespace
+
+int decode_max_items() { return kMaxItems; }
+int decode_max_cb() { return kCbMax; }
 
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s) {
     const int items = a.dense ? a.n_exact : a.n_exact + a.n_comp;

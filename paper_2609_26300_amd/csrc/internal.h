@@ -45,9 +45,9 @@ struct ScoreArgs {
     float* ws_a;       // [units][G][xmax]       log block weight estimate
     float* ws_v;       // [units][G][xmax]       projected variance
     uint32_t* ws_key;  // [units][xmax]          score bits
-    uint32_t* counters;
-    int bpc;      // blocks per chunk (multiple of 32)
-    int nchunks;  // grid.x
+    int bpc;          // blocks per chunk (multiple of 32)
+    int nchunks;      // grid.x
+    int keys_in_lds;  // set by the launcher: score bits kept in LDS (else in ws_key)
     int K, n_sink, n_recent;
     float scale;
 };
@@ -64,7 +64,6 @@ struct DecodeArgs {
     float* out;
     float* lse;      // nullable
     float* ws_part;  // [units][items][G][D + 2]
-    uint32_t* counters;
     int sel_stride;
     int n_exact;  // exact items per unit
     int eb;       // selected blocks per exact item (sparse) / tokens per item (dense)
@@ -78,7 +77,10 @@ struct DecodeArgs {
 
 hipError_t launch_build_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
 hipError_t launch_append_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
-hipError_t launch_score_select(const Geom& g, const ScoreArgs& a, hipStream_t s);
+hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s);
+int select_max_bpc();
+int decode_max_items();
+int decode_max_cb();
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 
 // ------------------------------------------------------------------ device helpers

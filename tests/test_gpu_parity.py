@@ -195,3 +195,34 @@ def test_append_matches_build_bitwise():
             okm, odv, ovm = oracle.block_stats(c.K_bits[b, h], c.V_bits[b, h], n0 + 40, 16, w.n_var_groups)
             assert rel_err(c.summ.kmean[b, h, :X].cpu().numpy(), okm, axis=1) <= TOL
             assert rel_err(c.summ.dvar[b, h, :X].cpu().numpy(), odv) <= TOL
+
+
+def test_graph_replays_match_eager():
+    """The library enqueues no memsets and leaves its arrival counters at zero after each call, so a
+    captured HIP graph of score_select + sparse_decode reproduces the eager outputs on every replay."""
+    c = Case(LLAMA.with_(batch=1, context=8192, seed=24))
+    c.run_all()
+    ref = [x.clone() for x in (c.sel, c.n_sel, c.blk_logit, c.out, c.lse)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        c.score_select()
+        c.sparse_decode()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    sel, n_sel, blk, out, lse = c.sel, c.n_sel, c.blk_logit, c.out, c.lse
+    import paper_2609_26300_amd as P
+    params = P.CompkvSelectParams(c.budget, c.n_sink, c.n_recent, c.scale)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        P.compkv_score_select(c.dims, params, c.q, c.summ.kmean, c.summ.dvar, c.sl, sel, n_sel, blk, None, c.ws)
+        P.compkv_sparse_decode(c.dims, c.scale, c.q, c.K, c.V, c.summ.vmean, blk, c.sl, sel, n_sel, out, lse, c.ws)
+    for rep in range(4):
+        for t in (sel, n_sel, blk, out, lse):
+            t.fill_(-3)
+        g.replay()
+        torch.cuda.synchronize()
+        for x, y in zip((sel, n_sel, blk, out, lse), ref):
+            assert torch.equal(x, y), f"replay {rep} differs"
+        c.dense_decode()  # unrelated eager work on the same workspace between replays
+        torch.cuda.synchronize()
