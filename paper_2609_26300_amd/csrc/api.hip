@@ -92,8 +92,8 @@ DenseShape dense_shape(const Geom& g) {
 size_t score_ws(const Geom& g) {
     const ScoreShape sh = score_shape(g);
     const size_t units = g.units(), xmax = g.xmax();
-    return align_up(units * sh.nchunks * g.G * 2 * sizeof(float)) +
-           2 * align_up(units * g.G * xmax * sizeof(float)) + align_up(units * xmax * sizeof(uint32_t));
+    return align_up(units * sh.nchunks * g.G * 2 * sizeof(float)) + align_up(units * xmax * g.G * sizeof(float)) +
+           align_up(units * xmax * sizeof(uint32_t));
 }
 
 size_t sparse_ws(const Geom& g, int K) {
@@ -203,10 +203,8 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     char* p = base;
     a.ws_part = reinterpret_cast<float*>(p);
     p += align_up(units * sh.nchunks * g.G * 2 * sizeof(float));
-    a.ws_a = reinterpret_cast<float*>(p);
-    p += align_up(units * g.G * xmax * sizeof(float));
-    a.ws_v = reinterpret_cast<float*>(p);
-    p += align_up(units * g.G * xmax * sizeof(float));
+    a.ws_w = reinterpret_cast<float*>(p);
+    p += align_up(units * xmax * g.G * sizeof(float));
     a.ws_key = reinterpret_cast<uint32_t*>(p);
     a.q = static_cast<const uint16_t*>(q);
     a.kmean = kmean;
@@ -240,7 +238,7 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
     const SparseShape sh = sparse_shape(g, sel_stride);
-    if (sh.cb > compkv::decode_max_cb()) return COMPKV_EUNSUPPORTED;
+    if (sh.cb > compkv::decode_max_cb() || sh.eb > compkv::decode_max_eb()) return COMPKV_EUNSUPPORTED;
     char* base = static_cast<char*>(workspace);
     compkv::DecodeArgs a{};
     a.ws_part = reinterpret_cast<float*>(base);

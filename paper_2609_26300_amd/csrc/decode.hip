@@ -19,9 +19,10 @@
 // P split into three bf16 terms (three MFMAs), which keeps P within 2^-27 of its fp32 value; products
 // with the bf16 values are exact and accumulate in fp32. The softmax max is taken per pair of tiles.
 //
-// Compensation items are plain fp32 streaming on the vector ALUs: pass 1 forms the pseudo-logits of
-// the item's unselected blocks and their per-head max, pass 2 streams the mean-value rows (d/4 lanes x
-// float4 per row) with all loads of a lane issued before use.
+// Compensation items are plain fp32 streaming on the vector ALUs: the mean-value rows (d/4 lanes x
+// float4 per row, 16 rows per thread in flight) are requested first; meanwhile the item marks its
+// selected blocks, forms the pseudo-logits of the others and their per-head max; then the weighted
+// rows are summed.
 #include "internal.h"
 
 namespace compkv {
@@ -33,6 +34,7 @@ typedef float v4f32 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxItems = 256;  // partials per unit, upper bound (checked by the host)
 constexpr int kCbMax = 512;     // blocks per compensation item, upper bound
+constexpr int kMaxEb = 128;     // selected blocks per exact item, upper bound
 constexpr int kTilesPerRound = 2;  // P.V pairs two 16-token tiles into one 32-deep MFMA
 
 template <int D, int G>
@@ -42,6 +44,7 @@ struct DecodeShared {
     float w[G][kCbMax];  // compensation weights
     float M[G], L[G];
     unsigned char flag[kCbMax];
+    int sel[kMaxEb];  // the exact item's selected ids
 };
 
 __device__ __forceinline__ short f32_to_bf16_rne(float f) {
@@ -99,27 +102,35 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
         uint4 vreg[kTilesPerRound][4];
         bool vvalid[kTilesPerRound][4];
         // issue every load of the round first
+        // (branch-free: a row past the item's tokens loads row 0 of the unit and is zeroed after)
+        bool kvalid[kTilesPerRound];
 #pragma unroll
         for (int t = 0; t < kTilesPerRound; ++t) {
             const int base = (t0 + t) * 16;
             const int rk = (t0 + t < ntiles) ? tm.row(base + col) : -1;
+            kvalid[t] = rk >= 0;
+            const uint16_t* kp = Ku + (size_t)(rk >= 0 ? rk : 0) * D + 8 * grp;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                kreg[t][ks] = rk >= 0 ? *reinterpret_cast<const uint4*>(Ku + (size_t)rk * D + 32 * ks + 8 * grp)
-                                      : make_uint4(0, 0, 0, 0);
+            for (int ks = 0; ks < KS; ++ks) kreg[t][ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int rv = (t0 + t < ntiles) ? tm.row(base + 4 * grp + e) : -1;
                 vvalid[t][e] = rv >= 0;
+                const uint16_t* vp = Vu + (size_t)(rv >= 0 ? rv : 0) * D + CPL * col;
                 if constexpr (CPL == 8) {
-                    vreg[t][e] = rv >= 0 ? *reinterpret_cast<const uint4*>(Vu + (size_t)rv * D + CPL * col)
-                                         : make_uint4(0, 0, 0, 0);
+                    vreg[t][e] = *reinterpret_cast<const uint4*>(vp);
                 } else {
-                    const uint2 h = rv >= 0 ? *reinterpret_cast<const uint2*>(Vu + (size_t)rv * D + CPL * col)
-                                            : make_uint2(0, 0);
-                    vreg[t][e] = make_uint4(h.x, h.y, 0, 0);
+                    const uint2 hv = *reinterpret_cast<const uint2*>(vp);
+                    vreg[t][e] = make_uint4(hv.x, hv.y, 0, 0);
                 }
             }
+        }
+#pragma unroll
+        for (int t = 0; t < kTilesPerRound; ++t) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) kreg[t][ks] = kvalid[t] ? kreg[t][ks] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) vreg[t][e] = vvalid[t][e] ? vreg[t][e] : make_uint4(0, 0, 0, 0);
         }
         // logits: lane holds head `col`, tokens 4*grp + i of each tile
         float z[kTilesPerRound][4];
@@ -242,9 +253,19 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
                              DecodeShared<D, G>& sh, float* part) {
     constexpr int LPB = D / 4;          // lanes per mean-value row (one float4 each)
     constexpr int RPS = kThreads / LPB;  // rows per workgroup step
-    constexpr int UNR = 8;
+    constexpr int ROWS = 16;             // rows in flight per thread
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int nb = max(0, c1 - c0);
+    const int li = tid % LPB, slot = tid / LPB;
+    // issue this thread's first ROWS mean-value rows before anything else (rows of selected blocks
+    // are fetched too and then weighted by zero)
+    const float4* vm = reinterpret_cast<const float4*>(a.vmean + ((size_t)u * geo.xcap + c0) * D) + li;
+    float4 v[ROWS];
+#pragma unroll
+    for (int k = 0; k < ROWS; ++k) {  // branch-free: a slot past the item reloads row 0, weighted by zero
+        const int lb = slot + k * RPS;
+        v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
+    }
     const int nsel = min(a.n_sel[u], a.sel_stride);
     const int32_t* selu = a.sel + (size_t)u * a.sel_stride;
     for (int i = tid; i < nb; i += kThreads) sh.flag[i] = 0;
@@ -254,7 +275,7 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
         if (sb >= c0 && sb < c1) sh.flag[sb - c0] = 1;
     }
     __syncthreads();
-    // pass 1: pseudo-logits log|b| + zbar and their per-head max
+    // pseudo-logits log|b| + zbar and their per-head max
     const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
     for (int idx = tid; idx < G * nb; idx += kThreads) {
         const int g = idx / nb, lb = idx % nb, b = c0 + lb;
@@ -279,21 +300,20 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
         }
     }
     __syncthreads();
-    // pass 2: weighted mean values; lane li of a row slot holds coordinates 4li..4li+3
-    const int li = tid % LPB, slot = tid / LPB;
+    // weighted mean values; lane li of a row slot holds coordinates 4li..4li+3
     float acc[G][4];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
-    const float4* vm = reinterpret_cast<const float4*>(a.vmean + ((size_t)u * geo.xcap + c0) * D) + li;
-    for (int lb0 = slot; lb0 < nb; lb0 += RPS * UNR) {
-        float4 v[UNR];
+    for (int lb0 = slot; lb0 < nb; lb0 += RPS * ROWS) {
+        if (lb0 != slot) {
 #pragma unroll
-        for (int k = 0; k < UNR; ++k) {
-            const int lb = lb0 + k * RPS;
-            v[k] = (lb < nb && !sh.flag[lb]) ? vm[(size_t)lb * (D / 4)] : make_float4(0, 0, 0, 0);
+            for (int k = 0; k < ROWS; ++k) {
+                const int lb = lb0 + k * RPS;
+                v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
+            }
         }
 #pragma unroll
-        for (int k = 0; k < UNR; ++k) {
+        for (int k = 0; k < ROWS; ++k) {
             const int lb = lb0 + k * RPS;
             if (lb >= nb) break;
 #pragma unroll
@@ -332,10 +352,10 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, DecodeArgs a) {
+__global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, DecodeArgs a, int nitems) {
     __shared__ DecodeShared<D, G> sh;
     const int tid = threadIdx.x;
-    const int u = blockIdx.y, item = blockIdx.x, nitems = gridDim.x;
+    const int u = blockIdx.y, item = blockIdx.x;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
@@ -355,8 +375,11 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
         } else {
             const int nsel = min(a.n_sel[u], a.sel_stride);
             const int e0 = item * a.eb;
-            tm.sel = a.sel + (size_t)u * a.sel_stride + e0;
             tm.nblk = max(0, min(a.eb, nsel - e0));
+            const int32_t* selu = a.sel + (size_t)u * a.sel_stride + e0;
+            for (int k = tid; k < tm.nblk; k += kThreads) sh.sel[k] = selu[k];
+            __syncthreads();
+            tm.sel = sh.sel;
             tm.t0 = tm.t1 = 0;
         }
         float m, l;
@@ -368,7 +391,6 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
         const int c0 = (item - a.n_exact) * a.cb;
         compensation<D, G>(a, geo, u, n, X, c0, min(c0 + a.cb, X), sh, part);
     }
-
 }
 
 // Merge of one (unit, query head): the item partials in item order, with every load issued well ahead.
@@ -411,15 +433,19 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, Decode
     const int i = tid % D, sub = tid / D;
     const float* pi = pu + 2 + i;
     float A = 0.0f;
-    int it = sub;
-    for (; it + (UNR - 1) * S < nitems; it += UNR * S) {
+    for (int it0 = sub; it0 < nitems; it0 += UNR * S) {
         float x[UNR];
 #pragma unroll
-        for (int k = 0; k < UNR; ++k) x[k] = pi[(size_t)(it + k * S) * stride];
+        for (int k = 0; k < UNR; ++k) {  // all loads of the batch first (branch-free), masked at the end
+            const int it = it0 + k * S;
+            x[k] = pi[(size_t)(it < nitems ? it : 0) * stride];
+        }
 #pragma unroll
-        for (int k = 0; k < UNR; ++k) A += pc[it + k * S] * x[k];
+        for (int k = 0; k < UNR; ++k) {
+            const int it = it0 + k * S;
+            if (it < nitems) A += pc[it] * x[k];
+        }
     }
-    for (; it < nitems; it += S) A += pc[it] * pi[(size_t)it * stride];
     part_acc[sub][i] = A;
     __syncthreads();
     if (sub == 0) {
@@ -435,10 +461,11 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, Decode
 
 template <int D, int G>
 hipError_t launch_pair(const Geom& g, const DecodeArgs& a, hipStream_t s, dim3 grid) {
-    decode_items_kernel<D, G><<<grid, kThreads, 0, s>>>(g, a);
+    const int items = (int)grid.x;
+    decode_items_kernel<D, G><<<grid, kThreads, 0, s>>>(g, a, items);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    decode_merge_kernel<D, G><<<dim3(g.units(), G), kThreads, 0, s>>>(g, a, (int)grid.x);
+    decode_merge_kernel<D, G><<<dim3(g.units(), G), kThreads, 0, s>>>(g, a, items);
     return hipGetLastError();
 }
 
@@ -457,10 +484,11 @@ hipError_t dispatch_g(const Geom& g, const DecodeArgs& a, hipStream_t s, dim3 gr
 
 int decode_max_items() { return kMaxItems; }
 int decode_max_cb() { return kCbMax; }
+int decode_max_eb() { return kMaxEb; }
 
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s) {
     const int items = a.dense ? a.n_exact : a.n_exact + a.n_comp;
-    if (items < 1 || items > kMaxItems || (!a.dense && a.cb > kCbMax)) return hipErrorInvalidValue;
+    if (items < 1 || items > kMaxItems || (!a.dense && (a.cb > kCbMax || a.eb > kMaxEb))) return hipErrorInvalidValue;
     dim3 grid(items, g.units());
     return g.D == 128 ? dispatch_g<128>(g, a, s, grid) : dispatch_g<64>(g, a, s, grid);
 }

@@ -41,10 +41,9 @@ struct ScoreArgs {
     int32_t* n_sel;
     float* blk_logit;
     float* scores;     // nullable
-    float* ws_part;    // [units][nchunks][G][2]  (chunk max, chunk sum of exp)
-    float* ws_a;       // [units][G][xmax]       log block weight estimate
-    float* ws_v;       // [units][G][xmax]       projected variance
-    uint32_t* ws_key;  // [units][xmax]          score bits
+    float* ws_part;    // [units][nchunks][G][2]  (chunk max m_c, chunk sum of exp(a - m_c))
+    float* ws_w;       // [units][xmax][G]       exp(a - m_c) * projected variance
+    uint32_t* ws_key;  // [units][xmax]          score bits (when they do not fit in LDS)
     int bpc;          // blocks per chunk (multiple of 32)
     int nchunks;      // grid.x
     int keys_in_lds;  // set by the launcher: score bits kept in LDS (else in ws_key)
@@ -81,6 +80,7 @@ hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s);
 int select_max_bpc();
 int decode_max_items();
 int decode_max_cb();
+int decode_max_eb();
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 
 // ------------------------------------------------------------------ device helpers

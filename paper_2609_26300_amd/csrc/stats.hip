@@ -3,9 +3,11 @@
 // One wave64 computes one block's summary. A key row of d bf16 is read as d/8 lanes x 16 bytes, so a
 // wave covers 64/(d/8) rows per load (4 rows for d = 128) and the loads of consecutive lanes are
 // contiguous. Each lane accumulates its 8 coordinates over the rows it visits; the row groups are then
-// combined with cross-lane adds. Two passes (mean, then squared deviations) keep the variance
-// numerically stable; the second pass re-reads the block from L1/L2. Per-coordinate sums of squared
-// deviations go through LDS to form the r group averages.
+// combined with cross-lane adds. Rows are loaded in batches of 8 load steps (32 rows for d = 128), all
+// loads of a batch issued before use. Two passes (mean, then squared deviations) keep the variance
+// numerically stable; a block that fits in one batch is still in registers for the second pass, a
+// larger one is re-read from L1/L2. Per-coordinate sums of squared deviations go through LDS to form
+// the r group averages.
 //
 // build and append share wave_block_stats with the same lane-to-row mapping, so an appended block's
 // summary is bit-identical to the prefill one.
@@ -38,21 +40,34 @@ __device__ void wave_block_stats(const uint16_t* __restrict__ Kb, const uint16_t
                                  bool active) {
     constexpr int LPR = D / 8;     // lanes per row
     constexpr int RPS = 64 / LPR;  // rows per load step
+    constexpr int NS = 8;          // load steps held in registers (32 rows for d = 128)
+    constexpr int BATCH = NS * RPS;
     const int lane = threadIdx.x & 63;
     const int ro = lane / LPR, li = lane % LPR;
+    auto krow = [&](int j) { return (j == new_j) ? k_new : Kb + (size_t)j * D; };
+    auto vrow = [&](int j) { return (j == new_j) ? v_new : Vb + (size_t)j * D; };
     float mk[8], mv[8], m2[8];
     if (active) {
         float sk[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int j = ro; j < nb; j += RPS) {
-            const uint16_t* kp = (j == new_j) ? k_new : Kb + (size_t)j * D;
-            const uint16_t* vp = (j == new_j) ? v_new : Vb + (size_t)j * D;
-            float kf[8], vf[8];
-            unpack_bf16x8(*reinterpret_cast<const uint4*>(kp + li * 8), kf);
-            unpack_bf16x8(*reinterpret_cast<const uint4*>(vp + li * 8), vf);
+        uint4 kw[NS];
+        for (int j0 = 0; j0 < nb; j0 += BATCH) {
+            uint4 vw[NS];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                sk[e] += kf[e];
-                sv[e] += vf[e];
+            for (int st = 0; st < NS; ++st) {  // every load of the batch before any use
+                const int j = j0 + st * RPS + ro;
+                kw[st] = j < nb ? *reinterpret_cast<const uint4*>(krow(j) + li * 8) : make_uint4(0, 0, 0, 0);
+                vw[st] = j < nb ? *reinterpret_cast<const uint4*>(vrow(j) + li * 8) : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int st = 0; st < NS; ++st) {
+                float kf[8], vf[8];
+                unpack_bf16x8(kw[st], kf);
+                unpack_bf16x8(vw[st], vf);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    sk[e] += kf[e];
+                    sv[e] += vf[e];
+                }
             }
         }
 #pragma unroll
@@ -69,14 +84,25 @@ __device__ void wave_block_stats(const uint16_t* __restrict__ Kb, const uint16_t
             mv[e] = sv[e] / fn;
             m2[e] = 0.0f;
         }
-        for (int j = ro; j < nb; j += RPS) {
-            const uint16_t* kp = (j == new_j) ? k_new : Kb + (size_t)j * D;
-            float kf[8];
-            unpack_bf16x8(*reinterpret_cast<const uint4*>(kp + li * 8), kf);
+        // squared deviations; a block of one batch is still in registers
+        for (int j0 = 0; j0 < nb; j0 += BATCH) {
+            if (nb > BATCH) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float dev = kf[e] - mk[e];
-                m2[e] += dev * dev;
+                for (int st = 0; st < NS; ++st) {
+                    const int j = j0 + st * RPS + ro;
+                    kw[st] = j < nb ? *reinterpret_cast<const uint4*>(krow(j) + li * 8) : make_uint4(0, 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int st = 0; st < NS; ++st) {
+                if (j0 + st * RPS + ro >= nb) continue;
+                float kf[8];
+                unpack_bf16x8(kw[st], kf);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float dev = kf[e] - mk[e];
+                    m2[e] += dev * dev;
+                }
             }
         }
 #pragma unroll
@@ -102,13 +128,16 @@ __device__ void wave_block_stats(const uint16_t* __restrict__ Kb, const uint16_t
     __syncthreads();
 }
 
-// grid = (ceil(xmax / 4), units); wave w of workgroup x summarizes block 4x + w.
+// Grid-stride over (unit, group of four blocks) with a capped grid; wave w of a group summarizes its
+// block w.
 template <int D>
 __global__ __launch_bounds__(kThreads) void build_stats_kernel(Geom g, StatsArgs a) {
     __shared__ float m2s[4][D];
-    const int u = blockIdx.y;
     const int wave = threadIdx.x >> 6;
-    const int b = blockIdx.x * 4 + wave;
+    const int quads = (g.xmax() + 3) / 4;
+    for (int flat = blockIdx.x; flat < quads * g.units(); flat += gridDim.x) {
+    const int u = flat / quads;
+    const int b = (flat % quads) * 4 + wave;
     const int n = clamp_len(a.seq_lens[u / g.hkv], g.max_seq);
     const int X = (n + g.B - 1) / g.B;
     const bool active = b < X;
@@ -117,6 +146,7 @@ __global__ __launch_bounds__(kThreads) void build_stats_kernel(Geom g, StatsArgs
     const size_t blk = (size_t)u * g.xcap + b;
     wave_block_stats<D>(a.K + row0 * D, a.V + row0 * D, nb, nullptr, nullptr, -1, g.r, g.layout,
                         a.kmean + blk * D, a.dvar + blk * g.r, a.vmean + blk * D, m2s[wave], active);
+    }
 }
 
 // grid = (ceil(units / 4)); wave w of workgroup x appends to unit 4x + w.
@@ -154,7 +184,8 @@ __global__ __launch_bounds__(kThreads) void append_stats_kernel(Geom g, StatsArg
 }  // namespace
 
 hipError_t launch_build_stats(const Geom& g, const StatsArgs& a, hipStream_t s) {
-    dim3 grid((g.xmax() + 3) / 4, g.units());
+    const int total = (g.xmax() + 3) / 4 * g.units();
+    dim3 grid(total < 2048 ? total : 2048);
     if (g.D == 128)
         build_stats_kernel<128><<<grid, kThreads, 0, s>>>(g, a);
     else

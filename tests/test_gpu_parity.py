@@ -35,6 +35,11 @@ CASES = {
     "wide_gqa_8k": lambda: Case(WORKLOADS["wide_gqa_64k"].with_(batch=2, context=8192, seed=18)),
     "long_16k_lognormal": lambda: Case(WORKLOADS["long_128k"].with_(batch=1, context=16384, budget_blocks=32,
                                                                     seed=19)),
+    # selection paths: > 8192 blocks (keys outside registers), ~1000 candidates ranked by brute force,
+    # and ~2000 candidates (radix select fallback)
+    "block1_9000": lambda: Case(TINY.with_(context=9000, block_size=1, budget_blocks=40, seed=25)),
+    "budget300_x1000": lambda: Case(TINY.with_(context=16000, budget_blocks=300, seed=26)),
+    "budget300_x2000": lambda: Case(TINY.with_(context=32000, budget_blocks=300, seed=27)),
 }
 _cache = {}
 
