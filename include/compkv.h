@@ -29,8 +29,9 @@
  *      out               fp32 [batch][n_q_heads][d]; lse fp32 [batch][n_q_heads] (natural log)
  *  - bf16 values are passed as their 16-bit patterns. Inputs must be finite.
  *  - workspace: device scratch of at least compkv_workspace_bytes(...) bytes, 256-byte aligned, with
- *    no initial contents required. Each call that takes one enqueues two kernels: the second reads
- *    what the first wrote there. Calls that may run concurrently need distinct workspaces.
+ *    no initial contents required. Each call that takes one enqueues two kernels (compkv_decode_step:
+ *    four), each reading what the previous one wrote there. Calls that may run concurrently need
+ *    distinct workspaces.
  *  - Return value: COMPKV_OK (0) or a negative status; compkv_status_string() names it. On error
  *    nothing has been enqueued, except for COMPKV_EHIP (a launch failed).
  *
@@ -85,6 +86,7 @@ typedef struct compkv_select_params {
 #define COMPKV_WS_SCORE_SELECT 1
 #define COMPKV_WS_SPARSE_DECODE 2
 #define COMPKV_WS_DENSE_DECODE 3
+#define COMPKV_WS_DECODE_STEP 4
 
 /*
  * Block summaries of the first seq_lens[b] tokens of every unit (prefill). Section 4.1, Eq.
@@ -116,7 +118,8 @@ int compkv_append_stats(const compkv_dims* dims, void* k_cache, void* v_cache, c
  * counted once). Ties rank the lower block id first; sel lists the ids in ascending order and
  * n_sel[u] = min(K, X); slots past n_sel are set to -1. If K >= X every block is selected.
  * blk_logit receives zbar (needed by compkv_sparse_decode); scores (nullable) receives S_b for every
- * block. q is bf16 [batch][n_q_heads][d]. Returns COMPKV_EBUDGET if K < n_sink + n_recent.
+ * block. q is bf16 [batch][n_q_heads][d]. Returns COMPKV_EBUDGET if K < n_sink + n_recent and
+ * COMPKV_EUNSUPPORTED above 4096 * 128 / G blocks per unit (ceil(max_seq_len / block_size)).
  */
 int compkv_score_select(const compkv_dims* dims, const compkv_select_params* params, const void* q,
                         const float* kmean, const float* dvar, const int32_t* seq_lens, int32_t* sel,
@@ -145,6 +148,29 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
 int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
                         const void* v_cache, const int32_t* seq_lens, float* out, float* lse,
                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * One whole decode step of one layer (Section 4.2 and Appendix E.1 in a single call): optional
+ * streaming append, scoring, selection and compensated sparse decode, with the results of the
+ * separate calls:
+ *  - seq_lens holds the lengths AFTER the new token (n = seq_lens[b] >= 1 per sequence). If k_new and
+ *    v_new are given (bf16 [batch][n_kv_heads][d], both or neither), row n - 1 of every unit is
+ *    stored from them and the summary of its block (n - 1) / B is refreshed, bit-identical to
+ *    compkv_append_stats with length n - 1. Units with n == 0 append nothing.
+ *  - sel, n_sel, blk_logit and scores (nullable) are bit-identical to compkv_score_select on the
+ *    refreshed summaries (sel has row stride params->budget_blocks).
+ *  - out and lse (nullable) follow Eq. compkv-output as in compkv_sparse_decode (same tolerance, not
+ *    bitwise: the pseudo-token sum is formed over all blocks while the summaries are streamed, and
+ *    the selected blocks' pseudo-terms are then subtracted).
+ * Enqueues four kernels. Workspace: compkv_workspace_bytes(dims, budget, COMPKV_WS_DECODE_STEP).
+ * Returns COMPKV_EUNSUPPORTED for shapes whose partial count exceeds the merge limit (then use the
+ * separate calls), otherwise the statuses of compkv_score_select.
+ */
+int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* params, const void* q,
+                       void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                       const int32_t* seq_lens, float* kmean, float* dvar, float* vmean, int32_t* sel,
+                       int32_t* n_sel, float* blk_logit, float* scores, float* out, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes needed by `which` (COMPKV_WS_*; COMPKV_WS_ALL = enough for every call) for these
  * dims and budget. Returns 0 if dims are invalid. */

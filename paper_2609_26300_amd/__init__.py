@@ -10,6 +10,7 @@ from .binding import (  # noqa: F401
     COMPKV_GROUPS_INTERLEAVED,
     COMPKV_GROUPS_ROTATE_HALF,
     COMPKV_WS_ALL,
+    COMPKV_WS_DECODE_STEP,
     COMPKV_WS_DENSE_DECODE,
     COMPKV_WS_SCORE_SELECT,
     COMPKV_WS_SPARSE_DECODE,
@@ -21,6 +22,7 @@ from .binding import (  # noqa: F401
     alloc_workspace,
     compkv_append_stats,
     compkv_build_stats,
+    compkv_decode_step,
     compkv_dense_decode,
     compkv_score_select,
     compkv_sparse_decode,

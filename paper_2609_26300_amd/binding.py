@@ -19,6 +19,7 @@ COMPKV_WS_ALL = 0
 COMPKV_WS_SCORE_SELECT = 1
 COMPKV_WS_SPARSE_DECODE = 2
 COMPKV_WS_DENSE_DECODE = 3
+COMPKV_WS_DECODE_STEP = 4
 
 
 class CompkvError(RuntimeError):
@@ -72,13 +73,15 @@ def library():
                                            _i32, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.compkv_dense_decode.argtypes = [dp, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                           ctypes.c_size_t, _vp]
+        L.compkv_decode_step.argtypes = [dp, ctypes.POINTER(CompkvSelectParams), _vp, _vp, _vp, _vp, _vp, _vp,
+                                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.compkv_workspace_bytes.argtypes = [dp, _i32, _i32]
         L.compkv_workspace_bytes.restype = ctypes.c_size_t
         L.compkv_status_string.argtypes = [ctypes.c_int]
         L.compkv_status_string.restype = ctypes.c_char_p
         L.compkv_version.argtypes = []
         for name in ("compkv_build_stats", "compkv_append_stats", "compkv_score_select",
-                     "compkv_sparse_decode", "compkv_dense_decode", "compkv_version"):
+                     "compkv_sparse_decode", "compkv_dense_decode", "compkv_decode_step", "compkv_version"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -233,6 +236,28 @@ def compkv_dense_decode(dims, scale, q, k_cache, v_cache, seq_lens, out, lse=Non
         _ptr(out, f32, qs, "out"), _ptr(lse, f32, qs[:2], "lse", nullable=True), ws, ws_bytes,
         _stream(stream))
     _check(st, "compkv_dense_decode")
+
+
+def compkv_decode_step(dims, params: CompkvSelectParams, q, k_cache, v_cache, k_new, v_new, seq_lens, kmean,
+                       dvar, vmean, sel, n_sel, blk_logit, scores, out, lse=None, workspace=None, stream=None):
+    """One fused decode step; seq_lens are the lengths after the new token (k_new/v_new may be None)."""
+    cache, summ, dv, qs = _shapes(dims)
+    bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+    units = (dims.batch, dims.n_kv_heads)
+    new = (*units, dims.head_dim)
+    if (k_new is None) != (v_new is None):
+        raise CompkvError("k_new and v_new must be given together")
+    ws, ws_bytes = _ws(workspace)
+    st = library().compkv_decode_step(
+        ctypes.byref(dims), ctypes.byref(params), _ptr(q, bf, qs, "q"), _ptr(k_cache, bf, cache, "k_cache"),
+        _ptr(v_cache, bf, cache, "v_cache"), _ptr(k_new, bf, new, "k_new", nullable=True),
+        _ptr(v_new, bf, new, "v_new", nullable=True), _ptr(seq_lens, i32, (dims.batch,), "seq_lens"),
+        _ptr(kmean, f32, summ, "kmean"), _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"),
+        _ptr(sel, i32, (*units, params.budget_blocks), "sel"), _ptr(n_sel, i32, units, "n_sel"),
+        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
+        _ptr(scores, f32, (*units, dims.xcap), "scores", nullable=True), _ptr(out, f32, qs, "out"),
+        _ptr(lse, f32, qs[:2], "lse", nullable=True), ws, ws_bytes, _stream(stream))
+    _check(st, "compkv_decode_step")
 
 
 def default_scale(head_dim: int) -> float:

@@ -106,8 +106,18 @@ size_t dense_ws(const Geom& g) {
     return align_up((size_t)g.units() * sh.items * g.G * (g.D + 2) * sizeof(float));
 }
 
+// fused step: the score region, then [units][nchunks + 2 n_exact][G][D + 2] decode partials
+int step_partials(const Geom& g, int K) {
+    return score_shape(g).nchunks + 2 * sparse_shape(g, K).n_exact;
+}
+
+size_t step_ws(const Geom& g, int K) {
+    return score_ws(g) + align_up((size_t)g.units() * step_partials(g, K) * g.G * (g.D + 2) * sizeof(float));
+}
+
 size_t ws_bytes(const Geom& g, int K, int which) {
     size_t body = 0;
+    if (which == COMPKV_WS_ALL || which == COMPKV_WS_DECODE_STEP) body = std::max(body, step_ws(g, K));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SCORE_SELECT) body = std::max(body, score_ws(g));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SPARSE_DECODE) body = std::max(body, sparse_ws(g, K));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_DENSE_DECODE) body = std::max(body, dense_ws(g));
@@ -121,6 +131,36 @@ int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
 }
 
 int launch_status(hipError_t e) { return e == hipSuccess ? COMPKV_OK : COMPKV_EHIP; }
+
+// Scoring arguments with the score region at the start of the workspace.
+compkv::ScoreArgs score_args(const Geom& g, const compkv_select_params* params, const void* q, const float* kmean,
+                             const float* dvar, const int32_t* seq_lens, int32_t* sel, int32_t* n_sel,
+                             float* blk_logit, float* scores, void* workspace) {
+    const ScoreShape sh = score_shape(g);
+    const size_t units = g.units(), xmax = g.xmax();
+    compkv::ScoreArgs a{};
+    char* p = static_cast<char*>(workspace);
+    a.ws_part = reinterpret_cast<float*>(p);
+    p += align_up(units * sh.nchunks * g.G * 2 * sizeof(float));
+    a.ws_w = reinterpret_cast<float*>(p);
+    p += align_up(units * xmax * g.G * sizeof(float));
+    a.ws_key = reinterpret_cast<uint32_t*>(p);
+    a.q = static_cast<const uint16_t*>(q);
+    a.kmean = kmean;
+    a.dvar = dvar;
+    a.seq_lens = seq_lens;
+    a.sel = sel;
+    a.n_sel = n_sel;
+    a.blk_logit = blk_logit;
+    a.scores = scores;
+    a.bpc = sh.bpc;
+    a.nchunks = sh.nchunks;
+    a.K = params->budget_blocks;
+    a.n_sink = params->n_sink;
+    a.n_recent = params->n_recent;
+    a.scale = params->scale;
+    return a;
+}
 
 }  // namespace
 
@@ -142,7 +182,7 @@ const char* compkv_status_string(int status) {
 
 size_t compkv_workspace_bytes(const compkv_dims* dims, int32_t budget_blocks, int32_t which) {
     Geom g;
-    if (check_dims(dims, &g) != COMPKV_OK || budget_blocks < 1 || which < 0 || which > 3) return 0;
+    if (check_dims(dims, &g) != COMPKV_OK || budget_blocks < 1 || which < 0 || which > 4) return 0;
     return ws_bytes(g, budget_blocks, which);
 }
 
@@ -193,33 +233,11 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel || !blk_logit) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
+    if (score_shape(g).nchunks * g.G > compkv::select_max_chunk_heads()) return COMPKV_EUNSUPPORTED;
     const size_t need = ws_bytes(g, params->budget_blocks, COMPKV_WS_SCORE_SELECT);
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
-    const ScoreShape sh = score_shape(g);
-    const size_t units = g.units(), xmax = g.xmax();
-    char* base = static_cast<char*>(workspace);
-    compkv::ScoreArgs a{};
-    char* p = base;
-    a.ws_part = reinterpret_cast<float*>(p);
-    p += align_up(units * sh.nchunks * g.G * 2 * sizeof(float));
-    a.ws_w = reinterpret_cast<float*>(p);
-    p += align_up(units * xmax * g.G * sizeof(float));
-    a.ws_key = reinterpret_cast<uint32_t*>(p);
-    a.q = static_cast<const uint16_t*>(q);
-    a.kmean = kmean;
-    a.dvar = dvar;
-    a.seq_lens = seq_lens;
-    a.sel = sel;
-    a.n_sel = n_sel;
-    a.blk_logit = blk_logit;
-    a.scores = scores;
-    a.bpc = sh.bpc;
-    a.nchunks = sh.nchunks;
-    a.K = params->budget_blocks;
-    a.n_sink = params->n_sink;
-    a.n_recent = params->n_recent;
-    a.scale = params->scale;
+    compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, workspace);
     return launch_status(compkv::launch_score_select(g, a, static_cast<hipStream_t>(stream)));
 }
 
@@ -287,6 +305,71 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
     a.dense = 1;
     a.scale = scale;
     return launch_status(compkv::launch_decode(g, a, static_cast<hipStream_t>(stream)));
+}
+
+int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* params, const void* q, void* k_cache,
+                       void* v_cache, const void* k_new, const void* v_new, const int32_t* seq_lens, float* kmean,
+                       float* dvar, float* vmean, int32_t* sel, int32_t* n_sel, float* blk_logit, float* scores,
+                       float* out, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!params || !q || !k_cache || !v_cache || !seq_lens || !kmean || !dvar || !vmean || !sel || !n_sel ||
+        !blk_logit || !out)
+        return COMPKV_EINVAL;
+    if ((k_new == nullptr) != (v_new == nullptr)) return COMPKV_EINVAL;
+    if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
+    if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
+    const int K = params->budget_blocks;
+    const SparseShape sp = sparse_shape(g, K);
+    const ScoreShape sc = score_shape(g);
+    const int parts = step_partials(g, K);
+    if (sp.eb > compkv::decode_max_eb() || sp.n_exact > compkv::decode_max_items() ||
+        parts > compkv::decode_max_partials() || sc.nchunks * g.G > compkv::select_max_chunk_heads())
+        return COMPKV_EUNSUPPORTED;
+    st = check_ws(g, workspace, workspace_bytes, ws_bytes(g, K, COMPKV_WS_DECODE_STEP));
+    if (st != COMPKV_OK) return st;
+    float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, workspace);
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
+    a.Kc = static_cast<uint16_t*>(k_cache);
+    a.Vc = static_cast<uint16_t*>(v_cache);
+    a.kmean_w = kmean;
+    a.dvar_w = dvar;
+    a.vmean = vmean;
+    a.comp_part = dpart;
+    a.part_count = parts;
+    hipError_t e = compkv::launch_score_select(g, a, s);
+    if (e != hipSuccess) return COMPKV_EHIP;
+
+    compkv::DecodeArgs d{};
+    d.ws_part = dpart;
+    d.q = static_cast<const uint16_t*>(q);
+    d.K = static_cast<const uint16_t*>(k_cache);
+    d.V = static_cast<const uint16_t*>(v_cache);
+    d.vmean = vmean;
+    d.blk_logit = blk_logit;
+    d.seq_lens = seq_lens;
+    d.sel = sel;
+    d.n_sel = n_sel;
+    d.out = out;
+    d.lse = lse;
+    d.sel_stride = K;
+    d.n_exact = sp.n_exact;
+    d.eb = sp.eb;
+    d.n_comp = 0;
+    d.cb = 0;
+    d.dense = 0;
+    d.scale = params->scale;
+    d.part_count = parts;
+    d.part_base = sc.nchunks;
+    d.neg_pseudo = 1;
+    e = compkv::launch_decode_items(g, d, sp.n_exact, s);
+    if (e != hipSuccess) return COMPKV_EHIP;
+    return launch_status(compkv::launch_decode_merge(g, d, sc.nchunks + sp.n_exact, sp.n_exact, s));
 }
 
 }  // extern "C"

@@ -32,7 +32,8 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf16 __attribute__((ext_vector_type(8)));
 typedef float v4f32 __attribute__((ext_vector_type(4)));
 
-constexpr int kMaxItems = 256;  // partials per unit, upper bound (checked by the host)
+constexpr int kMaxItems = 256;     // items per unit and launch, upper bound (checked by the host)
+constexpr int kMaxPartials = 2048;  // partials per unit in a merge, upper bound
 constexpr int kCbMax = 512;     // blocks per compensation item, upper bound
 constexpr int kMaxEb = 128;     // selected blocks per exact item, upper bound
 constexpr int kTilesPerRound = 2;  // P.V pairs two 16-token tiles into one 32-deep MFMA
@@ -351,6 +352,124 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
     }
 }
 
+// Pseudo-terms (logit log|b| + zbar_b, value vmean_b) of an exact item's selected blocks, written as
+// one partial that the merge subtracts: the fused step's chunks add the pseudo-terms of every block.
+// Their loads are issued before the exact tokens (PseudoPf) so their latency overlaps that work.
+constexpr int kPfRows = 2;    // mean-value rows per thread prefetched
+constexpr int kPfLogits = 2;  // block logits per thread prefetched
+static_assert(kPfLogits == 2, "selected_pseudo picks the prefetched logits by hand");
+
+struct PseudoPf {
+    float4 v[kPfRows];
+    float lg[kPfLogits];
+};
+
+template <int D, int G>
+__device__ __forceinline__ float4 pseudo_row(const DecodeArgs& a, const Geom& geo, int u, int X, int nblk,
+                                             const int* ids, int k) {
+    const int li = threadIdx.x % (D / 4);
+    const int b = k < nblk ? ids[k] : -1;
+    const bool ok = b >= 0 && b < X;  // invalid: row 0 of the unit, weighted by zero
+    return reinterpret_cast<const float4*>(a.vmean + ((size_t)u * geo.xcap + (ok ? b : 0)) * D)[li];
+}
+
+template <int G>
+__device__ __forceinline__ float pseudo_logit(const DecodeArgs& a, const Geom& geo, int u, int X, int nblk,
+                                              const int* ids, int idx) {
+    const int g = idx / nblk, k = idx - g * nblk;
+    const int b = idx < G * nblk ? ids[k] : -1;
+    const bool ok = b >= 0 && b < X;
+    return a.blk_logit[((size_t)u * G + (idx < G * nblk ? g : 0)) * geo.xcap + (ok ? b : 0)];
+}
+
+template <int D, int G>
+__device__ __forceinline__ void pseudo_prefetch(const DecodeArgs& a, const Geom& geo, int u, int X, int nblk,
+                                                const int* ids, PseudoPf& pf) {
+    constexpr int RPS = kThreads / (D / 4);
+    const int slot = threadIdx.x / (D / 4);
+#pragma unroll
+    for (int j = 0; j < kPfRows; ++j) pf.v[j] = pseudo_row<D, G>(a, geo, u, X, nblk, ids, slot + j * RPS);
+#pragma unroll
+    for (int j = 0; j < kPfLogits; ++j)
+        pf.lg[j] = nblk > 0 ? pseudo_logit<G>(a, geo, u, X, nblk, ids, threadIdx.x + j * kThreads) : 0.0f;
+}
+
+template <int D, int G>
+__device__ void selected_pseudo(const DecodeArgs& a, const Geom& geo, int u, int n, int X, int nblk,
+                                const PseudoPf& pf, DecodeShared<D, G>& sh, float* part) {
+    constexpr int LPB = D / 4, RPS = kThreads / LPB;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = tid % LPB, slot = tid / LPB;
+    for (int idx = tid, j = 0; idx < G * nblk; idx += kThreads, ++j) {
+        const int g = idx / nblk, k = idx % nblk, b = sh.sel[k];
+        const float lg = j < kPfLogits ? (j == 0 ? pf.lg[0] : pf.lg[1]) : pseudo_logit<G>(a, geo, u, X, nblk, sh.sel, idx);
+        sh.w[g][k] = (b >= 0 && b < X) ? logf((float)min(geo.B, n - b * geo.B)) + lg : -INFINITY;
+    }
+    __syncthreads();
+    for (int g = wave; g < G; g += 4) {
+        float mx = -INFINITY;
+        for (int k = lane; k < nblk; k += 64) mx = fmaxf(mx, sh.w[g][k]);
+        mx = wave_max(mx);
+        float sum = 0.0f;
+        for (int k = lane; k < nblk; k += 64) {
+            const float wv = (mx == -INFINITY || sh.w[g][k] == -INFINITY) ? 0.0f : __expf(sh.w[g][k] - mx);
+            sh.w[g][k] = wv;
+            sum += wv;
+        }
+        sum = wave_sum(sum);
+        if (lane == 0) {
+            sh.M[g] = mx;
+            sh.L[g] = sum;
+        }
+    }
+    __syncthreads();  // also: finish_exact's reads of sh.acc are done
+    float acc[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
+    auto add_row = [&](int k, const float4& v4) {
+        if (k >= nblk) return;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const float wv = sh.w[g][k];
+            acc[g][0] += wv * v4.x;
+            acc[g][1] += wv * v4.y;
+            acc[g][2] += wv * v4.z;
+            acc[g][3] += wv * v4.w;
+        }
+    };
+#pragma unroll
+    for (int j = 0; j < kPfRows; ++j) add_row(slot + j * RPS, pf.v[j]);
+    for (int k0 = slot + kPfRows * RPS; k0 < nblk; k0 += 4 * RPS) {  // larger items: 4 rows in flight
+        float4 v4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v4[j] = pseudo_row<D, G>(a, geo, u, X, nblk, sh.sel, k0 + j * RPS);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) add_row(k0 + j * RPS, v4[j]);
+    }
+#pragma unroll
+    for (int off = LPB; off < 64; off <<= 1)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
+    if (lane < LPB) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sh.acc[wave][g][4 * li + e] = acc[g][e];
+    }
+    __syncthreads();
+    for (int idx = tid; idx < G * D; idx += kThreads) {
+        const int g = idx / D, i = idx % D;
+        float* p = part + (size_t)g * (D + 2);
+        if (i == 0) {
+            p[0] = sh.M[g];
+            p[1] = sh.L[g];
+        }
+        p[2 + i] = sh.acc[0][g][i] + sh.acc[1][g][i] + sh.acc[2][g][i] + sh.acc[3][g][i];
+    }
+}
+
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, DecodeArgs a, int nitems) {
     __shared__ DecodeShared<D, G> sh;
@@ -359,7 +478,7 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
-    float* part = a.ws_part + ((size_t)u * nitems + item) * G * (D + 2);
+    float* part = a.ws_part + ((size_t)u * a.part_count + a.part_base + item) * G * (D + 2);
 
     if (a.dense || item < a.n_exact) {
         TokenMap tm;
@@ -385,8 +504,14 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
         float m, l;
         v4f32 acc[D / 16];
         const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+        const bool pseudo = a.neg_pseudo && !tm.dense;
+        PseudoPf pf;
+        if (pseudo) pseudo_prefetch<D, G>(a, geo, u, X, tm.nblk, sh.sel, pf);
         exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh, a.scale, m, l, acc);
         finish_exact<D, G>(m, l, acc, sh, part);
+        if (pseudo)
+            selected_pseudo<D, G>(a, geo, u, n, X, tm.nblk, pf, sh,
+                                  a.ws_part + ((size_t)u * a.part_count + a.part_base + a.n_exact + item) * G * (D + 2));
     } else {
         const int c0 = (item - a.n_exact) * a.cb;
         compensation<D, G>(a, geo, u, n, X, c0, min(c0 + a.cb, X), sh, part);
@@ -397,16 +522,17 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
 // grid = (units, G); thread (s, i) sums items s, s + S, ... for coordinate i, then the S partial sums
 // are added in LDS in a fixed order.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, DecodeArgs a, int nitems) {
+__global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, DecodeArgs a, int npos, int nneg) {
     constexpr int S = kThreads / D;  // item subsets
     constexpr int UNR = 16;
-    __shared__ float pm[kMaxItems], pc[kMaxItems];
+    const int nitems = npos + nneg;
+    __shared__ float pm[kMaxPartials], pc[kMaxPartials];
     __shared__ float part_acc[S][D];
     __shared__ float sM, sL;
     const int tid = threadIdx.x, lane = tid & 63;
     const int u = blockIdx.x, g = blockIdx.y;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
-    const float* pu = a.ws_part + (size_t)u * nitems * G * (D + 2) + (size_t)g * (D + 2);
+    const float* pu = a.ws_part + (size_t)u * a.part_count * G * (D + 2) + (size_t)g * (D + 2);
     const size_t stride = (size_t)G * (D + 2);
     for (int it = tid; it < nitems; it += kThreads) {
         pm[it] = pu[it * stride];
@@ -414,14 +540,16 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, Decode
     }
     __syncthreads();
     if (tid < 64) {
+        // the max over the added partials bounds every subtracted one (they are terms of the added ones)
         float M = -INFINITY;
-        for (int it = lane; it < nitems; it += 64) M = fmaxf(M, pm[it]);
+        for (int it = lane; it < npos; it += 64) M = fmaxf(M, pm[it]);
         M = wave_max(M);
         float L = 0.0f;
         for (int it = lane; it < nitems; it += 64) {
-            const float c = (pm[it] == -INFINITY) ? 0.0f : __expf(pm[it] - M);
+            float c = (pm[it] == -INFINITY) ? 0.0f : __expf(pm[it] - M);
+            if (it >= npos) c = -c;
             L += c * pc[it];
-            pc[it] = c;  // from here on: the item's rescale factor
+            pc[it] = c;  // from here on: the partial's signed rescale factor
         }
         L = wave_sum(L);
         if (lane == 0) {
@@ -460,22 +588,35 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, Decode
 }
 
 template <int D, int G>
-hipError_t launch_pair(const Geom& g, const DecodeArgs& a, hipStream_t s, dim3 grid) {
-    const int items = (int)grid.x;
-    decode_items_kernel<D, G><<<grid, kThreads, 0, s>>>(g, a, items);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    decode_merge_kernel<D, G><<<dim3(g.units(), G), kThreads, 0, s>>>(g, a, items);
+hipError_t items_g(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
+    decode_items_kernel<D, G><<<dim3(items, g.units()), kThreads, 0, s>>>(g, a, items);
+    return hipGetLastError();
+}
+
+template <int D, int G>
+hipError_t merge_g(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s) {
+    decode_merge_kernel<D, G><<<dim3(g.units(), G), kThreads, 0, s>>>(g, a, npos, nneg);
     return hipGetLastError();
 }
 
 template <int D>
-hipError_t dispatch_g(const Geom& g, const DecodeArgs& a, hipStream_t s, dim3 grid) {
+hipError_t items_d(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
     switch (g.G) {
-        case 1: return launch_pair<D, 1>(g, a, s, grid);
-        case 2: return launch_pair<D, 2>(g, a, s, grid);
-        case 4: return launch_pair<D, 4>(g, a, s, grid);
-        case 8: return launch_pair<D, 8>(g, a, s, grid);
+        case 1: return items_g<D, 1>(g, a, items, s);
+        case 2: return items_g<D, 2>(g, a, items, s);
+        case 4: return items_g<D, 4>(g, a, items, s);
+        case 8: return items_g<D, 8>(g, a, items, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <int D>
+hipError_t merge_d(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s) {
+    switch (g.G) {
+        case 1: return merge_g<D, 1>(g, a, npos, nneg, s);
+        case 2: return merge_g<D, 2>(g, a, npos, nneg, s);
+        case 4: return merge_g<D, 4>(g, a, npos, nneg, s);
+        case 8: return merge_g<D, 8>(g, a, npos, nneg, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -483,14 +624,32 @@ hipError_t dispatch_g(const Geom& g, const DecodeArgs& a, hipStream_t s, dim3 gr
 }  // namespace
 
 int decode_max_items() { return kMaxItems; }
+int decode_max_partials() { return kMaxPartials; }
 int decode_max_cb() { return kCbMax; }
 int decode_max_eb() { return kMaxEb; }
 
-hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s) {
+hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
+    if (items < 1 || a.part_base + items * (a.neg_pseudo ? 2 : 1) > a.part_count || a.part_count > kMaxPartials ||
+        (!a.dense && (a.cb > kCbMax || a.eb > kMaxEb)))
+        return hipErrorInvalidValue;
+    return g.D == 128 ? items_d<128>(g, a, items, s) : items_d<64>(g, a, items, s);
+}
+
+hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s) {
+    if (npos < 1 || nneg < 0 || npos + nneg > a.part_count || a.part_count > kMaxPartials) return hipErrorInvalidValue;
+    return g.D == 128 ? merge_d<128>(g, a, npos, nneg, s) : merge_d<64>(g, a, npos, nneg, s);
+}
+
+// A whole sparse or dense decode call: items, then the merge.
+hipError_t launch_decode(const Geom& g, const DecodeArgs& a0, hipStream_t s) {
+    DecodeArgs a = a0;
     const int items = a.dense ? a.n_exact : a.n_exact + a.n_comp;
-    if (items < 1 || items > kMaxItems || (!a.dense && (a.cb > kCbMax || a.eb > kMaxEb))) return hipErrorInvalidValue;
-    dim3 grid(items, g.units());
-    return g.D == 128 ? dispatch_g<128>(g, a, s, grid) : dispatch_g<64>(g, a, s, grid);
+    a.part_count = items;
+    a.part_base = 0;
+    a.neg_pseudo = 0;
+    hipError_t e = launch_decode_items(g, a, items, s);
+    if (e != hipSuccess) return e;
+    return launch_decode_merge(g, a, items, 0, s);
 }
 
 }  // namespace compkv

@@ -49,6 +49,16 @@ struct ScoreArgs {
     int keys_in_lds;  // set by the launcher: score bits kept in LDS (else in ws_key)
     int K, n_sink, n_recent;
     float scale;
+    // fused decode step only (comp_part == nullptr otherwise)
+    const uint16_t* k_new;  // nullable: [units][D] row n - 1 to store; its block's summary is refreshed first
+    const uint16_t* v_new;
+    uint16_t* Kc;           // caches: row n - 1 written, the active block's rows read
+    uint16_t* Vc;
+    float* kmean_w;         // writable views of kmean / dvar (the active block only)
+    float* dvar_w;
+    float* vmean;           // [units][xcap][D]: read by the compensation; the active block written
+    float* comp_part;       // [units][part_count][G][D + 2]: chunk c writes compensation partial c
+    int part_count;
 };
 
 struct DecodeArgs {
@@ -70,6 +80,10 @@ struct DecodeArgs {
     int cb;       // blocks per compensation item
     int dense;    // 1: every item is a token range of the dense decode
     float scale;
+    int part_count;  // partials per unit in ws_part (row stride of the partial array)
+    int part_base;   // partial index of this launch's item 0
+    int neg_pseudo;  // exact items also write, at part_base + n_exact + item, the pseudo-terms of their
+                     // selected blocks, which the merge subtracts (fused step)
 };
 
 // ------------------------------------------------------------------ launchers (one per kernel family)
@@ -78,10 +92,14 @@ hipError_t launch_build_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
 hipError_t launch_append_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
 hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s);
 int select_max_bpc();
+int select_max_chunk_heads();  // nchunks * G limit of the selection's partial merge
 int decode_max_items();
+int decode_max_partials();
 int decode_max_cb();
 int decode_max_eb();
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
+hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s);
+hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s);
 
 // ------------------------------------------------------------------ device helpers
 
@@ -112,6 +130,25 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
     return v;
+}
+
+// all-reduce over aligned groups of 8 lanes (two quad DPP exchanges, then a swizzle across quads)
+__device__ __forceinline__ float sum8(float x) {
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // xor 1
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // xor 2
+    x += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x101F));                    // xor 4
+    return x;
+}
+
+// block b is mandatory: one of the first n_sink or last n_recent blocks (Section 4.2)
+__device__ __forceinline__ bool mandatory(int b, int X, int n_sink, int n_recent) {
+    return b < n_sink || b >= X - n_recent;
+}
+
+// number of set bits of a wave mask below this lane
+__device__ __forceinline__ int lanes_below(unsigned long long mask) {
+    const int lane = threadIdx.x & 63;
+    return __popcll(mask & ((1ull << lane) - 1ull));
 }
 
 // Merge two softmax partials (max m, sum l, accumulators) into the first.

@@ -21,7 +21,9 @@
 // keys in that bin or above are ranked exactly, by brute force, and a bitmap of the selected and
 // mandatory blocks is compacted into ascending ids. Larger inputs, or ties that leave too many keys at
 // or above the cut's bin, go through a three-pass radix select on the score bits instead.
-#include "internal.h"
+#include "block_stats.h"
+
+#include <type_traits>
 
 namespace compkv {
 namespace {
@@ -30,23 +32,6 @@ constexpr int kBpcMax = 128;  // blocks per chunk, upper bound
 constexpr int kPMax = kBpcMax / 32;
 constexpr int kHistBins = 2048;
 constexpr size_t kDynBudget = 32768;  // dynamic LDS of the finalize launch
-
-// all-reduce over aligned groups of 8 lanes
-__device__ __forceinline__ float sum8(float x) {
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // xor 1
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // xor 2
-    x += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x101F));                    // xor 4
-    return x;
-}
-
-__device__ __forceinline__ bool mandatory(int b, int X, int n_sink, int n_recent) {
-    return b < n_sink || b >= X - n_recent;
-}
-
-__device__ __forceinline__ int lanes_below(unsigned long long mask) {
-    const int lane = threadIdx.x & 63;
-    return __popcll(mask & ((1ull << lane) - 1ull));
-}
 
 template <int D, int G>
 struct ChunkShared {
@@ -58,10 +43,31 @@ struct ChunkShared {
     float m[G];
 };
 
+// Extra state of the fused decode step: the refreshed summary of the active block, the compensation
+// weights and the per-wave compensation sums.
 template <int D, int G>
+struct StepShared {
+    alignas(16) float km[D];
+    alignas(16) float vm[D];
+    float dv[D], m2s[D];
+    float cw[G][kBpcMax];
+    float cm[G], cl[G];
+    alignas(16) float acc[4][G][D];
+};
+struct NoStep {};
+
+// kStep (fused decode step): before scoring, the workgroup whose chunk holds the active block stores the
+// new row and recomputes that block's summary (the append's routine, so bit-identical), then scores the
+// block from the LDS copy. After scoring, every chunk also forms the compensation partial of all its
+// blocks: pseudo-logits log|b| + zbar_g,b, weights exp(. - chunk max), weighted mean values.
+template <int D, int G, bool kStep>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
     constexpr int NF4 = D / 32;  // float4 of the mean-key row per lane
+    constexpr int LPB = D / 4;             // compensation: lanes per mean-value row (one float4 each)
+    constexpr int RPS = kThreads / LPB;    // mean-value rows per workgroup step
+    constexpr int VROWS = kStep ? kBpcMax / RPS : 1;
     __shared__ ChunkShared<D, G> sh;
+    __shared__ std::conditional_t<kStep, StepShared<D, G>, NoStep> st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = blockIdx.y, chunk = blockIdx.x;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
@@ -72,6 +78,29 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const int chunk0 = chunk * a.bpc;
     const int P = a.bpc / 32;
     const int li = tid & 7, grp = tid >> 3;
+    const int vli = tid % LPB, vslot = tid / LPB;
+
+    int ab = -1;  // active block refreshed by this workgroup
+    if constexpr (kStep) {
+        if (a.k_new && n >= 1 && (n - 1) / geo.B / a.bpc == chunk) {  // uniform over the workgroup
+            ab = (n - 1) / geo.B;
+            const int nb = n - ab * geo.B;
+            const uint16_t* kn = a.k_new + (size_t)u * D;
+            const uint16_t* vn = a.v_new + (size_t)u * D;
+            if (wave == 0) {
+                const size_t row = (size_t)u * geo.cap + (n - 1);
+                for (int i = lane; i < D / 8; i += 64) {
+                    reinterpret_cast<uint4*>(a.Kc + row * D)[i] = reinterpret_cast<const uint4*>(kn)[i];
+                    reinterpret_cast<uint4*>(a.Vc + row * D)[i] = reinterpret_cast<const uint4*>(vn)[i];
+                }
+            }
+            const size_t row0 = (size_t)u * geo.cap + (size_t)ab * geo.B;
+            const size_t blk = (size_t)u * geo.xcap + ab;
+            wave_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, kn, vn, nb - 1, geo.r, geo.layout,
+                                a.kmean_w + blk * D, a.dvar_w + blk * geo.r, a.vmean + blk * D, st.m2s, wave == 0,
+                                st.km, st.dv, st.vm);
+        }
+    }
 
     // issue the summary loads of this thread's blocks first
     float4 kv[kPMax][NF4];
@@ -87,12 +116,35 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         for (int m = 0; m < NF4; ++m) kv[p][m] = kp[li + 8 * m];
         dv0[p] = a.dvar[blk * geo.r + min(li, geo.r - 1)];
     }
+    float4 vrow[VROWS];
+    if constexpr (kStep) {
+        const float4* vm = reinterpret_cast<const float4*>(a.vmean + (size_t)u * geo.xcap * D) + vli;
+#pragma unroll
+        for (int k = 0; k < VROWS; ++k) {
+            if (k * RPS >= a.bpc) break;
+            const int b = chunk0 + vslot + k * RPS;
+            vrow[k] = vm[(size_t)(b < X ? b : 0) * (D / 4)];
+        }
+    }
 #pragma unroll
     for (int p = 0; p < kPMax; ++p) {
-        const bool valid = p < P && chunk0 + p * 32 + grp < X;
+        const int b = chunk0 + p * 32 + grp;
+        const bool valid = p < P && b < X;
 #pragma unroll
         for (int m = 0; m < NF4; ++m) kv[p][m] = valid ? kv[p][m] : make_float4(0, 0, 0, 0);
         dv0[p] = (valid && li < geo.r) ? dv0[p] : 0.0f;
+        if constexpr (kStep) {
+            if (b == ab) {  // the refreshed summary (the global copy may predate the refresh)
+#pragma unroll
+                for (int m = 0; m < NF4; ++m) kv[p][m] = *reinterpret_cast<const float4*>(&st.km[4 * (li + 8 * m)]);
+                dv0[p] = li < geo.r ? st.dv[li] : 0.0f;
+            }
+        }
+    }
+    if constexpr (kStep) {
+#pragma unroll
+        for (int k = 0; k < VROWS; ++k)
+            if (chunk0 + vslot + k * RPS == ab) vrow[k] = *reinterpret_cast<const float4*>(&st.vm[4 * vli]);
     }
     const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     for (int idx = tid; idx < G * D; idx += kThreads) sh.q[idx / D][idx % D] = s * bf16_at(qh + idx);
@@ -135,7 +187,8 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         if (geo.r > 8 && valid) {
             const size_t blk = (size_t)u * geo.xcap + b;
             for (int t = li + 8; t < geo.r; t += 8) {
-                const float dv = a.dvar[blk * geo.r + t];
+                float dv = a.dvar[blk * geo.r + t];
+                if constexpr (kStep) dv = (b == ab) ? st.dv[t] : dv;
 #pragma unroll
                 for (int g = 0; g < G; ++g) v[g] += sh.Qv[g][t] * dv;
             }
@@ -152,6 +205,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
                 sh.z[g][lb] = z[g];
                 sh.v[g][lb] = v[g];
                 sh.a[g][lb] = valid ? lnb + z[g] + 0.5f * v[g] : -INFINITY;
+                if constexpr (kStep) st.cw[g][lb] = valid ? lnb + z[g] : -INFINITY;  // pseudo-logit
             }
         }
     }
@@ -180,6 +234,30 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             pp[0] = m;
             pp[1] = ssum;
         }
+        if constexpr (kStep) {  // compensation weights of every block of the chunk
+            float cv[kBpcMax / 64];
+            float cm = -INFINITY;
+#pragma unroll
+            for (int k = 0; k < kBpcMax / 64; ++k) {
+                const int lb = lane + 64 * k;
+                cv[k] = lb < nvalid ? st.cw[g][lb] : -INFINITY;
+                cm = fmaxf(cm, cv[k]);
+            }
+            cm = wave_max(cm);
+            float csum = 0.0f;
+#pragma unroll
+            for (int k = 0; k < kBpcMax / 64; ++k) {
+                const int lb = lane + 64 * k;
+                const float wv = (cv[k] == -INFINITY) ? 0.0f : __expf(cv[k] - cm);
+                st.cw[g][lb] = wv;
+                csum += wv;
+            }
+            csum = wave_sum(csum);
+            if (lane == 0) {
+                st.cm[g] = cm;
+                st.cl[g] = csum;
+            }
+        }
     }
     __syncthreads();
     // coalesced stores: block logits [g][b] and score terms [b][g]
@@ -190,6 +268,50 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     for (int idx = tid; idx < G * nvalid; idx += kThreads) {
         const int lb = idx / G, g = idx % G;
         a.ws_w[((size_t)u * xmax + chunk0 + lb) * G + g] = expf(sh.a[g][lb] - sh.m[g]) * sh.v[g][lb];
+    }
+    if constexpr (kStep) {
+        // weighted mean values; lane vli of a row slot holds coordinates 4 vli .. 4 vli + 3
+        float acc[G][4];
+#pragma unroll
+        for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
+#pragma unroll
+        for (int k = 0; k < VROWS; ++k) {
+            const int lb = vslot + k * RPS;
+            if (k * RPS >= a.bpc) break;
+            if (lb < nvalid) {
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const float wv = st.cw[g][lb];
+                    acc[g][0] += wv * vrow[k].x;
+                    acc[g][1] += wv * vrow[k].y;
+                    acc[g][2] += wv * vrow[k].z;
+                    acc[g][3] += wv * vrow[k].w;
+                }
+            }
+        }
+#pragma unroll
+        for (int off = LPB; off < 64; off <<= 1)
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
+        if (lane < LPB) {
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) st.acc[wave][g][4 * vli + e] = acc[g][e];
+        }
+        __syncthreads();
+        float* cp = a.comp_part + ((size_t)u * a.part_count + chunk) * G * (D + 2);
+        for (int idx = tid; idx < G * D; idx += kThreads) {
+            const int g = idx / D, i = idx % D;
+            float* p = cp + (size_t)g * (D + 2);
+            if (i == 0) {
+                p[0] = st.cm[g];
+                p[1] = st.cl[g];
+            }
+            p[2 + i] = st.acc[0][g][i] + st.acc[1][g][i] + st.acc[2][g][i] + st.acc[3][g][i];
+        }
     }
 }
 
@@ -551,7 +673,10 @@ size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
 
 template <int D, int G>
 hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
-    score_chunks_kernel<D, G><<<dim3(a.nchunks, g.units()), kThreads, 0, s>>>(g, a);
+    if (a.comp_part)
+        score_chunks_kernel<D, G, true><<<dim3(a.nchunks, g.units()), kThreads, 0, s>>>(g, a);
+    else
+        score_chunks_kernel<D, G, false><<<dim3(a.nchunks, g.units()), kThreads, 0, s>>>(g, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     select_finalize_kernel<G><<<dim3(g.units()), kThreads, finalize_dyn_lds(g, a), s>>>(g, a);
@@ -572,6 +697,7 @@ hipError_t dispatch_g(const Geom& g, const ScoreArgs& a, hipStream_t s) {
 }  // namespace
 
 int select_max_bpc() { return kBpcMax; }
+int select_max_chunk_heads() { return (int)(kDynBudget / (2 * sizeof(float))); }
 
 hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s) {
     if (a.bpc % 32 != 0 || a.bpc > kBpcMax || a.bpc < 32) return hipErrorInvalidValue;

@@ -18,7 +18,7 @@ import torch
 
 import oracle
 import paper_2609_26300_amd as P
-from workloads import Workload, gen_layer
+from workloads import WORKLOADS, Workload, gen_layer
 
 TOL = 2e-3
 BAND = 1e-5
@@ -122,6 +122,24 @@ class Case:
                                self.out, self.lse, self.ws)
         return self.out, self.lse
 
+    def decode_step(self, k_new=None, v_new=None, sl=None, summ=None, K=None, V=None, ws=None):
+        """compkv_decode_step on this case's tensors (or the given ones); returns its outputs."""
+        d = self.dims
+        units = (d.batch, d.n_kv_heads)
+        summ = self.summ if summ is None else summ
+        r = dict(
+            sel=torch.full((*units, self.budget), -7, dtype=torch.int32, device="cuda"),
+            n_sel=torch.zeros(units, dtype=torch.int32, device="cuda"),
+            blk_logit=torch.zeros((*units, self.G, d.xcap), dtype=torch.float32, device="cuda"),
+            scores=torch.zeros((*units, d.xcap), dtype=torch.float32, device="cuda"),
+            out=torch.zeros((d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device="cuda"),
+            lse=torch.zeros((d.batch, d.n_q_heads), dtype=torch.float32, device="cuda"))
+        params = P.CompkvSelectParams(self.budget, self.n_sink, self.n_recent, self.scale)
+        P.compkv_decode_step(d, params, self.q, self.K if K is None else K, self.V if V is None else V, k_new, v_new,
+                             self.sl if sl is None else sl, summ.kmean, summ.dvar, summ.vmean, r["sel"], r["n_sel"],
+                             r["blk_logit"], r["scores"], r["out"], r["lse"], self.ws if ws is None else ws)
+        return r
+
     def dense_decode(self):
         d = self.dims
         out = torch.zeros((d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device="cuda")
@@ -151,3 +169,32 @@ class Case:
 
     def units(self):
         return [(b, h) for b in range(self.w.batch) for h in range(self.w.n_kv_heads)]
+
+
+TINY = WORKLOADS["tiny_4k"]
+LLAMA = WORKLOADS["llama8b_32k"]
+
+# Parity cases: the tiny 4K workload, the Llama-3-8B-shaped 32K layer at full size, and edge cases.
+CASES = {
+    "tiny_4k": lambda: Case(TINY),
+    "llama8b_32k": lambda: Case(LLAMA),
+    "partial_tail": lambda: Case(TINY.with_(context=4001, seed=7)),
+    "block1": lambda: Case(TINY.with_(context=300, block_size=1, budget_blocks=40, seed=8)),
+    "r_eq_d": lambda: Case(TINY.with_(n_var_groups=128, seed=9)),
+    "interleaved_r8": lambda: Case(TINY.with_(n_var_groups=8, seed=10), layout=1),
+    "d64": lambda: Case(TINY.with_(head_dim=64, seed=11)),
+    "g1": lambda: Case(TINY.with_(n_q_heads=2, seed=12)),
+    "g2_b32": lambda: Case(TINY.with_(n_q_heads=4, block_size=32, budget_blocks=9, seed=13)),
+    "g8_b64": lambda: Case(TINY.with_(n_q_heads=16, block_size=64, context=8000, budget_blocks=12, seed=14)),
+    "varlen": lambda: Case(TINY.with_(batch=4, seed=15), seq_lens=[4096, 1000, 17, 49]),
+    "short": lambda: Case(TINY.with_(batch=4, seed=16), seq_lens=[1, 10, 16, 40], budget=3),
+    "budget_ge_x": lambda: Case(TINY.with_(context=1000, budget_blocks=80, seed=17)),
+    "wide_gqa_8k": lambda: Case(WORKLOADS["wide_gqa_64k"].with_(batch=2, context=8192, seed=18)),
+    "long_16k_lognormal": lambda: Case(WORKLOADS["long_128k"].with_(batch=1, context=16384, budget_blocks=32,
+                                                                    seed=19)),
+    # selection paths: > 8192 blocks (keys outside registers), ~1000 candidates ranked by brute force,
+    # and ~2000 candidates (radix select fallback)
+    "block1_9000": lambda: Case(TINY.with_(context=9000, block_size=1, budget_blocks=40, seed=25)),
+    "budget300_x1000": lambda: Case(TINY.with_(context=16000, budget_blocks=300, seed=26)),
+    "budget300_x2000": lambda: Case(TINY.with_(context=32000, budget_blocks=300, seed=27)),
+}

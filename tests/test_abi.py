@@ -26,7 +26,7 @@ def test_library_exports_every_declared_function():
     L = P.library()
     names = P.exported_symbols()
     assert {"compkv_build_stats", "compkv_append_stats", "compkv_score_select", "compkv_sparse_decode",
-            "compkv_dense_decode", "compkv_workspace_bytes", "compkv_status_string",
+            "compkv_dense_decode", "compkv_decode_step", "compkv_workspace_bytes", "compkv_status_string",
             "compkv_version"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
@@ -41,10 +41,14 @@ def test_status_strings_and_version():
 
 def test_workspace_sizing():
     d = dims()
-    for which in range(4):
+    for which in range(5):
         assert P.compkv_workspace_bytes(d, 16, which) > 0
+    assert P.compkv_workspace_bytes(d, 16, 5) == 0
     all_ = P.compkv_workspace_bytes(d, 16, 0)
-    assert all(all_ >= P.compkv_workspace_bytes(d, 16, w) for w in (1, 2, 3))
+    assert all(all_ >= P.compkv_workspace_bytes(d, 16, w) for w in (1, 2, 3, 4))
+    # the fused step holds the scoring region plus its decode partials
+    assert P.compkv_workspace_bytes(d, 16, P.COMPKV_WS_DECODE_STEP) > P.compkv_workspace_bytes(
+        d, 16, P.COMPKV_WS_SCORE_SELECT)
     assert P.compkv_workspace_bytes(d, 0, 0) == 0
     assert P.compkv_workspace_bytes(dims(head_dim=96), 16, 0) == 0
     # grows with context
@@ -127,3 +131,44 @@ def test_product_path_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(binding.CompkvError):
         binding.library()
+
+
+def _step(L, d, p, ws=FAKE, ws_bytes=1 << 30, k_new=FAKE, v_new=FAKE, **null):
+    args = dict(q=FAKE, k_cache=FAKE, v_cache=FAKE, k_new=k_new, v_new=v_new, seq_lens=FAKE, kmean=FAKE,
+                dvar=FAKE, vmean=FAKE, sel=FAKE, n_sel=FAKE, blk_logit=FAKE, scores=None, out=FAKE, lse=None)
+    args.update(null)
+    return L.compkv_decode_step(ctypes.byref(d), ctypes.byref(p), *args.values(), ws, ws_bytes, None)
+
+
+def test_decode_step_validation():
+    d = dims()
+    L = P.library()
+    p = P.CompkvSelectParams(16, 1, 2, 0.088)
+    for name in ("q", "k_cache", "v_cache", "seq_lens", "kmean", "dvar", "vmean", "sel", "n_sel",
+                 "blk_logit", "out"):
+        assert _step(L, d, p, **{name: None}) == EINVAL, name
+    assert _step(L, d, p, k_new=None) == EINVAL  # k_new and v_new come together
+    assert _step(L, d, p, v_new=None) == EINVAL
+    assert _step(L, dims(head_dim=96), p) == EUNSUP
+    assert _step(L, d, P.CompkvSelectParams(2, 1, 2, 0.088)) == EBUDGET
+    need = P.compkv_workspace_bytes(d, 16, P.COMPKV_WS_DECODE_STEP)
+    assert _step(L, d, p, ws_bytes=need - 1) == EWS
+    assert _step(L, d, p, ws=ctypes.c_void_p(4100), ws_bytes=need) == EWS
+    assert _step(L, d, p, ws=None, ws_bytes=need) == EWS
+    # more partials than one merge holds: the separate calls remain available for such shapes
+    huge = dims(block_size=1, capacity_tokens=1 << 20, max_seq_len=1 << 20)
+    assert _step(L, huge, P.CompkvSelectParams(64, 1, 2, 0.088)) == EUNSUP
+
+
+def test_score_select_block_count_limit():
+    """Above 4096 * 128 / G blocks per unit the selection's partial merge does not fit: the call says
+    so before enqueuing anything."""
+    L = P.library()
+    p = P.CompkvSelectParams(64, 1, 2, 0.088)
+    args = [FAKE] * 6 + [FAKE, None]
+    ok = dims(block_size=1, capacity_tokens=65536, max_seq_len=65536)  # G = 4: 512 chunks of 128
+    big = dims(block_size=1, capacity_tokens=1 << 20, max_seq_len=(1 << 20))
+    need = P.compkv_workspace_bytes(big, 64, P.COMPKV_WS_SCORE_SELECT)
+    assert L.compkv_score_select(ctypes.byref(big), ctypes.byref(p), *args, FAKE, need, None) == EUNSUP
+    need = P.compkv_workspace_bytes(ok, 64, P.COMPKV_WS_SCORE_SELECT)
+    assert L.compkv_score_select(ctypes.byref(ok), ctypes.byref(p), *args, FAKE, need - 1, None) == EWS

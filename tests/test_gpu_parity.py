@@ -10,37 +10,10 @@ import pytest
 import torch
 
 import oracle
-from gpu_case import TOL, Case, check_selection, dev_bf16, rel_err
-from workloads import WORKLOADS
+from gpu_case import CASES, LLAMA, TINY, TOL, Case, check_selection, dev_bf16, rel_err
 
 pytestmark = pytest.mark.gpu
 
-TINY = WORKLOADS["tiny_4k"]
-LLAMA = WORKLOADS["llama8b_32k"]
-
-CASES = {
-    "tiny_4k": lambda: Case(TINY),
-    "llama8b_32k": lambda: Case(LLAMA),
-    "partial_tail": lambda: Case(TINY.with_(context=4001, seed=7)),
-    "block1": lambda: Case(TINY.with_(context=300, block_size=1, budget_blocks=40, seed=8)),
-    "r_eq_d": lambda: Case(TINY.with_(n_var_groups=128, seed=9)),
-    "interleaved_r8": lambda: Case(TINY.with_(n_var_groups=8, seed=10), layout=1),
-    "d64": lambda: Case(TINY.with_(head_dim=64, seed=11)),
-    "g1": lambda: Case(TINY.with_(n_q_heads=2, seed=12)),
-    "g2_b32": lambda: Case(TINY.with_(n_q_heads=4, block_size=32, budget_blocks=9, seed=13)),
-    "g8_b64": lambda: Case(TINY.with_(n_q_heads=16, block_size=64, context=8000, budget_blocks=12, seed=14)),
-    "varlen": lambda: Case(TINY.with_(batch=4, seed=15), seq_lens=[4096, 1000, 17, 49]),
-    "short": lambda: Case(TINY.with_(batch=4, seed=16), seq_lens=[1, 10, 16, 40], budget=3),
-    "budget_ge_x": lambda: Case(TINY.with_(context=1000, budget_blocks=80, seed=17)),
-    "wide_gqa_8k": lambda: Case(WORKLOADS["wide_gqa_64k"].with_(batch=2, context=8192, seed=18)),
-    "long_16k_lognormal": lambda: Case(WORKLOADS["long_128k"].with_(batch=1, context=16384, budget_blocks=32,
-                                                                    seed=19)),
-    # selection paths: > 8192 blocks (keys outside registers), ~1000 candidates ranked by brute force,
-    # and ~2000 candidates (radix select fallback)
-    "block1_9000": lambda: Case(TINY.with_(context=9000, block_size=1, budget_blocks=40, seed=25)),
-    "budget300_x1000": lambda: Case(TINY.with_(context=16000, budget_blocks=300, seed=26)),
-    "budget300_x2000": lambda: Case(TINY.with_(context=32000, budget_blocks=300, seed=27)),
-}
 _cache = {}
 
 
