@@ -119,7 +119,8 @@ int compkv_append_stats(const compkv_dims* dims, void* k_cache, void* v_cache, c
  * n_sel[u] = min(K, X); slots past n_sel are set to -1. If K >= X every block is selected.
  * blk_logit receives zbar (needed by compkv_sparse_decode); scores (nullable) receives S_b for every
  * block. q is bf16 [batch][n_q_heads][d]. Returns COMPKV_EBUDGET if K < n_sink + n_recent and
- * COMPKV_EUNSUPPORTED above 4096 * 128 / G blocks per unit (ceil(max_seq_len / block_size)).
+ * COMPKV_EUNSUPPORTED when a unit can hold more than 128 * (4096 / G - 1) blocks
+ * (ceil(max_seq_len / block_size)).
  */
 int compkv_score_select(const compkv_dims* dims, const compkv_select_params* params, const void* q,
                         const float* kmean, const float* dvar, const int32_t* seq_lens, int32_t* sel,

@@ -92,8 +92,8 @@ DenseShape dense_shape(const Geom& g) {
 size_t score_ws(const Geom& g) {
     const ScoreShape sh = score_shape(g);
     const size_t units = g.units(), xmax = g.xmax();
-    return align_up(units * sh.nchunks * g.G * 2 * sizeof(float)) + align_up(units * xmax * g.G * sizeof(float)) +
-           align_up(units * xmax * sizeof(uint32_t));
+    return align_up(units * (sh.nchunks + 1) * g.G * 2 * sizeof(float)) +
+           align_up(units * xmax * g.G * sizeof(float)) + align_up(units * xmax * sizeof(uint32_t));
 }
 
 size_t sparse_ws(const Geom& g, int K) {
@@ -106,9 +106,11 @@ size_t dense_ws(const Geom& g) {
     return align_up((size_t)g.units() * sh.items * g.G * (g.D + 2) * sizeof(float));
 }
 
-// fused step: the score region, then [units][nchunks + 2 n_exact][G][D + 2] decode partials
+// fused step: the score region, then [units][nchunks + 1 + 2 n_exact][G][D + 2] decode partials:
+// compensation of each chunk and of the last block, then each exact item's partial, then the
+// pseudo-terms each exact item subtracts
 int step_partials(const Geom& g, int K) {
-    return score_shape(g).nchunks + 2 * sparse_shape(g, K).n_exact;
+    return score_shape(g).nchunks + 1 + 2 * sparse_shape(g, K).n_exact;
 }
 
 size_t step_ws(const Geom& g, int K) {
@@ -141,7 +143,7 @@ compkv::ScoreArgs score_args(const Geom& g, const compkv_select_params* params, 
     compkv::ScoreArgs a{};
     char* p = static_cast<char*>(workspace);
     a.ws_part = reinterpret_cast<float*>(p);
-    p += align_up(units * sh.nchunks * g.G * 2 * sizeof(float));
+    p += align_up(units * (sh.nchunks + 1) * g.G * 2 * sizeof(float));
     a.ws_w = reinterpret_cast<float*>(p);
     p += align_up(units * xmax * g.G * sizeof(float));
     a.ws_key = reinterpret_cast<uint32_t*>(p);
@@ -233,7 +235,7 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel || !blk_logit) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
-    if (score_shape(g).nchunks * g.G > compkv::select_max_chunk_heads()) return COMPKV_EUNSUPPORTED;
+    if ((score_shape(g).nchunks + 1) * g.G > compkv::select_max_chunk_heads()) return COMPKV_EUNSUPPORTED;
     const size_t need = ws_bytes(g, params->budget_blocks, COMPKV_WS_SCORE_SELECT);
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
@@ -325,7 +327,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     const ScoreShape sc = score_shape(g);
     const int parts = step_partials(g, K);
     if (sp.eb > compkv::decode_max_eb() || sp.n_exact > compkv::decode_max_items() ||
-        parts > compkv::decode_max_partials() || sc.nchunks * g.G > compkv::select_max_chunk_heads())
+        parts > compkv::decode_max_partials() || (sc.nchunks + 1) * g.G > compkv::select_max_chunk_heads())
         return COMPKV_EUNSUPPORTED;
     st = check_ws(g, workspace, workspace_bytes, ws_bytes(g, K, COMPKV_WS_DECODE_STEP));
     if (st != COMPKV_OK) return st;
@@ -365,11 +367,11 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.dense = 0;
     d.scale = params->scale;
     d.part_count = parts;
-    d.part_base = sc.nchunks;
+    d.part_base = sc.nchunks + 1;
     d.neg_pseudo = 1;
     e = compkv::launch_decode_items(g, d, sp.n_exact, s);
     if (e != hipSuccess) return COMPKV_EHIP;
-    return launch_status(compkv::launch_decode_merge(g, d, sc.nchunks + sp.n_exact, sp.n_exact, s));
+    return launch_status(compkv::launch_decode_merge(g, d, sc.nchunks + 1 + sp.n_exact, sp.n_exact, s));
 }
 
 }  // extern "C"

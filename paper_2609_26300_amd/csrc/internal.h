@@ -120,16 +120,72 @@ __device__ __forceinline__ void unpack_bf16x8(const uint4 w, float f[8]) {
 
 __device__ __forceinline__ int clamp_len(int n, int cap) { return n < 0 ? 0 : (n > cap ? cap : n); }
 
+// Cross-lane moves with DPP (data-parallel primitives): `old` is kept by lanes whose source is outside
+// the row or whose row/bank is masked off.
+template <int CTRL, int ROW_MASK = 0xF, int BANK_MASK = 0xF>
+__device__ __forceinline__ int dpp_i(int old, int x) {
+    return __builtin_amdgcn_update_dpp(old, x, CTRL, ROW_MASK, BANK_MASK, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float readlane_f(float x, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
+// Wave64 all-reductions (every lane of the wave must be active; the result is wave-uniform). Within
+// each 16-lane row: xor 1 and xor 2 (quad permutes), then rotations by 4 and 8; the four row results
+// are combined in a fixed order.
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
-    return v;
+    v = fmaxf(v, dpp_f<0xB1>(v));
+    v = fmaxf(v, dpp_f<0x4E>(v));
+    v = fmaxf(v, dpp_f<0x124>(v));
+    v = fmaxf(v, dpp_f<0x128>(v));
+    return fmaxf(fmaxf(readlane_f(v, 0), readlane_f(v, 16)), fmaxf(readlane_f(v, 32), readlane_f(v, 48)));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    return v;
+    v += dpp_f<0xB1>(v);
+    v += dpp_f<0x4E>(v);
+    v += dpp_f<0x124>(v);
+    v += dpp_f<0x128>(v);
+    return (readlane_f(v, 0) + readlane_f(v, 16)) + (readlane_f(v, 32) + readlane_f(v, 48));
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    auto mx = [](uint32_t a, uint32_t b) { return a > b ? a : b; };
+    v = mx(v, (uint32_t)dpp_i<0xB1>((int)v, (int)v));
+    v = mx(v, (uint32_t)dpp_i<0x4E>((int)v, (int)v));
+    v = mx(v, (uint32_t)dpp_i<0x124>((int)v, (int)v));
+    v = mx(v, (uint32_t)dpp_i<0x128>((int)v, (int)v));
+    const uint32_t r0 = __builtin_amdgcn_readlane((int)v, 0), r1 = __builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane((int)v, 32), r3 = __builtin_amdgcn_readlane((int)v, 48);
+    return mx(mx(r0, r1), mx(r2, r3));
+}
+
+// Inclusive prefix sum over the 64 lanes (row shifts by 1, 2, 4, 8, then the row-15 and row-31
+// broadcasts carry row totals upward).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+    x += dpp_i<0x111>(0, x);
+    x += dpp_i<0x112>(0, x);
+    x += dpp_i<0x114>(0, x);
+    x += dpp_i<0x118>(0, x);
+    x += dpp_i<0x142, 0xA>(0, x);
+    x += dpp_i<0x143, 0xC>(0, x);
+    return x;
+}
+
+// x + (x of lane ^ off), for a power of two off < 64
+__device__ __forceinline__ float xor_add(float x, int off) {
+    switch (off) {
+        case 1: return x + dpp_f<0xB1>(x);
+        case 2: return x + dpp_f<0x4E>(x);
+        case 4: return x + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x101F));
+        case 8: return x + dpp_f<0x128>(x);
+        case 16: return x + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F));
+        default: return x + __shfl_xor(x, off);
+    }
 }
 
 // all-reduce over aligned groups of 8 lanes (two quad DPP exchanges, then a swizzle across quads)

@@ -1,26 +1,35 @@
 // select.hip -- block scoring and Top-K selection (Sections 4.1, 4.2; Appendix E.1). Two launches.
 //
-// Launch 1, grid = (nchunks, units): each workgroup streams the fp32 summaries (mean key, grouped
+// Launch 1, grid = (nchunks + 1, units). Chunk workgroups stream the fp32 summaries (mean key, grouped
 // variances) of `bpc` consecutive blocks of one unit. Eight lanes share a block: lane i of the eight
 // reads float4 i, i+8, ... of the mean-key row (the eight lanes read 128 contiguous bytes per load) and
-// the variance groups t = i, i+8, .... Every load of a thread is issued before any arithmetic. For
-// each of the unit's G query heads it forms the block-mean logit zbar = s q.kmean, the projected
-// variance sig2 = s^2 sum_t Q_t dvar_t and the log weight estimate a = log|b| + zbar + sig2/2 (the log
-// of the numerator of Eq. compkv-mass-estimate). It writes zbar (block logits, reused by the decode),
-// the chunk's per-head (max m_c of a, sum of exp(a - m_c)), and per block the G terms
+// the variance groups t = i, i+8, .... Every load is issued first, before the sequence length is even
+// read (block ids are clamped to the allocated range and masked afterwards). For each of the unit's G
+// query heads a workgroup forms the block-mean logit zbar = s q.kmean, the projected variance
+// sig2 = s^2 sum_t Q_t dvar_t and the log weight estimate a = log|b| + zbar + sig2/2 (the log of the
+// numerator of Eq. compkv-mass-estimate). It writes zbar (block logits, reused by the decode), the
+// chunk's per-head (max m_c of a, sum of exp(a - m_c)), and per block the G terms
 // w_g = exp(a_g - m_c) sig2_g, stored contiguously so one vector load fetches a block's terms.
+// The last block of each unit (the one a decode step appends to) is scored by one extra workgroup per
+// unit (blockIdx.x == nchunks), which writes its own partial; the chunks skip it.
 //
-// Launch 2, grid = (units): the kernel boundary makes every chunk's results visible (no
-// cross-workgroup fences or atomics). One workgroup per unit merges the chunk partials into each
-// head's log normalizer lse_g and forms S_b = sum_g exp(m_c - lse_g) w_g (= Eq. compkv-score). Block b
-// is ranked by the 64-bit key (bits of S_b) << 32 | ~b: scores are >= 0, so their IEEE bit patterns order
-// like the values, and the keys are unique and order exactly like (S_b descending, b ascending), the
-// stable Top-K of the paper. Up to 8192 blocks the keys stay in registers (32 per thread). One
-// histogram of each key's distance below the largest score (bins of 1/16 octave on the float bits; keys
-// farther than 255 bins are not counted) locates the bin that holds the (K-|F|)-th largest key; only the
-// keys in that bin or above are ranked exactly, by brute force, and a bitmap of the selected and
-// mandatory blocks is compacted into ascending ids. Larger inputs, or ties that leave too many keys at
-// or above the cut's bin, go through a three-pass radix select on the score bits instead.
+// Fused decode step (kStep): the extra workgroup first stores the new row and recomputes the last
+// block's summary with the append's routine (bit-identical), so no chunk waits for it; every workgroup
+// also forms the compensation partial of its blocks: pseudo-logits log|b| + zbar, weights
+// exp(. - max) and the weighted mean values (streamed alongside the mean keys).
+//
+// Launch 2, grid = (units): the kernel boundary makes every partial visible (no cross-workgroup fences
+// or atomics). One workgroup per unit merges the partials into each head's log normalizer lse_g and
+// forms S_b = sum_g exp(m_c - lse_g) w_g (= Eq. compkv-score). Block b is ranked by the 64-bit key
+// (bits of S_b) << 32 | ~b: scores are >= 0, so their IEEE bit patterns order like the values, and the
+// keys are unique and order exactly like (S_b descending, b ascending), the stable Top-K of the paper.
+// Up to 8192 blocks the keys stay in registers (32 per thread). One histogram of each key's distance
+// below the largest score (bins of 1/16 octave on the float bits; keys farther than 255 bins are not
+// counted) locates the bin that holds the (K-|F|)-th largest key; only the keys in that bin or above
+// are ranked exactly, by brute force, and a bitmap of the selected and mandatory blocks is compacted
+// into ascending ids. Larger inputs, or ties that leave too many keys at or above the cut's bin, go
+// through a three-pass radix select on the score bits instead. Wave-level reductions and prefix sums
+// use DPP lane moves.
 #include "block_stats.h"
 
 #include <type_traits>
@@ -33,6 +42,32 @@ constexpr int kPMax = kBpcMax / 32;
 constexpr int kHistBins = 2048;
 constexpr size_t kDynBudget = 32768;  // dynamic LDS of the finalize launch
 
+// s^2 Q_{g,t} (Appendix A.4: the scaled query's squared coordinates summed over coordinate group t) for
+// the heads g = wave, wave + 4, ..., into Qv[g][t]. Lane f takes frequency pair f; a group is a run of
+// (d/2)/r consecutive pairs, summed by butterflies. With r == d every coordinate is its own group.
+template <int D, int G>
+__device__ void group_query_energy(const uint16_t* qh, float s, int r, int layout, float (*Qv)[D]) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int g = wave; g < G; g += 4) {
+        const uint16_t* qg = qh + g * D;
+        if (r == D) {
+            for (int i = lane; i < D; i += 64) {
+                const float x = s * bf16_at(qg + i);
+                Qv[g][i] = x * x;
+            }
+            continue;
+        }
+        const int f = lane < D / 2 ? lane : 0;
+        const int ia = layout == 0 ? f : 2 * f;
+        const int ib = layout == 0 ? f + D / 2 : 2 * f + 1;
+        const float xa = s * bf16_at(qg + ia), xb = s * bf16_at(qg + ib);
+        float e = lane < D / 2 ? xa * xa + xb * xb : 0.0f;
+        const int w = (D / 2) / r;
+        for (int off = 1; off < w; off <<= 1) e = xor_add(e, off);
+        if (lane < D / 2 && lane % w == 0) Qv[g][lane / w] = e;
+    }
+}
+
 template <int D, int G>
 struct ChunkShared {
     float q[G][D];   // scaled query
@@ -43,36 +78,119 @@ struct ChunkShared {
     float m[G];
 };
 
-// Extra state of the fused decode step: the refreshed summary of the active block, the compensation
-// weights and the per-wave compensation sums.
+// Compensation state of the fused decode step.
 template <int D, int G>
-struct StepShared {
-    alignas(16) float km[D];
-    alignas(16) float vm[D];
-    float dv[D], m2s[D];
+struct CompShared {
     float cw[G][kBpcMax];
     float cm[G], cl[G];
     alignas(16) float acc[4][G][D];
 };
-struct NoStep {};
+struct NoComp {};
 
-// kStep (fused decode step): before scoring, the workgroup whose chunk holds the active block stores the
-// new row and recomputes that block's summary (the append's routine, so bit-identical), then scores the
-// block from the LDS copy. After scoring, every chunk also forms the compensation partial of all its
-// blocks: pseudo-logits log|b| + zbar_g,b, weights exp(. - chunk max), weighted mean values.
+template <int D, int G>
+struct TailShared {
+    alignas(16) float km[D];
+    alignas(16) float vm[D];
+    float dv[D], m2s[D];
+    float Qv[G][D];
+    float z[G], v[G];
+};
+
+// The extra workgroup of unit u: the last block X - 1 (refreshed first when the step appends).
+template <int D, int G, bool kStep>
+__device__ void score_tail(const Geom& geo, const ScoreArgs& a) {
+    __shared__ TailShared<D, G> ts;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int u = blockIdx.y, bseq = u / geo.hkv, h = u % geo.hkv;
+    const int nc = a.nchunks;
+    const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+    group_query_energy<D, G>(qh, a.scale, geo.r, geo.layout, ts.Qv);
+    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
+    float* pp = a.ws_part + ((size_t)u * (nc + 1) + nc) * G * 2;
+    float* cp = kStep ? a.comp_part + ((size_t)u * a.part_count + nc) * G * (D + 2) : nullptr;
+    if (X == 0) {  // empty sequence: neutral partials
+        for (int g = tid; g < G; g += kThreads) {
+            pp[2 * g] = -INFINITY;
+            pp[2 * g + 1] = 0.0f;
+        }
+        if constexpr (kStep)
+            for (int idx = tid; idx < G * (D + 2); idx += kThreads) cp[idx] = (idx % (D + 2) == 0) ? -INFINITY : 0.0f;
+        return;
+    }
+    const int b = X - 1, nb = n - b * geo.B;
+    const size_t blk = (size_t)u * geo.xcap + b;
+    if (kStep && a.k_new) {
+        const uint16_t* kn = a.k_new + (size_t)u * D;
+        const uint16_t* vn = a.v_new + (size_t)u * D;
+        if (wave == 0) {
+            const size_t row = (size_t)u * geo.cap + (n - 1);
+            for (int i = lane; i < D / 8; i += 64) {
+                reinterpret_cast<uint4*>(a.Kc + row * D)[i] = reinterpret_cast<const uint4*>(kn)[i];
+                reinterpret_cast<uint4*>(a.Vc + row * D)[i] = reinterpret_cast<const uint4*>(vn)[i];
+            }
+        }
+        const size_t row0 = (size_t)u * geo.cap + (size_t)b * geo.B;
+        wave_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, kn, vn, nb - 1, geo.r, geo.layout,
+                            a.kmean_w + blk * D, a.dvar_w + blk * geo.r, a.vmean + blk * D, ts.m2s, wave == 0,
+                            ts.km, ts.dv, ts.vm);
+    } else {
+        for (int i = tid; i < D; i += kThreads) {
+            ts.km[i] = a.kmean[blk * D + i];
+            if constexpr (kStep) ts.vm[i] = a.vmean[blk * D + i];
+        }
+        for (int t = tid; t < geo.r; t += kThreads) ts.dv[t] = a.dvar[blk * geo.r + t];
+        __syncthreads();
+    }
+    const float s = a.scale;
+    for (int g = wave; g < G; g += 4) {
+        float z = 0.0f, v = 0.0f;
+        for (int i = lane; i < D; i += 64) z += (s * bf16_at(qh + g * D + i)) * ts.km[i];
+        for (int t = lane; t < geo.r; t += 64) v += ts.Qv[g][t] * ts.dv[t];
+        z = wave_sum(z);
+        v = wave_sum(v);
+        if (lane == 0) {
+            ts.z[g] = z;
+            ts.v[g] = v;
+        }
+    }
+    __syncthreads();
+    const float lnb = logf((float)nb);
+    for (int g = tid; g < G; g += kThreads) {
+        const float z = ts.z[g], v = ts.v[g];
+        a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
+        pp[2 * g] = lnb + z + 0.5f * v;  // the partial of one block: max a, sum exp(a - a) = 1
+        pp[2 * g + 1] = 1.0f;
+        a.ws_w[((size_t)u * geo.xmax() + b) * G + g] = v;
+    }
+    if constexpr (kStep) {
+        for (int idx = tid; idx < G * D; idx += kThreads) {
+            const int g = idx / D, i = idx % D;
+            float* p = cp + (size_t)g * (D + 2);
+            if (i == 0) {
+                p[0] = lnb + ts.z[g];
+                p[1] = 1.0f;
+            }
+            p[2 + i] = ts.vm[i];
+        }
+    }
+}
+
 template <int D, int G, bool kStep>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
-    constexpr int NF4 = D / 32;  // float4 of the mean-key row per lane
-    constexpr int LPB = D / 4;             // compensation: lanes per mean-value row (one float4 each)
-    constexpr int RPS = kThreads / LPB;    // mean-value rows per workgroup step
+    if (blockIdx.x == (unsigned)a.nchunks) {
+        score_tail<D, G, kStep>(geo, a);
+        return;
+    }
+    constexpr int NF4 = D / 32;           // float4 of the mean-key row per lane
+    constexpr int LPB = D / 4;            // compensation: lanes per mean-value row (one float4 each)
+    constexpr int RPS = kThreads / LPB;   // mean-value rows per workgroup step
     constexpr int VROWS = kStep ? kBpcMax / RPS : 1;
     __shared__ ChunkShared<D, G> sh;
-    __shared__ std::conditional_t<kStep, StepShared<D, G>, NoStep> st;
+    __shared__ std::conditional_t<kStep, CompShared<D, G>, NoComp> st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = blockIdx.y, chunk = blockIdx.x;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
     const int xmax = geo.xmax();
     const float s = a.scale;
     const int chunk0 = chunk * a.bpc;
@@ -80,37 +198,14 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const int li = tid & 7, grp = tid >> 3;
     const int vli = tid % LPB, vslot = tid / LPB;
 
-    int ab = -1;  // active block refreshed by this workgroup
-    if constexpr (kStep) {
-        if (a.k_new && n >= 1 && (n - 1) / geo.B / a.bpc == chunk) {  // uniform over the workgroup
-            ab = (n - 1) / geo.B;
-            const int nb = n - ab * geo.B;
-            const uint16_t* kn = a.k_new + (size_t)u * D;
-            const uint16_t* vn = a.v_new + (size_t)u * D;
-            if (wave == 0) {
-                const size_t row = (size_t)u * geo.cap + (n - 1);
-                for (int i = lane; i < D / 8; i += 64) {
-                    reinterpret_cast<uint4*>(a.Kc + row * D)[i] = reinterpret_cast<const uint4*>(kn)[i];
-                    reinterpret_cast<uint4*>(a.Vc + row * D)[i] = reinterpret_cast<const uint4*>(vn)[i];
-                }
-            }
-            const size_t row0 = (size_t)u * geo.cap + (size_t)ab * geo.B;
-            const size_t blk = (size_t)u * geo.xcap + ab;
-            wave_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, kn, vn, nb - 1, geo.r, geo.layout,
-                                a.kmean_w + blk * D, a.dvar_w + blk * geo.r, a.vmean + blk * D, st.m2s, wave == 0,
-                                st.km, st.dv, st.vm);
-        }
-    }
-
-    // issue the summary loads of this thread's blocks first
+    // issue the summary loads of this thread's blocks first (branch-free: a block id past the
+    // allocated range loads block 0 of the unit; masked below once the length is known)
     float4 kv[kPMax][NF4];
     float dv0[kPMax];
-    // (branch-free: an invalid slot loads block 0 of the unit, always allocated, and is zeroed after)
 #pragma unroll
     for (int p = 0; p < kPMax; ++p) {
         const int b = chunk0 + p * 32 + grp;
-        const bool valid = p < P && b < X;
-        const size_t blk = (size_t)u * geo.xcap + (valid ? b : 0);
+        const size_t blk = (size_t)u * geo.xcap + ((p < P && b < xmax) ? b : 0);
         const float4* kp = reinterpret_cast<const float4*>(a.kmean + blk * D);
 #pragma unroll
         for (int m = 0; m < NF4; ++m) kv[p][m] = kp[li + 8 * m];
@@ -123,46 +218,21 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         for (int k = 0; k < VROWS; ++k) {
             if (k * RPS >= a.bpc) break;
             const int b = chunk0 + vslot + k * RPS;
-            vrow[k] = vm[(size_t)(b < X ? b : 0) * (D / 4)];
+            vrow[k] = vm[(size_t)(b < xmax ? b : 0) * (D / 4)];
         }
-    }
-#pragma unroll
-    for (int p = 0; p < kPMax; ++p) {
-        const int b = chunk0 + p * 32 + grp;
-        const bool valid = p < P && b < X;
-#pragma unroll
-        for (int m = 0; m < NF4; ++m) kv[p][m] = valid ? kv[p][m] : make_float4(0, 0, 0, 0);
-        dv0[p] = (valid && li < geo.r) ? dv0[p] : 0.0f;
-        if constexpr (kStep) {
-            if (b == ab) {  // the refreshed summary (the global copy may predate the refresh)
-#pragma unroll
-                for (int m = 0; m < NF4; ++m) kv[p][m] = *reinterpret_cast<const float4*>(&st.km[4 * (li + 8 * m)]);
-                dv0[p] = li < geo.r ? st.dv[li] : 0.0f;
-            }
-        }
-    }
-    if constexpr (kStep) {
-#pragma unroll
-        for (int k = 0; k < VROWS; ++k)
-            if (chunk0 + vslot + k * RPS == ab) vrow[k] = *reinterpret_cast<const float4*>(&st.vm[4 * vli]);
     }
     const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     for (int idx = tid; idx < G * D; idx += kThreads) sh.q[idx / D][idx % D] = s * bf16_at(qh + idx);
-    __syncthreads();
-    for (int idx = tid; idx < G * geo.r; idx += kThreads) {
-        // s^2 Q_{g,t}: squared (scaled) query coordinates summed over group t (Appendix A.4)
-        const int g = idx / geo.r, t = idx % geo.r;
-        float acc = 0.0f;
-        if (geo.r == D) {
-            acc = sh.q[g][t] * sh.q[g][t];
-        } else {
-            const int w = (D / 2) / geo.r;
-            for (int k = 0; k < 2 * w; ++k) {
-                const int i = geo.layout == 0 ? (k < w ? t * w + k : D / 2 + t * w + (k - w)) : 2 * t * w + k;
-                acc += sh.q[g][i] * sh.q[g][i];
-            }
-        }
-        sh.Qv[g][t] = acc;
+    group_query_energy<D, G>(qh, s, geo.r, geo.layout, sh.Qv);
+    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
+    const int xs = X - 1;  // blocks [0, X - 1) are scored here; the last one by the extra workgroup
+#pragma unroll
+    for (int p = 0; p < kPMax; ++p) {
+        const bool valid = p < P && chunk0 + p * 32 + grp < xs;
+#pragma unroll
+        for (int m = 0; m < NF4; ++m) kv[p][m] = valid ? kv[p][m] : make_float4(0, 0, 0, 0);
+        dv0[p] = (valid && li < geo.r) ? dv0[p] : 0.0f;
     }
     __syncthreads();
 
@@ -171,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         if (p >= P) break;
         const int lb = p * 32 + grp;
         const int b = chunk0 + lb;
-        const bool valid = b < X;
+        const bool valid = b < xs;
         float z[G], v[G];
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -187,8 +257,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         if (geo.r > 8 && valid) {
             const size_t blk = (size_t)u * geo.xcap + b;
             for (int t = li + 8; t < geo.r; t += 8) {
-                float dv = a.dvar[blk * geo.r + t];
-                if constexpr (kStep) dv = (b == ab) ? st.dv[t] : dv;
+                const float dv = a.dvar[blk * geo.r + t];
 #pragma unroll
                 for (int g = 0; g < G; ++g) v[g] += sh.Qv[g][t] * dv;
             }
@@ -210,8 +279,8 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         }
     }
     __syncthreads();
-    // the chunk's per-head max and sum of exp(a - max)
-    const int nvalid = max(0, min(a.bpc, X - chunk0));
+    // the chunk's per-head max and sum of exp(a - max) (and, fused, of the pseudo-logits)
+    const int nvalid = max(0, min(a.bpc, xs - chunk0));
     for (int g = wave; g < G; g += 4) {
         float av[kBpcMax / 64];
         float m = -INFINITY;
@@ -230,11 +299,11 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         ssum = wave_sum(ssum);
         if (lane == 0) {
             sh.m[g] = m;
-            float* pp = a.ws_part + (((size_t)u * a.nchunks + chunk) * G + g) * 2;
+            float* pp = a.ws_part + (((size_t)u * (a.nchunks + 1) + chunk) * G + g) * 2;
             pp[0] = m;
             pp[1] = ssum;
         }
-        if constexpr (kStep) {  // compensation weights of every block of the chunk
+        if constexpr (kStep) {
             float cv[kBpcMax / 64];
             float cm = -INFINITY;
 #pragma unroll
@@ -294,7 +363,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
+                for (int e = 0; e < 4; ++e) acc[g][e] = xor_add(acc[g][e], off);
         if (lane < LPB) {
 #pragma unroll
             for (int g = 0; g < G; ++g)
@@ -315,7 +384,8 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     }
 }
 
-constexpr int kRegKeys = 32;    // score keys one thread keeps in registers (fast path: X <= 8192)
+constexpr int kRegKeys = 32;    // score keys one thread keeps in registers (fast path: xmax <= 8192)
+constexpr int kPreKeys = 8;     // of which the score terms are loaded before the normalizers are known
 constexpr int kCandCap = 1024;  // candidates ranked by brute force on the fast path
 constexpr int kHistTail = 255;  // distance bins counted on the fast path (bin 255 = everything farther)
 
@@ -327,37 +397,75 @@ struct FinalShared {
     int digit, above;
     unsigned long long cand[kCandCap];
     uint32_t bitmap[kThreads];
-    int ncand, beta;
+    int beta;
 };
+
+// bits [lo, hi) of the 32-bit word holding ids base .. base + 31
+__device__ __forceinline__ uint32_t range_bits(int lo, int hi, int base) {
+    const int l = max(lo - base, 0), r = min(hi - base, 32);
+    if (l >= r) return 0u;
+    const uint32_t upto = r == 32 ? 0xFFFFFFFFu : ((1u << r) - 1u);
+    return upto & ~((1u << l) - 1u);
+}
+
+// score terms of block b (G floats, contiguous)
+template <int G>
+__device__ __forceinline__ void load_terms(const float* wu, int b, float (&w)[G]) {
+    if constexpr (G % 4 == 0) {
+#pragma unroll
+        for (int g4 = 0; g4 < G; g4 += 4) {
+            const float4 t4 = *reinterpret_cast<const float4*>(wu + (size_t)b * G + g4);
+            w[g4] = t4.x;
+            w[g4 + 1] = t4.y;
+            w[g4 + 2] = t4.z;
+            w[g4 + 3] = t4.w;
+        }
+    } else {
+#pragma unroll
+        for (int g = 0; g < G; ++g) w[g] = wu[(size_t)b * G + g];
+    }
+}
 
 template <int G>
 __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
     constexpr int NBATCH = 8;  // blocks whose score terms one thread loads at once
     __shared__ FinalShared sh;
-    extern __shared__ float dyn[];  // [nchunks][G] factors, [nchunks][G] sums, then [xmax] score bits
+    extern __shared__ float dyn[];  // [np][G] factors, [np][G] sums, then [xmax] score bits
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = blockIdx.x;
     const int bseq = u / geo.hkv;
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
     const int xmax = geo.xmax();
-    const int nc = a.nchunks;
+    const int nc = a.nchunks, np = nc + 1;  // partial nc: the last block's
+    const float* wu = a.ws_w + (size_t)u * xmax * G;
+    const bool fast = xmax <= kRegKeys * kThreads;
 
-    // ---- per-head log normalizer over every block, then each chunk's factor exp(m_c - lse)
+    // score terms of the first blocks, requested before anything else (ids below xmax are allocated)
+    float w0[kPreKeys][G];
+    if (fast) {
+#pragma unroll
+        for (int k = 0; k < kPreKeys; ++k) {
+            const int b = tid + k * kThreads;
+            if (k * kThreads < xmax) load_terms<G>(wu, b < xmax ? b : 0, w0[k]);
+        }
+    }
+    // ---- per-head log normalizer over every block, then each partial's factor exp(m_c - lse)
     float* fac = dyn;
-    float* sums = dyn + nc * G;
-    const float* pu = a.ws_part + (size_t)u * nc * G * 2;
-    for (int idx = tid; idx < nc * G; idx += kThreads) {
+    float* sums = dyn + np * G;
+    const float* pu = a.ws_part + (size_t)u * np * G * 2;
+    for (int idx = tid; idx < np * G; idx += kThreads) {
         fac[idx] = pu[2 * idx];
         sums[idx] = pu[2 * idx + 1];
     }
+    sh.bitmap[tid] = 0u;
+    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
     __syncthreads();
     for (int g = wave; g < G; g += 4) {
         float m = -INFINITY;
-        for (int c = lane; c < nc; c += 64) m = fmaxf(m, fac[c * G + g]);
+        for (int c = lane; c < np; c += 64) m = fmaxf(m, fac[c * G + g]);
         m = wave_max(m);
         float l = 0.0f;
-        for (int c = lane; c < nc; c += 64) {
+        for (int c = lane; c < np; c += 64) {
             const float pm = fac[c * G + g];
             if (pm != -INFINITY) l += sums[c * G + g] * expf(pm - m);
         }
@@ -365,7 +473,7 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
         if (lane == 0) sh.lse[g] = m + logf(l);
     }
     __syncthreads();
-    for (int idx = tid; idx < nc * G; idx += kThreads) {
+    for (int idx = tid; idx < np * G; idx += kThreads) {
         const float pm = fac[idx];
         fac[idx] = pm == -INFINITY ? 0.0f : expf(pm - sh.lse[idx % G]);
     }
@@ -373,72 +481,57 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
 
     const int K = a.K;
     const bool take_all = K >= X;
-    int n_mand;
-    {
-        const int sink = min(a.n_sink, X);
-        const int rec_lo = max(X - a.n_recent, 0);
-        n_mand = sink + (X - rec_lo) - max(0, sink - rec_lo);
-    }
+    const int sink = min(a.n_sink, X);
+    const int rec_lo = max(X - a.n_recent, 0);
+    const int n_mand = sink + (X - rec_lo) - max(0, sink - rec_lo);
     const int kk = take_all ? 0 : K - n_mand;  // >= 0: the host checks K >= n_sink + n_recent
     int32_t* sel = a.sel + (size_t)u * K;
-    uint32_t* keys = a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * nc * G) : a.ws_key + (size_t)u * xmax;
-    const float* wu = a.ws_w + (size_t)u * xmax * G;
+    uint32_t* keys = a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * np * G) : a.ws_key + (size_t)u * xmax;
+    auto part_of = [&](int b) { return b == X - 1 ? nc : b / a.bpc; };
 
     // ---- fast path. Block b's key is (bits of S_b) << 32 | ~b: unique, and ordered exactly like
     // (S_b descending, b ascending). Thread t keeps the keys of blocks t + 256k in registers.
-    if (X <= kRegKeys * kThreads) {
+    if (fast) {
         unsigned long long ck[kRegKeys];
+        auto make_key = [&](int b, const float (&w)[G]) -> unsigned long long {
+            if (b >= X) return 0ull;
+            const float* f = fac + part_of(b) * G;
+            float S = 0.0f;
 #pragma unroll
-        for (int k0 = 0; k0 < kRegKeys; k0 += NBATCH) {
+            for (int g = 0; g < G; ++g) S += f[g] * w[g];
+            if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+            if (mandatory(b, X, a.n_sink, a.n_recent)) return 0ull;
+            return ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
+        };
+#pragma unroll
+        for (int k = 0; k < kPreKeys; ++k) ck[k] = k * kThreads < xmax ? make_key(tid + k * kThreads, w0[k]) : 0ull;
+#pragma unroll
+        for (int k0 = kPreKeys; k0 < kRegKeys; k0 += NBATCH) {
+            if (k0 * kThreads >= xmax) {
+#pragma unroll
+                for (int k = 0; k < NBATCH; ++k) ck[k0 + k] = 0ull;
+                continue;
+            }
             float w[NBATCH][G];
 #pragma unroll
             for (int k = 0; k < NBATCH; ++k) {
                 const int b = tid + (k0 + k) * kThreads;
-                const size_t bs = (size_t)(b < X ? b : 0) * G;  // branch-free; unused when b >= X
-                if constexpr (G % 4 == 0) {
-#pragma unroll
-                    for (int g4 = 0; g4 < G; g4 += 4) {
-                        const float4 t4 = *reinterpret_cast<const float4*>(wu + bs + g4);
-                        w[k][g4] = t4.x;
-                        w[k][g4 + 1] = t4.y;
-                        w[k][g4 + 2] = t4.z;
-                        w[k][g4 + 3] = t4.w;
-                    }
-                } else {
-#pragma unroll
-                    for (int g = 0; g < G; ++g) w[k][g] = wu[bs + g];
-                }
+                load_terms<G>(wu, b < xmax ? b : 0, w[k]);
             }
 #pragma unroll
-            for (int k = 0; k < NBATCH; ++k) {
-                const int b = tid + (k0 + k) * kThreads;
-                ck[k0 + k] = 0ull;
-                if (b < X) {
-                    const float* f = fac + (b / a.bpc) * G;
-                    float S = 0.0f;
-#pragma unroll
-                    for (int g = 0; g < G; ++g) S += f[g] * w[k][g];
-                    if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
-                    if (!mandatory(b, X, a.n_sink, a.n_recent))
-                        ck[k0 + k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
-                }
-            }
+            for (int k = 0; k < NBATCH; ++k) ck[k0 + k] = make_key(tid + (k0 + k) * kThreads, w[k]);
         }
         // histogram of the keys' distance below the largest score, in bins of 2^19 float ulps (1/16 of
         // an octave); keys more than 255 bins below are not counted
         uint32_t mx = 0u;
 #pragma unroll
         for (int k = 0; k < kRegKeys; ++k) mx = ck[k] ? max(mx, (uint32_t)(ck[k] >> 32)) : mx;
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        mx = wave_max_u32(mx);
         if (lane == 0) sh.scan[wave] = (int)mx;
         sh.hist[tid] = 0;
-        sh.bitmap[tid] = 0u;
-        if (tid == 0) {
-            sh.beta = kHistTail;
-            sh.ncand = 0;
-        }
+        if (tid == 0) sh.beta = kHistTail;
         __syncthreads();
+        int m = 0;  // candidates ranked exactly
         if (!take_all && kk > 0) {
             const uint32_t smax = max(max((uint32_t)sh.scan[0], (uint32_t)sh.scan[1]),
                                       max((uint32_t)sh.scan[2], (uint32_t)sh.scan[3]));
@@ -452,33 +545,28 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
             __syncthreads();
             // inclusive prefix over bins (thread t holds bin t); the bin reaching kk holds the cut
             const int c = sh.hist[tid];
-            int incl = c;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int o = __shfl_up(incl, off);
-                if (lane >= off) incl += o;
-            }
+            int incl = wave_incl_scan(c);
             if (lane == 63) sh.cnt[wave] = incl;
             __syncthreads();
             for (int w = 0; w < wave; ++w) incl += sh.cnt[w];
             if (tid < kHistTail && incl - c < kk && incl >= kk) sh.beta = tid;
             __syncthreads();
             const uint32_t beta = (uint32_t)sh.beta;  // kHistTail: the cut lies below the counted range
+            // candidates: keys in the cut's bin or above, placed by a prefix sum of per-thread counts
+            int mine = 0;
 #pragma unroll
-            for (int k = 0; k < kRegKeys; ++k) {
-                const bool cnd = bin[k] <= beta;
-                const unsigned long long mask = __ballot(cnd);
-                if (mask == 0ull) continue;
-                const int first = __ffsll((long long)mask) - 1;
-                int base = 0;
-                if (lane == first) base = atomicAdd(&sh.ncand, __popcll(mask));
-                base = __shfl(base, first);
-                const int pos = base + lanes_below(mask);
-                if (cnd && pos < kCandCap) sh.cand[pos] = ck[k];
-            }
+            for (int k = 0; k < kRegKeys; ++k) mine += bin[k] <= beta;
+            int off = wave_incl_scan(mine);
+            if (lane == 63) sh.cnt2[wave] = off;
             __syncthreads();
-            const int m = sh.ncand;
+            off -= mine;
+            for (int w = 0; w < wave; ++w) off += sh.cnt2[w];
+            m = sh.cnt2[0] + sh.cnt2[1] + sh.cnt2[2] + sh.cnt2[3];
             if (m <= kCandCap) {
+#pragma unroll
+                for (int k = 0; k < kRegKeys; ++k)
+                    if (bin[k] <= beta) sh.cand[off++] = ck[k];
+                __syncthreads();
                 // exact rank among the candidates; the kk best are selected
                 for (int i = tid; i < m; i += kThreads) {
                     const unsigned long long ci = sh.cand[i];
@@ -502,24 +590,15 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
                     if (b < X) keys[b] = (uint32_t)(ck[k] >> 32);
                 }
             }
-            if (m > kCandCap) goto radix_path;  // block-uniform (every thread read the same m)
         }
-        // mandatory blocks (or every block when K >= X); thread t owns ids 32t .. 32t+31
-        {
+        if (m <= kCandCap) {  // block-uniform
             __syncthreads();  // every selected bit is set
+            // thread t owns ids 32t .. 32t+31: selected, mandatory (or every block when K >= X)
             uint32_t word = sh.bitmap[tid];
-#pragma unroll
-            for (int bit = 0; bit < 32; ++bit) {
-                const int b = 32 * tid + bit;
-                if (b < X && (take_all || mandatory(b, X, a.n_sink, a.n_recent))) word |= 1u << bit;
-            }
+            if (take_all) word = range_bits(0, X, 32 * tid);
+            else word |= range_bits(0, sink, 32 * tid) | range_bits(rec_lo, X, 32 * tid);
             const int c = __popc(word);
-            int incl = c;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int o = __shfl_up(incl, off);
-                if (lane >= off) incl += o;
-            }
+            int incl = wave_incl_scan(c);
             if (lane == 63) sh.scan[wave] = incl;
             __syncthreads();
             int pos = incl - c, total = 0;
@@ -535,8 +614,9 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
             }
             for (int k = total + tid; k < K; k += kThreads) sel[k] = -1;
             if (tid == 0) a.n_sel[u] = min(total, K);
+            return;
         }
-        return;
+        goto radix_path;
     }
 
     // ---- general path (more than 8192 blocks): scores and their bits into the key array
@@ -552,7 +632,7 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
         for (int k = 0; k < NBATCH; ++k) {
             const int b = b0 + k * kThreads;
             if (b >= X) break;
-            const float* f = fac + (b / a.bpc) * G;
+            const float* f = fac + part_of(b) * G;
             float S = 0.0f;
 #pragma unroll
             for (int g = 0; g < G; ++g) S += f[g] * w[k][g];
@@ -668,15 +748,16 @@ radix_path:
 }
 
 size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
-    return ((size_t)2 * a.nchunks * g.G + (a.keys_in_lds ? (size_t)g.xmax() : 0)) * sizeof(float);
+    return ((size_t)2 * (a.nchunks + 1) * g.G + (a.keys_in_lds ? (size_t)g.xmax() : 0)) * sizeof(float);
 }
 
 template <int D, int G>
 hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
+    const dim3 grid(a.nchunks + 1, g.units());
     if (a.comp_part)
-        score_chunks_kernel<D, G, true><<<dim3(a.nchunks, g.units()), kThreads, 0, s>>>(g, a);
+        score_chunks_kernel<D, G, true><<<grid, kThreads, 0, s>>>(g, a);
     else
-        score_chunks_kernel<D, G, false><<<dim3(a.nchunks, g.units()), kThreads, 0, s>>>(g, a);
+        score_chunks_kernel<D, G, false><<<grid, kThreads, 0, s>>>(g, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     select_finalize_kernel<G><<<dim3(g.units()), kThreads, finalize_dyn_lds(g, a), s>>>(g, a);

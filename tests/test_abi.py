@@ -161,7 +161,7 @@ def test_decode_step_validation():
 
 
 def test_score_select_block_count_limit():
-    """Above 4096 * 128 / G blocks per unit the selection's partial merge does not fit: the call says
+    """Above 128 * (4096 / G - 1) blocks per unit the selection's partial merge does not fit: the call says
     so before enqueuing anything."""
     L = P.library()
     p = P.CompkvSelectParams(64, 1, 2, 0.088)
