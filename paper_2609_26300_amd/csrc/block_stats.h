@@ -1,132 +1,150 @@
-// block_stats.h -- the one-wave block summary routine shared by the prefill, the append and the fused
-// decode step (private to libcompkv). Every caller uses the same lane-to-row mapping and reduction
-// order, so a summary does not depend on which of them computed it.
+// block_stats.h -- the block summary routine shared by the prefill, the append and the fused decode
+// step (private to libcompkv). Every caller runs the same workgroup-wide routine, so a summary does not
+// depend on which of them computed it (Section 4.2: an appended block's summary equals a rebuild).
 #pragma once
 
 #include "internal.h"
 
 namespace compkv {
 
-// Sum the coordinates of group t (Appendix A.4) from a per-coordinate array in LDS.
-__device__ inline float group_sum(const float* m2, int t, int D, int r, int layout) {
-    float s = 0.0f;
-    if (r == D) return m2[t];
-    const int w = (D / 2) / r;  // frequency pairs per group
-    if (layout == 0) {          // rotate-half: pair f = (f, f + D/2)
-        for (int f = t * w; f < (t + 1) * w; ++f) s += m2[f] + m2[f + D / 2];
-    } else {  // interleaved: pair f = (2f, 2f + 1)
-        for (int i = 2 * t * w; i < 2 * (t + 1) * w; ++i) s += m2[i];
-    }
-    return s;
-}
-
-// Summary of one block of nb rows (row j at Kb + j*D). Row new_j (if >= 0) is read from k_new / v_new
-// instead of the cache. m2s: D floats of LDS private to this wave. km_lds / dv_lds / vm_lds (optional)
-// receive a copy of the result in LDS. Called by whole waves; every wave
-// of the workgroup must reach the trailing __syncthreads() the same number of times.
 template <int D>
-__device__ inline void wave_block_stats(const uint16_t* __restrict__ Kb, const uint16_t* __restrict__ Vb, int nb,
-                                 const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
-                                 int new_j, int r, int layout, float* __restrict__ km_out,
-                                 float* __restrict__ dv_out, float* __restrict__ vm_out, float* m2s,
-                                 bool active, float* km_lds = nullptr, float* dv_lds = nullptr,
-                                 float* vm_lds = nullptr) {
+struct BlockStatsLds {
+    float part[4][2][D];  // per-wave partial sums (key, value), later (squared deviations)
+    alignas(16) float km[D];
+    alignas(16) float vm[D];
+    float dv[D];
+};
+
+// Summary of one block of nb >= 1 rows (row j at Kb + j*D; row new_j, if >= 0, is read from k_new /
+// v_new instead of the cache): mean key, mean value and the r grouped population variances of
+// Section 4.1 (Appendix A.4 groups). Called by all four waves of the workgroup with uniform arguments.
+//
+// A row of d bf16 is d/8 lanes x 16 bytes; a wave covers 64/(d/8) rows per load step and the workgroup
+// four times that. Wave w takes rows 16s + 4w + (lane / 16) (for d = 128) of each step s, up to four
+// steps per batch with every load of a batch issued before use. Per-lane sums over the rows, then
+// cross-lane sums within the wave, then the four waves in a fixed order. Two passes (mean, then
+// squared deviations from the mean) keep the variance stable; a block of at most one batch per wave
+// (64 rows for d = 128) is still in registers for the second pass. On return the results are written
+// to km_out / vm_out / dv_out and their copies in L.km / L.vm / L.dv are visible to the workgroup.
+template <int D>
+__device__ void wg_block_stats(const uint16_t* __restrict__ Kb, const uint16_t* __restrict__ Vb, int nb,
+                               const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new, int new_j,
+                               int r, int layout, float* __restrict__ km_out, float* __restrict__ dv_out,
+                               float* __restrict__ vm_out, BlockStatsLds<D>& L) {
     constexpr int LPR = D / 8;     // lanes per row
-    constexpr int RPS = 64 / LPR;  // rows per load step
-    constexpr int NS = 8;          // load steps held in registers (32 rows for d = 128)
-    constexpr int BATCH = NS * RPS;
-    const int lane = threadIdx.x & 63;
+    constexpr int RPW = 64 / LPR;  // rows per wave step
+    constexpr int RPG = 4 * RPW;   // rows per workgroup step
+    constexpr int NS = 4;          // steps per batch held in registers
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int ro = lane / LPR, li = lane % LPR;
+    const int nsteps = (nb + RPG - 1) / RPG;
+    auto row_of = [&](int st) { return st * RPG + wave * RPW + ro; };
     auto krow = [&](int j) { return (j == new_j) ? k_new : Kb + (size_t)j * D; };
     auto vrow = [&](int j) { return (j == new_j) ? v_new : Vb + (size_t)j * D; };
-    float mk[8], mv[8], m2[8];
-    if (active) {
-        float sk[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        uint4 kw[NS];
-        for (int j0 = 0; j0 < nb; j0 += BATCH) {
-            uint4 vw[NS];
+
+    float sk[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    uint4 kw[NS];
+    for (int s0 = 0; s0 < nsteps; s0 += NS) {
+        uint4 vw[NS];
 #pragma unroll
-            for (int st = 0; st < NS; ++st) {  // every load of the batch before any use
-                const int j = j0 + st * RPS + ro;
-                kw[st] = j < nb ? *reinterpret_cast<const uint4*>(krow(j) + li * 8) : make_uint4(0, 0, 0, 0);
-                vw[st] = j < nb ? *reinterpret_cast<const uint4*>(vrow(j) + li * 8) : make_uint4(0, 0, 0, 0);
-            }
-#pragma unroll
-            for (int st = 0; st < NS; ++st) {
-                float kf[8], vf[8];
-                unpack_bf16x8(kw[st], kf);
-                unpack_bf16x8(vw[st], vf);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    sk[e] += kf[e];
-                    sv[e] += vf[e];
-                }
-            }
+        for (int st = 0; st < NS; ++st) {  // branch-free: a row past the block reloads row 0, unused
+            const int j = row_of(s0 + st);
+            const int jj = j < nb ? j : 0;
+            kw[st] = *reinterpret_cast<const uint4*>(krow(jj) + li * 8);
+            vw[st] = *reinterpret_cast<const uint4*>(vrow(jj) + li * 8);
         }
 #pragma unroll
-        for (int off = LPR; off < 64; off <<= 1)
+        for (int st = 0; st < NS; ++st) {
+            const bool ok = row_of(s0 + st) < nb;
+            float kf[8], vf[8];
+            unpack_bf16x8(kw[st], kf);
+            unpack_bf16x8(vw[st], vf);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                sk[e] += __shfl_xor(sk[e], off);
-                sv[e] += __shfl_xor(sv[e], off);
+                sk[e] += ok ? kf[e] : 0.0f;
+                sv[e] += ok ? vf[e] : 0.0f;
             }
-        const float fn = (float)nb;
+        }
+    }
+#pragma unroll
+    for (int off = LPR; off < 64; off <<= 1)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            mk[e] = sk[e] / fn;
-            mv[e] = sv[e] / fn;
-            m2[e] = 0.0f;
+            sk[e] = xor_add(sk[e], off);
+            sv[e] = xor_add(sv[e], off);
         }
-        // squared deviations; a block of one batch is still in registers
-        for (int j0 = 0; j0 < nb; j0 += BATCH) {
-            if (nb > BATCH) {
+    if (ro == 0) {
 #pragma unroll
-                for (int st = 0; st < NS; ++st) {
-                    const int j = j0 + st * RPS + ro;
-                    kw[st] = j < nb ? *reinterpret_cast<const uint4*>(krow(j) + li * 8) : make_uint4(0, 0, 0, 0);
-                }
-            }
-#pragma unroll
-            for (int st = 0; st < NS; ++st) {
-                if (j0 + st * RPS + ro >= nb) continue;
-                float kf[8];
-                unpack_bf16x8(kw[st], kf);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float dev = kf[e] - mk[e];
-                    m2[e] += dev * dev;
-                }
-            }
-        }
-#pragma unroll
-        for (int off = LPR; off < 64; off <<= 1)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) m2[e] += __shfl_xor(m2[e], off);
-        if (ro == 0) {
-            float4* kmo = reinterpret_cast<float4*>(km_out + li * 8);
-            float4* vmo = reinterpret_cast<float4*>(vm_out + li * 8);
-            kmo[0] = make_float4(mk[0], mk[1], mk[2], mk[3]);
-            kmo[1] = make_float4(mk[4], mk[5], mk[6], mk[7]);
-            vmo[0] = make_float4(mv[0], mv[1], mv[2], mv[3]);
-            vmo[1] = make_float4(mv[4], mv[5], mv[6], mv[7]);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) m2s[li * 8 + e] = m2[e];
-            if (km_lds) {  // optional LDS copy of the result for the caller's workgroup
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    km_lds[li * 8 + e] = mk[e];
-                    vm_lds[li * 8 + e] = mv[e];
-                }
-            }
+        for (int e = 0; e < 8; ++e) {
+            L.part[wave][0][li * 8 + e] = sk[e];
+            L.part[wave][1][li * 8 + e] = sv[e];
         }
     }
     __syncthreads();
-    if (active) {
-        const float denom = (float)nb * (float)(D / r);
-        for (int t = lane; t < r; t += 64) {
-            const float dv = group_sum(m2s, t, D, r, layout) / denom;
+    const float fn = (float)nb;
+    for (int i = tid; i < D; i += kThreads) {
+        const float mk = ((L.part[0][0][i] + L.part[1][0][i]) + (L.part[2][0][i] + L.part[3][0][i])) / fn;
+        const float mv = ((L.part[0][1][i] + L.part[1][1][i]) + (L.part[2][1][i] + L.part[3][1][i])) / fn;
+        L.km[i] = mk;
+        L.vm[i] = mv;
+        km_out[i] = mk;
+        vm_out[i] = mv;
+    }
+    __syncthreads();
+    float mk[8], m2[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        mk[e] = L.km[li * 8 + e];
+        m2[e] = 0.0f;
+    }
+    for (int s0 = 0; s0 < nsteps; s0 += NS) {
+        if (nsteps > NS) {  // larger blocks: reload this batch's keys (L1/L2 hits)
+#pragma unroll
+            for (int st = 0; st < NS; ++st) {
+                const int j = row_of(s0 + st);
+                kw[st] = *reinterpret_cast<const uint4*>(krow(j < nb ? j : 0) + li * 8);
+            }
+        }
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            const bool ok = row_of(s0 + st) < nb;
+            float kf[8];
+            unpack_bf16x8(kw[st], kf);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float dev = kf[e] - mk[e];
+                m2[e] += ok ? dev * dev : 0.0f;
+            }
+        }
+    }
+#pragma unroll
+    for (int off = LPR; off < 64; off <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m2[e] = xor_add(m2[e], off);
+    if (ro == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) L.part[wave][0][li * 8 + e] = m2[e];
+    }
+    __syncthreads();
+    auto m2_of = [&](int i) { return (L.part[0][0][i] + L.part[1][0][i]) + (L.part[2][0][i] + L.part[3][0][i]); };
+    if (r == D) {
+        for (int t = tid; t < D; t += kThreads) {
+            const float dv = m2_of(t) / fn;
+            L.dv[t] = dv;
             dv_out[t] = dv;
-            if (dv_lds) dv_lds[t] = dv;
+        }
+    } else if (wave == 0) {
+        // group t = a run of (d/2)/r consecutive frequency pairs (Appendix A.4); lane f holds pair f
+        const bool in = lane < D / 2;
+        const int f = in ? lane : 0;
+        const int ia = layout == 0 ? f : 2 * f, ib = layout == 0 ? f + D / 2 : 2 * f + 1;
+        float e = in ? m2_of(ia) + m2_of(ib) : 0.0f;
+        const int w = (D / 2) / r;
+        for (int off = 1; off < w; off <<= 1) e = xor_add(e, off);
+        if (in && lane % w == 0) {
+            const float dv = e / (fn * (float)(D / r));
+            L.dv[lane / w] = dv;
+            dv_out[lane / w] = dv;
         }
     }
     __syncthreads();

@@ -38,33 +38,62 @@ namespace compkv {
 namespace {
 
 constexpr int kBpcMax = 128;  // blocks per chunk, upper bound
-constexpr int kPMax = kBpcMax / 32;
 constexpr int kHistBins = 2048;
 constexpr size_t kDynBudget = 32768;  // dynamic LDS of the finalize launch
 
-// s^2 Q_{g,t} (Appendix A.4: the scaled query's squared coordinates summed over coordinate group t) for
-// the heads g = wave, wave + 4, ..., into Qv[g][t]. Lane f takes frequency pair f; a group is a run of
-// (d/2)/r consecutive pairs, summed by butterflies. With r == d every coordinate is its own group.
+// The query enters through frequency pairs (Appendix A.4): lane f of wave w holds pair f of heads
+// g = w, w + 4, ... (coordinates f, f + d/2 for rotate-half; 2f, 2f + 1 interleaved). The loads are
+// issued before the summaries' so that waiting for them never waits for the summaries.
 template <int D, int G>
-__device__ void group_query_energy(const uint16_t* qh, float s, int r, int layout, float (*Qv)[D]) {
+struct QueryPairs {
+    static constexpr int J = (G + 3) / 4;
+    uint16_t xa[J], xb[J];
+};
+
+__device__ __forceinline__ int pair_a(int f, int layout) { return layout == 0 ? f : 2 * f; }
+__device__ __forceinline__ int pair_b(int f, int layout, int D) { return layout == 0 ? f + D / 2 : 2 * f + 1; }
+
+template <int D, int G>
+__device__ __forceinline__ void load_query_pairs(const uint16_t* qh, int layout, QueryPairs<D, G>& qp) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int g = wave; g < G; g += 4) {
-        const uint16_t* qg = qh + g * D;
+    const int f = lane < D / 2 ? lane : 0;
+#pragma unroll
+    for (int j = 0; j < QueryPairs<D, G>::J; ++j) {
+        const int g = wave + 4 * j < G ? wave + 4 * j : 0;  // branch-free: unused when past G
+        qp.xa[j] = qh[g * D + pair_a(f, layout)];
+        qp.xb[j] = qh[g * D + pair_b(f, layout, D)];
+    }
+}
+
+// From the loaded pairs: the scaled query s q into q (nullable) and s^2 Q_{g,t} -- the squared scaled
+// coordinates summed over group t -- into Qv[g][t]. A group is a run of (d/2)/r consecutive pairs,
+// summed by butterflies; with r == d every coordinate is its own group.
+template <int D, int G>
+__device__ __forceinline__ void store_query(const QueryPairs<D, G>& qp, float s, int r, int layout, float (*q)[D],
+                                            float (*Qv)[D]) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const bool in = lane < D / 2;
+    const int ia = pair_a(in ? lane : 0, layout), ib = pair_b(in ? lane : 0, layout, D);
+#pragma unroll
+    for (int j = 0; j < QueryPairs<D, G>::J; ++j) {
+        const int g = wave + 4 * j;
+        if (g >= G) break;  // wave-uniform
+        const float xa = s * bf16_at(&qp.xa[j]), xb = s * bf16_at(&qp.xb[j]);
+        if (q && in) {
+            q[g][ia] = xa;
+            q[g][ib] = xb;
+        }
         if (r == D) {
-            for (int i = lane; i < D; i += 64) {
-                const float x = s * bf16_at(qg + i);
-                Qv[g][i] = x * x;
+            if (in) {
+                Qv[g][ia] = xa * xa;
+                Qv[g][ib] = xb * xb;
             }
             continue;
         }
-        const int f = lane < D / 2 ? lane : 0;
-        const int ia = layout == 0 ? f : 2 * f;
-        const int ib = layout == 0 ? f + D / 2 : 2 * f + 1;
-        const float xa = s * bf16_at(qg + ia), xb = s * bf16_at(qg + ib);
-        float e = lane < D / 2 ? xa * xa + xb * xb : 0.0f;
+        float e = in ? xa * xa + xb * xb : 0.0f;
         const int w = (D / 2) / r;
         for (int off = 1; off < w; off <<= 1) e = xor_add(e, off);
-        if (lane < D / 2 && lane % w == 0) Qv[g][lane / w] = e;
+        if (in && lane % w == 0) Qv[g][lane / w] = e;
     }
 }
 
@@ -89,9 +118,8 @@ struct NoComp {};
 
 template <int D, int G>
 struct TailShared {
-    alignas(16) float km[D];
-    alignas(16) float vm[D];
-    float dv[D], m2s[D];
+    BlockStatsLds<D> bs;  // the last block's summary (km, vm, dv)
+    float q[G][D];
     float Qv[G][D];
     float z[G], v[G];
 };
@@ -104,7 +132,9 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a) {
     const int u = blockIdx.y, bseq = u / geo.hkv, h = u % geo.hkv;
     const int nc = a.nchunks;
     const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
-    group_query_energy<D, G>(qh, a.scale, geo.r, geo.layout, ts.Qv);
+    QueryPairs<D, G> qp;
+    load_query_pairs<D, G>(qh, geo.layout, qp);
+    store_query<D, G>(qp, a.scale, geo.r, geo.layout, ts.q, ts.Qv);
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* pp = a.ws_part + ((size_t)u * (nc + 1) + nc) * G * 2;
@@ -131,22 +161,20 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a) {
             }
         }
         const size_t row0 = (size_t)u * geo.cap + (size_t)b * geo.B;
-        wave_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, kn, vn, nb - 1, geo.r, geo.layout,
-                            a.kmean_w + blk * D, a.dvar_w + blk * geo.r, a.vmean + blk * D, ts.m2s, wave == 0,
-                            ts.km, ts.dv, ts.vm);
+        wg_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, kn, vn, nb - 1, geo.r, geo.layout,
+                          a.kmean_w + blk * D, a.dvar_w + blk * geo.r, a.vmean + blk * D, ts.bs);
     } else {
         for (int i = tid; i < D; i += kThreads) {
-            ts.km[i] = a.kmean[blk * D + i];
-            if constexpr (kStep) ts.vm[i] = a.vmean[blk * D + i];
+            ts.bs.km[i] = a.kmean[blk * D + i];
+            if constexpr (kStep) ts.bs.vm[i] = a.vmean[blk * D + i];
         }
-        for (int t = tid; t < geo.r; t += kThreads) ts.dv[t] = a.dvar[blk * geo.r + t];
+        for (int t = tid; t < geo.r; t += kThreads) ts.bs.dv[t] = a.dvar[blk * geo.r + t];
         __syncthreads();
     }
-    const float s = a.scale;
     for (int g = wave; g < G; g += 4) {
         float z = 0.0f, v = 0.0f;
-        for (int i = lane; i < D; i += 64) z += (s * bf16_at(qh + g * D + i)) * ts.km[i];
-        for (int t = lane; t < geo.r; t += 64) v += ts.Qv[g][t] * ts.dv[t];
+        for (int i = lane; i < D; i += 64) z += ts.q[g][i] * ts.bs.km[i];
+        for (int t = lane; t < geo.r; t += 64) v += ts.Qv[g][t] * ts.bs.dv[t];
         z = wave_sum(z);
         v = wave_sum(v);
         if (lane == 0) {
@@ -171,12 +199,13 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a) {
                 p[0] = lnb + ts.z[g];
                 p[1] = 1.0f;
             }
-            p[2 + i] = ts.vm[i];
+            p[2 + i] = ts.bs.vm[i];
         }
     }
 }
 
-template <int D, int G, bool kStep>
+// PMAX = bpc / 32: block slots per thread (the chunk is 32 PMAX blocks).
+template <int D, int G, bool kStep, int PMAX>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
     if (blockIdx.x == (unsigned)a.nchunks) {
         score_tail<D, G, kStep>(geo, a);
@@ -185,7 +214,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     constexpr int NF4 = D / 32;           // float4 of the mean-key row per lane
     constexpr int LPB = D / 4;            // compensation: lanes per mean-value row (one float4 each)
     constexpr int RPS = kThreads / LPB;   // mean-value rows per workgroup step
-    constexpr int VROWS = kStep ? kBpcMax / RPS : 1;
+    constexpr int VROWS = kStep ? 32 * PMAX / RPS : 1;
     __shared__ ChunkShared<D, G> sh;
     __shared__ std::conditional_t<kStep, CompShared<D, G>, NoComp> st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -194,18 +223,22 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const int xmax = geo.xmax();
     const float s = a.scale;
     const int chunk0 = chunk * a.bpc;
-    const int P = a.bpc / 32;
     const int li = tid & 7, grp = tid >> 3;
     const int vli = tid % LPB, vslot = tid / LPB;
 
-    // issue the summary loads of this thread's blocks first (branch-free: a block id past the
-    // allocated range loads block 0 of the unit; masked below once the length is known)
-    float4 kv[kPMax][NF4];
-    float dv0[kPMax];
+    // loads in the order of their use: query pairs, then per slot the mean key and first variance
+    // group, then the mean values. Block ids past the allocated range load block 0 of the unit; values
+    // of blocks that turn out invalid are never used (every result below is selected by validity).
+    const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+    QueryPairs<D, G> qp;
+    load_query_pairs<D, G>(qh, geo.layout, qp);
+    __asm__ volatile("" ::: "memory");  // keep the query loads ahead of the summary loads
+    float4 kv[PMAX][NF4];
+    float dv0[PMAX];
 #pragma unroll
-    for (int p = 0; p < kPMax; ++p) {
+    for (int p = 0; p < PMAX; ++p) {
         const int b = chunk0 + p * 32 + grp;
-        const size_t blk = (size_t)u * geo.xcap + ((p < P && b < xmax) ? b : 0);
+        const size_t blk = (size_t)u * geo.xcap + (b < xmax ? b : 0);
         const float4* kp = reinterpret_cast<const float4*>(a.kmean + blk * D);
 #pragma unroll
         for (int m = 0; m < NF4; ++m) kv[p][m] = kp[li + 8 * m];
@@ -216,29 +249,18 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         const float4* vm = reinterpret_cast<const float4*>(a.vmean + (size_t)u * geo.xcap * D) + vli;
 #pragma unroll
         for (int k = 0; k < VROWS; ++k) {
-            if (k * RPS >= a.bpc) break;
             const int b = chunk0 + vslot + k * RPS;
             vrow[k] = vm[(size_t)(b < xmax ? b : 0) * (D / 4)];
         }
     }
-    const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
-    for (int idx = tid; idx < G * D; idx += kThreads) sh.q[idx / D][idx % D] = s * bf16_at(qh + idx);
-    group_query_energy<D, G>(qh, s, geo.r, geo.layout, sh.Qv);
+    store_query<D, G>(qp, s, geo.r, geo.layout, sh.q, sh.Qv);
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     const int xs = X - 1;  // blocks [0, X - 1) are scored here; the last one by the extra workgroup
-#pragma unroll
-    for (int p = 0; p < kPMax; ++p) {
-        const bool valid = p < P && chunk0 + p * 32 + grp < xs;
-#pragma unroll
-        for (int m = 0; m < NF4; ++m) kv[p][m] = valid ? kv[p][m] : make_float4(0, 0, 0, 0);
-        dv0[p] = (valid && li < geo.r) ? dv0[p] : 0.0f;
-    }
     __syncthreads();
 
 #pragma unroll
-    for (int p = 0; p < kPMax; ++p) {
-        if (p >= P) break;
+    for (int p = 0; p < PMAX; ++p) {
         const int lb = p * 32 + grp;
         const int b = chunk0 + lb;
         const bool valid = b < xs;
@@ -346,7 +368,6 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
 #pragma unroll
         for (int k = 0; k < VROWS; ++k) {
             const int lb = vslot + k * RPS;
-            if (k * RPS >= a.bpc) break;
             if (lb < nvalid) {
 #pragma unroll
                 for (int g = 0; g < G; ++g) {
@@ -439,26 +460,34 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
     const float* wu = a.ws_w + (size_t)u * xmax * G;
     const bool fast = xmax <= kRegKeys * kThreads;
 
-    // score terms of the first blocks, requested before anything else (ids below xmax are allocated)
-    float w0[kPreKeys][G];
-    if (fast) {
-#pragma unroll
-        for (int k = 0; k < kPreKeys; ++k) {
-            const int b = tid + k * kThreads;
-            if (k * kThreads < xmax) load_terms<G>(wu, b < xmax ? b : 0, w0[k]);
-        }
-    }
     // ---- per-head log normalizer over every block, then each partial's factor exp(m_c - lse)
+    // Loads in the order of their use: the length, the partials, the first blocks' score terms.
+    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
     float* fac = dyn;
     float* sums = dyn + np * G;
     const float* pu = a.ws_part + (size_t)u * np * G * 2;
-    for (int idx = tid; idx < np * G; idx += kThreads) {
-        fac[idx] = pu[2 * idx];
-        sums[idx] = pu[2 * idx + 1];
+    const bool one_pass = np * G <= kThreads;  // usual case: one partial per thread
+    float2 pv = make_float2(0.0f, 0.0f);
+    if (one_pass && tid < np * G) pv = reinterpret_cast<const float2*>(pu)[tid];
+    __asm__ volatile("" ::: "memory");
+    float w0[kPreKeys][G];
+#pragma unroll
+    for (int k = 0; k < kPreKeys; ++k) {  // branch-free: ids past xmax load block 0, unused
+        const int b = tid + k * kThreads;
+        load_terms<G>(wu, b < xmax ? b : 0, w0[k]);
+    }
+    if (one_pass && tid < np * G) {
+        fac[tid] = pv.x;
+        sums[tid] = pv.y;
+    }
+    if (!one_pass) {
+        for (int idx = tid; idx < np * G; idx += kThreads) {
+            fac[idx] = pu[2 * idx];
+            sums[idx] = pu[2 * idx + 1];
+        }
     }
     sh.bitmap[tid] = 0u;
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
     __syncthreads();
     for (int g = wave; g < G; g += 4) {
         float m = -INFINITY;
@@ -751,13 +780,22 @@ size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
     return ((size_t)2 * (a.nchunks + 1) * g.G + (a.keys_in_lds ? (size_t)g.xmax() : 0)) * sizeof(float);
 }
 
+template <int D, int G, bool kStep>
+void launch_chunks(const Geom& g, const ScoreArgs& a, hipStream_t s) {
+    const dim3 grid(a.nchunks + 1, g.units());
+    switch (a.bpc / 32) {
+        case 1: score_chunks_kernel<D, G, kStep, 1><<<grid, kThreads, 0, s>>>(g, a); break;
+        case 2: score_chunks_kernel<D, G, kStep, 2><<<grid, kThreads, 0, s>>>(g, a); break;
+        default: score_chunks_kernel<D, G, kStep, 4><<<grid, kThreads, 0, s>>>(g, a); break;
+    }
+}
+
 template <int D, int G>
 hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
-    const dim3 grid(a.nchunks + 1, g.units());
     if (a.comp_part)
-        score_chunks_kernel<D, G, true><<<grid, kThreads, 0, s>>>(g, a);
+        launch_chunks<D, G, true>(g, a, s);
     else
-        score_chunks_kernel<D, G, false><<<grid, kThreads, 0, s>>>(g, a);
+        launch_chunks<D, G, false>(g, a, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     select_finalize_kernel<G><<<dim3(g.units()), kThreads, finalize_dyn_lds(g, a), s>>>(g, a);
@@ -781,7 +819,7 @@ int select_max_bpc() { return kBpcMax; }
 int select_max_chunk_heads() { return (int)(kDynBudget / (2 * sizeof(float))); }
 
 hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s) {
-    if (a.bpc % 32 != 0 || a.bpc > kBpcMax || a.bpc < 32) return hipErrorInvalidValue;
+    if (a.bpc != 32 && a.bpc != 64 && a.bpc != 128) return hipErrorInvalidValue;
     a.keys_in_lds = 0;
     a.keys_in_lds = finalize_dyn_lds(g, a) + (size_t)g.xmax() * sizeof(float) <= kDynBudget;
     if (finalize_dyn_lds(g, a) > kDynBudget) return hipErrorInvalidValue;
