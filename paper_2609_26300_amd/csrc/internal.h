@@ -188,11 +188,12 @@ __device__ __forceinline__ float xor_add(float x, int off) {
     }
 }
 
-// all-reduce over aligned groups of 8 lanes (two quad DPP exchanges, then a swizzle across quads)
-__device__ __forceinline__ float sum8(float x) {
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // xor 1
-    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // xor 2
-    x += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x101F));                    // xor 4
+// Sum over each aligned group of 8 lanes, valid in the group's first four lanes (xor 1 and xor 2 quad
+// permutes, then a row shift left by 4: lane i adds lane i + 4).
+__device__ __forceinline__ float sum8_lead(float x) {
+    x += dpp_f<0xB1>(x);
+    x += dpp_f<0x4E>(x);
+    x += dpp_f<0x104>(x);
     return x;
 }
 

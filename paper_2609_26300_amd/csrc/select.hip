@@ -227,8 +227,9 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const int vli = tid % LPB, vslot = tid / LPB;
 
     // loads in the order of their use: query pairs, then per slot the mean key and first variance
-    // group, then the mean values. Block ids past the allocated range load block 0 of the unit; values
-    // of blocks that turn out invalid are never used (every result below is selected by validity).
+    // group (the mean values follow once the keys are consumed, which halves the registers held).
+    // Block ids past the allocated range load block 0 of the unit; values of blocks that turn out
+    // invalid are never used (every result below is selected by validity).
     const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     QueryPairs<D, G> qp;
     load_query_pairs<D, G>(qh, geo.layout, qp);
@@ -245,59 +246,75 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         dv0[p] = a.dvar[blk * geo.r + min(li, geo.r - 1)];
     }
     float4 vrow[VROWS];
-    if constexpr (kStep) {
-        const float4* vm = reinterpret_cast<const float4*>(a.vmean + (size_t)u * geo.xcap * D) + vli;
-#pragma unroll
-        for (int k = 0; k < VROWS; ++k) {
-            const int b = chunk0 + vslot + k * RPS;
-            vrow[k] = vm[(size_t)(b < xmax ? b : 0) * (D / 4)];
-        }
-    }
     store_query<D, G>(qp, s, geo.r, geo.layout, sh.q, sh.Qv);
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     const int xs = X - 1;  // blocks [0, X - 1) are scored here; the last one by the extra workgroup
     __syncthreads();
 
+    // block-mean logits: the query slice a lane needs is the same for all its slots, so it is read
+    // from LDS once per pair of heads (and the slots' sums are formed in the order the loads arrive)
+    constexpr int GB = G < 2 ? G : 2;
+    float z[PMAX][G], v[PMAX][G];
+#pragma unroll
+    for (int g0 = 0; g0 < G; g0 += GB) {
+        float4 qq[GB][NF4];
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+            for (int m = 0; m < NF4; ++m) qq[gb][m] = *reinterpret_cast<const float4*>(&sh.q[g0 + gb][4 * (li + 8 * m)]);
+#pragma unroll
+        for (int p = 0; p < PMAX; ++p)
+#pragma unroll
+            for (int gb = 0; gb < GB; ++gb) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int m = 0; m < NF4; ++m)
+                    acc += qq[gb][m].x * kv[p][m].x + qq[gb][m].y * kv[p][m].y + qq[gb][m].z * kv[p][m].z +
+                           qq[gb][m].w * kv[p][m].w;
+                z[p][g0 + gb] = acc;
+            }
+    }
+    float qv[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) qv[g] = li < geo.r ? sh.Qv[g][li] : 0.0f;
 #pragma unroll
     for (int p = 0; p < PMAX; ++p) {
         const int lb = p * 32 + grp;
         const int b = chunk0 + lb;
         const bool valid = b < xs;
-        float z[G], v[G];
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            float acc = 0.0f;
-#pragma unroll
-            for (int m = 0; m < NF4; ++m) {
-                const float4 qq = *reinterpret_cast<const float4*>(&sh.q[g][4 * (li + 8 * m)]);
-                acc += qq.x * kv[p][m].x + qq.y * kv[p][m].y + qq.z * kv[p][m].z + qq.w * kv[p][m].w;
-            }
-            z[g] = acc;
-            v[g] = li < geo.r ? sh.Qv[g][li] * dv0[p] : 0.0f;
-        }
+        for (int g = 0; g < G; ++g) v[p][g] = qv[g] * dv0[p];
         if (geo.r > 8 && valid) {
             const size_t blk = (size_t)u * geo.xcap + b;
             for (int t = li + 8; t < geo.r; t += 8) {
                 const float dv = a.dvar[blk * geo.r + t];
 #pragma unroll
-                for (int g = 0; g < G; ++g) v[g] += sh.Qv[g][t] * dv;
+                for (int g = 0; g < G; ++g) v[p][g] += sh.Qv[g][t] * dv;
             }
         }
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-            z[g] = sum8(z[g]);
-            v[g] = sum8(v[g]);
+            z[p][g] = sum8_lead(z[p][g]);
+            v[p][g] = sum8_lead(v[p][g]);
         }
         if (li == 0) {
             const float lnb = valid ? logf((float)min(geo.B, n - b * geo.B)) : 0.0f;
 #pragma unroll
             for (int g = 0; g < G; ++g) {
-                sh.z[g][lb] = z[g];
-                sh.v[g][lb] = v[g];
-                sh.a[g][lb] = valid ? lnb + z[g] + 0.5f * v[g] : -INFINITY;
-                if constexpr (kStep) st.cw[g][lb] = valid ? lnb + z[g] : -INFINITY;  // pseudo-logit
+                sh.z[g][lb] = z[p][g];
+                sh.v[g][lb] = v[p][g];
+                sh.a[g][lb] = valid ? lnb + z[p][g] + 0.5f * v[p][g] : -INFINITY;
+                if constexpr (kStep) st.cw[g][lb] = valid ? lnb + z[p][g] : -INFINITY;  // pseudo-logit
             }
+        }
+    }
+    if constexpr (kStep) {  // mean-value rows, requested once the mean keys are consumed
+        const float4* vm = reinterpret_cast<const float4*>(a.vmean + (size_t)u * geo.xcap * D) + vli;
+#pragma unroll
+        for (int k = 0; k < VROWS; ++k) {
+            const int b = chunk0 + vslot + k * RPS;
+            vrow[k] = vm[(size_t)(b < xmax ? b : 0) * (D / 4)];
         }
     }
     __syncthreads();
