@@ -422,20 +422,20 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     }
 }
 
-constexpr int kRegKeys = 32;    // score keys one thread keeps in registers (fast path: xmax <= 8192)
-constexpr int kPreKeys = 8;     // of which the score terms are loaded before the normalizers are known
-constexpr int kCandCap = 1024;  // candidates ranked by brute force on the fast path
-constexpr int kHistTail = 255;  // distance bins counted on the fast path (bin 255 = everything farther)
+constexpr int kFinThreads = 1024;  // threads of the selection workgroup (one per unit)
+constexpr int kFinWaves = kFinThreads / 64;
+constexpr int kKeysPerThread = 8;  // fast path: up to 8192 keys in registers
+constexpr int kBitmapWords = kKeysPerThread * kFinThreads / 32;
+constexpr int kCandCap = 1024;     // candidates ranked by brute force on the fast path
+constexpr int kHistTail = 255;     // distance bins counted on the fast path (bin 255 = everything farther)
 
 struct FinalShared {
-    float lse[8];
     int hist[kHistBins];
-    int cnt[4], cnt2[4];
-    int scan[4];
-    int digit, above;
+    uint32_t wmax[kFinWaves];
+    int cnt[kFinWaves], cnt2[kFinWaves];
+    int digit, above, beta, ncand;
     unsigned long long cand[kCandCap];
-    uint32_t bitmap[kThreads];
-    int beta;
+    uint32_t bitmap[kBitmapWords];
 };
 
 // bits [lo, hi) of the 32-bit word holding ids base .. base + 31
@@ -465,48 +465,55 @@ __device__ __forceinline__ void load_terms(const float* wu, int b, float (&w)[G]
 }
 
 template <int G>
-__global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
-    constexpr int NBATCH = 8;  // blocks whose score terms one thread loads at once
+__global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
+    constexpr int FT = kFinThreads, NW = kFinWaves, KPT = kKeysPerThread;
     __shared__ FinalShared sh;
-    extern __shared__ float dyn[];  // [np][G] factors, [np][G] sums, then [xmax] score bits
+    extern __shared__ float dyn[];  // [np][G] partial maxima, then factors; [np][G] sums; [xmax] key bits
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = blockIdx.x;
     const int bseq = u / geo.hkv;
     const int xmax = geo.xmax();
     const int nc = a.nchunks, np = nc + 1;  // partial nc: the last block's
     const float* wu = a.ws_w + (size_t)u * xmax * G;
-    const bool fast = xmax <= kRegKeys * kThreads;
+    const bool fast = xmax <= KPT * FT;
 
-    // ---- per-head log normalizer over every block, then each partial's factor exp(m_c - lse)
-    // Loads in the order of their use: the length, the partials, the first blocks' score terms.
+    // ---- loads in the order of their use: the length, the partials, this thread's score terms
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* fac = dyn;
     float* sums = dyn + np * G;
-    const float* pu = a.ws_part + (size_t)u * np * G * 2;
-    const bool one_pass = np * G <= kThreads;  // usual case: one partial per thread
+    const float2* pu = reinterpret_cast<const float2*>(a.ws_part + (size_t)u * np * G * 2);
+    const bool one_pass = np * G <= FT;  // usual case: one partial per thread
     float2 pv = make_float2(0.0f, 0.0f);
-    if (one_pass && tid < np * G) pv = reinterpret_cast<const float2*>(pu)[tid];
+    if (one_pass && tid < np * G) pv = pu[tid];
     __asm__ volatile("" ::: "memory");
-    float w0[kPreKeys][G];
+    float w[KPT][G];
 #pragma unroll
-    for (int k = 0; k < kPreKeys; ++k) {  // branch-free: ids past xmax load block 0, unused
-        const int b = tid + k * kThreads;
-        load_terms<G>(wu, b < xmax ? b : 0, w0[k]);
+    for (int k = 0; k < KPT; ++k) {  // branch-free: ids past xmax load block 0, unused
+        const int b = tid + k * FT;
+        load_terms<G>(wu, b < xmax ? b : 0, w[k]);
     }
     if (one_pass && tid < np * G) {
         fac[tid] = pv.x;
         sums[tid] = pv.y;
     }
     if (!one_pass) {
-        for (int idx = tid; idx < np * G; idx += kThreads) {
-            fac[idx] = pu[2 * idx];
-            sums[idx] = pu[2 * idx + 1];
+        for (int idx = tid; idx < np * G; idx += FT) {
+            const float2 t = pu[idx];
+            fac[idx] = t.x;
+            sums[idx] = t.y;
         }
     }
-    sh.bitmap[tid] = 0u;
+    if (tid < kBitmapWords) sh.bitmap[tid] = 0u;
+    if (tid <= kHistTail) sh.hist[tid] = 0;
+    if (tid == 0) {
+        sh.beta = kHistTail;
+        sh.ncand = 0;
+    }
     __syncthreads();
-    for (int g = wave; g < G; g += 4) {
+    // ---- wave g: head g's log normalizer over every block, then each partial's factor exp(m_c - lse)
+    if (wave < G) {
+        const int g = wave;
         float m = -INFINITY;
         for (int c = lane; c < np; c += 64) m = fmaxf(m, fac[c * G + g]);
         m = wave_max(m);
@@ -515,13 +522,12 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
             const float pm = fac[c * G + g];
             if (pm != -INFINITY) l += sums[c * G + g] * expf(pm - m);
         }
-        l = wave_sum(l);
-        if (lane == 0) sh.lse[g] = m + logf(l);
-    }
-    __syncthreads();
-    for (int idx = tid; idx < np * G; idx += kThreads) {
-        const float pm = fac[idx];
-        fac[idx] = pm == -INFINITY ? 0.0f : expf(pm - sh.lse[idx % G]);
+        l = wave_sum(l);  // (every lane's reads above are complete)
+        const float lse = m + logf(l);
+        for (int c = lane; c < np; c += 64) {
+            const float pm = fac[c * G + g];
+            fac[c * G + g] = pm == -INFINITY ? 0.0f : expf(pm - lse);
+        }
     }
     __syncthreads();
 
@@ -531,99 +537,107 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
     const int rec_lo = max(X - a.n_recent, 0);
     const int n_mand = sink + (X - rec_lo) - max(0, sink - rec_lo);
     const int kk = take_all ? 0 : K - n_mand;  // >= 0: the host checks K >= n_sink + n_recent
+    const bool ranked = !take_all && kk > 0;
     int32_t* sel = a.sel + (size_t)u * K;
     uint32_t* keys = a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * np * G) : a.ws_key + (size_t)u * xmax;
-    auto part_of = [&](int b) { return b == X - 1 ? nc : b / a.bpc; };
+    auto score_of = [&](int b, const float (&wt)[G]) {
+        const float* f = fac + (b == X - 1 ? nc : b / a.bpc) * G;
+        float S = 0.0f;
+#pragma unroll
+        for (int g = 0; g < G; ++g) S += f[g] * wt[g];
+        return S;
+    };
 
     // ---- fast path. Block b's key is (bits of S_b) << 32 | ~b: unique, and ordered exactly like
-    // (S_b descending, b ascending). Thread t keeps the keys of blocks t + 256k in registers.
+    // (S_b descending, b ascending). Thread t keeps the keys of blocks t + 1024k in registers.
     if (fast) {
-        unsigned long long ck[kRegKeys];
-        auto make_key = [&](int b, const float (&w)[G]) -> unsigned long long {
-            if (b >= X) return 0ull;
-            const float* f = fac + part_of(b) * G;
-            float S = 0.0f;
-#pragma unroll
-            for (int g = 0; g < G; ++g) S += f[g] * w[g];
-            if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
-            if (mandatory(b, X, a.n_sink, a.n_recent)) return 0ull;
-            return ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
-        };
-#pragma unroll
-        for (int k = 0; k < kPreKeys; ++k) ck[k] = k * kThreads < xmax ? make_key(tid + k * kThreads, w0[k]) : 0ull;
-#pragma unroll
-        for (int k0 = kPreKeys; k0 < kRegKeys; k0 += NBATCH) {
-            if (k0 * kThreads >= xmax) {
-#pragma unroll
-                for (int k = 0; k < NBATCH; ++k) ck[k0 + k] = 0ull;
-                continue;
-            }
-            float w[NBATCH][G];
-#pragma unroll
-            for (int k = 0; k < NBATCH; ++k) {
-                const int b = tid + (k0 + k) * kThreads;
-                load_terms<G>(wu, b < xmax ? b : 0, w[k]);
-            }
-#pragma unroll
-            for (int k = 0; k < NBATCH; ++k) ck[k0 + k] = make_key(tid + (k0 + k) * kThreads, w[k]);
-        }
-        // histogram of the keys' distance below the largest score, in bins of 2^19 float ulps (1/16 of
-        // an octave); keys more than 255 bins below are not counted
+        unsigned long long ck[KPT];
         uint32_t mx = 0u;
 #pragma unroll
-        for (int k = 0; k < kRegKeys; ++k) mx = ck[k] ? max(mx, (uint32_t)(ck[k] >> 32)) : mx;
-        mx = wave_max_u32(mx);
-        if (lane == 0) sh.scan[wave] = (int)mx;
-        sh.hist[tid] = 0;
-        if (tid == 0) sh.beta = kHistTail;
-        __syncthreads();
+        for (int k = 0; k < KPT; ++k) {
+            const int b = tid + k * FT;
+            ck[k] = 0ull;
+            if (b < X) {
+                const float S = score_of(b, w[k]);
+                if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+                if (!mandatory(b, X, a.n_sink, a.n_recent)) {
+                    ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
+                    mx = max(mx, __float_as_uint(S));
+                }
+            }
+        }
         int m = 0;  // candidates ranked exactly
-        if (!take_all && kk > 0) {
-            const uint32_t smax = max(max((uint32_t)sh.scan[0], (uint32_t)sh.scan[1]),
-                                      max((uint32_t)sh.scan[2], (uint32_t)sh.scan[3]));
-            uint32_t bin[kRegKeys];
+        if (ranked) {
+            mx = wave_max_u32(mx);
+            if (lane == 0) sh.wmax[wave] = mx;
+            __syncthreads();
+            uint32_t smax = 0u;
 #pragma unroll
-            for (int k = 0; k < kRegKeys; ++k) {
+            for (int w2 = 0; w2 < NW; ++w2) smax = max(smax, sh.wmax[w2]);
+            // histogram of the keys' distance below the largest score, in bins of 2^19 float ulps (1/16
+            // of an octave); keys more than 255 bins below are not counted
+            uint32_t bin[KPT];
+#pragma unroll
+            for (int k = 0; k < KPT; ++k) {
                 const uint32_t bits = (uint32_t)(ck[k] >> 32);
                 bin[k] = ck[k] ? min((smax - bits) >> 19, (uint32_t)kHistTail) : 0xFFFFFFFFu;
                 if (bin[k] < (uint32_t)kHistTail) atomicAdd(&sh.hist[bin[k]], 1);
             }
             __syncthreads();
-            // inclusive prefix over bins (thread t holds bin t); the bin reaching kk holds the cut
-            const int c = sh.hist[tid];
-            int incl = wave_incl_scan(c);
-            if (lane == 63) sh.cnt[wave] = incl;
-            __syncthreads();
-            for (int w = 0; w < wave; ++w) incl += sh.cnt[w];
-            if (tid < kHistTail && incl - c < kk && incl >= kk) sh.beta = tid;
+            // wave 0: prefix over the counted bins (four per lane); the bin reaching kk holds the cut
+            if (wave == 0) {
+                int c[4], tot = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int bi = 4 * lane + e;
+                    c[e] = bi < kHistTail ? sh.hist[bi] : 0;
+                    tot += c[e];
+                }
+                int run = wave_incl_scan(tot) - tot;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (run < kk && run + c[e] >= kk) sh.beta = 4 * lane + e;
+                    run += c[e];
+                }
+            }
             __syncthreads();
             const uint32_t beta = (uint32_t)sh.beta;  // kHistTail: the cut lies below the counted range
-            // candidates: keys in the cut's bin or above, placed by a prefix sum of per-thread counts
+            // candidates: keys in the cut's bin or above; each wave reserves its slots with one atomic
             int mine = 0;
 #pragma unroll
-            for (int k = 0; k < kRegKeys; ++k) mine += bin[k] <= beta;
-            int off = wave_incl_scan(mine);
-            if (lane == 63) sh.cnt2[wave] = off;
-            __syncthreads();
-            off -= mine;
-            for (int w = 0; w < wave; ++w) off += sh.cnt2[w];
-            m = sh.cnt2[0] + sh.cnt2[1] + sh.cnt2[2] + sh.cnt2[3];
-            if (m <= kCandCap) {
+            for (int k = 0; k < KPT; ++k) mine += bin[k] <= beta;
+            const int incl = wave_incl_scan(mine);
+            int base = 0;
+            if (lane == 63) base = atomicAdd(&sh.ncand, incl);
+            int off = __builtin_amdgcn_readlane(base, 63) + incl - mine;
 #pragma unroll
-                for (int k = 0; k < kRegKeys; ++k)
-                    if (bin[k] <= beta) sh.cand[off++] = ck[k];
-                __syncthreads();
-                // exact rank among the candidates; the kk best are selected
-                for (int i = tid; i < m; i += kThreads) {
+            for (int k = 0; k < KPT; ++k) {
+                if (bin[k] <= beta) {
+                    if (off < kCandCap) sh.cand[off] = ck[k];
+                    ++off;
+                }
+            }
+            __syncthreads();
+            m = sh.ncand;
+            if (m <= kCandCap) {
+                // exact rank among the candidates (order-independent); the kk best are selected. With
+                // few candidates the four lanes of a quad share one.
+                const int share = m <= FT / 4 ? 4 : 1;
+                const int i = tid / share, part = tid % share;
+                if (i < m) {  // quad-uniform
                     const unsigned long long ci = sh.cand[i];
                     int r = 0;
-                    int j = 0;
-                    for (; j + 16 <= m; j += 16) {
+                    int j = part;
+                    for (; j + 7 * share < m; j += 8 * share) {
 #pragma unroll
-                        for (int e = 0; e < 16; ++e) r += sh.cand[j + e] > ci;
+                        for (int e = 0; e < 8; ++e) r += sh.cand[j + e * share] > ci;
                     }
-                    for (; j < m; ++j) r += sh.cand[j] > ci;
-                    if (r < kk) {
+                    for (; j < m; j += share) r += sh.cand[j] > ci;
+                    if (share == 4) {
+                        r += dpp_i<0xB1>(r, r);
+                        r += dpp_i<0x4E>(r, r);
+                    }
+                    if (part == 0 && r < kk) {
                         const uint32_t b = 0xFFFFFFFFu - (uint32_t)(ci & 0xFFFFFFFFull);
                         atomicOr(&sh.bitmap[b >> 5], 1u << (b & 31));
                     }
@@ -631,26 +645,29 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
             } else {
                 // too many ties around the threshold: keep the bits for the radix path below
 #pragma unroll
-                for (int k = 0; k < kRegKeys; ++k) {
-                    const int b = tid + k * kThreads;
+                for (int k = 0; k < KPT; ++k) {
+                    const int b = tid + k * FT;
                     if (b < X) keys[b] = (uint32_t)(ck[k] >> 32);
                 }
             }
+            __syncthreads();
         }
         if (m <= kCandCap) {  // block-uniform
-            __syncthreads();  // every selected bit is set
-            // thread t owns ids 32t .. 32t+31: selected, mandatory (or every block when K >= X)
-            uint32_t word = sh.bitmap[tid];
-            if (take_all) word = range_bits(0, X, 32 * tid);
-            else word |= range_bits(0, sink, 32 * tid) | range_bits(rec_lo, X, 32 * tid);
+            // thread t < 256 owns ids 32t .. 32t+31: selected, mandatory (or every block when K >= X)
+            uint32_t word = 0u;
+            if (tid < kBitmapWords) {
+                word = take_all ? range_bits(0, X, 32 * tid)
+                                : (sh.bitmap[tid] | range_bits(0, sink, 32 * tid) | range_bits(rec_lo, X, 32 * tid));
+            }
             const int c = __popc(word);
-            int incl = wave_incl_scan(c);
-            if (lane == 63) sh.scan[wave] = incl;
+            const int incl = wave_incl_scan(c);
+            if (lane == 63) sh.cnt[wave] = incl;
             __syncthreads();
             int pos = incl - c, total = 0;
-            for (int w = 0; w < 4; ++w) {
-                pos += w < wave ? sh.scan[w] : 0;
-                total += sh.scan[w];
+#pragma unroll
+            for (int w2 = 0; w2 < kBitmapWords / 64; ++w2) {
+                pos += w2 < wave ? sh.cnt[w2] : 0;
+                total += sh.cnt[w2];
             }
             while (word) {
                 const int bit = __ffs(word) - 1;
@@ -658,7 +675,7 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
                 if (pos < K) sel[pos] = 32 * tid + bit;
                 ++pos;
             }
-            for (int k = total + tid; k < K; k += kThreads) sel[k] = -1;
+            for (int k = total + tid; k < K; k += FT) sel[k] = -1;
             if (tid == 0) a.n_sel[u] = min(total, K);
             return;
         }
@@ -666,68 +683,56 @@ __global__ __launch_bounds__(kThreads) void select_finalize_kernel(Geom geo, Sco
     }
 
     // ---- general path (more than 8192 blocks): scores and their bits into the key array
-    for (int b0 = tid; b0 < X; b0 += NBATCH * kThreads) {
-        float w[NBATCH][G];
-#pragma unroll
-        for (int k = 0; k < NBATCH; ++k) {
-            const int b = b0 + k * kThreads;
-#pragma unroll
-            for (int g = 0; g < G; ++g) w[k][g] = b < X ? wu[(size_t)b * G + g] : 0.0f;
-        }
-#pragma unroll
-        for (int k = 0; k < NBATCH; ++k) {
-            const int b = b0 + k * kThreads;
-            if (b >= X) break;
-            const float* f = fac + part_of(b) * G;
-            float S = 0.0f;
-#pragma unroll
-            for (int g = 0; g < G; ++g) S += f[g] * w[k][g];
-            if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
-            keys[b] = __float_as_uint(S);
-        }
+    for (int b = tid; b < X; b += FT) {
+        float wt[G];
+        load_terms<G>(wu, b, wt);
+        const float S = score_of(b, wt);
+        if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+        keys[b] = __float_as_uint(S);
     }
 radix_path:
     __syncthreads();
 
     // ---- threshold of the Top-(K-|F|) among non-mandatory blocks (radix select on the score bits)
-    uint32_t thr = 0xFFFFFFFFu;                // keys above thr are taken; keys equal to thr up to need_eq
+    uint32_t thr = 0xFFFFFFFFu;  // keys above thr are taken; keys equal to thr up to need_eq
     int need_eq = 0;
-    if (!take_all && kk > 0) {
+    if (ranked) {
         uint32_t prefix = 0, pmask = 0;
         int remaining = kk;
 #pragma unroll
         for (int pass = 0; pass < 3; ++pass) {
             const int shft = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
             const uint32_t dmask = pass == 2 ? 0x3FFu : 0x7FFu;
-            for (int i = tid; i < kHistBins; i += kThreads) sh.hist[i] = 0;
+            for (int i = tid; i < kHistBins; i += FT) sh.hist[i] = 0;
             __syncthreads();
-            for (int b = tid; b < X; b += kThreads) {
+            for (int b = tid; b < X; b += FT) {
                 if (mandatory(b, X, a.n_sink, a.n_recent)) continue;
                 const uint32_t key = keys[b];
                 if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shft) & dmask], 1);
             }
             __syncthreads();
-            // suffix counts: thread t owns bins [8t, 8t + 8)
+            // suffix counts: thread t < 256 owns bins [8t, 8t + 8)
             int local = 0;
+            if (tid < kHistBins / 8) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) local += sh.hist[tid * 8 + e];
-            int incl = local;  // inclusive suffix sum within the wave (higher lanes own higher bins)
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int o = __shfl_down(incl, off);
-                if (lane + off < 64) incl += o;
+                for (int e = 0; e < 8; ++e) local += sh.hist[tid * 8 + e];
             }
-            if (lane == 0) sh.scan[wave] = incl;
+            const int pre = wave_incl_scan(local);
+            const int wtot = __builtin_amdgcn_readlane(pre, 63);
+            const int incl = wtot - pre + local;  // over this lane and the higher ones (higher bins)
+            if (lane == 0) sh.cnt[wave] = wtot;
             __syncthreads();
-            int cum = incl - local;
-            for (int w = wave + 1; w < 4; ++w) cum += sh.scan[w];
-            for (int e = 7; e >= 0; --e) {
-                const int c = sh.hist[tid * 8 + e];
-                if (cum < remaining && cum + c >= remaining) {
-                    sh.digit = tid * 8 + e;
-                    sh.above = cum;
+            if (tid < kHistBins / 8) {
+                int cum = incl - local;
+                for (int w2 = wave + 1; w2 < kHistBins / 8 / 64; ++w2) cum += sh.cnt[w2];
+                for (int e = 7; e >= 0; --e) {
+                    const int c = sh.hist[tid * 8 + e];
+                    if (cum < remaining && cum + c >= remaining) {
+                        sh.digit = tid * 8 + e;
+                        sh.above = cum;
+                    }
+                    cum += c;
                 }
-                cum += c;
             }
             __syncthreads();
             remaining -= sh.above;
@@ -740,9 +745,8 @@ radix_path:
     }
 
     // ---- mark and compact in ascending id order; wave w scans its own id segment
-    const int seg = ((X + 3) / 4 + 63) / 64 * 64;
+    const int seg = ((X + NW - 1) / NW + 63) / 64 * 64;
     const int s0 = min(X, wave * seg), s1 = min(X, s0 + seg);
-    const bool ranked = !take_all && kk > 0;
     int cnt_eq = 0;
     for (int base = s0; base < s1; base += 64) {
         const int b = base + lane;
@@ -752,7 +756,7 @@ radix_path:
     if (lane == 0) sh.cnt[wave] = cnt_eq;
     __syncthreads();
     int eq_run = 0;
-    for (int w = 0; w < wave; ++w) eq_run += sh.cnt[w];
+    for (int w2 = 0; w2 < wave; ++w2) eq_run += sh.cnt[w2];
     const int eq_before = eq_run;
     int cnt_take = 0;
     for (int base = s0; base < s1; base += 64) {
@@ -770,9 +774,9 @@ radix_path:
     if (lane == 0) sh.cnt2[wave] = cnt_take;
     __syncthreads();
     int pos = 0;
-    for (int w = 0; w < wave; ++w) pos += sh.cnt2[w];
+    for (int w2 = 0; w2 < wave; ++w2) pos += sh.cnt2[w2];
     int total = 0;
-    for (int w = 0; w < 4; ++w) total += sh.cnt2[w];
+    for (int w2 = 0; w2 < NW; ++w2) total += sh.cnt2[w2];
     eq_run = eq_before;
     for (int base = s0; base < s1; base += 64) {
         const int b = base + lane;
@@ -789,7 +793,7 @@ radix_path:
         if (take && p < K) sel[p] = b;
         pos += __popcll(tm);
     }
-    for (int k = total + tid; k < K; k += kThreads) sel[k] = -1;
+    for (int k = total + tid; k < K; k += FT) sel[k] = -1;
     if (tid == 0) a.n_sel[u] = min(total, K);
 }
 
@@ -815,7 +819,7 @@ hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
         launch_chunks<D, G, false>(g, a, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    select_finalize_kernel<G><<<dim3(g.units()), kThreads, finalize_dyn_lds(g, a), s>>>(g, a);
+    select_finalize_kernel<G><<<dim3(g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a);
     return hipGetLastError();
 }
 
