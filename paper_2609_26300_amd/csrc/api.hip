@@ -106,11 +106,10 @@ size_t dense_ws(const Geom& g) {
     return align_up((size_t)g.units() * sh.items * g.G * (g.D + 2) * sizeof(float));
 }
 
-// fused step: the score region, then [units][nchunks + 1 + 2 n_exact][G][D + 2] decode partials:
-// compensation of each chunk and of the last block, then each exact item's partial, then the
-// pseudo-terms each exact item subtracts
+// fused step: the score region, then [units][nchunks + 1 + n_exact][G][D + 2] decode partials:
+// compensation of each chunk and of the last block, then each exact item's partial
 int step_partials(const Geom& g, int K) {
-    return score_shape(g).nchunks + 1 + 2 * sparse_shape(g, K).n_exact;
+    return score_shape(g).nchunks + 1 + sparse_shape(g, K).n_exact;
 }
 
 size_t step_ws(const Geom& g, int K) {
@@ -371,7 +370,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.neg_pseudo = 1;
     e = compkv::launch_decode_items(g, d, sp.n_exact, s);
     if (e != hipSuccess) return COMPKV_EHIP;
-    return launch_status(compkv::launch_decode_merge(g, d, sc.nchunks + 1 + sp.n_exact, sp.n_exact, s));
+    return launch_status(compkv::launch_decode_merge(g, d, parts, s));
 }
 
 }  // extern "C"

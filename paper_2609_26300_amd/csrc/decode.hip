@@ -42,6 +42,8 @@ template <int D, int G>
 struct DecodeShared {
     float m[4][G], l[4][G];
     float acc[4][G][D];
+    float em[G], el[G];  // the exact item's merged state (fused step: before the pseudo-terms come off)
+    float ea[G][D];
     float w[G][kCbMax];  // compensation weights
     float M[G], L[G];
     unsigned char flag[kCbMax];
@@ -209,7 +211,8 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
     l += __shfl_xor(l, 32);
 }
 
-// Combine the four waves' exact states in LDS and write the item's partial.
+// Combine the four waves' exact states in LDS and write the item's partial (part), or keep it in
+// sh.em / sh.el / sh.ea when part is null.
 template <int D, int G>
 __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part) {
     constexpr int CPL = D / 16;
@@ -238,6 +241,14 @@ __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], Decod
             ll = ll * ca + sh.l[w][g] * cb;
             aa = aa * ca + sh.acc[w][g][i] * cb;
             mm = mn;
+        }
+        if (!part) {
+            if (i == 0) {
+                sh.em[g] = mm;
+                sh.el[g] = ll;
+            }
+            sh.ea[g][i] = aa;
+            continue;
         }
         float* p = part + (size_t)g * (D + 2);
         if (i == 0) {
@@ -352,9 +363,11 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
     }
 }
 
-// Pseudo-terms (logit log|b| + zbar_b, value vmean_b) of an exact item's selected blocks, written as
-// one partial that the merge subtracts: the fused step's chunks add the pseudo-terms of every block.
-// Their loads are issued before the exact tokens (PseudoPf) so their latency overlaps that work.
+// Fused step: the chunks add the pseudo-terms (logit log|b| + zbar_b, value vmean_b) of every block,
+// so an exact item subtracts those of its selected blocks from its own partial (the exact state in
+// sh.em / sh.el / sh.ea). By Jensen's inequality a block's pseudo-weight |b| exp(zbar_b) never exceeds
+// its exact weight sum_j exp(z_j), so the difference stays a sum of non-negative terms. The loads are
+// issued before the exact tokens (PseudoPf) so their latency overlaps that work.
 constexpr int kPfRows = 2;    // mean-value rows per thread prefetched
 constexpr int kPfLogits = 2;  // block logits per thread prefetched
 static_assert(kPfLogits == 2, "selected_pseudo picks the prefetched logits by hand");
@@ -461,12 +474,15 @@ __device__ void selected_pseudo(const DecodeArgs& a, const Geom& geo, int u, int
     __syncthreads();
     for (int idx = tid; idx < G * D; idx += kThreads) {
         const int g = idx / D, i = idx % D;
+        const float mm = sh.em[g], mp = sh.M[g];
+        // pseudo-logits never exceed log B + the exact maximum, so the factor stays finite
+        const float e = (mm == -INFINITY || mp == -INFINITY) ? 0.0f : __expf(mp - mm);
         float* p = part + (size_t)g * (D + 2);
         if (i == 0) {
-            p[0] = sh.M[g];
-            p[1] = sh.L[g];
+            p[0] = mm;
+            p[1] = sh.el[g] - e * sh.L[g];
         }
-        p[2 + i] = sh.acc[0][g][i] + sh.acc[1][g][i] + sh.acc[2][g][i] + sh.acc[3][g][i];
+        p[2 + i] = sh.ea[g][i] - e * (sh.acc[0][g][i] + sh.acc[1][g][i] + sh.acc[2][g][i] + sh.acc[3][g][i]);
     }
 }
 
@@ -508,48 +524,59 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
         PseudoPf pf;
         if (pseudo) pseudo_prefetch<D, G>(a, geo, u, X, tm.nblk, sh.sel, pf);
         exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh, a.scale, m, l, acc);
-        finish_exact<D, G>(m, l, acc, sh, part);
-        if (pseudo)
-            selected_pseudo<D, G>(a, geo, u, n, X, tm.nblk, pf, sh,
-                                  a.ws_part + ((size_t)u * a.part_count + a.part_base + a.n_exact + item) * G * (D + 2));
+        finish_exact<D, G>(m, l, acc, sh, pseudo ? nullptr : part);
+        if (pseudo) selected_pseudo<D, G>(a, geo, u, n, X, tm.nblk, pf, sh, part);
     } else {
         const int c0 = (item - a.n_exact) * a.cb;
         compensation<D, G>(a, geo, u, n, X, c0, min(c0 + a.cb, X), sh, part);
     }
 }
 
-// Merge of one (unit, query head): the item partials in item order, with every load issued well ahead.
-// grid = (units, G); thread (s, i) sums items s, s + S, ... for coordinate i, then the S partial sums
-// are added in LDS in a fixed order.
+// Merge of one (unit, query head): the item partials in item order. grid = (units, G); thread (s, i)
+// sums items s, s + S, ... for coordinate i, then the S partial sums are added in LDS in a fixed order.
+// The partial maxima/sums and this thread's first R partial values are all requested at the start,
+// so the usual merge costs one memory round trip.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, DecodeArgs a, int npos, int nneg) {
+__global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, DecodeArgs a, int nitems) {
     constexpr int S = kThreads / D;  // item subsets
-    constexpr int UNR = 16;
-    const int nitems = npos + nneg;
+    constexpr int R = 32;            // partial values per thread requested up front
+    constexpr int UNR = 16;          // later batches
     __shared__ float pm[kMaxPartials], pc[kMaxPartials];
     __shared__ float part_acc[S][D];
     __shared__ float sM, sL;
     const int tid = threadIdx.x, lane = tid & 63;
     const int u = blockIdx.x, g = blockIdx.y;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
-    const float* pu = a.ws_part + (size_t)u * a.part_count * G * (D + 2) + (size_t)g * (D + 2);
     const size_t stride = (size_t)G * (D + 2);
-    for (int it = tid; it < nitems; it += kThreads) {
-        pm[it] = pu[it * stride];
-        pc[it] = pu[it * stride + 1];
+    const float* pu = a.ws_part + (size_t)u * a.part_count * stride + (size_t)g * (D + 2);
+    const int i = tid % D, sub = tid / D;
+    const float* pi = pu + 2 + i;
+    const float2 mc = tid < nitems ? *reinterpret_cast<const float2*>(pu + tid * stride) : make_float2(0.0f, 0.0f);
+    float x[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {  // branch-free: past nitems reloads item 0, unused
+        const int it = sub + k * S;
+        x[k] = pi[(size_t)(it < nitems ? it : 0) * stride];
+    }
+    if (tid < nitems) {
+        pm[tid] = mc.x;
+        pc[tid] = mc.y;
+    }
+    for (int it = tid + kThreads; it < nitems; it += kThreads) {
+        const float2 t = *reinterpret_cast<const float2*>(pu + it * stride);
+        pm[it] = t.x;
+        pc[it] = t.y;
     }
     __syncthreads();
     if (tid < 64) {
-        // the max over the added partials bounds every subtracted one (they are terms of the added ones)
         float M = -INFINITY;
-        for (int it = lane; it < npos; it += 64) M = fmaxf(M, pm[it]);
+        for (int it = lane; it < nitems; it += 64) M = fmaxf(M, pm[it]);
         M = wave_max(M);
         float L = 0.0f;
         for (int it = lane; it < nitems; it += 64) {
-            float c = (pm[it] == -INFINITY) ? 0.0f : __expf(pm[it] - M);
-            if (it >= npos) c = -c;
+            const float c = (pm[it] == -INFINITY) ? 0.0f : __expf(pm[it] - M);
             L += c * pc[it];
-            pc[it] = c;  // from here on: the partial's signed rescale factor
+            pc[it] = c;  // from here on: the partial's rescale factor
         }
         L = wave_sum(L);
         if (lane == 0) {
@@ -558,20 +585,23 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, Decode
         }
     }
     __syncthreads();
-    const int i = tid % D, sub = tid / D;
-    const float* pi = pu + 2 + i;
     float A = 0.0f;
-    for (int it0 = sub; it0 < nitems; it0 += UNR * S) {
-        float x[UNR];
 #pragma unroll
-        for (int k = 0; k < UNR; ++k) {  // all loads of the batch first (branch-free), masked at the end
+    for (int k = 0; k < R; ++k) {
+        const int it = sub + k * S;
+        if (it < nitems) A += pc[it] * x[k];
+    }
+    for (int it0 = sub + R * S; it0 < nitems; it0 += UNR * S) {
+        float y[UNR];
+#pragma unroll
+        for (int k = 0; k < UNR; ++k) {
             const int it = it0 + k * S;
-            x[k] = pi[(size_t)(it < nitems ? it : 0) * stride];
+            y[k] = pi[(size_t)(it < nitems ? it : 0) * stride];
         }
 #pragma unroll
         for (int k = 0; k < UNR; ++k) {
             const int it = it0 + k * S;
-            if (it < nitems) A += pc[it] * x[k];
+            if (it < nitems) A += pc[it] * y[k];
         }
     }
     part_acc[sub][i] = A;
@@ -594,8 +624,8 @@ hipError_t items_g(const Geom& g, const DecodeArgs& a, int items, hipStream_t s)
 }
 
 template <int D, int G>
-hipError_t merge_g(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s) {
-    decode_merge_kernel<D, G><<<dim3(g.units(), G), kThreads, 0, s>>>(g, a, npos, nneg);
+hipError_t merge_g(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s) {
+    decode_merge_kernel<D, G><<<dim3(g.units(), G), kThreads, 0, s>>>(g, a, nitems);
     return hipGetLastError();
 }
 
@@ -611,12 +641,12 @@ hipError_t items_d(const Geom& g, const DecodeArgs& a, int items, hipStream_t s)
 }
 
 template <int D>
-hipError_t merge_d(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s) {
+hipError_t merge_d(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s) {
     switch (g.G) {
-        case 1: return merge_g<D, 1>(g, a, npos, nneg, s);
-        case 2: return merge_g<D, 2>(g, a, npos, nneg, s);
-        case 4: return merge_g<D, 4>(g, a, npos, nneg, s);
-        case 8: return merge_g<D, 8>(g, a, npos, nneg, s);
+        case 1: return merge_g<D, 1>(g, a, nitems, s);
+        case 2: return merge_g<D, 2>(g, a, nitems, s);
+        case 4: return merge_g<D, 4>(g, a, nitems, s);
+        case 8: return merge_g<D, 8>(g, a, nitems, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -629,15 +659,15 @@ int decode_max_cb() { return kCbMax; }
 int decode_max_eb() { return kMaxEb; }
 
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
-    if (items < 1 || a.part_base + items * (a.neg_pseudo ? 2 : 1) > a.part_count || a.part_count > kMaxPartials ||
+    if (items < 1 || a.part_base + items > a.part_count || a.part_count > kMaxPartials ||
         (!a.dense && (a.cb > kCbMax || a.eb > kMaxEb)))
         return hipErrorInvalidValue;
     return g.D == 128 ? items_d<128>(g, a, items, s) : items_d<64>(g, a, items, s);
 }
 
-hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s) {
-    if (npos < 1 || nneg < 0 || npos + nneg > a.part_count || a.part_count > kMaxPartials) return hipErrorInvalidValue;
-    return g.D == 128 ? merge_d<128>(g, a, npos, nneg, s) : merge_d<64>(g, a, npos, nneg, s);
+hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s) {
+    if (nitems < 1 || nitems > a.part_count || a.part_count > kMaxPartials) return hipErrorInvalidValue;
+    return g.D == 128 ? merge_d<128>(g, a, nitems, s) : merge_d<64>(g, a, nitems, s);
 }
 
 // A whole sparse or dense decode call: items, then the merge.
@@ -649,7 +679,7 @@ hipError_t launch_decode(const Geom& g, const DecodeArgs& a0, hipStream_t s) {
     a.neg_pseudo = 0;
     hipError_t e = launch_decode_items(g, a, items, s);
     if (e != hipSuccess) return e;
-    return launch_decode_merge(g, a, items, 0, s);
+    return launch_decode_merge(g, a, items, s);
 }
 
 }  // namespace compkv

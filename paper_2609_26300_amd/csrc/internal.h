@@ -82,8 +82,7 @@ struct DecodeArgs {
     float scale;
     int part_count;  // partials per unit in ws_part (row stride of the partial array)
     int part_base;   // partial index of this launch's item 0
-    int neg_pseudo;  // exact items also write, at part_base + n_exact + item, the pseudo-terms of their
-                     // selected blocks, which the merge subtracts (fused step)
+    int neg_pseudo;  // exact items subtract the pseudo-terms of their selected blocks (fused step)
 };
 
 // ------------------------------------------------------------------ launchers (one per kernel family)
@@ -99,7 +98,7 @@ int decode_max_cb();
 int decode_max_eb();
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s);
-hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int npos, int nneg, hipStream_t s);
+hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s);
 
 // ------------------------------------------------------------------ device helpers
 
