@@ -42,8 +42,7 @@ template <int D, int G>
 struct DecodeShared {
     float m[4][G], l[4][G];
     float acc[4][G][D];
-    float em[G], el[G];  // the exact item's merged state (fused step: before the pseudo-terms come off)
-    float ea[G][D];
+    float pa[G][D];  // fused step: the item's weighted pseudo-values (relative to sh.M)
     float w[G][kCbMax];  // compensation weights
     float M[G], L[G];
     unsigned char flag[kCbMax];
@@ -79,10 +78,12 @@ struct TokenMap {
 
 // Exact tokens of one item with MFMA. Leaves this wave's (m, l) for head lane%16 (lanes with the same
 // lane%16 agree) and acc[j][i] = sum over the wave's tokens of p * v for head 4(lane/16)+i at
-// coordinate (D/16)*(lane%16) + j.
-template <int D, int G>
+// coordinate (D/16)*(lane%16) + j. `mid` is workgroup-wide work (every wave calls it once) run while
+// the first round's loads are in flight.
+template <int D, int G, typename Mid>
 __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku, const uint16_t* __restrict__ Vu,
-                             const uint16_t* __restrict__ qh, float scale, float& m, float& l, v4f32 (&acc)[D / 16]) {
+                             const uint16_t* __restrict__ qh, float scale, float& m, float& l, v4f32 (&acc)[D / 16],
+                             Mid&& mid) {
     constexpr int KS = D / 32;   // k-steps of the logit MFMA
     constexpr int CPL = D / 16;  // value coordinates per lane (= output blocks)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -100,13 +101,13 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
 #pragma unroll
     for (int j = 0; j < CPL; ++j) acc[j] = v4f32{0.0f, 0.0f, 0.0f, 0.0f};
     const int ntiles = (tm.count() + 15) / 16;
-    for (int t0 = wave * kTilesPerRound; t0 < ntiles; t0 += 4 * kTilesPerRound) {
-        uint4 kreg[kTilesPerRound][KS];
-        uint4 vreg[kTilesPerRound][4];
-        bool vvalid[kTilesPerRound][4];
-        // issue every load of the round first
-        // (branch-free: a row past the item's tokens loads row 0 of the unit and is zeroed after)
-        bool kvalid[kTilesPerRound];
+    uint4 kreg[kTilesPerRound][KS];
+    uint4 vreg[kTilesPerRound][4];
+    bool vvalid[kTilesPerRound][4];
+    bool kvalid[kTilesPerRound];
+    // every load of a round is issued first (branch-free: a row past the item's tokens loads row 0 of
+    // the unit and is zeroed after)
+    auto issue = [&](int t0) {
 #pragma unroll
         for (int t = 0; t < kTilesPerRound; ++t) {
             const int base = (t0 + t) * 16;
@@ -128,6 +129,11 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
                 }
             }
         }
+    };
+    issue(wave * kTilesPerRound);
+    mid();
+    for (int t0 = wave * kTilesPerRound; t0 < ntiles; t0 += 4 * kTilesPerRound) {
+        if (t0 != wave * kTilesPerRound) issue(t0);
 #pragma unroll
         for (int t = 0; t < kTilesPerRound; ++t) {
 #pragma unroll
@@ -211,10 +217,11 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
     l += __shfl_xor(l, 32);
 }
 
-// Combine the four waves' exact states in LDS and write the item's partial (part), or keep it in
-// sh.em / sh.el / sh.ea when part is null.
+// Combine the four waves' exact states in LDS and write the item's partial. With `pseudo` (fused
+// step) the pseudo-terms of the item's selected blocks (sh.M, sh.L, sh.pa) come off first.
 template <int D, int G>
-__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part) {
+__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part,
+                             bool pseudo) {
     constexpr int CPL = D / 16;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -242,13 +249,12 @@ __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], Decod
             aa = aa * ca + sh.acc[w][g][i] * cb;
             mm = mn;
         }
-        if (!part) {
-            if (i == 0) {
-                sh.em[g] = mm;
-                sh.el[g] = ll;
-            }
-            sh.ea[g][i] = aa;
-            continue;
+        if (pseudo) {
+            // pseudo-logits never exceed log B + the exact maximum, so the factor stays finite
+            const float mp = sh.M[g];
+            const float e = (mm == -INFINITY || mp == -INFINITY) ? 0.0f : __expf(mp - mm);
+            ll -= e * sh.L[g];
+            aa -= e * sh.pa[g][i];
         }
         float* p = part + (size_t)g * (D + 2);
         if (i == 0) {
@@ -370,7 +376,7 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
 // issued before the exact tokens (PseudoPf) so their latency overlaps that work.
 constexpr int kPfRows = 2;    // mean-value rows per thread prefetched
 constexpr int kPfLogits = 2;  // block logits per thread prefetched
-static_assert(kPfLogits == 2, "selected_pseudo picks the prefetched logits by hand");
+static_assert(kPfLogits == 2, "pseudo_sums picks the prefetched logits by hand");
 
 struct PseudoPf {
     float4 v[kPfRows];
@@ -408,8 +414,8 @@ __device__ __forceinline__ void pseudo_prefetch(const DecodeArgs& a, const Geom&
 }
 
 template <int D, int G>
-__device__ void selected_pseudo(const DecodeArgs& a, const Geom& geo, int u, int n, int X, int nblk,
-                                const PseudoPf& pf, DecodeShared<D, G>& sh, float* part) {
+__device__ void pseudo_sums(const DecodeArgs& a, const Geom& geo, int u, int n, int X, int nblk, const PseudoPf& pf,
+                            DecodeShared<D, G>& sh) {
     constexpr int LPB = D / 4, RPS = kThreads / LPB;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int li = tid % LPB, slot = tid / LPB;
@@ -435,7 +441,7 @@ __device__ void selected_pseudo(const DecodeArgs& a, const Geom& geo, int u, int
             sh.L[g] = sum;
         }
     }
-    __syncthreads();  // also: finish_exact's reads of sh.acc are done
+    __syncthreads();
     float acc[G][4];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
@@ -474,16 +480,9 @@ __device__ void selected_pseudo(const DecodeArgs& a, const Geom& geo, int u, int
     __syncthreads();
     for (int idx = tid; idx < G * D; idx += kThreads) {
         const int g = idx / D, i = idx % D;
-        const float mm = sh.em[g], mp = sh.M[g];
-        // pseudo-logits never exceed log B + the exact maximum, so the factor stays finite
-        const float e = (mm == -INFINITY || mp == -INFINITY) ? 0.0f : __expf(mp - mm);
-        float* p = part + (size_t)g * (D + 2);
-        if (i == 0) {
-            p[0] = mm;
-            p[1] = sh.el[g] - e * sh.L[g];
-        }
-        p[2 + i] = sh.ea[g][i] - e * (sh.acc[0][g][i] + sh.acc[1][g][i] + sh.acc[2][g][i] + sh.acc[3][g][i]);
+        sh.pa[g][i] = (sh.acc[0][g][i] + sh.acc[1][g][i]) + (sh.acc[2][g][i] + sh.acc[3][g][i]);
     }
+    __syncthreads();
 }
 
 template <int D, int G>
@@ -523,9 +522,11 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
         const bool pseudo = a.neg_pseudo && !tm.dense;
         PseudoPf pf;
         if (pseudo) pseudo_prefetch<D, G>(a, geo, u, X, tm.nblk, sh.sel, pf);
-        exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh, a.scale, m, l, acc);
-        finish_exact<D, G>(m, l, acc, sh, pseudo ? nullptr : part);
-        if (pseudo) selected_pseudo<D, G>(a, geo, u, n, X, tm.nblk, pf, sh, part);
+        exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh, a.scale, m, l, acc,
+                           [&] {
+                               if (pseudo) pseudo_sums<D, G>(a, geo, u, n, X, tm.nblk, pf, sh);
+                           });
+        finish_exact<D, G>(m, l, acc, sh, part, pseudo);
     } else {
         const int c0 = (item - a.n_exact) * a.cb;
         compensation<D, G>(a, geo, u, n, X, c0, min(c0 + a.cb, X), sh, part);
