@@ -1,6 +1,6 @@
 // select.hip -- block scoring and Top-K selection (Sections 4.1, 4.2; Appendix E.1). Two launches.
 //
-// Launch 1, grid = (nchunks + 1, units). Chunk workgroups stream the fp32 summaries (mean key, grouped
+// Launch 1, grid = units * (nchunks + 1). Chunk workgroups stream the fp32 summaries (mean key, grouped
 // variances) of `bpc` consecutive blocks of one unit. Eight lanes share a block: lane i of the eight
 // reads float4 i, i+8, ... of the mean-key row (the eight lanes read 128 contiguous bytes per load) and
 // the variance groups t = i, i+8, .... Every load is issued first, before the sequence length is even
@@ -11,7 +11,8 @@
 // chunk's per-head (max m_c of a, sum of exp(a - m_c)), and per block the G terms
 // w_g = exp(a_g - m_c) sig2_g, stored contiguously so one vector load fetches a block's terms.
 // The last block of each unit (the one a decode step appends to) is scored by one extra workgroup per
-// unit (blockIdx.x == nchunks), which writes its own partial; the chunks skip it.
+// unit, which writes its own partial; the chunks skip it. The grid is one-dimensional with these
+// workgroups first (ids 0 .. units-1), so they are dispatched before any chunk.
 //
 // Fused decode step (kStep): the extra workgroup first stores the new row and recomputes the last
 // block's summary with the append's routine (bit-identical), so no chunk waits for it; every workgroup
@@ -126,15 +127,14 @@ struct TailShared {
 
 // The extra workgroup of unit u: the last block X - 1 (refreshed first when the step appends).
 template <int D, int G, bool kStep>
-__device__ void score_tail(const Geom& geo, const ScoreArgs& a) {
+__device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u) {
     __shared__ TailShared<D, G> ts;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int u = blockIdx.y, bseq = u / geo.hkv, h = u % geo.hkv;
+    const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int nc = a.nchunks;
     const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     QueryPairs<D, G> qp;
-    load_query_pairs<D, G>(qh, geo.layout, qp);
-    store_query<D, G>(qp, a.scale, geo.r, geo.layout, ts.q, ts.Qv);
+    load_query_pairs<D, G>(qh, geo.layout, qp);  // consumed only after the block's own loads are issued
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* pp = a.ws_part + ((size_t)u * (nc + 1) + nc) * G * 2;
@@ -150,27 +150,21 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a) {
     }
     const int b = X - 1, nb = n - b * geo.B;
     const size_t blk = (size_t)u * geo.xcap + b;
-    if (kStep && a.k_new) {
-        const uint16_t* kn = a.k_new + (size_t)u * D;
-        const uint16_t* vn = a.v_new + (size_t)u * D;
-        if (wave == 0) {
-            const size_t row = (size_t)u * geo.cap + (n - 1);
-            for (int i = lane; i < D / 8; i += 64) {
-                reinterpret_cast<uint4*>(a.Kc + row * D)[i] = reinterpret_cast<const uint4*>(kn)[i];
-                reinterpret_cast<uint4*>(a.Vc + row * D)[i] = reinterpret_cast<const uint4*>(vn)[i];
-            }
-        }
+    const bool append = kStep && a.k_new;
+    if (append) {  // the summary reads row n - 1 from k_new / v_new; the cache row is stored at the end
         const size_t row0 = (size_t)u * geo.cap + (size_t)b * geo.B;
-        wg_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, kn, vn, nb - 1, geo.r, geo.layout,
-                          a.kmean_w + blk * D, a.dvar_w + blk * geo.r, a.vmean + blk * D, ts.bs);
+        wg_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, a.k_new + (size_t)u * D, a.v_new + (size_t)u * D,
+                          nb - 1, geo.r, geo.layout, a.kmean_w + blk * D, a.dvar_w + blk * geo.r,
+                          a.vmean + blk * D, ts.bs);
     } else {
         for (int i = tid; i < D; i += kThreads) {
             ts.bs.km[i] = a.kmean[blk * D + i];
             if constexpr (kStep) ts.bs.vm[i] = a.vmean[blk * D + i];
         }
         for (int t = tid; t < geo.r; t += kThreads) ts.bs.dv[t] = a.dvar[blk * geo.r + t];
-        __syncthreads();
     }
+    store_query<D, G>(qp, a.scale, geo.r, geo.layout, ts.q, ts.Qv);
+    __syncthreads();
     for (int g = wave; g < G; g += 4) {
         float z = 0.0f, v = 0.0f;
         for (int i = lane; i < D; i += 64) z += ts.q[g][i] * ts.bs.km[i];
@@ -202,13 +196,23 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a) {
             p[2 + i] = ts.bs.vm[i];
         }
     }
+    if (append && wave == 0) {  // the new token's cache row
+        const size_t row = (size_t)u * geo.cap + (n - 1);
+        const uint4* kn = reinterpret_cast<const uint4*>(a.k_new + (size_t)u * D);
+        const uint4* vn = reinterpret_cast<const uint4*>(a.v_new + (size_t)u * D);
+        for (int i = lane; i < D / 8; i += 64) {
+            reinterpret_cast<uint4*>(a.Kc + row * D)[i] = kn[i];
+            reinterpret_cast<uint4*>(a.Vc + row * D)[i] = vn[i];
+        }
+    }
 }
 
 // PMAX = bpc / 32: block slots per thread (the chunk is 32 PMAX blocks).
 template <int D, int G, bool kStep, int PMAX>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
-    if (blockIdx.x == (unsigned)a.nchunks) {
-        score_tail<D, G, kStep>(geo, a);
+    const int units = geo.units();
+    if ((int)blockIdx.x < units) {
+        score_tail<D, G, kStep>(geo, a, blockIdx.x);
         return;
     }
     constexpr int NF4 = D / 32;           // float4 of the mean-key row per lane
@@ -218,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     __shared__ ChunkShared<D, G> sh;
     __shared__ std::conditional_t<kStep, CompShared<D, G>, NoComp> st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int u = blockIdx.y, chunk = blockIdx.x;
+    const int u = (blockIdx.x - units) / a.nchunks, chunk = (blockIdx.x - units) % a.nchunks;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int xmax = geo.xmax();
     const float s = a.scale;
@@ -803,7 +807,7 @@ size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
 
 template <int D, int G, bool kStep>
 void launch_chunks(const Geom& g, const ScoreArgs& a, hipStream_t s) {
-    const dim3 grid(a.nchunks + 1, g.units());
+    const dim3 grid((a.nchunks + 1) * g.units());
     switch (a.bpc / 32) {
         case 1: score_chunks_kernel<D, G, kStep, 1><<<grid, kThreads, 0, s>>>(g, a); break;
         case 2: score_chunks_kernel<D, G, kStep, 2><<<grid, kThreads, 0, s>>>(g, a); break;

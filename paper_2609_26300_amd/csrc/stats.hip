@@ -27,8 +27,8 @@ __global__ __launch_bounds__(kThreads) void build_stats_kernel(Geom g, StatsArgs
     }
 }
 
-// grid = (units): workgroup u stores the new row n = seq_lens (before the append) and recomputes
-// block n / B.
+// grid = (units): workgroup u recomputes block n / B with the new row n = seq_lens (before the append)
+// taken from k_new / v_new, then stores that row in the cache.
 template <int D>
 __global__ __launch_bounds__(kThreads) void append_stats_kernel(Geom g, StatsArgs a) {
     __shared__ BlockStatsLds<D> L;
@@ -40,17 +40,17 @@ __global__ __launch_bounds__(kThreads) void append_stats_kernel(Geom g, StatsArg
     const int nb = n - blk_id * g.B + 1;
     const uint16_t* kn = a.k_new + (size_t)u * D;
     const uint16_t* vn = a.v_new + (size_t)u * D;
-    if (wave == 0) {  // the cache row (the summary below reads it from k_new / v_new)
+    const size_t row0 = (size_t)u * g.cap + (size_t)blk_id * g.B;
+    const size_t blk = (size_t)u * g.xcap + blk_id;
+    wg_block_stats<D>(a.K + row0 * D, a.V + row0 * D, nb, kn, vn, nb - 1, g.r, g.layout, a.kmean + blk * D,
+                      a.dvar + blk * g.r, a.vmean + blk * D, L);
+    if (wave == 0) {  // the cache row (the summary above read it from k_new / v_new)
         const size_t row = (size_t)u * g.cap + n;
         for (int i = lane; i < D / 8; i += 64) {
             reinterpret_cast<uint4*>(a.K_out + row * D)[i] = reinterpret_cast<const uint4*>(kn)[i];
             reinterpret_cast<uint4*>(a.V_out + row * D)[i] = reinterpret_cast<const uint4*>(vn)[i];
         }
     }
-    const size_t row0 = (size_t)u * g.cap + (size_t)blk_id * g.B;
-    const size_t blk = (size_t)u * g.xcap + blk_id;
-    wg_block_stats<D>(a.K + row0 * D, a.V + row0 * D, nb, kn, vn, nb - 1, g.r, g.layout, a.kmean + blk * D,
-                      a.dvar + blk * g.r, a.vmean + blk * D, L);
 }
 
 }  // namespace
