@@ -37,8 +37,9 @@ def parse():
     ap.add_argument("--layers", type=int, default=0, help="resident layer copies (0: enough for > 1 GB)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--only", choices=["all", "sparse", "dense"], default="all",
-                    help="limit the timed work (for profiler runs)")
+    ap.add_argument("--only", choices=["all", "sparse", "dense", "fused"], default="all",
+                    help="limit the timed work (for profiler runs): sparse = fused step and separate calls, "
+                         "fused = the fused step alone")
     ap.add_argument("--eager", action="store_true",
                     help="launch kernels directly instead of replaying HIP graphs (for counter collection)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -254,11 +255,13 @@ def main():
         return t0.elapsed_time(t1) * 1e3 / steps, time.perf_counter() - wall0
 
     result = {}
-    if args.only in ("all", "sparse"):
+    if args.only in ("all", "sparse", "fused"):
         us, wall = run_steps([fused], args.steps, args.warmup)
-        us_sep, _ = run_steps([append, score, decode], args.steps, args.warmup)
-        per_k = {name: run_steps([f], args.steps, args.warmup)[0]
-                 for name, f in (("append_stats", append), ("score_select", score), ("sparse_decode", decode))}
+        us_sep, per_k = None, {}
+        if args.only != "fused":
+            us_sep, _ = run_steps([append, score, decode], args.steps, args.warmup)
+            per_k = {name: run_steps([f], args.steps, args.warmup)[0]
+                     for name, f in (("append_stats", append), ("score_select", score), ("sparse_decode", decode))}
         # leave the outputs of a complete step for the checks below
         fused(0)
         torch.cuda.synchronize()
@@ -298,7 +301,7 @@ def main():
             "hbm_gbps": round(ach, 1),
             "hbm_frac": round(ach / HBM_PEAK_GBPS, 4),
             "algorithmic_bytes_per_step": step_bytes,
-            "separate_calls_us_per_step": round(us_sep, 3),
+            "separate_calls_us_per_step": round(us_sep, 3) if us_sep is not None else None,
             "separate_call_us": {k: round(v, 3) for k, v in per_k.items()},
             # the timed call: its four dispatches (chunk scoring with the append and the compensation
             # stream, selection, exact tokens, merge) are the whole step
