@@ -26,39 +26,74 @@ struct BlockStatsLds {
 // squared deviations from the mean) keep the variance stable; a block of at most one batch per wave
 // (64 rows for d = 128) is still in registers for the second pass. On return the results are written
 // to km_out / vm_out / dv_out and their copies in L.km / L.vm / L.dv are visible to the workgroup.
+//
+// The first batch's loads are separate (BlockRows / load_block_rows) so that a caller can request the
+// next block's rows before computing the current one.
+constexpr int kStatsSteps = 4;  // load steps per batch held in registers
+
+struct BlockSrc {
+    const uint16_t* Kb;
+    const uint16_t* Vb;
+    const uint16_t* k_new;
+    const uint16_t* v_new;
+    int nb, new_j;
+};
+
+struct BlockRows {
+    uint4 kw[kStatsSteps], vw[kStatsSteps];
+};
+
 template <int D>
-__device__ void wg_block_stats(const uint16_t* __restrict__ Kb, const uint16_t* __restrict__ Vb, int nb,
-                               const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new, int new_j,
-                               int r, int layout, float* __restrict__ km_out, float* __restrict__ dv_out,
-                               float* __restrict__ vm_out, BlockStatsLds<D>& L) {
+__device__ __forceinline__ int stats_row(int st) {
+    constexpr int LPR = D / 8, RPW = 64 / LPR, RPG = 4 * RPW;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    return st * RPG + wave * RPW + lane / LPR;
+}
+
+template <int D>
+__device__ __forceinline__ const uint16_t* stats_krow(const BlockSrc& b, int j) {
+    return (j == b.new_j) ? b.k_new : b.Kb + (size_t)j * D;
+}
+template <int D>
+__device__ __forceinline__ const uint16_t* stats_vrow(const BlockSrc& b, int j) {
+    return (j == b.new_j) ? b.v_new : b.Vb + (size_t)j * D;
+}
+
+// rows of the batch starting at step s0 (branch-free: a row past the block reloads row 0, unused)
+template <int D>
+__device__ __forceinline__ void load_block_rows(const BlockSrc& b, int s0, BlockRows& R, bool values = true) {
+    const int li = (threadIdx.x & 63) % (D / 8);
+#pragma unroll
+    for (int st = 0; st < kStatsSteps; ++st) {
+        const int j = stats_row<D>(s0 + st);
+        const int jj = j < b.nb ? j : 0;
+        R.kw[st] = *reinterpret_cast<const uint4*>(stats_krow<D>(b, jj) + li * 8);
+        if (values) R.vw[st] = *reinterpret_cast<const uint4*>(stats_vrow<D>(b, jj) + li * 8);
+    }
+}
+
+// The summary from the rows of the first batch (already requested into R) and the rest of the block.
+template <int D>
+__device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int layout, float* __restrict__ km_out,
+                                 float* __restrict__ dv_out, float* __restrict__ vm_out, BlockStatsLds<D>& L) {
     constexpr int LPR = D / 8;     // lanes per row
     constexpr int RPW = 64 / LPR;  // rows per wave step
     constexpr int RPG = 4 * RPW;   // rows per workgroup step
-    constexpr int NS = 4;          // steps per batch held in registers
+    constexpr int NS = kStatsSteps;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int ro = lane / LPR, li = lane % LPR;
+    const int nb = b.nb;
     const int nsteps = (nb + RPG - 1) / RPG;
-    auto row_of = [&](int st) { return st * RPG + wave * RPW + ro; };
-    auto krow = [&](int j) { return (j == new_j) ? k_new : Kb + (size_t)j * D; };
-    auto vrow = [&](int j) { return (j == new_j) ? v_new : Vb + (size_t)j * D; };
 
     float sk[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    uint4 kw[NS];
     for (int s0 = 0; s0 < nsteps; s0 += NS) {
-        uint4 vw[NS];
-#pragma unroll
-        for (int st = 0; st < NS; ++st) {  // branch-free: a row past the block reloads row 0, unused
-            const int j = row_of(s0 + st);
-            const int jj = j < nb ? j : 0;
-            kw[st] = *reinterpret_cast<const uint4*>(krow(jj) + li * 8);
-            vw[st] = *reinterpret_cast<const uint4*>(vrow(jj) + li * 8);
-        }
+        if (s0 > 0) load_block_rows<D>(b, s0, R);
 #pragma unroll
         for (int st = 0; st < NS; ++st) {
-            const bool ok = row_of(s0 + st) < nb;
+            const bool ok = stats_row<D>(s0 + st) < nb;
             float kf[8], vf[8];
-            unpack_bf16x8(kw[st], kf);
-            unpack_bf16x8(vw[st], vf);
+            unpack_bf16x8(R.kw[st], kf);
+            unpack_bf16x8(R.vw[st], vf);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 sk[e] += ok ? kf[e] : 0.0f;
@@ -98,18 +133,12 @@ __device__ void wg_block_stats(const uint16_t* __restrict__ Kb, const uint16_t* 
         m2[e] = 0.0f;
     }
     for (int s0 = 0; s0 < nsteps; s0 += NS) {
-        if (nsteps > NS) {  // larger blocks: reload this batch's keys (L1/L2 hits)
-#pragma unroll
-            for (int st = 0; st < NS; ++st) {
-                const int j = row_of(s0 + st);
-                kw[st] = *reinterpret_cast<const uint4*>(krow(j < nb ? j : 0) + li * 8);
-            }
-        }
+        if (nsteps > NS) load_block_rows<D>(b, s0, R, false);  // larger blocks: reload (L1/L2 hits)
 #pragma unroll
         for (int st = 0; st < NS; ++st) {
-            const bool ok = row_of(s0 + st) < nb;
+            const bool ok = stats_row<D>(s0 + st) < nb;
             float kf[8];
-            unpack_bf16x8(kw[st], kf);
+            unpack_bf16x8(R.kw[st], kf);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float dev = kf[e] - mk[e];
@@ -148,6 +177,17 @@ __device__ void wg_block_stats(const uint16_t* __restrict__ Kb, const uint16_t* 
         }
     }
     __syncthreads();
+}
+
+template <int D>
+__device__ void wg_block_stats(const uint16_t* __restrict__ Kb, const uint16_t* __restrict__ Vb, int nb,
+                               const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new, int new_j,
+                               int r, int layout, float* __restrict__ km_out, float* __restrict__ dv_out,
+                               float* __restrict__ vm_out, BlockStatsLds<D>& L) {
+    const BlockSrc b{Kb, Vb, k_new, v_new, nb, new_j};
+    BlockRows R;
+    load_block_rows<D>(b, 0, R);
+    block_stats_from<D>(b, R, r, layout, km_out, dv_out, vm_out, L);
 }
 
 }  // namespace compkv

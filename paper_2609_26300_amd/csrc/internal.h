@@ -100,6 +100,22 @@ hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s);
 hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s);
 
+// Resident workgroups of `kern` (kThreads each) on the current device, cached per device.
+template <typename Kern>
+int resident_slots(Kern kern) {
+    constexpr int kMaxDev = 64;
+    static int cache[kMaxDev];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) dev = 0;
+    if (cache[dev] > 0) return cache[dev];
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kThreads, 0) != hipSuccess || per_cu < 1)
+        per_cu = 1;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 1;
+    cache[dev] = per_cu * cus;
+    return cache[dev];
+}
+
 // ------------------------------------------------------------------ device helpers
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

@@ -9,21 +9,46 @@
 namespace compkv {
 namespace {
 
-// Grid-stride over (unit, block); the workgroup summarizes one block per iteration.
+// Grid-stride over (unit, block); the workgroup summarizes one block per iteration and requests the
+// next block's rows before computing the current one.
 template <int D>
 __global__ __launch_bounds__(kThreads) void build_stats_kernel(Geom g, StatsArgs a) {
     __shared__ BlockStatsLds<D> L;
     const int xmax = g.xmax();
-    for (int flat = blockIdx.x; flat < xmax * g.units(); flat += gridDim.x) {
+    const int total = xmax * g.units();
+    struct Item {
+        BlockSrc src;
+        size_t blk;
+        bool valid;
+    };
+    auto item = [&](int flat) {
+        Item it{};
+        it.valid = false;
+        if (flat >= total) return it;
         const int u = flat / xmax, b = flat % xmax;
         const int n = clamp_len(a.seq_lens[u / g.hkv], g.max_seq);
-        const int X = (n + g.B - 1) / g.B;
-        if (b >= X) continue;  // workgroup-uniform
-        const int nb = min(g.B, n - b * g.B);
+        if (b >= (n + g.B - 1) / g.B) return it;
         const size_t row0 = (size_t)u * g.cap + (size_t)b * g.B;
-        const size_t blk = (size_t)u * g.xcap + b;
-        wg_block_stats<D>(a.K + row0 * D, a.V + row0 * D, nb, nullptr, nullptr, -1, g.r, g.layout,
-                          a.kmean + blk * D, a.dvar + blk * g.r, a.vmean + blk * D, L);
+        it.src = BlockSrc{a.K + row0 * D, a.V + row0 * D, nullptr, nullptr, min(g.B, n - b * g.B), -1};
+        it.blk = (size_t)u * g.xcap + b;
+        it.valid = true;
+        return it;
+    };
+    int flat = blockIdx.x;
+    Item cur = item(flat);
+    BlockRows rc;
+    if (cur.valid) load_block_rows<D>(cur.src, 0, rc);
+    while (flat < total) {  // workgroup-uniform
+        const int nf = flat + gridDim.x;
+        const Item nxt = item(nf);
+        BlockRows rn;
+        if (nxt.valid) load_block_rows<D>(nxt.src, 0, rn);
+        if (cur.valid)
+            block_stats_from<D>(cur.src, rc, g.r, g.layout, a.kmean + cur.blk * D, a.dvar + cur.blk * g.r,
+                                a.vmean + cur.blk * D, L);
+        cur = nxt;
+        rc = rn;
+        flat = nf;
     }
 }
 
@@ -55,13 +80,18 @@ __global__ __launch_bounds__(kThreads) void append_stats_kernel(Geom g, StatsArg
 
 }  // namespace
 
-hipError_t launch_build_stats(const Geom& g, const StatsArgs& a, hipStream_t s) {
+template <int D>
+void launch_build_d(const Geom& g, const StatsArgs& a, hipStream_t s) {
     const long long total = (long long)g.xmax() * g.units();
-    dim3 grid(total < 4096 ? (unsigned)total : 4096u);
+    const long long slots = resident_slots(build_stats_kernel<D>);  // one resident round, grid-stride
+    build_stats_kernel<D><<<dim3((unsigned)(total < slots ? total : slots)), kThreads, 0, s>>>(g, a);
+}
+
+hipError_t launch_build_stats(const Geom& g, const StatsArgs& a, hipStream_t s) {
     if (g.D == 128)
-        build_stats_kernel<128><<<grid, kThreads, 0, s>>>(g, a);
+        launch_build_d<128>(g, a, s);
     else
-        build_stats_kernel<64><<<grid, kThreads, 0, s>>>(g, a);
+        launch_build_d<64>(g, a, s);
     return hipGetLastError();
 }
 
