@@ -167,3 +167,29 @@ def test_step_graph_replays_match_eager():
         assert torch.equal(summ2.kmean, c.summ.kmean)
         c.dense_decode()  # unrelated eager work on the same workspace between replays
         torch.cuda.synchronize()
+
+
+def test_empty_sequence_in_batch():
+    """A sequence with no tokens has no blocks: nothing is selected, its output is zero and its lse is
+    -inf, in the separate calls and in the fused step (which appends nothing for it); the other
+    sequences of the batch are unaffected."""
+    c = Case(TINY.with_(batch=3, seed=33), seq_lens=[0, 700, 1500], max_seq_len=1500)
+    c.run_all()
+    for r in (dict(sel=c.sel, n_sel=c.n_sel, out=c.out, lse=c.lse), c.decode_step()):
+        torch.cuda.synchronize()
+        assert int(r["n_sel"][0].max()) == 0 and bool((r["sel"][0] == -1).all())
+        assert float(r["out"][0].abs().max()) == 0.0
+        assert bool(torch.isinf(r["lse"][0]).all()) and float(r["lse"][0].max()) < 0
+    # the non-empty sequences against the oracle
+    G = c.G
+    for b, h in c.units():
+        if b == 0:
+            continue
+        q, K, V, n = c.unit_inputs(b, h)
+        st = c.oracle_stats(b, h)
+        sc = c.oracle_scores(b, h, st)
+        for sel, nsel, out in ((c.sel, c.n_sel, c.out),):
+            s = _gpu(sel)[b, h, :int(_gpu(nsel)[b, h])]
+            check_selection(s, sc["score"], c.budget, c.n_sink, c.n_recent)
+            o, _ = oracle.sparse_decode(q, K, V, st[0], st[2], n, c.w.block_size, c.scale, s)
+            assert rel_err(_gpu(out)[b, h * G:(h + 1) * G], o, axis=1) <= TOL
