@@ -153,18 +153,22 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u) {
     const bool append = kStep && a.k_new;
     if (append) {  // the summary reads row n - 1 from k_new / v_new; the cache row is stored at the end
         const size_t row0 = (size_t)u * geo.cap + (size_t)b * geo.B;
-        wg_block_stats<D>(a.Kc + row0 * D, a.Vc + row0 * D, nb, a.k_new + (size_t)u * D, a.v_new + (size_t)u * D,
-                          nb - 1, geo.r, geo.layout, a.kmean_w + blk * D, a.dvar_w + blk * geo.r,
-                          a.vmean + blk * D, ts.bs);
+        const BlockSrc src{a.Kc + row0 * D, a.Vc + row0 * D, a.k_new + (size_t)u * D, a.v_new + (size_t)u * D, nb,
+                           nb - 1};
+        BlockRows rows;
+        load_block_rows<D>(src, 0, rows);
+        store_query<D, G>(qp, a.scale, geo.r, geo.layout, ts.q, ts.Qv);  // while the rows are in flight
+        block_stats_from<D>(src, rows, geo.r, geo.layout, a.kmean_w + blk * D, a.dvar_w + blk * geo.r,
+                            a.vmean + blk * D, ts.bs);  // (its barriers also publish ts.q / ts.Qv)
     } else {
         for (int i = tid; i < D; i += kThreads) {
             ts.bs.km[i] = a.kmean[blk * D + i];
             if constexpr (kStep) ts.bs.vm[i] = a.vmean[blk * D + i];
         }
         for (int t = tid; t < geo.r; t += kThreads) ts.bs.dv[t] = a.dvar[blk * geo.r + t];
+        store_query<D, G>(qp, a.scale, geo.r, geo.layout, ts.q, ts.Qv);
+        __syncthreads();
     }
-    store_query<D, G>(qp, a.scale, geo.r, geo.layout, ts.q, ts.Qv);
-    __syncthreads();
     for (int g = wave; g < G; g += 4) {
         float z = 0.0f, v = 0.0f;
         for (int i = lane; i < D; i += 64) z += ts.q[g][i] * ts.bs.km[i];
