@@ -472,233 +472,182 @@ __device__ __forceinline__ void load_terms(const float* wu, int b, float (&w)[G]
     }
 }
 
-template <int G>
-__global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
-    constexpr int FT = kFinThreads, NW = kFinWaves, KPT = kKeysPerThread;
-    __shared__ FinalShared sh;
-    extern __shared__ float dyn[];  // [np][G] partial maxima, then factors; [np][G] sums; [xmax] key bits
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int u = blockIdx.x;
-    const int bseq = u / geo.hkv;
-    const int xmax = geo.xmax();
-    const int nc = a.nchunks, np = nc + 1;  // partial nc: the last block's
-    const float* wu = a.ws_w + (size_t)u * xmax * G;
-    const bool fast = xmax <= KPT * FT;
+// Selection shared by the workgroups that rank one unit's blocks (kFinThreads threads, keys as in
+// select_finalize_kernel).
+struct SelectCtx {
+    int X, K, kk, sink, rec_lo, n_sink, n_recent;
+    bool take_all, ranked;
+    int32_t* sel;    // this unit's row of selected ids
+    int32_t* n_sel;  // this unit's count
+    uint32_t* keys;  // [X] score bits, for the radix path
+};
 
-    // ---- loads in the order of their use: the length, the partials, this thread's score terms
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
-    float* fac = dyn;
-    float* sums = dyn + np * G;
-    const float2* pu = reinterpret_cast<const float2*>(a.ws_part + (size_t)u * np * G * 2);
-    const bool one_pass = np * G <= FT;  // usual case: one partial per thread
-    float2 pv = make_float2(0.0f, 0.0f);
-    if (one_pass && tid < np * G) pv = pu[tid];
-    __asm__ volatile("" ::: "memory");
-    float w[KPT][G];
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {  // branch-free: ids past xmax load block 0, unused
-        const int b = tid + k * FT;
-        load_terms<G>(wu, b < xmax ? b : 0, w[k]);
-    }
-    if (one_pass && tid < np * G) {
-        fac[tid] = pv.x;
-        sums[tid] = pv.y;
-    }
-    if (!one_pass) {
-        for (int idx = tid; idx < np * G; idx += FT) {
-            const float2 t = pu[idx];
-            fac[idx] = t.x;
-            sums[idx] = t.y;
-        }
-    }
+__device__ inline SelectCtx make_select_ctx(int X, int K, int n_sink, int n_recent, int32_t* sel, int32_t* n_sel,
+                                            uint32_t* keys) {
+    SelectCtx c;
+    c.X = X;
+    c.K = K;
+    c.n_sink = n_sink;
+    c.n_recent = n_recent;
+    c.take_all = K >= X;
+    c.sink = min(n_sink, X);
+    c.rec_lo = max(X - n_recent, 0);
+    const int n_mand = c.sink + (X - c.rec_lo) - max(0, c.sink - c.rec_lo);
+    c.kk = c.take_all ? 0 : K - n_mand;  // >= 0: the host checks K >= n_sink + n_recent
+    c.ranked = !c.take_all && c.kk > 0;
+    c.sel = sel;
+    c.n_sel = n_sel;
+    c.keys = keys;
+    return c;
+}
+
+// before the first barrier that precedes select_fast
+__device__ inline void select_init(FinalShared& sh) {
+    const int tid = threadIdx.x;
     if (tid < kBitmapWords) sh.bitmap[tid] = 0u;
     if (tid <= kHistTail) sh.hist[tid] = 0;
     if (tid == 0) {
         sh.beta = kHistTail;
         sh.ncand = 0;
     }
-    __syncthreads();
-    // ---- wave g: head g's log normalizer over every block, then each partial's factor exp(m_c - lse)
-    if (wave < G) {
-        const int g = wave;
-        float m = -INFINITY;
-        for (int c = lane; c < np; c += 64) m = fmaxf(m, fac[c * G + g]);
-        m = wave_max(m);
-        float l = 0.0f;
-        for (int c = lane; c < np; c += 64) {
-            const float pm = fac[c * G + g];
-            if (pm != -INFINITY) l += sums[c * G + g] * expf(pm - m);
-        }
-        l = wave_sum(l);  // (every lane's reads above are complete)
-        const float lse = m + logf(l);
-        for (int c = lane; c < np; c += 64) {
-            const float pm = fac[c * G + g];
-            fac[c * G + g] = pm == -INFINITY ? 0.0f : expf(pm - lse);
-        }
-    }
-    __syncthreads();
+}
 
-    const int K = a.K;
-    const bool take_all = K >= X;
-    const int sink = min(a.n_sink, X);
-    const int rec_lo = max(X - a.n_recent, 0);
-    const int n_mand = sink + (X - rec_lo) - max(0, sink - rec_lo);
-    const int kk = take_all ? 0 : K - n_mand;  // >= 0: the host checks K >= n_sink + n_recent
-    const bool ranked = !take_all && kk > 0;
-    int32_t* sel = a.sel + (size_t)u * K;
-    uint32_t* keys = a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * np * G) : a.ws_key + (size_t)u * xmax;
-    auto score_of = [&](int b, const float (&wt)[G]) {
-        const float* f = fac + (b == X - 1 ? nc : b / a.bpc) * G;
-        float S = 0.0f;
+// Fast path: the keys ck (each non-zero key held by exactly one thread; zero = no key) and this
+// thread's largest score bits mx. Returns false when too many keys tie around the cut: their bits are
+// then in c.keys and select_radix finishes.
+template <int KPT>
+__device__ bool select_fast(const SelectCtx& ctx, const unsigned long long (&ck)[KPT], uint32_t mx, FinalShared& sh) {
+    constexpr int FT = kFinThreads, NW = kFinWaves;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int X = ctx.X, K = ctx.K, kk = ctx.kk, sink = ctx.sink, rec_lo = ctx.rec_lo;
+    const bool take_all = ctx.take_all, ranked = ctx.ranked;
+    int32_t* sel = ctx.sel;
+    uint32_t* keys = ctx.keys;
+    int m = 0;  // candidates ranked exactly
+    if (ranked) {
+        mx = wave_max_u32(mx);
+        if (lane == 0) sh.wmax[wave] = mx;
+        __syncthreads();
+        uint32_t smax = 0u;
 #pragma unroll
-        for (int g = 0; g < G; ++g) S += f[g] * wt[g];
-        return S;
-    };
-
-    // ---- fast path. Block b's key is (bits of S_b) << 32 | ~b: unique, and ordered exactly like
-    // (S_b descending, b ascending). Thread t keeps the keys of blocks t + 1024k in registers.
-    if (fast) {
-        unsigned long long ck[KPT];
-        uint32_t mx = 0u;
+        for (int w2 = 0; w2 < NW; ++w2) smax = max(smax, sh.wmax[w2]);
+        // histogram of the keys' distance below the largest score, in bins of 2^19 float ulps (1/16
+        // of an octave); keys more than 255 bins below are not counted
+        uint32_t bin[KPT];
 #pragma unroll
         for (int k = 0; k < KPT; ++k) {
-            const int b = tid + k * FT;
-            ck[k] = 0ull;
-            if (b < X) {
-                const float S = score_of(b, w[k]);
-                if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
-                if (!mandatory(b, X, a.n_sink, a.n_recent)) {
-                    ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
-                    mx = max(mx, __float_as_uint(S));
-                }
+            const uint32_t bits = (uint32_t)(ck[k] >> 32);
+            bin[k] = ck[k] ? min((smax - bits) >> 19, (uint32_t)kHistTail) : 0xFFFFFFFFu;
+            if (bin[k] < (uint32_t)kHistTail) atomicAdd(&sh.hist[bin[k]], 1);
+        }
+        __syncthreads();
+        // wave 0: prefix over the counted bins (four per lane); the bin reaching kk holds the cut
+        if (wave == 0) {
+            int c[4], tot = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int bi = 4 * lane + e;
+                c[e] = bi < kHistTail ? sh.hist[bi] : 0;
+                tot += c[e];
+            }
+            int run = wave_incl_scan(tot) - tot;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (run < kk && run + c[e] >= kk) sh.beta = 4 * lane + e;
+                run += c[e];
             }
         }
-        int m = 0;  // candidates ranked exactly
-        if (ranked) {
-            mx = wave_max_u32(mx);
-            if (lane == 0) sh.wmax[wave] = mx;
-            __syncthreads();
-            uint32_t smax = 0u;
+        __syncthreads();
+        const uint32_t beta = (uint32_t)sh.beta;  // kHistTail: the cut lies below the counted range
+        // candidates: keys in the cut's bin or above; each wave reserves its slots with one atomic
+        int mine = 0;
 #pragma unroll
-            for (int w2 = 0; w2 < NW; ++w2) smax = max(smax, sh.wmax[w2]);
-            // histogram of the keys' distance below the largest score, in bins of 2^19 float ulps (1/16
-            // of an octave); keys more than 255 bins below are not counted
-            uint32_t bin[KPT];
+        for (int k = 0; k < KPT; ++k) mine += bin[k] <= beta;
+        const int incl = wave_incl_scan(mine);
+        int base = 0;
+        if (lane == 63) base = atomicAdd(&sh.ncand, incl);
+        int off = __builtin_amdgcn_readlane(base, 63) + incl - mine;
 #pragma unroll
-            for (int k = 0; k < KPT; ++k) {
-                const uint32_t bits = (uint32_t)(ck[k] >> 32);
-                bin[k] = ck[k] ? min((smax - bits) >> 19, (uint32_t)kHistTail) : 0xFFFFFFFFu;
-                if (bin[k] < (uint32_t)kHistTail) atomicAdd(&sh.hist[bin[k]], 1);
+        for (int k = 0; k < KPT; ++k) {
+            if (bin[k] <= beta) {
+                if (off < kCandCap) sh.cand[off] = ck[k];
+                ++off;
             }
-            __syncthreads();
-            // wave 0: prefix over the counted bins (four per lane); the bin reaching kk holds the cut
-            if (wave == 0) {
-                int c[4], tot = 0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int bi = 4 * lane + e;
-                    c[e] = bi < kHistTail ? sh.hist[bi] : 0;
-                    tot += c[e];
-                }
-                int run = wave_incl_scan(tot) - tot;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    if (run < kk && run + c[e] >= kk) sh.beta = 4 * lane + e;
-                    run += c[e];
-                }
-            }
-            __syncthreads();
-            const uint32_t beta = (uint32_t)sh.beta;  // kHistTail: the cut lies below the counted range
-            // candidates: keys in the cut's bin or above; each wave reserves its slots with one atomic
-            int mine = 0;
-#pragma unroll
-            for (int k = 0; k < KPT; ++k) mine += bin[k] <= beta;
-            const int incl = wave_incl_scan(mine);
-            int base = 0;
-            if (lane == 63) base = atomicAdd(&sh.ncand, incl);
-            int off = __builtin_amdgcn_readlane(base, 63) + incl - mine;
-#pragma unroll
-            for (int k = 0; k < KPT; ++k) {
-                if (bin[k] <= beta) {
-                    if (off < kCandCap) sh.cand[off] = ck[k];
-                    ++off;
-                }
-            }
-            __syncthreads();
-            m = sh.ncand;
-            if (m <= kCandCap) {
-                // exact rank among the candidates (order-independent); the kk best are selected. With
-                // few candidates the four lanes of a quad share one.
-                const int share = m <= FT / 4 ? 4 : 1;
-                const int i = tid / share, part = tid % share;
-                if (i < m) {  // quad-uniform
-                    const unsigned long long ci = sh.cand[i];
-                    int r = 0;
-                    int j = part;
-                    for (; j + 7 * share < m; j += 8 * share) {
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) r += sh.cand[j + e * share] > ci;
-                    }
-                    for (; j < m; j += share) r += sh.cand[j] > ci;
-                    if (share == 4) {
-                        r += dpp_i<0xB1>(r, r);
-                        r += dpp_i<0x4E>(r, r);
-                    }
-                    if (part == 0 && r < kk) {
-                        const uint32_t b = 0xFFFFFFFFu - (uint32_t)(ci & 0xFFFFFFFFull);
-                        atomicOr(&sh.bitmap[b >> 5], 1u << (b & 31));
-                    }
-                }
-            } else {
-                // too many ties around the threshold: keep the bits for the radix path below
-#pragma unroll
-                for (int k = 0; k < KPT; ++k) {
-                    const int b = tid + k * FT;
-                    if (b < X) keys[b] = (uint32_t)(ck[k] >> 32);
-                }
-            }
-            __syncthreads();
         }
-        if (m <= kCandCap) {  // block-uniform
-            // thread t < 256 owns ids 32t .. 32t+31: selected, mandatory (or every block when K >= X)
-            uint32_t word = 0u;
-            if (tid < kBitmapWords) {
-                word = take_all ? range_bits(0, X, 32 * tid)
-                                : (sh.bitmap[tid] | range_bits(0, sink, 32 * tid) | range_bits(rec_lo, X, 32 * tid));
-            }
-            const int c = __popc(word);
-            const int incl = wave_incl_scan(c);
-            if (lane == 63) sh.cnt[wave] = incl;
-            __syncthreads();
-            int pos = incl - c, total = 0;
+        __syncthreads();
+        m = sh.ncand;
+        if (m <= kCandCap) {
+            // exact rank among the candidates (order-independent); the kk best are selected. With
+            // few candidates the four lanes of a quad share one.
+            const int share = m <= FT / 4 ? 4 : 1;
+            const int i = tid / share, part = tid % share;
+            if (i < m) {  // quad-uniform
+                const unsigned long long ci = sh.cand[i];
+                int r = 0;
+                int j = part;
+                for (; j + 7 * share < m; j += 8 * share) {
 #pragma unroll
-            for (int w2 = 0; w2 < kBitmapWords / 64; ++w2) {
-                pos += w2 < wave ? sh.cnt[w2] : 0;
-                total += sh.cnt[w2];
+                    for (int e = 0; e < 8; ++e) r += sh.cand[j + e * share] > ci;
+                }
+                for (; j < m; j += share) r += sh.cand[j] > ci;
+                if (share == 4) {
+                    r += dpp_i<0xB1>(r, r);
+                    r += dpp_i<0x4E>(r, r);
+                }
+                if (part == 0 && r < kk) {
+                    const uint32_t b = 0xFFFFFFFFu - (uint32_t)(ci & 0xFFFFFFFFull);
+                    atomicOr(&sh.bitmap[b >> 5], 1u << (b & 31));
+                }
             }
-            while (word) {
-                const int bit = __ffs(word) - 1;
-                word &= word - 1;
-                if (pos < K) sel[pos] = 32 * tid + bit;
-                ++pos;
-            }
-            for (int k = total + tid; k < K; k += FT) sel[k] = -1;
-            if (tid == 0) a.n_sel[u] = min(total, K);
-            return;
+        } else {
+            // too many ties around the threshold: keep the bits for the radix path below
+#pragma unroll
+            for (int k = 0; k < KPT; ++k)
+                if (ck[k]) keys[0xFFFFFFFFu - (uint32_t)(ck[k] & 0xFFFFFFFFull)] = (uint32_t)(ck[k] >> 32);
         }
-        goto radix_path;
+        __syncthreads();
     }
+    if (m <= kCandCap) {  // block-uniform
+        // thread t < 256 owns ids 32t .. 32t+31: selected, mandatory (or every block when K >= X)
+        uint32_t word = 0u;
+        if (tid < kBitmapWords) {
+            word = take_all ? range_bits(0, X, 32 * tid)
+                            : (sh.bitmap[tid] | range_bits(0, sink, 32 * tid) | range_bits(rec_lo, X, 32 * tid));
+        }
+        const int c = __popc(word);
+        const int incl = wave_incl_scan(c);
+        if (lane == 63) sh.cnt[wave] = incl;
+        __syncthreads();
+        int pos = incl - c, total = 0;
+#pragma unroll
+        for (int w2 = 0; w2 < kBitmapWords / 64; ++w2) {
+            pos += w2 < wave ? sh.cnt[w2] : 0;
+            total += sh.cnt[w2];
+        }
+        while (word) {
+            const int bit = __ffs(word) - 1;
+            word &= word - 1;
+            if (pos < K) sel[pos] = 32 * tid + bit;
+            ++pos;
+        }
+        for (int k = total + tid; k < K; k += FT) sel[k] = -1;
+        if (tid == 0) *ctx.n_sel = min(total, K);
+        return true;
+    }
+    return false;
+}
 
-    // ---- general path (more than 8192 blocks): scores and their bits into the key array
-    for (int b = tid; b < X; b += FT) {
-        float wt[G];
-        load_terms<G>(wu, b, wt);
-        const float S = score_of(b, wt);
-        if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
-        keys[b] = __float_as_uint(S);
-    }
-radix_path:
+// General path: radix select on the key bits of blocks [0, X), then ascending compaction.
+__device__ void select_radix(const SelectCtx& c, FinalShared& sh) {
+    constexpr int FT = kFinThreads, NW = kFinWaves;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int X = c.X, K = c.K, kk = c.kk;
+    const bool take_all = c.take_all, ranked = c.ranked;
+    int32_t* sel = c.sel;
+    const uint32_t* keys = c.keys;
+    struct {
+        int n_sink, n_recent;
+    } a{c.n_sink, c.n_recent};
     __syncthreads();
 
     // ---- threshold of the Top-(K-|F|) among non-mandatory blocks (radix select on the score bits)
@@ -802,7 +751,113 @@ radix_path:
         pos += __popcll(tm);
     }
     for (int k = total + tid; k < K; k += FT) sel[k] = -1;
-    if (tid == 0) a.n_sel[u] = min(total, K);
+    if (tid == 0) *c.n_sel = min(total, K);
+}
+
+template <int G>
+__global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
+    constexpr int FT = kFinThreads, KPT = kKeysPerThread;
+    __shared__ FinalShared sh;
+    extern __shared__ float dyn[];  // [np][G] partial maxima, then factors; [np][G] sums; [xmax] key bits
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int u = blockIdx.x;
+    const int bseq = u / geo.hkv;
+    const int xmax = geo.xmax();
+    const int nc = a.nchunks, np = nc + 1;  // partial nc: the last block's
+    const float* wu = a.ws_w + (size_t)u * xmax * G;
+    const bool fast = xmax <= KPT * FT;
+
+    // ---- loads in the order of their use: the length, the partials, this thread's score terms
+    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
+    float* fac = dyn;
+    float* sums = dyn + np * G;
+    const float2* pu = reinterpret_cast<const float2*>(a.ws_part + (size_t)u * np * G * 2);
+    const bool one_pass = np * G <= FT;  // usual case: one partial per thread
+    float2 pv = make_float2(0.0f, 0.0f);
+    if (one_pass && tid < np * G) pv = pu[tid];
+    __asm__ volatile("" ::: "memory");
+    float w[KPT][G];
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {  // branch-free: ids past xmax load block 0, unused
+        const int b = tid + k * FT;
+        load_terms<G>(wu, b < xmax ? b : 0, w[k]);
+    }
+    if (one_pass && tid < np * G) {
+        fac[tid] = pv.x;
+        sums[tid] = pv.y;
+    }
+    if (!one_pass) {
+        for (int idx = tid; idx < np * G; idx += FT) {
+            const float2 t = pu[idx];
+            fac[idx] = t.x;
+            sums[idx] = t.y;
+        }
+    }
+    select_init(sh);
+    __syncthreads();
+    // ---- wave g: head g's log normalizer over every block, then each partial's factor exp(m_c - lse)
+    if (wave < G) {
+        const int g = wave;
+        float m = -INFINITY;
+        for (int c = lane; c < np; c += 64) m = fmaxf(m, fac[c * G + g]);
+        m = wave_max(m);
+        float l = 0.0f;
+        for (int c = lane; c < np; c += 64) {
+            const float pm = fac[c * G + g];
+            if (pm != -INFINITY) l += sums[c * G + g] * expf(pm - m);
+        }
+        l = wave_sum(l);  // (every lane's reads above are complete)
+        const float lse = m + logf(l);
+        for (int c = lane; c < np; c += 64) {
+            const float pm = fac[c * G + g];
+            fac[c * G + g] = pm == -INFINITY ? 0.0f : expf(pm - lse);
+        }
+    }
+    __syncthreads();
+
+    const SelectCtx sc = make_select_ctx(X, a.K, a.n_sink, a.n_recent, a.sel + (size_t)u * a.K, a.n_sel + u,
+                                         a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * np * G)
+                                                       : a.ws_key + (size_t)u * xmax);
+    auto score_of = [&](int b, const float (&wt)[G]) {
+        const float* f = fac + (b == X - 1 ? nc : b / a.bpc) * G;
+        float S = 0.0f;
+#pragma unroll
+        for (int g = 0; g < G; ++g) S += f[g] * wt[g];
+        return S;
+    };
+
+    // ---- fast path. Block b's key is (bits of S_b) << 32 | ~b: unique, and ordered exactly like
+    // (S_b descending, b ascending). Thread t keeps the keys of blocks t + 1024k in registers.
+    if (fast) {
+        unsigned long long ck[KPT];
+        uint32_t mx = 0u;
+#pragma unroll
+        for (int k = 0; k < KPT; ++k) {
+            const int b = tid + k * FT;
+            ck[k] = 0ull;
+            if (b < X) {
+                const float S = score_of(b, w[k]);
+                if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+                if (!mandatory(b, X, a.n_sink, a.n_recent)) {
+                    ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
+                    mx = max(mx, __float_as_uint(S));
+                }
+            }
+        }
+        if (select_fast<KPT>(sc, ck, mx, sh)) return;
+    } else {
+        // ---- general path (more than 8192 blocks): scores and their bits into the key array
+        for (int b = tid; b < X; b += FT) {
+            float wt[G];
+            load_terms<G>(wu, b, wt);
+            const float S = score_of(b, wt);
+            if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+            sc.keys[b] = __float_as_uint(S);
+        }
+    }
+    __syncthreads();
+    select_radix(sc, sh);
 }
 
 size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
