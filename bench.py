@@ -35,6 +35,8 @@ def parse():
     ap.add_argument("--workload", default="llama8b_32k")
     ap.add_argument("--budget", type=int, default=None, help="override the workload's block budget")
     ap.add_argument("--layers", type=int, default=0, help="resident layer copies (0: enough for > 1 GB)")
+    ap.add_argument("--select-path", choices=["auto", "chunked", "one_group"], default="auto",
+                    help="scoring / selection launch shape (auto: one workgroup per unit where it fits)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--only", choices=["all", "sparse", "dense", "fused"], default="all",
@@ -171,7 +173,11 @@ def main():
     blk_logit = torch.empty((*units, w.group, dims.xcap), dtype=torch.float32, device=dev)
     out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
     lse = torch.empty((w.batch, w.n_q_heads), dtype=torch.float32, device=dev)
-    params = P.CompkvSelectParams(budget, 1, 2, scale)
+    path = {"auto": P.COMPKV_SELECT_AUTO, "chunked": P.COMPKV_SELECT_CHUNKED,
+            "one_group": P.COMPKV_SELECT_ONE_GROUP}[args.select_path]
+    one_group = path == P.COMPKV_SELECT_ONE_GROUP or (
+        path == P.COMPKV_SELECT_AUTO and dims.xmax <= 256)
+    params = P.CompkvSelectParams(budget, 1, 2, scale, path)
     torch.cuda.synchronize()
 
     def append(L):
@@ -288,7 +294,8 @@ def main():
         "data": "synthetic (seeded block-structured keys, N(0,1) values, N(0,1)/sqrt(128) queries)",
         "config": {"workload": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "context": n, "block_size": w.block_size, "budget_blocks": budget,
-                   "n_var_groups": w.n_var_groups, "layer_copies": layers, "parallelism": "single GPU"},
+                   "n_var_groups": w.n_var_groups, "layer_copies": layers, "parallelism": "single GPU",
+                   "select_path": "one_group" if one_group else "chunked"},
     }
     if "sparse" in result:
         us, per_k, wall, us_sep = result["sparse"]
@@ -303,9 +310,11 @@ def main():
             "algorithmic_bytes_per_step": step_bytes,
             "separate_calls_us_per_step": round(us_sep, 3) if us_sep is not None else None,
             "separate_call_us": {k: round(v, 3) for k, v in per_k.items()},
-            # the timed call: its four dispatches (chunk scoring with the append and the compensation
-            # stream, selection, exact tokens, merge) are the whole step
-            "roofline": {"kernel": "compkv_decode_step (its four dispatches)", "bound": "hbm",
+            # the timed call: its dispatches are the whole step -- chunked: chunk scoring with the
+            # append and the compensation stream, selection, exact tokens, merge; one group: scoring
+            # with the append and selection, exact and compensation items, merge
+            "roofline": {"kernel": "compkv_decode_step (its %s dispatches)" % ("three" if one_group else "four"),
+                         "bound": "hbm",
                          "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(w.name, "decode_step"),
                          "algorithmic_bytes_per_launch": step_bytes},

@@ -79,7 +79,23 @@ typedef struct compkv_select_params {
     int32_t n_sink;        /* leading blocks always selected (the paper uses 1; Section 4.2) */
     int32_t n_recent;      /* most recent blocks always selected (the paper uses 2; Section 4.2) */
     float scale;           /* logit scale s; the paper's 1/sqrt(d) (Section 3.1) */
+    int32_t select_path;   /* COMPKV_SELECT_*: how the scores are formed and ranked (0 = automatic) */
 } compkv_select_params;
+
+/*
+ * Scoring / selection launch shapes (compkv_select_params.select_path). Both compute the same
+ * quantities; their floating-point sums run in different orders, so scores may differ in the last
+ * bits and selections only among blocks whose scores tie within that rounding.
+ *   CHUNKED:   chunks of blocks spread over many workgroups, then one workgroup per unit merges the
+ *              per-chunk normalizers and selects (two launches).
+ *   ONE_GROUP: one workgroup per unit scores every block and selects (one launch); needs
+ *              G * ceil(max_seq_len / block_size) <= 8192, else COMPKV_EUNSUPPORTED.
+ *   AUTO:      ONE_GROUP when a unit holds at most 256 blocks (one workgroup then reads every summary
+ *              in a single round of loads), else CHUNKED.
+ */
+#define COMPKV_SELECT_AUTO 0
+#define COMPKV_SELECT_CHUNKED 1
+#define COMPKV_SELECT_ONE_GROUP 2
 
 /* Which call a workspace is sized for (compkv_workspace_bytes). */
 #define COMPKV_WS_ALL 0

@@ -9,6 +9,9 @@ every call raises.
 from .binding import (  # noqa: F401
     COMPKV_GROUPS_INTERLEAVED,
     COMPKV_GROUPS_ROTATE_HALF,
+    COMPKV_SELECT_AUTO,
+    COMPKV_SELECT_CHUNKED,
+    COMPKV_SELECT_ONE_GROUP,
     COMPKV_WS_ALL,
     COMPKV_WS_DECODE_STEP,
     COMPKV_WS_DENSE_DECODE,

@@ -20,6 +20,9 @@ COMPKV_WS_SCORE_SELECT = 1
 COMPKV_WS_SPARSE_DECODE = 2
 COMPKV_WS_DENSE_DECODE = 3
 COMPKV_WS_DECODE_STEP = 4
+COMPKV_SELECT_AUTO = 0
+COMPKV_SELECT_CHUNKED = 1
+COMPKV_SELECT_ONE_GROUP = 2
 
 
 class CompkvError(RuntimeError):
@@ -39,10 +42,15 @@ class CompkvDims(ctypes.Structure):
     def xcap(self) -> int:
         return -(-self.capacity_tokens // self.block_size)
 
+    @property
+    def xmax(self) -> int:
+        """Blocks of the longest sequence (max_seq_len)."""
+        return -(-self.max_seq_len // self.block_size)
+
 
 class CompkvSelectParams(ctypes.Structure):
     _fields_ = [("budget_blocks", ctypes.c_int32), ("n_sink", ctypes.c_int32),
-                ("n_recent", ctypes.c_int32), ("scale", ctypes.c_float)]
+                ("n_recent", ctypes.c_int32), ("scale", ctypes.c_float), ("select_path", ctypes.c_int32)]
 
 
 def make_dims(batch, n_q_heads, n_kv_heads, head_dim, block_size, n_var_groups, capacity_tokens,

@@ -118,11 +118,26 @@ size_t step_ws(const Geom& g, int K) {
 
 size_t ws_bytes(const Geom& g, int K, int which) {
     size_t body = 0;
-    if (which == COMPKV_WS_ALL || which == COMPKV_WS_DECODE_STEP) body = std::max(body, step_ws(g, K));
+    if (which == COMPKV_WS_ALL || which == COMPKV_WS_DECODE_STEP)  // either selection path
+        body = std::max(body, std::max(step_ws(g, K), sparse_ws(g, K)));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SCORE_SELECT) body = std::max(body, score_ws(g));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SPARSE_DECODE) body = std::max(body, sparse_ws(g, K));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_DENSE_DECODE) body = std::max(body, dense_ws(g));
     return body;
+}
+
+// select_path of the call: true for the one-workgroup-per-unit selection; *st receives the status
+bool one_group_path(const Geom& g, int path, int* st) {
+    *st = COMPKV_OK;
+    if (path < COMPKV_SELECT_AUTO || path > COMPKV_SELECT_ONE_GROUP) {
+        *st = COMPKV_EINVAL;
+        return false;
+    }
+    const bool fits = (long long)g.G * g.xmax() <= compkv::select_one_group_terms();
+    if (path == COMPKV_SELECT_ONE_GROUP && !fits) *st = COMPKV_EUNSUPPORTED;
+    if (path == COMPKV_SELECT_AUTO)  // one workgroup reads at most one batch of summaries per unit
+        return fits && g.xmax() <= compkv::select_one_group_auto_blocks();
+    return path == COMPKV_SELECT_ONE_GROUP && fits;
 }
 
 int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
@@ -234,11 +249,14 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel || !blk_logit) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
-    if ((score_shape(g).nchunks + 1) * g.G > compkv::select_max_chunk_heads()) return COMPKV_EUNSUPPORTED;
+    const bool one = one_group_path(g, params->select_path, &st);
+    if (st != COMPKV_OK) return st;
+    if (!one && (score_shape(g).nchunks + 1) * g.G > compkv::select_max_chunk_heads()) return COMPKV_EUNSUPPORTED;
     const size_t need = ws_bytes(g, params->budget_blocks, COMPKV_WS_SCORE_SELECT);
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
     compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, workspace);
+    a.one_group = one;
     return launch_status(compkv::launch_score_select(g, a, static_cast<hipStream_t>(stream)));
 }
 
@@ -322,15 +340,17 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
     const int K = params->budget_blocks;
+    const bool one = one_group_path(g, params->select_path, &st);
+    if (st != COMPKV_OK) return st;
     const SparseShape sp = sparse_shape(g, K);
     const ScoreShape sc = score_shape(g);
     const int parts = step_partials(g, K);
-    if (sp.eb > compkv::decode_max_eb() || sp.n_exact > compkv::decode_max_items() ||
-        parts > compkv::decode_max_partials() || (sc.nchunks + 1) * g.G > compkv::select_max_chunk_heads())
+    if (sp.eb > compkv::decode_max_eb() || sp.n_exact > compkv::decode_max_items()) return COMPKV_EUNSUPPORTED;
+    if (one ? sp.cb > compkv::decode_max_cb()
+            : (parts > compkv::decode_max_partials() || (sc.nchunks + 1) * g.G > compkv::select_max_chunk_heads()))
         return COMPKV_EUNSUPPORTED;
     st = check_ws(g, workspace, workspace_bytes, ws_bytes(g, K, COMPKV_WS_DECODE_STEP));
     if (st != COMPKV_OK) return st;
-    float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, workspace);
@@ -341,12 +361,39 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     a.kmean_w = kmean;
     a.dvar_w = dvar;
     a.vmean = vmean;
+    a.one_group = one;
+    compkv::DecodeArgs d{};
+    if (one) {
+        // one workgroup per unit refreshes, scores and selects; then the compensated sparse decode
+        // (exact and compensation items, merge) with its partials at the start of the workspace
+        hipError_t e = compkv::launch_score_select(g, a, s);
+        if (e != hipSuccess) return COMPKV_EHIP;
+        d.ws_part = static_cast<float*>(workspace);
+        d.q = static_cast<const uint16_t*>(q);
+        d.K = static_cast<const uint16_t*>(k_cache);
+        d.V = static_cast<const uint16_t*>(v_cache);
+        d.vmean = vmean;
+        d.blk_logit = blk_logit;
+        d.seq_lens = seq_lens;
+        d.sel = sel;
+        d.n_sel = n_sel;
+        d.out = out;
+        d.lse = lse;
+        d.sel_stride = K;
+        d.n_exact = sp.n_exact;
+        d.eb = sp.eb;
+        d.n_comp = sp.n_comp;
+        d.cb = sp.cb;
+        d.dense = 0;
+        d.scale = params->scale;
+        return launch_status(compkv::launch_decode(g, d, s));
+    }
+    float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
     a.comp_part = dpart;
     a.part_count = parts;
     hipError_t e = compkv::launch_score_select(g, a, s);
     if (e != hipSuccess) return COMPKV_EHIP;
 
-    compkv::DecodeArgs d{};
     d.ws_part = dpart;
     d.q = static_cast<const uint16_t*>(q);
     d.K = static_cast<const uint16_t*>(k_cache);

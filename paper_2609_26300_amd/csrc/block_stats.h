@@ -73,9 +73,12 @@ __device__ __forceinline__ void load_block_rows(const BlockSrc& b, int s0, Block
 }
 
 // The summary from the rows of the first batch (already requested into R) and the rest of the block.
+// In a workgroup larger than four waves only waves 0-3 work (`active`); every thread reaches the
+// barriers.
 template <int D>
 __device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int layout, float* __restrict__ km_out,
-                                 float* __restrict__ dv_out, float* __restrict__ vm_out, BlockStatsLds<D>& L) {
+                                 float* __restrict__ dv_out, float* __restrict__ vm_out, BlockStatsLds<D>& L,
+                                 bool active = true) {
     constexpr int LPR = D / 8;     // lanes per row
     constexpr int RPW = 64 / LPR;  // rows per wave step
     constexpr int RPG = 4 * RPW;   // rows per workgroup step
@@ -86,7 +89,7 @@ __device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int lay
     const int nsteps = (nb + RPG - 1) / RPG;
 
     float sk[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int s0 = 0; s0 < nsteps; s0 += NS) {
+    for (int s0 = 0; active && s0 < nsteps; s0 += NS) {
         if (s0 > 0) load_block_rows<D>(b, s0, R);
 #pragma unroll
         for (int st = 0; st < NS; ++st) {
@@ -101,14 +104,16 @@ __device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int lay
             }
         }
     }
+    if (active) {
 #pragma unroll
-    for (int off = LPR; off < 64; off <<= 1)
+        for (int off = LPR; off < 64; off <<= 1)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            sk[e] = xor_add(sk[e], off);
-            sv[e] = xor_add(sv[e], off);
-        }
-    if (ro == 0) {
+            for (int e = 0; e < 8; ++e) {
+                sk[e] = xor_add(sk[e], off);
+                sv[e] = xor_add(sv[e], off);
+            }
+    }
+    if (active && ro == 0) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             L.part[wave][0][li * 8 + e] = sk[e];
@@ -132,7 +137,7 @@ __device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int lay
         mk[e] = L.km[li * 8 + e];
         m2[e] = 0.0f;
     }
-    for (int s0 = 0; s0 < nsteps; s0 += NS) {
+    for (int s0 = 0; active && s0 < nsteps; s0 += NS) {
         if (nsteps > NS) load_block_rows<D>(b, s0, R, false);  // larger blocks: reload (L1/L2 hits)
 #pragma unroll
         for (int st = 0; st < NS; ++st) {
@@ -146,11 +151,13 @@ __device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int lay
             }
         }
     }
+    if (active) {
 #pragma unroll
-    for (int off = LPR; off < 64; off <<= 1)
+        for (int off = LPR; off < 64; off <<= 1)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) m2[e] = xor_add(m2[e], off);
-    if (ro == 0) {
+            for (int e = 0; e < 8; ++e) m2[e] = xor_add(m2[e], off);
+    }
+    if (active && ro == 0) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) L.part[wave][0][li * 8 + e] = m2[e];
     }

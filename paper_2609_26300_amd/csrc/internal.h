@@ -59,6 +59,7 @@ struct ScoreArgs {
     float* vmean;           // [units][xcap][D]: read by the compensation; the active block written
     float* comp_part;       // [units][part_count][G][D + 2]: chunk c writes compensation partial c
     int part_count;
+    int one_group;          // 1: one workgroup per unit scores and selects (no chunks, no partials)
 };
 
 struct DecodeArgs {
@@ -92,6 +93,8 @@ hipError_t launch_append_stats(const Geom& g, const StatsArgs& a, hipStream_t s)
 hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s);
 int select_max_bpc();
 int select_max_chunk_heads();  // nchunks * G limit of the selection's partial merge
+int select_one_group_terms();  // G * xmax limit of the one-workgroup-per-unit selection
+int select_one_group_auto_blocks();  // xmax up to which the automatic choice takes that selection
 int decode_max_items();
 int decode_max_partials();
 int decode_max_cb();

@@ -41,6 +41,7 @@ namespace {
 constexpr int kBpcMax = 128;  // blocks per chunk, upper bound
 constexpr int kHistBins = 2048;
 constexpr size_t kDynBudget = 32768;  // dynamic LDS of the finalize launch
+constexpr int kUnitTerms = 8192;      // G * xmax bound of the one-workgroup-per-unit path (64 KB of LDS)
 
 // The query enters through frequency pairs (Appendix A.4): lane f of wave w holds pair f of heads
 // g = w, w + 4, ... (coordinates f, f + d/2 for rotate-half; 2f, 2f + 1 interleaved). The loads are
@@ -860,6 +861,195 @@ __global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, 
     select_radix(sc, sh);
 }
 
+
+// ---------------------------------------------------------------- one workgroup per unit
+// For units with few blocks (G * xmax <= kUnitTerms) one 1024-thread workgroup per unit refreshes the
+// active block (fused step), forms every block's block-mean logits, projected variances and log
+// weight estimates (kept in LDS), the per-head log normalizers over every block, the scores and the
+// selection: one launch, no partials. The summaries are read in batches of passes of 128 blocks (8
+// lanes per block, as in the chunk kernel), each batch's loads issued before its arithmetic.
+constexpr int kUnitBatch = 2;  // passes whose summaries a thread requests at once
+
+template <int D, int G>
+struct UnitShared {
+    float q[G][D];
+    float Qv[G][D];
+    BlockStatsLds<D> bs;
+    float lse[G];
+};
+
+template <int D, int G, bool kStep>
+__global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, ScoreArgs a) {
+    constexpr int FT = kFinThreads, KPT = kKeysPerThread, NF4 = D / 32, PB = kUnitBatch;
+    constexpr int GPP = FT / 8;  // blocks per pass
+    __shared__ FinalShared sh;
+    __shared__ UnitShared<D, G> us;
+    extern __shared__ float dyn[];  // [xmax][G] log weights (later the key bits), [xmax][G] projected variances
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int u = blockIdx.x, bseq = u / geo.hkv, h = u % geo.hkv;
+    const int xmax = geo.xmax();
+    const int li = tid & 7, grp = tid >> 3;
+    float* A = dyn;
+    float* Vp = dyn + (size_t)xmax * G;
+    const float s = a.scale;
+
+    // loads in the order of their use: query pairs, the refreshed block's rows, the first batch
+    const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+    QueryPairs<D, G> qp;
+    if (wave < 4) load_query_pairs<D, G>(qh, geo.layout, qp);
+    __asm__ volatile("" ::: "memory");
+    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
+    const int npass = (X + GPP - 1) / GPP;
+    const bool refresh = kStep && a.k_new && X >= 1;  // workgroup-uniform
+    const int lastb = X - 1;
+    const size_t blk_last = (size_t)u * geo.xcap + (lastb >= 0 ? lastb : 0);
+    BlockSrc src{};
+    BlockRows rows;
+    if (refresh) {
+        const size_t row0 = (size_t)u * geo.cap + (size_t)lastb * geo.B;
+        const int nb = n - lastb * geo.B;
+        src = BlockSrc{a.Kc + row0 * D, a.Vc + row0 * D, a.k_new + (size_t)u * D, a.v_new + (size_t)u * D, nb, nb - 1};
+        if (wave < 4) load_block_rows<D>(src, 0, rows);
+    }
+    float4 kv[PB][NF4];
+    float dv0[PB];
+    auto issue = [&](int p0) {  // branch-free: ids past xmax load block 0, unused
+#pragma unroll
+        for (int p = 0; p < PB; ++p) {
+            const int b = (p0 + p) * GPP + grp;
+            const size_t blk = (size_t)u * geo.xcap + (b < xmax ? b : 0);
+            const float4* kp = reinterpret_cast<const float4*>(a.kmean + blk * D);
+#pragma unroll
+            for (int m = 0; m < NF4; ++m) kv[p][m] = kp[li + 8 * m];
+            dv0[p] = a.dvar[blk * geo.r + min(li, geo.r - 1)];
+        }
+    };
+    issue(0);
+    if (wave < 4) store_query<D, G>(qp, s, geo.r, geo.layout, us.q, us.Qv);
+    select_init(sh);
+    if (refresh)  // (its barriers also publish the query)
+        block_stats_from<D>(src, rows, geo.r, geo.layout, a.kmean_w + blk_last * D, a.dvar_w + blk_last * geo.r,
+                            a.vmean + blk_last * D, us.bs, wave < 4);
+    else
+        __syncthreads();
+
+    // every block: zbar, sig2 and a = log|b| + zbar + sig2 / 2 per head. A block's sig2 goes to LDS
+    // first; the lane that wrote it reads it back for a.
+    constexpr int GB = G < 2 ? G : 2;
+    float qv0[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) qv0[g] = li < geo.r ? us.Qv[g][li] : 0.0f;
+    for (int p0 = 0; p0 < npass; p0 += PB) {  // workgroup-uniform
+        if (p0 > 0) issue(p0);
+        if (refresh) {
+#pragma unroll
+            for (int p = 0; p < PB; ++p) {
+                if ((p0 + p) * GPP + grp == lastb) {  // the refreshed summary
+#pragma unroll
+                    for (int m = 0; m < NF4; ++m) kv[p][m] = *reinterpret_cast<const float4*>(&us.bs.km[4 * (li + 8 * m)]);
+                    dv0[p] = us.bs.dv[min(li, geo.r - 1)];
+                }
+            }
+        }
+#pragma unroll
+        for (int p = 0; p < PB; ++p) {
+            const int b = (p0 + p) * GPP + grp;
+            const bool valid = b < X;
+            float v[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) v[g] = qv0[g] * dv0[p];
+            if (geo.r > 8 && valid) {
+                const size_t blk = (size_t)u * geo.xcap + b;
+                for (int t = li + 8; t < geo.r; t += 8) {
+                    const float dv = (refresh && b == lastb) ? us.bs.dv[t] : a.dvar[blk * geo.r + t];
+#pragma unroll
+                    for (int g = 0; g < G; ++g) v[g] += us.Qv[g][t] * dv;
+                }
+            }
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                v[g] = sum8_lead(v[g]);
+                if (li == 0 && valid) Vp[b * G + g] = v[g];
+            }
+        }
+#pragma unroll 1
+        for (int g0 = 0; g0 < G; g0 += GB) {  // (not unrolled: one head pair's query in registers at a time)
+            float4 qq[GB][NF4];
+#pragma unroll
+            for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+                for (int m = 0; m < NF4; ++m) qq[gb][m] = *reinterpret_cast<const float4*>(&us.q[g0 + gb][4 * (li + 8 * m)]);
+#pragma unroll
+            for (int p = 0; p < PB; ++p) {
+                const int b = (p0 + p) * GPP + grp;
+                const bool valid = b < X;
+#pragma unroll
+                for (int gb = 0; gb < GB; ++gb) {
+                    float z = 0.0f;
+#pragma unroll
+                    for (int m = 0; m < NF4; ++m)
+                        z += qq[gb][m].x * kv[p][m].x + qq[gb][m].y * kv[p][m].y + qq[gb][m].z * kv[p][m].z +
+                             qq[gb][m].w * kv[p][m].w;
+                    z = sum8_lead(z);
+                    if (li == 0 && valid) {
+                        const int g = g0 + gb;
+                        const float lnb = logf((float)min(geo.B, n - b * geo.B));
+                        A[b * G + g] = lnb + z + 0.5f * Vp[b * G + g];
+                        a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
+                    }
+                }
+            }
+        }
+    }
+    if (refresh && wave == 4) {  // the new token's cache row (the refresh read it from k_new / v_new)
+        const size_t row = (size_t)u * geo.cap + (n - 1);
+        const uint4* kn = reinterpret_cast<const uint4*>(a.k_new + (size_t)u * D);
+        const uint4* vn = reinterpret_cast<const uint4*>(a.v_new + (size_t)u * D);
+        for (int i = lane; i < D / 8; i += 64) {
+            reinterpret_cast<uint4*>(a.Kc + row * D)[i] = kn[i];
+            reinterpret_cast<uint4*>(a.Vc + row * D)[i] = vn[i];
+        }
+    }
+    __syncthreads();
+    // wave g: head g's log normalizer over every block
+    if (wave < G) {
+        const int g = wave;
+        float m = -INFINITY;
+        for (int b = lane; b < X; b += 64) m = fmaxf(m, A[b * G + g]);
+        m = wave_max(m);
+        float l = 0.0f;
+        for (int b = lane; b < X; b += 64) l += expf(A[b * G + g] - m);
+        l = wave_sum(l);
+        if (lane == 0) us.lse[g] = m + logf(l);
+    }
+    __syncthreads();
+    // scores and keys; thread t holds blocks t + 1024k
+    unsigned long long ck[KPT];
+    uint32_t mx = 0u;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+        const int b = tid + k * FT;
+        ck[k] = 0ull;
+        if (b < X) {
+            float S = 0.0f;
+#pragma unroll
+            for (int g = 0; g < G; ++g) S += expf(A[b * G + g] - us.lse[g]) * Vp[b * G + g];
+            if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+            if (!mandatory(b, X, a.n_sink, a.n_recent)) {
+                ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
+                mx = max(mx, __float_as_uint(S));
+            }
+        }
+    }
+    // (the key bits of the radix path overwrite the log weights, which every thread has read by then)
+    const SelectCtx sc = make_select_ctx(X, a.K, a.n_sink, a.n_recent, a.sel + (size_t)u * a.K, a.n_sel + u,
+                                         reinterpret_cast<uint32_t*>(A));
+    if (select_fast<KPT>(sc, ck, mx, sh)) return;
+    __syncthreads();
+    select_radix(sc, sh);
+}
+
 size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
     return ((size_t)2 * (a.nchunks + 1) * g.G + (a.keys_in_lds ? (size_t)g.xmax() : 0)) * sizeof(float);
 }
@@ -876,6 +1066,14 @@ void launch_chunks(const Geom& g, const ScoreArgs& a, hipStream_t s) {
 
 template <int D, int G>
 hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
+    if (a.one_group) {
+        const size_t dyn = (size_t)2 * g.xmax() * G * sizeof(float);
+        if (a.k_new)
+            unit_select_kernel<D, G, true><<<dim3(g.units()), kFinThreads, dyn, s>>>(g, a);
+        else
+            unit_select_kernel<D, G, false><<<dim3(g.units()), kFinThreads, dyn, s>>>(g, a);
+        return hipGetLastError();
+    }
     if (a.comp_part)
         launch_chunks<D, G, true>(g, a, s);
     else
@@ -900,9 +1098,15 @@ hipError_t dispatch_g(const Geom& g, const ScoreArgs& a, hipStream_t s) {
 }  // namespace
 
 int select_max_bpc() { return kBpcMax; }
+int select_one_group_terms() { return kUnitTerms; }
+int select_one_group_auto_blocks() { return kUnitBatch * kFinThreads / 8; }
 int select_max_chunk_heads() { return (int)(kDynBudget / (2 * sizeof(float))); }
 
 hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s) {
+    if (a.one_group) {
+        if (g.G * g.xmax() > kUnitTerms) return hipErrorInvalidValue;
+        return g.D == 128 ? dispatch_g<128>(g, a, s) : dispatch_g<64>(g, a, s);
+    }
     if (a.bpc != 32 && a.bpc != 64 && a.bpc != 128) return hipErrorInvalidValue;
     a.keys_in_lds = 0;
     a.keys_in_lds = finalize_dyn_lds(g, a) + (size_t)g.xmax() * sizeof(float) <= kDynBudget;

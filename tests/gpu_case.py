@@ -95,6 +95,14 @@ class Case:
         self.sl = torch.from_numpy(self.seq_lens).to("cuda")
         self.ws = P.alloc_workspace(self.dims, self.budget)
         self.G = w.group
+        self.select_path = P.COMPKV_SELECT_AUTO
+
+    def one_group_ok(self) -> bool:
+        """Whether the one-workgroup-per-unit selection accepts these dims (G * blocks <= 8192)."""
+        return self.G * self.dims.xmax <= 8192
+
+    def params(self):
+        return P.CompkvSelectParams(self.budget, self.n_sink, self.n_recent, self.scale, self.select_path)
 
     # ---------------------------------------------------------------- library calls
     def build_stats(self):
@@ -109,8 +117,7 @@ class Case:
         self.n_sel = torch.zeros(units, dtype=torch.int32, device="cuda")
         self.blk_logit = torch.zeros((*units, self.G, d.xcap), dtype=torch.float32, device="cuda")
         self.scores = torch.zeros((*units, d.xcap), dtype=torch.float32, device="cuda")
-        params = P.CompkvSelectParams(self.budget, self.n_sink, self.n_recent, self.scale)
-        P.compkv_score_select(d, params, self.q if q is None else q, self.summ.kmean, self.summ.dvar, self.sl,
+        P.compkv_score_select(d, self.params(), self.q if q is None else q, self.summ.kmean, self.summ.dvar, self.sl,
                               self.sel, self.n_sel, self.blk_logit, self.scores, self.ws)
 
     def sparse_decode(self, sel=None, n_sel=None):
@@ -134,8 +141,7 @@ class Case:
             scores=torch.zeros((*units, d.xcap), dtype=torch.float32, device="cuda"),
             out=torch.zeros((d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device="cuda"),
             lse=torch.zeros((d.batch, d.n_q_heads), dtype=torch.float32, device="cuda"))
-        params = P.CompkvSelectParams(self.budget, self.n_sink, self.n_recent, self.scale)
-        P.compkv_decode_step(d, params, self.q, self.K if K is None else K, self.V if V is None else V, k_new, v_new,
+        P.compkv_decode_step(d, self.params(), self.q, self.K if K is None else K, self.V if V is None else V, k_new, v_new,
                              self.sl if sl is None else sl, summ.kmean, summ.dvar, summ.vmean, r["sel"], r["n_sel"],
                              r["blk_logit"], r["scores"], r["out"], r["lse"], self.ws if ws is None else ws)
         return r
@@ -169,6 +175,21 @@ class Case:
 
     def units(self):
         return [(b, h) for b in range(self.w.batch) for h in range(self.w.n_kv_heads)]
+
+
+# selection paths under test; a case the one-group path does not accept runs on the chunked path only
+PATHS = {"chunked": P.COMPKV_SELECT_CHUNKED, "one_group": P.COMPKV_SELECT_ONE_GROUP}
+
+
+def make_case(name: str, path: str) -> Case:
+    """Parity case ``name`` with its selection path set; skips an ineligible one-group variant."""
+    import pytest
+
+    c = CASES[name]()
+    c.select_path = PATHS[path]
+    if path == "one_group" and not c.one_group_ok():
+        pytest.skip("the one-group selection needs G * blocks <= 8192")
+    return c
 
 
 TINY = WORKLOADS["tiny_4k"]

@@ -172,3 +172,33 @@ def test_score_select_block_count_limit():
     assert L.compkv_score_select(ctypes.byref(big), ctypes.byref(p), *args, FAKE, need, None) == EUNSUP
     need = P.compkv_workspace_bytes(ok, 64, P.COMPKV_WS_SCORE_SELECT)
     assert L.compkv_score_select(ctypes.byref(ok), ctypes.byref(p), *args, FAKE, need - 1, None) == EWS
+
+
+def test_select_path_validation():
+    """select_path: an unknown value is EINVAL; the one-group path is refused (before anything is
+    enqueued) when G * blocks exceeds 8192, and accepted up to that bound."""
+    L = P.library()
+    args = [FAKE] * 6 + [FAKE, None]
+
+    def score(d, path, ws_bytes=None):
+        p = P.CompkvSelectParams(64, 1, 2, 0.088, path)
+        need = P.compkv_workspace_bytes(d, 64, P.COMPKV_WS_SCORE_SELECT)
+        return L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), *args, FAKE,
+                                     need - 1 if ws_bytes is None else ws_bytes, None)
+
+    fits = dims(block_size=16, capacity_tokens=2048 * 16, max_seq_len=2048 * 16)  # G = 4: 4 * 2048 = 8192
+    over = dims(block_size=16, capacity_tokens=2049 * 16, max_seq_len=2049 * 16)
+    for bad in (-1, 3):
+        assert score(fits, bad) == EINVAL
+        assert _step(L, fits, P.CompkvSelectParams(64, 1, 2, 0.088, bad)) == EINVAL
+    assert score(over, P.COMPKV_SELECT_ONE_GROUP) == EUNSUP
+    assert _step(L, over, P.CompkvSelectParams(64, 1, 2, 0.088, P.COMPKV_SELECT_ONE_GROUP)) == EUNSUP
+    # accepted: the calls get as far as the workspace check
+    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP):
+        assert score(fits, path) == EWS
+    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED):
+        assert score(over, path) == EWS
+    # one workspace size serves the fused step on either path
+    need = P.compkv_workspace_bytes(fits, 64, P.COMPKV_WS_DECODE_STEP)
+    for path in (P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP):
+        assert _step(L, fits, P.CompkvSelectParams(64, 1, 2, 0.088, path), ws_bytes=need - 1) == EWS

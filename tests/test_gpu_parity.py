@@ -10,22 +10,33 @@ import pytest
 import torch
 
 import oracle
-from gpu_case import CASES, LLAMA, TINY, TOL, Case, check_selection, dev_bf16, rel_err
+from gpu_case import CASES, LLAMA, PATHS, TINY, TOL, Case, check_selection, dev_bf16, make_case, rel_err
 
 pytestmark = pytest.mark.gpu
 
 _cache = {}
 
 
+def _get(name, path):
+    if (name, path) not in _cache:
+        print(f"\n[case {name} / {path} selection] generating + running", flush=True)
+        c = make_case(name, path)
+        c.run_all()
+        _cache[name, path] = c
+    return _cache[name, path]
+
+
 @pytest.fixture(params=sorted(CASES), scope="module")
 def case(request):
-    name = request.param
-    if name not in _cache:
-        print(f"\n[case {name}] generating + running", flush=True)
-        c = CASES[name]()
-        c.run_all()
-        _cache[name] = c
-    return _cache[name]
+    """A case for the calls that do not depend on the selection path (chunked selection run)."""
+    return _get(request.param, "chunked")
+
+
+@pytest.fixture(params=[(n, p) for n in sorted(CASES) for p in PATHS], ids=lambda x: f"{x[0]}-{x[1]}",
+                scope="module")
+def case_p(request):
+    """A case on each selection path."""
+    return _get(*request.param)
 
 
 def _gpu(t):
@@ -42,7 +53,8 @@ def test_build_stats_parity(case):
         assert rel_err(dv[b, h, :X], odv) <= TOL
 
 
-def test_score_select_parity(case):
+def test_score_select_parity(case_p):
+    case = case_p
     sel, nsel = _gpu(case.sel), _gpu(case.n_sel)
     scores, zbar = _gpu(case.scores), _gpu(case.blk_logit)
     for b, h in case.units():
@@ -78,9 +90,10 @@ def test_sparse_decode_with_oracle_selection(case):
     case.sparse_decode()  # restore the pipeline's own output
 
 
-def test_end_to_end_parity(case):
+def test_end_to_end_parity(case_p):
     """Whole step: once the GPU's selection passes the band rule, the oracle output recomputed on
     that same selection must match the GPU output."""
+    case = case_p
     sel, nsel = _gpu(case.sel), _gpu(case.n_sel)
     out, lse = _gpu(case.out), _gpu(case.lse)
     G = case.G
@@ -105,8 +118,9 @@ def test_dense_decode_parity(case):
         assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, np.max(np.abs(l)))
 
 
-def test_rerun_is_bit_identical(case):
+def test_rerun_is_bit_identical(case_p):
     """No float atomics: a second run reproduces every output bit."""
+    case = case_p
     before = [x.clone() for x in (case.summ.kmean, case.summ.dvar, case.summ.vmean, case.sel, case.n_sel,
                                   case.scores, case.out, case.lse)]
     case.run_all()
@@ -175,10 +189,12 @@ def test_append_matches_build_bitwise():
             assert rel_err(c.summ.dvar[b, h, :X].cpu().numpy(), odv) <= TOL
 
 
-def test_graph_replays_match_eager():
+@pytest.mark.parametrize("path", sorted(PATHS))
+def test_graph_replays_match_eager(path):
     """The library enqueues no memsets and leaves its arrival counters at zero after each call, so a
     captured HIP graph of score_select + sparse_decode reproduces the eager outputs on every replay."""
     c = Case(LLAMA.with_(batch=1, context=8192, seed=24))
+    c.select_path = PATHS[path]
     c.run_all()
     ref = [x.clone() for x in (c.sel, c.n_sel, c.blk_logit, c.out, c.lse)]
     side = torch.cuda.Stream()
@@ -190,7 +206,7 @@ def test_graph_replays_match_eager():
     torch.cuda.synchronize()
     sel, n_sel, blk, out, lse = c.sel, c.n_sel, c.blk_logit, c.out, c.lse
     import paper_2609_26300_amd as P
-    params = P.CompkvSelectParams(c.budget, c.n_sink, c.n_recent, c.scale)
+    params = c.params()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         P.compkv_score_select(c.dims, params, c.q, c.summ.kmean, c.summ.dvar, c.sl, sel, n_sel, blk, None, c.ws)

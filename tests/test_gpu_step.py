@@ -14,7 +14,7 @@ import torch
 
 import oracle
 import paper_2609_26300_amd as P
-from gpu_case import CASES, LLAMA, TINY, TOL, Case, bits_of, check_selection, dev_bf16, rel_err
+from gpu_case import CASES, LLAMA, PATHS, TINY, TOL, Case, bits_of, check_selection, dev_bf16, make_case, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -39,12 +39,14 @@ def _prefix_state(c: Case):
     return K2, V2, kn.contiguous(), vn.contiguous(), summ
 
 
-@pytest.fixture(params=sorted(CASES), scope="module")
+@pytest.fixture(params=[(n, p) for n in sorted(CASES) for p in PATHS], ids=lambda x: f"{x[0]}-{x[1]}",
+                scope="module")
 def step(request):
+    """Separate calls and fused steps (plain and appended) on one selection path."""
     name = request.param
     if name not in _cache:
-        print(f"\n[step case {name}] generating + running", flush=True)
-        c = CASES[name]()
+        print(f"\n[step case {name[0]} / {name[1]} selection] generating + running", flush=True)
+        c = make_case(*name)
         c.run_all()
         plain = c.decode_step()
         K2, V2, kn, vn, summ2 = _prefix_state(c)
@@ -107,11 +109,13 @@ def test_step_append_outputs(step):
     _oracle_end_to_end(c, appended)
 
 
-def test_step_streaming_appends_match_build():
+@pytest.mark.parametrize("path", sorted(PATHS))
+def test_step_streaming_appends_match_build(path):
     """Forty fused steps, each appending one token: summaries stay bit-identical to a rebuild, and the
     last step's output matches the oracle."""
     w = TINY.with_(batch=2, context=1000, decode_steps=40, block_size=16, seed=31)
     c = Case(w, max_seq_len=w.capacity)
+    c.select_path = PATHS[path]
     n0, T = 1000, 40
     c.K[:, :, n0:] = 0
     c.V[:, :, n0:] = 0
@@ -131,17 +135,19 @@ def test_step_streaming_appends_match_build():
     _oracle_end_to_end(c, r)
 
 
-def test_step_graph_replays_match_eager():
+@pytest.mark.parametrize("path", sorted(PATHS))
+def test_step_graph_replays_match_eager(path):
     """A captured fused step (with its append, which rewrites the same row and block each time)
     reproduces the eager outputs on every replay."""
     c = Case(LLAMA.with_(batch=1, context=8192, seed=32))
+    c.select_path = PATHS[path]
     c.build_stats()
     K2, V2, kn, vn, summ2 = _prefix_state(c)
     ref = c.decode_step(kn, vn, summ=summ2, K=K2, V=V2)
     torch.cuda.synchronize()
     d = c.dims
     outs = {k: torch.empty_like(v) for k, v in ref.items()}
-    params = P.CompkvSelectParams(c.budget, c.n_sink, c.n_recent, c.scale)
+    params = c.params()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
 
@@ -169,11 +175,13 @@ def test_step_graph_replays_match_eager():
         torch.cuda.synchronize()
 
 
-def test_empty_sequence_in_batch():
+@pytest.mark.parametrize("path", sorted(PATHS))
+def test_empty_sequence_in_batch(path):
     """A sequence with no tokens has no blocks: nothing is selected, its output is zero and its lse is
     -inf, in the separate calls and in the fused step (which appends nothing for it); the other
     sequences of the batch are unaffected."""
     c = Case(TINY.with_(batch=3, seed=33), seq_lens=[0, 700, 1500], max_seq_len=1500)
+    c.select_path = PATHS[path]
     c.run_all()
     for r in (dict(sel=c.sel, n_sel=c.n_sel, out=c.out, lse=c.lse), c.decode_step()):
         torch.cuda.synchronize()
