@@ -16,8 +16,15 @@
 // without any data movement. For P.V the value row of each of the lane's 4 tokens is loaded as one
 // contiguous chunk of d/16 coordinates (coordinate (d/16)*(l%16) + j goes to output block j), so every
 // load is a contiguous piece of a row. P.V runs as v_mfma_f32_16x16x32_bf16 over a pair of tiles, with
-// P split into three bf16 terms (three MFMAs), which keeps P within 2^-27 of its fp32 value; products
-// with the bf16 values are exact and accumulate in fp32. The softmax max is taken per pair of tiles.
+// P split into three bf16 terms (three MFMAs), which keeps P within 2^-27 of its fp32 value (two terms,
+// 2^-17, are not enough for outputs that cancel to near zero); products with the bf16 values are exact
+// and accumulate in fp32. The softmax max is taken per pair of tiles.
+//
+// In the fused step the compensation partials already hold the pseudo-token of every block (logit
+// log|b| + zbar_b, value vmean_b), so an exact item takes its own blocks' pseudo-tokens back out. As
+// |b| e^{zbar_b} vmean_b = sum over the block's tokens of e^{zbar_b} v_j, this is a per-token weight
+// p'_j = e^{zbar_b - m}: the item multiplies V by p_j - p'_j in the same MFMAs, and by Jensen's
+// inequality each block's sum of these weights is non-negative.
 //
 // Compensation items are plain fp32 streaming on the vector ALUs: the mean-value rows (d/4 lanes x
 // float4 per row, 16 rows per thread in flight) are requested first; meanwhile the item marks its
@@ -42,8 +49,8 @@ template <int D, int G>
 struct DecodeShared {
     float m[4][G], l[4][G];
     float acc[4][G][D];
-    float pa[G][D];  // fused step: the item's weighted pseudo-values (relative to sh.M)
     float w[G][kCbMax];  // compensation weights
+    float zb[G][kMaxEb];  // fused step: the block logits of the exact item's selected blocks
     float M[G], L[G];
     unsigned char flag[kCbMax];
     int sel[kMaxEb];  // the exact item's selected ids
@@ -55,10 +62,18 @@ __device__ __forceinline__ short f32_to_bf16_rne(float f) {
 }
 __device__ __forceinline__ float bf16_bits_to_f32(short h) { return __uint_as_float(uint32_t((unsigned short)h) << 16); }
 
+// floor(v / B) for 0 <= v < 2^23: the float quotient is within one of it, and one step corrects it
+__device__ __forceinline__ int div_small(int v, int B, float invB) {
+    int k = (int)((float)v * invB);
+    const int r = v - k * B;
+    return k + (r >= B ? 1 : 0) - (r < 0 ? 1 : 0);
+}
+
 // virtual token v of an item -> cache row, or -1 if v is past the item's tokens / the block's length
 struct TokenMap {
     const int32_t* sel;  // sparse: the item's selected ids (first entry of the item)
     int nblk, B, n, X;   // sparse
+    float invB;
     int t0, t1;          // dense: row range
     bool dense;
     __device__ int row(int v) const {
@@ -66,7 +81,7 @@ struct TokenMap {
             const int r = t0 + v;
             return r < t1 ? r : -1;
         }
-        const int k = v / B;
+        const int k = div_small(v, B, invB);
         if (k >= nblk) return -1;
         const int blk = sel[k];
         const int off = v - k * B;
@@ -78,29 +93,23 @@ struct TokenMap {
 
 // Exact tokens of one item with MFMA. Leaves this wave's (m, l) for head lane%16 (lanes with the same
 // lane%16 agree) and acc[j][i] = sum over the wave's tokens of p * v for head 4(lane/16)+i at
-// coordinate (D/16)*(lane%16) + j. `mid` is workgroup-wide work (every wave calls it once) run while
-// the first round's loads are in flight.
+// coordinate (D/16)*(lane%16) + j. With zt (fused step: zt[g][k] = block logit of head g and the item's
+// k-th block, filled by `mid`) every token's weight is p_j - p'_j with p'_j = e^{zbar_b - m} for its
+// block b. `mid` is workgroup-wide work (every wave calls it once, after its first loads are issued).
 template <int D, int G, typename Mid>
 __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku, const uint16_t* __restrict__ Vu,
-                             const uint16_t* __restrict__ qh, float scale, float& m, float& l, v4f32 (&acc)[D / 16],
-                             Mid&& mid) {
+                             const uint16_t* __restrict__ qh, const float (*zt)[kMaxEb], float scale, float& m,
+                             float& l, v4f32 (&acc)[D / 16], Mid&& mid) {
     constexpr int KS = D / 32;   // k-steps of the logit MFMA
     constexpr int CPL = D / 16;  // value coordinates per lane (= output blocks)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
-    // B operand of the logit product: query head `col` (zero for padding heads)
-    v8bf16 qb[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        uint4 w = make_uint4(0, 0, 0, 0);
-        if (col < G) w = *reinterpret_cast<const uint4*>(qh + col * D + 32 * ks + 8 * grp);
-        qb[ks] = __builtin_bit_cast(v8bf16, w);
-    }
     m = -INFINITY;
     l = 0.0f;
 #pragma unroll
     for (int j = 0; j < CPL; ++j) acc[j] = v4f32{0.0f, 0.0f, 0.0f, 0.0f};
     const int ntiles = (tm.count() + 15) / 16;
+    const bool pseudo = zt != nullptr && col < G;
     uint4 kreg[kTilesPerRound][KS];
     uint4 vreg[kTilesPerRound][4];
     bool vvalid[kTilesPerRound][4];
@@ -130,10 +139,20 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
             }
         }
     };
-    issue(wave * kTilesPerRound);
+    const int first = wave * kTilesPerRound;
+    issue(first);
     mid();
-    for (int t0 = wave * kTilesPerRound; t0 < ntiles; t0 += 4 * kTilesPerRound) {
-        if (t0 != wave * kTilesPerRound) issue(t0);
+    for (int t0 = first; t0 < ntiles; t0 += 4 * kTilesPerRound) {
+        if (t0 != first) issue(t0);
+        // B operand of the logit product: query head `col` (zero for padding heads), requested after the
+        // round's K/V loads and not held across rounds
+        v8bf16 qb[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            uint4 w = make_uint4(0, 0, 0, 0);
+            if (col < G) w = *reinterpret_cast<const uint4*>(qh + col * D + 32 * ks + 8 * grp);
+            qb[ks] = __builtin_bit_cast(v8bf16, w);
+        }
 #pragma unroll
         for (int t = 0; t < kTilesPerRound; ++t) {
 #pragma unroll
@@ -141,7 +160,12 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
 #pragma unroll
             for (int e = 0; e < 4; ++e) vreg[t][e] = vvalid[t][e] ? vreg[t][e] : make_uint4(0, 0, 0, 0);
         }
-        // logits: lane holds head `col`, tokens 4*grp + i of each tile
+        // logits: lane holds head `col`, tokens 4*grp + i of each tile; the pseudo-logits join the max
+        // so that both weights stay at most 1 (they are read from LDS again below rather than held)
+        auto zpseudo = [&](int t, int i) {
+            return (pseudo && vvalid[t][i]) ? zt[col][div_small((t0 + t) * 16 + 4 * grp + i, tm.B, tm.invB)]
+                                            : -INFINITY;
+        };
         float z[kTilesPerRound][4];
         float rmax = -INFINITY;
 #pragma unroll
@@ -153,32 +177,37 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 z[t][i] = vvalid[t][i] ? scale * s[i] : -INFINITY;
-                rmax = fmaxf(rmax, z[t][i]);
+                rmax = fmaxf(rmax, fmaxf(z[t][i], zpseudo(t, i)));
             }
         }
         rmax = fmaxf(rmax, __shfl_xor(rmax, 16));
         rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
         const float m_new = fmaxf(m, rmax);
         if (m_new == -INFINITY) continue;  // nothing valid for this head yet (uniform per wave-round)
-        const float c = (m == -INFINITY) ? 0.0f : __expf(m - m_new);
-        m = m_new;
-        l *= c;
-        // rescale accumulator rows: row i holds head 4*grp + i, whose factor lives in lane 4*grp + i
+        if (m != -INFINITY) {  // a later round: rescale the running state
+            const float c = __expf(m - m_new);
+            l *= c;
+            // accumulator row i holds head 4*grp + i, whose factor lives in lane 4*grp + i
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float ci = __shfl(c, 4 * grp + i);
+            for (int i = 0; i < 4; ++i) {
+                const float ci = __shfl(c, 4 * grp + i);
 #pragma unroll
-            for (int j = 0; j < CPL; ++j) acc[j][i] *= ci;
+                for (int j = 0; j < CPL; ++j) acc[j][i] *= ci;
+            }
         }
+        m = m_new;
+        __asm__ volatile("" ::: "memory");  // re-read the pseudo-logits
         // P.V over the pair of tiles with v_mfma_f32_16x16x32_bf16: k-index 8*grp + e is token 4*grp + e
-        // of tile 0 for e < 4 and token 4*grp + e - 4 of tile 1 for e >= 4, in both operands. P is split
-        // into three bf16 terms (hi + mid + lo equals p to within 2^-27 relative).
+        // of tile 0 for e < 4 and token 4*grp + e - 4 of tile 1 for e >= 4, in both operands. The weight
+        // is split into three bf16 terms (hi + mid + lo equals it to within 2^-27 relative).
         v8bf16 pa[3];
 #pragma unroll
         for (int t = 0; t < kTilesPerRound; ++t)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float p = z[t][i] == -INFINITY ? 0.0f : __expf(z[t][i] - m);
+                const float zpi = zpseudo(t, i);
+                const float p = (z[t][i] == -INFINITY ? 0.0f : __expf(z[t][i] - m)) -
+                                (zpi == -INFINITY ? 0.0f : __expf(zpi - m));
                 l += p;
                 const short hi = f32_to_bf16_rne(p);
                 const float r1 = p - bf16_bits_to_f32(hi);
@@ -217,11 +246,9 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
     l += __shfl_xor(l, 32);
 }
 
-// Combine the four waves' exact states in LDS and write the item's partial. With `pseudo` (fused
-// step) the pseudo-terms of the item's selected blocks (sh.M, sh.L, sh.pa) come off first.
+// Combine the four waves' exact states in LDS and write the item's partial.
 template <int D, int G>
-__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part,
-                             bool pseudo) {
+__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part) {
     constexpr int CPL = D / 16;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -248,13 +275,6 @@ __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], Decod
             ll = ll * ca + sh.l[w][g] * cb;
             aa = aa * ca + sh.acc[w][g][i] * cb;
             mm = mn;
-        }
-        if (pseudo) {
-            // pseudo-logits never exceed log B + the exact maximum, so the factor stays finite
-            const float mp = sh.M[g];
-            const float e = (mm == -INFINITY || mp == -INFINITY) ? 0.0f : __expf(mp - mm);
-            ll -= e * sh.L[g];
-            aa -= e * sh.pa[g][i];
         }
         float* p = part + (size_t)g * (D + 2);
         if (i == 0) {
@@ -369,122 +389,6 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
     }
 }
 
-// Fused step: the chunks add the pseudo-terms (logit log|b| + zbar_b, value vmean_b) of every block,
-// so an exact item subtracts those of its selected blocks from its own partial (the exact state in
-// sh.em / sh.el / sh.ea). By Jensen's inequality a block's pseudo-weight |b| exp(zbar_b) never exceeds
-// its exact weight sum_j exp(z_j), so the difference stays a sum of non-negative terms. The loads are
-// issued before the exact tokens (PseudoPf) so their latency overlaps that work.
-constexpr int kPfRows = 2;    // mean-value rows per thread prefetched
-constexpr int kPfLogits = 2;  // block logits per thread prefetched
-static_assert(kPfLogits == 2, "pseudo_sums picks the prefetched logits by hand");
-
-struct PseudoPf {
-    float4 v[kPfRows];
-    float lg[kPfLogits];
-};
-
-template <int D, int G>
-__device__ __forceinline__ float4 pseudo_row(const DecodeArgs& a, const Geom& geo, int u, int X, int nblk,
-                                             const int* ids, int k) {
-    const int li = threadIdx.x % (D / 4);
-    const int b = k < nblk ? ids[k] : -1;
-    const bool ok = b >= 0 && b < X;  // invalid: row 0 of the unit, weighted by zero
-    return reinterpret_cast<const float4*>(a.vmean + ((size_t)u * geo.xcap + (ok ? b : 0)) * D)[li];
-}
-
-template <int G>
-__device__ __forceinline__ float pseudo_logit(const DecodeArgs& a, const Geom& geo, int u, int X, int nblk,
-                                              const int* ids, int idx) {
-    const int g = idx / nblk, k = idx - g * nblk;
-    const int b = idx < G * nblk ? ids[k] : -1;
-    const bool ok = b >= 0 && b < X;
-    return a.blk_logit[((size_t)u * G + (idx < G * nblk ? g : 0)) * geo.xcap + (ok ? b : 0)];
-}
-
-template <int D, int G>
-__device__ __forceinline__ void pseudo_prefetch(const DecodeArgs& a, const Geom& geo, int u, int X, int nblk,
-                                                const int* ids, PseudoPf& pf) {
-    constexpr int RPS = kThreads / (D / 4);
-    const int slot = threadIdx.x / (D / 4);
-#pragma unroll
-    for (int j = 0; j < kPfRows; ++j) pf.v[j] = pseudo_row<D, G>(a, geo, u, X, nblk, ids, slot + j * RPS);
-#pragma unroll
-    for (int j = 0; j < kPfLogits; ++j)
-        pf.lg[j] = nblk > 0 ? pseudo_logit<G>(a, geo, u, X, nblk, ids, threadIdx.x + j * kThreads) : 0.0f;
-}
-
-template <int D, int G>
-__device__ void pseudo_sums(const DecodeArgs& a, const Geom& geo, int u, int n, int X, int nblk, const PseudoPf& pf,
-                            DecodeShared<D, G>& sh) {
-    constexpr int LPB = D / 4, RPS = kThreads / LPB;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int li = tid % LPB, slot = tid / LPB;
-    for (int idx = tid, j = 0; idx < G * nblk; idx += kThreads, ++j) {
-        const int g = idx / nblk, k = idx % nblk, b = sh.sel[k];
-        const float lg = j < kPfLogits ? (j == 0 ? pf.lg[0] : pf.lg[1]) : pseudo_logit<G>(a, geo, u, X, nblk, sh.sel, idx);
-        sh.w[g][k] = (b >= 0 && b < X) ? logf((float)min(geo.B, n - b * geo.B)) + lg : -INFINITY;
-    }
-    __syncthreads();
-    for (int g = wave; g < G; g += 4) {
-        float mx = -INFINITY;
-        for (int k = lane; k < nblk; k += 64) mx = fmaxf(mx, sh.w[g][k]);
-        mx = wave_max(mx);
-        float sum = 0.0f;
-        for (int k = lane; k < nblk; k += 64) {
-            const float wv = (mx == -INFINITY || sh.w[g][k] == -INFINITY) ? 0.0f : __expf(sh.w[g][k] - mx);
-            sh.w[g][k] = wv;
-            sum += wv;
-        }
-        sum = wave_sum(sum);
-        if (lane == 0) {
-            sh.M[g] = mx;
-            sh.L[g] = sum;
-        }
-    }
-    __syncthreads();
-    float acc[G][4];
-#pragma unroll
-    for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
-    auto add_row = [&](int k, const float4& v4) {
-        if (k >= nblk) return;
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const float wv = sh.w[g][k];
-            acc[g][0] += wv * v4.x;
-            acc[g][1] += wv * v4.y;
-            acc[g][2] += wv * v4.z;
-            acc[g][3] += wv * v4.w;
-        }
-    };
-#pragma unroll
-    for (int j = 0; j < kPfRows; ++j) add_row(slot + j * RPS, pf.v[j]);
-    for (int k0 = slot + kPfRows * RPS; k0 < nblk; k0 += 4 * RPS) {  // larger items: 4 rows in flight
-        float4 v4[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) v4[j] = pseudo_row<D, G>(a, geo, u, X, nblk, sh.sel, k0 + j * RPS);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) add_row(k0 + j * RPS, v4[j]);
-    }
-#pragma unroll
-    for (int off = LPB; off < 64; off <<= 1)
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[g][e] += __shfl_xor(acc[g][e], off);
-    if (lane < LPB) {
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) sh.acc[wave][g][4 * li + e] = acc[g][e];
-    }
-    __syncthreads();
-    for (int idx = tid; idx < G * D; idx += kThreads) {
-        const int g = idx / D, i = idx % D;
-        sh.pa[g][i] = (sh.acc[0][g][i] + sh.acc[1][g][i]) + (sh.acc[2][g][i] + sh.acc[3][g][i]);
-    }
-    __syncthreads();
-}
-
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, DecodeArgs a, int nitems) {
     __shared__ DecodeShared<D, G> sh;
@@ -499,6 +403,7 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
         TokenMap tm;
         tm.dense = a.dense != 0;
         tm.B = geo.B;
+        tm.invB = 1.0f / (float)geo.B;
         tm.n = n;
         tm.X = X;
         if (tm.dense) {
@@ -519,14 +424,20 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
         float m, l;
         v4f32 acc[D / 16];
         const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+        // fused step: the block logits of the item's blocks, requested once its K/V loads are issued
         const bool pseudo = a.neg_pseudo && !tm.dense;
-        PseudoPf pf;
-        if (pseudo) pseudo_prefetch<D, G>(a, geo, u, X, tm.nblk, sh.sel, pf);
-        exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh, a.scale, m, l, acc,
-                           [&] {
-                               if (pseudo) pseudo_sums<D, G>(a, geo, u, n, X, tm.nblk, pf, sh);
+        exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh,
+                           pseudo ? sh.zb : nullptr, a.scale, m, l, acc, [&] {
+                               if (!pseudo) return;  // workgroup-uniform
+                               const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
+                               for (int idx = tid; idx < G * tm.nblk; idx += kThreads) {
+                                   const int g = idx / tm.nblk, k = idx - g * tm.nblk;
+                                   const int b = sh.sel[k];
+                                   sh.zb[g][k] = lg[(size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0)];
+                               }
+                               __syncthreads();
                            });
-        finish_exact<D, G>(m, l, acc, sh, part, pseudo);
+        finish_exact<D, G>(m, l, acc, sh, part);
     } else {
         const int c0 = (item - a.n_exact) * a.cb;
         compensation<D, G>(a, geo, u, n, X, c0, min(c0 + a.cb, X), sh, part);

@@ -126,10 +126,19 @@ struct TailShared {
     float z[G], v[G];
 };
 
+// A chunk workgroup and a last-block workgroup share one LDS allocation.
+template <int D, int G, bool kStep>
+union ChunkLds {
+    struct {
+        ChunkShared<D, G> sh;
+        std::conditional_t<kStep, CompShared<D, G>, NoComp> st;
+    } c;
+    TailShared<D, G> t;
+};
+
 // The extra workgroup of unit u: the last block X - 1 (refreshed first when the step appends).
 template <int D, int G, bool kStep>
-__device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u) {
-    __shared__ TailShared<D, G> ts;
+__device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShared<D, G>& ts) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int nc = a.nchunks;
@@ -215,17 +224,18 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u) {
 // PMAX = bpc / 32: block slots per thread (the chunk is 32 PMAX blocks).
 template <int D, int G, bool kStep, int PMAX>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
+    __shared__ ChunkLds<D, G, kStep> lds;
     const int units = geo.units();
     if ((int)blockIdx.x < units) {
-        score_tail<D, G, kStep>(geo, a, blockIdx.x);
+        score_tail<D, G, kStep>(geo, a, blockIdx.x, lds.t);
         return;
     }
     constexpr int NF4 = D / 32;           // float4 of the mean-key row per lane
     constexpr int LPB = D / 4;            // compensation: lanes per mean-value row (one float4 each)
     constexpr int RPS = kThreads / LPB;   // mean-value rows per workgroup step
     constexpr int VROWS = kStep ? 32 * PMAX / RPS : 1;
-    __shared__ ChunkShared<D, G> sh;
-    __shared__ std::conditional_t<kStep, CompShared<D, G>, NoComp> st;
+    ChunkShared<D, G>& sh = lds.c.sh;
+    auto& st = lds.c.st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = (blockIdx.x - units) / a.nchunks, chunk = (blockIdx.x - units) % a.nchunks;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
