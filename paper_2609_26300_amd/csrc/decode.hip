@@ -9,16 +9,17 @@
 // A second launch, grid = (units, G), merges each unit's partials in item order, so the result does
 // not depend on scheduling; the kernel boundary makes the partials visible (no cross-workgroup fences).
 //
-// Exact tokens run on the matrix cores, 16 tokens per wave and tile. The logits are formed as
-// S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = 16 key rows, B = the unit's query heads as columns,
+// Item workgroups have eight waves (kItemThreads). Exact tokens run on the matrix cores, one 16-token
+// tile per wave and round, so a 128-token item is one round of the eight waves. The logits are formed
+// as S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = 16 key rows, B = the unit's query heads as columns,
 // zero-padded to 16): lane l then holds the logits of head l%16 for tokens 4(l/16)..4(l/16)+3, which is
 // exactly the A-operand layout of v_mfma_f32_16x16x16bf16_1k, so the probabilities feed the P.V product
 // without any data movement. For P.V the value row of each of the lane's 4 tokens is loaded as one
 // contiguous chunk of d/16 coordinates (coordinate (d/16)*(l%16) + j goes to output block j), so every
-// load is a contiguous piece of a row. P.V runs as v_mfma_f32_16x16x32_bf16 over a pair of tiles, with
-// P split into three bf16 terms (three MFMAs), which keeps P within 2^-27 of its fp32 value (two terms,
-// 2^-17, are not enough for outputs that cancel to near zero); products with the bf16 values are exact
-// and accumulate in fp32. The softmax max is taken per pair of tiles.
+// load is a contiguous piece of a row. P.V runs as v_mfma_f32_16x16x16bf16_1k per tile, with P split
+// into three bf16 terms (three MFMAs), which keeps P within 2^-27 of its fp32 value (two terms, 2^-17,
+// are not enough for outputs that cancel to near zero); products with the bf16 values are exact and
+// accumulate in fp32. The softmax max is taken per tile.
 //
 // In the fused step the compensation partials already hold the pseudo-token of every block (logit
 // log|b| + zbar_b, value vmean_b), so an exact item takes its own blocks' pseudo-tokens back out. As
@@ -43,12 +44,13 @@ constexpr int kMaxItems = 256;     // items per unit and launch, upper bound (ch
 constexpr int kMaxPartials = 2048;  // partials per unit in a merge, upper bound
 constexpr int kCbMax = 512;     // blocks per compensation item, upper bound
 constexpr int kMaxEb = 128;     // selected blocks per exact item, upper bound
-constexpr int kTilesPerRound = 2;  // P.V pairs two 16-token tiles into one 32-deep MFMA
+constexpr int kItemWaves = 8;  // waves of an item workgroup
+constexpr int kItemThreads = 64 * kItemWaves;
 
 template <int D, int G>
 struct DecodeShared {
-    float m[4][G], l[4][G];
-    float acc[4][G][D];
+    float m[kItemWaves][G], l[kItemWaves][G];
+    float acc[kItemWaves][G][D];
     float w[G][kCbMax];  // compensation weights
     float zb[G][kMaxEb];  // fused step: the block logits of the exact item's selected blocks
     float M[G], L[G];
@@ -110,42 +112,38 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
     for (int j = 0; j < CPL; ++j) acc[j] = v4f32{0.0f, 0.0f, 0.0f, 0.0f};
     const int ntiles = (tm.count() + 15) / 16;
     const bool pseudo = zt != nullptr && col < G;
-    uint4 kreg[kTilesPerRound][KS];
-    uint4 vreg[kTilesPerRound][4];
-    bool vvalid[kTilesPerRound][4];
-    bool kvalid[kTilesPerRound];
-    // every load of a round is issued first (branch-free: a row past the item's tokens loads row 0 of
+    uint4 kreg[KS];
+    uint4 vreg[4];
+    bool vvalid[4];
+    bool kvalid;
+    // every load of a tile is issued first (branch-free: a row past the item's tokens loads row 0 of
     // the unit and is zeroed after)
-    auto issue = [&](int t0) {
+    auto issue = [&](int t) {
+        const int base = t * 16;
+        const int rk = t < ntiles ? tm.row(base + col) : -1;
+        kvalid = rk >= 0;
+        const uint16_t* kp = Ku + (size_t)(rk >= 0 ? rk : 0) * D + 8 * grp;
 #pragma unroll
-        for (int t = 0; t < kTilesPerRound; ++t) {
-            const int base = (t0 + t) * 16;
-            const int rk = (t0 + t < ntiles) ? tm.row(base + col) : -1;
-            kvalid[t] = rk >= 0;
-            const uint16_t* kp = Ku + (size_t)(rk >= 0 ? rk : 0) * D + 8 * grp;
+        for (int ks = 0; ks < KS; ++ks) kreg[ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kreg[t][ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int rv = (t0 + t < ntiles) ? tm.row(base + 4 * grp + e) : -1;
-                vvalid[t][e] = rv >= 0;
-                const uint16_t* vp = Vu + (size_t)(rv >= 0 ? rv : 0) * D + CPL * col;
-                if constexpr (CPL == 8) {
-                    vreg[t][e] = *reinterpret_cast<const uint4*>(vp);
-                } else {
-                    const uint2 hv = *reinterpret_cast<const uint2*>(vp);
-                    vreg[t][e] = make_uint4(hv.x, hv.y, 0, 0);
-                }
+        for (int e = 0; e < 4; ++e) {
+            const int rv = t < ntiles ? tm.row(base + 4 * grp + e) : -1;
+            vvalid[e] = rv >= 0;
+            const uint16_t* vp = Vu + (size_t)(rv >= 0 ? rv : 0) * D + CPL * col;
+            if constexpr (CPL == 8) {
+                vreg[e] = *reinterpret_cast<const uint4*>(vp);
+            } else {
+                const uint2 hv = *reinterpret_cast<const uint2*>(vp);
+                vreg[e] = make_uint4(hv.x, hv.y, 0, 0);
             }
         }
     };
-    const int first = wave * kTilesPerRound;
-    issue(first);
+    issue(wave);
     mid();
-    for (int t0 = first; t0 < ntiles; t0 += 4 * kTilesPerRound) {
-        if (t0 != first) issue(t0);
+    for (int t = wave; t < ntiles; t += kItemWaves) {
+        if (t != wave) issue(t);
         // B operand of the logit product: query head `col` (zero for padding heads), requested after the
-        // round's K/V loads and not held across rounds
+        // tile's K/V loads
         v8bf16 qb[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -154,31 +152,25 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
             qb[ks] = __builtin_bit_cast(v8bf16, w);
         }
 #pragma unroll
-        for (int t = 0; t < kTilesPerRound; ++t) {
+        for (int ks = 0; ks < KS; ++ks) kreg[ks] = kvalid ? kreg[ks] : make_uint4(0, 0, 0, 0);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) kreg[t][ks] = kvalid[t] ? kreg[t][ks] : make_uint4(0, 0, 0, 0);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) vreg[t][e] = vvalid[t][e] ? vreg[t][e] : make_uint4(0, 0, 0, 0);
-        }
-        // logits: lane holds head `col`, tokens 4*grp + i of each tile; the pseudo-logits join the max
-        // so that both weights stay at most 1 (they are read from LDS again below rather than held)
-        auto zpseudo = [&](int t, int i) {
-            return (pseudo && vvalid[t][i]) ? zt[col][div_small((t0 + t) * 16 + 4 * grp + i, tm.B, tm.invB)]
-                                            : -INFINITY;
+        for (int e = 0; e < 4; ++e) vreg[e] = vvalid[e] ? vreg[e] : make_uint4(0, 0, 0, 0);
+        // logits: lane holds head `col`, tokens 4*grp + i of the tile; the pseudo-logits join the max so
+        // that both weights stay at most 1
+        auto zpseudo = [&](int i) {
+            return (pseudo && vvalid[i]) ? zt[col][div_small(t * 16 + 4 * grp + i, tm.B, tm.invB)] : -INFINITY;
         };
-        float z[kTilesPerRound][4];
+        v4f32 sv = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            sv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf16, kreg[ks]), qb[ks], sv, 0, 0, 0);
+        float z[4], zp[4];
         float rmax = -INFINITY;
 #pragma unroll
-        for (int t = 0; t < kTilesPerRound; ++t) {
-            v4f32 s = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf16, kreg[t][ks]), qb[ks], s, 0, 0, 0);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                z[t][i] = vvalid[t][i] ? scale * s[i] : -INFINITY;
-                rmax = fmaxf(rmax, fmaxf(z[t][i], zpseudo(t, i)));
-            }
+        for (int i = 0; i < 4; ++i) {
+            z[i] = vvalid[i] ? scale * sv[i] : -INFINITY;
+            zp[i] = zpseudo(i);
+            rmax = fmaxf(rmax, fmaxf(z[i], zp[i]));
         }
         rmax = fmaxf(rmax, __shfl_xor(rmax, 16));
         rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
@@ -196,57 +188,46 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
             }
         }
         m = m_new;
-        __asm__ volatile("" ::: "memory");  // re-read the pseudo-logits
-        // P.V over the pair of tiles with v_mfma_f32_16x16x32_bf16: k-index 8*grp + e is token 4*grp + e
-        // of tile 0 for e < 4 and token 4*grp + e - 4 of tile 1 for e >= 4, in both operands. The weight
-        // is split into three bf16 terms (hi + mid + lo equals it to within 2^-27 relative).
-        v8bf16 pa[3];
+        // P.V with v_mfma_f32_16x16x16bf16_1k: k-index 4*grp + e is token 4*grp + e in both operands.
+        // The weight is split into three bf16 terms (hi + mid + lo equals it to within 2^-27 relative).
+        v4i16 pa[3];
 #pragma unroll
-        for (int t = 0; t < kTilesPerRound; ++t)
+        for (int i = 0; i < 4; ++i) {
+            const float p = (z[i] == -INFINITY ? 0.0f : __expf(z[i] - m)) - (zp[i] == -INFINITY ? 0.0f : __expf(zp[i] - m));
+            l += p;
+            const short hi = f32_to_bf16_rne(p);
+            const float r1 = p - bf16_bits_to_f32(hi);
+            const short md = f32_to_bf16_rne(r1);
+            const short lo = f32_to_bf16_rne(r1 - bf16_bits_to_f32(md));
+            pa[0][i] = hi;
+            pa[1][i] = md;
+            pa[2][i] = lo;
+        }
+        const uint32_t* w[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float zpi = zpseudo(t, i);
-                const float p = (z[t][i] == -INFINITY ? 0.0f : __expf(z[t][i] - m)) -
-                                (zpi == -INFINITY ? 0.0f : __expf(zpi - m));
-                l += p;
-                const short hi = f32_to_bf16_rne(p);
-                const float r1 = p - bf16_bits_to_f32(hi);
-                const short mid = f32_to_bf16_rne(r1);
-                const short lo = f32_to_bf16_rne(r1 - bf16_bits_to_f32(mid));
-                pa[0][4 * t + i] = __builtin_bit_cast(__bf16, hi);
-                pa[1][4 * t + i] = __builtin_bit_cast(__bf16, mid);
-                pa[2][4 * t + i] = __builtin_bit_cast(__bf16, lo);
-            }
-        const uint32_t* w[2][4];
-#pragma unroll
-        for (int t = 0; t < kTilesPerRound; ++t)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) w[t][e] = reinterpret_cast<const uint32_t*>(&vreg[t][e]);
+        for (int e = 0; e < 4; ++e) w[e] = reinterpret_cast<const uint32_t*>(&vreg[e]);
 #pragma unroll
         for (int j = 0; j < CPL; ++j) {
-            // B operand for output block j: element 8*grp + e = coordinate CPL*col + j of that token
+            // B operand for output block j: element 4*grp + e = coordinate CPL*col + j of token 4*grp + e
             const int wi = j >> 1;
-            uint32_t pk[4];
-#pragma unroll
-            for (int t = 0; t < kTilesPerRound; ++t) {
-                if ((j & 1) == 0) {
-                    pk[2 * t] = (w[t][0][wi] & 0xFFFFu) | (w[t][1][wi] << 16);
-                    pk[2 * t + 1] = (w[t][2][wi] & 0xFFFFu) | (w[t][3][wi] << 16);
-                } else {
-                    pk[2 * t] = (w[t][0][wi] >> 16) | (w[t][1][wi] & 0xFFFF0000u);
-                    pk[2 * t + 1] = (w[t][2][wi] >> 16) | (w[t][3][wi] & 0xFFFF0000u);
-                }
+            uint32_t pk0, pk1;
+            if ((j & 1) == 0) {
+                pk0 = (w[0][wi] & 0xFFFFu) | (w[1][wi] << 16);
+                pk1 = (w[2][wi] & 0xFFFFu) | (w[3][wi] << 16);
+            } else {
+                pk0 = (w[0][wi] >> 16) | (w[1][wi] & 0xFFFF0000u);
+                pk1 = (w[2][wi] >> 16) | (w[3][wi] & 0xFFFF0000u);
             }
-            const v8bf16 bv = __builtin_bit_cast(v8bf16, make_uint4(pk[0], pk[1], pk[2], pk[3]));
+            const v4i16 bv = __builtin_bit_cast(v4i16, make_uint2(pk0, pk1));
 #pragma unroll
-            for (int k = 0; k < 3; ++k) acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[k], bv, acc[j], 0, 0, 0);
+            for (int k = 0; k < 3; ++k) acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[k], bv, acc[j], 0, 0, 0);
         }
     }
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
 }
 
-// Combine the four waves' exact states in LDS and write the item's partial.
+// Combine the waves' exact states in LDS and write the item's partial.
 template <int D, int G>
 __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part) {
     constexpr int CPL = D / 16;
@@ -265,11 +246,11 @@ __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], Decod
         }
     }
     __syncthreads();
-    for (int idx = tid; idx < G * D; idx += kThreads) {
+    for (int idx = tid; idx < G * D; idx += kItemThreads) {
         const int g = idx / D, i = idx % D;
         float mm = -INFINITY, ll = 0.0f, aa = 0.0f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
+        for (int w = 0; w < kItemWaves; ++w) {
             float mn, ca, cb;
             merge_scales(mm, sh.m[w][g], mn, ca, cb);
             ll = ll * ca + sh.l[w][g] * cb;
@@ -290,8 +271,8 @@ template <int D, int G>
 __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n, int X, int c0, int c1,
                              DecodeShared<D, G>& sh, float* part) {
     constexpr int LPB = D / 4;          // lanes per mean-value row (one float4 each)
-    constexpr int RPS = kThreads / LPB;  // rows per workgroup step
-    constexpr int ROWS = 16;             // rows in flight per thread
+    constexpr int RPS = kItemThreads / LPB;  // rows per workgroup step
+    constexpr int ROWS = 8;                  // rows in flight per thread
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int nb = max(0, c1 - c0);
     const int li = tid % LPB, slot = tid / LPB;
@@ -306,22 +287,22 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
     }
     const int nsel = min(a.n_sel[u], a.sel_stride);
     const int32_t* selu = a.sel + (size_t)u * a.sel_stride;
-    for (int i = tid; i < nb; i += kThreads) sh.flag[i] = 0;
+    for (int i = tid; i < nb; i += kItemThreads) sh.flag[i] = 0;
     __syncthreads();
-    for (int k = tid; k < nsel; k += kThreads) {
+    for (int k = tid; k < nsel; k += kItemThreads) {
         const int sb = selu[k];
         if (sb >= c0 && sb < c1) sh.flag[sb - c0] = 1;
     }
     __syncthreads();
     // pseudo-logits log|b| + zbar and their per-head max
     const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
-    for (int idx = tid; idx < G * nb; idx += kThreads) {
+    for (int idx = tid; idx < G * nb; idx += kItemThreads) {
         const int g = idx / nb, lb = idx % nb, b = c0 + lb;
         sh.w[g][lb] = sh.flag[lb] ? -INFINITY
                                   : logf((float)min(geo.B, n - b * geo.B)) + lg[(size_t)g * geo.xcap + b];
     }
     __syncthreads();
-    for (int g = wave; g < G; g += 4) {
+    for (int g = wave; g < G; g += kItemWaves) {
         float mx = -INFINITY;
         for (int lb = lane; lb < nb; lb += 64) mx = fmaxf(mx, sh.w[g][lb]);
         mx = wave_max(mx);
@@ -364,7 +345,7 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
             }
         }
     }
-    // reduce over row slots: lanes li and li + LPB of a wave, then the four waves
+    // reduce over row slots: lanes li and li + LPB of a wave, then the waves in order
 #pragma unroll
     for (int off = LPB; off < 64; off <<= 1)
 #pragma unroll
@@ -378,19 +359,24 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
             for (int e = 0; e < 4; ++e) sh.acc[wave][g][4 * li + e] = acc[g][e];
     }
     __syncthreads();
-    for (int idx = tid; idx < G * D; idx += kThreads) {
+    for (int idx = tid; idx < G * D; idx += kItemThreads) {
         const int g = idx / D, i = idx % D;
         float* p = part + (size_t)g * (D + 2);
         if (i == 0) {
             p[0] = sh.M[g];
             p[1] = sh.L[g];
         }
-        p[2 + i] = sh.acc[0][g][i] + sh.acc[1][g][i] + sh.acc[2][g][i] + sh.acc[3][g][i];
+        float tot = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kItemWaves; ++w) tot += sh.acc[w][g][i];
+        p[2 + i] = tot;
     }
 }
 
+// Two workgroups per CU (at most 128 registers per lane).
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, DecodeArgs a, int nitems) {
+__global__ __launch_bounds__(kItemThreads) __attribute__((amdgpu_waves_per_eu(4))) void decode_items_kernel(
+    Geom geo, DecodeArgs a, int nitems) {
     __shared__ DecodeShared<D, G> sh;
     const int tid = threadIdx.x;
     const int u = blockIdx.y, item = blockIdx.x;
@@ -416,7 +402,7 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
             const int e0 = item * a.eb;
             tm.nblk = max(0, min(a.eb, nsel - e0));
             const int32_t* selu = a.sel + (size_t)u * a.sel_stride + e0;
-            for (int k = tid; k < tm.nblk; k += kThreads) sh.sel[k] = selu[k];
+            for (int k = tid; k < tm.nblk; k += kItemThreads) sh.sel[k] = selu[k];
             __syncthreads();
             tm.sel = sh.sel;
             tm.t0 = tm.t1 = 0;
@@ -430,7 +416,7 @@ __global__ __launch_bounds__(kThreads) void decode_items_kernel(Geom geo, Decode
                            pseudo ? sh.zb : nullptr, a.scale, m, l, acc, [&] {
                                if (!pseudo) return;  // workgroup-uniform
                                const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
-                               for (int idx = tid; idx < G * tm.nblk; idx += kThreads) {
+                               for (int idx = tid; idx < G * tm.nblk; idx += kItemThreads) {
                                    const int g = idx / tm.nblk, k = idx - g * tm.nblk;
                                    const int b = sh.sel[k];
                                    sh.zb[g][k] = lg[(size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0)];
@@ -531,7 +517,7 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, Decode
 
 template <int D, int G>
 hipError_t items_g(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
-    decode_items_kernel<D, G><<<dim3(items, g.units()), kThreads, 0, s>>>(g, a, items);
+    decode_items_kernel<D, G><<<dim3(items, g.units()), kItemThreads, 0, s>>>(g, a, items);
     return hipGetLastError();
 }
 
