@@ -38,10 +38,10 @@ def lib():
         L.orc_group_of.argtypes = [c_int, c_int, c_int, c_int]
         L.orc_block_stats.argtypes = [u16p, u16p, c_int, c_int, c_int, c_int, c_int, f64p, f64p, f64p]
         L.orc_block_scores.argtypes = [u16p, c_int, f64p, f64p, c_int, c_int, c_int, c_int, c_int,
-                                       c_double, f64p, f64p, f64p, f64p]
+                                       c_double, c_int, f64p, f64p, f64p, f64p]
         L.orc_select.argtypes = [f64p, c_int, c_int, c_int, c_int, i32p]
         L.orc_sparse_decode.argtypes = [u16p, c_int, u16p, u16p, f64p, f64p, c_int, c_int, c_int,
-                                        c_double, i32p, c_int, f64p, f64p]
+                                        c_double, i32p, c_int, c_int, f64p, f64p]
         L.orc_dense_decode.argtypes = [u16p, c_int, u16p, u16p, c_int, c_int, c_double, f64p, f64p]
         _lib = L
     return _lib
@@ -84,7 +84,15 @@ def block_stats(K, V, n: int, B: int, r: int, layout: int = ROTATE_HALF):
     return kmean[:X], dvar[:X], vmean[:X]
 
 
-def block_scores(q, kmean, dvar, n: int, B: int, r: int, scale: float, layout: int = ROTATE_HALF):
+# score kinds (Section 5.4 ablations): the CompKV score, the mass-only score sum_g phat, and the
+# first-order score whose mass estimate uses the mean-key logits alone
+SCORE_COMPKV = 0
+SCORE_MASS = 1
+SCORE_FIRST_ORDER = 2
+
+
+def block_scores(q, kmean, dvar, n: int, B: int, r: int, scale: float, layout: int = ROTATE_HALF,
+                 kind: int = SCORE_COMPKV):
     """dict(zbar, sig2, phat [G][X], score [X]) for the G query heads q ([G][d] bf16 bits)."""
     q = _u16(q)
     G, d = q.shape
@@ -94,9 +102,10 @@ def block_scores(q, kmean, dvar, n: int, B: int, r: int, scale: float, layout: i
     km[:X], dv[:X] = kmean[:X], dvar[:X]
     zbar, sig2, phat = (np.zeros((G, max(X, 1))) for _ in range(3))
     score = np.zeros(max(X, 1))
-    rc = lib().orc_block_scores(q, G, km, dv, n, d, B, r, layout, float(scale), zbar, sig2, phat, score)
+    rc = lib().orc_block_scores(q, G, km, dv, n, d, B, r, layout, float(scale), int(kind), zbar, sig2, phat,
+                                score)
     if rc != 0:
-        raise OracleError(f"invalid (d={d}, r={r}, layout={layout}, B={B})")
+        raise OracleError(f"invalid (d={d}, r={r}, layout={layout}, B={B}, kind={kind})")
     return dict(zbar=zbar[:, :X], sig2=sig2[:, :X], phat=phat[:, :X], score=score[:X])
 
 
@@ -111,8 +120,9 @@ def select(score, K: int, n_sink: int = 1, n_recent: int = 2) -> np.ndarray:
     return sel[:cnt].copy()
 
 
-def sparse_decode(q, K, V, kmean, vmean, n: int, B: int, scale: float, sel):
-    """Compensated output (out [G][d], lse [G]) for the selected ids ``sel``."""
+def sparse_decode(q, K, V, kmean, vmean, n: int, B: int, scale: float, sel, compensate: bool = True):
+    """Compensated output (out [G][d], lse [G]) for the selected ids ``sel``; with compensate=False the
+    Drop output (the selected tokens alone, renormalized)."""
     q, K, V = _u16(q), _u16(K), _u16(V)
     G, d = q.shape
     X = num_blocks(n, B)
@@ -123,7 +133,8 @@ def sparse_decode(q, K, V, kmean, vmean, n: int, B: int, scale: float, sel):
     out = np.zeros((G, d))
     lse = np.zeros(G)
     rc = lib().orc_sparse_decode(q, G, K, V, km, vm, n, d, B, float(scale),
-                                 sel if sel.size else np.zeros(1, np.int32), int(sel.size), out, lse)
+                                 sel if sel.size else np.zeros(1, np.int32), int(sel.size), int(bool(compensate)),
+                                 out, lse)
     if rc != 0:
         raise OracleError("selected ids out of range or repeated")
     return out, lse
@@ -140,10 +151,10 @@ def dense_decode(q, K, V, n: int, scale: float):
 
 
 def unit_step(q, K, V, n: int, B: int, r: int, budget: int, scale: float, layout: int = ROTATE_HALF,
-              n_sink: int = 1, n_recent: int = 2):
+              n_sink: int = 1, n_recent: int = 2, kind: int = SCORE_COMPKV, compensate: bool = True):
     """Whole decode step of one unit: stats, scores, selection and compensated output."""
     kmean, dvar, vmean = block_stats(K, V, n, B, r, layout)
-    sc = block_scores(q, kmean, dvar, n, B, r, scale, layout)
+    sc = block_scores(q, kmean, dvar, n, B, r, scale, layout, kind)
     sel = select(sc["score"], budget, n_sink, n_recent)
-    out, lse = sparse_decode(q, K, V, kmean, vmean, n, B, scale, sel)
+    out, lse = sparse_decode(q, K, V, kmean, vmean, n, B, scale, sel, compensate)
     return dict(kmean=kmean, dvar=dvar, vmean=vmean, sel=sel, out=out, lse=lse, **sc)

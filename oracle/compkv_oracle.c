@@ -103,12 +103,18 @@ int orc_block_stats(const uint16_t* K, const uint16_t* V, int n, int d, int B, i
  *   phat[g][b] = |b| exp(zbar + sig2/2) / sum_c |c| exp(zbar_c + sig2_c/2), per query head, over
  *                every block                                          (Eq. compkv-mass-estimate)
  *   score[b]   = sum_g phat[g][b] sig2[g][b]                           (Eq. compkv-score)
- * q is [G][d] bf16 bits. Returns 0, or -1 for an invalid (d, r, layout).
+ * kind selects the score of the ablations of Section 5.4:
+ *   0  the CompKV score above;
+ *   1  mass only: score[b] = sum_g phat[g][b] (the second-order mass estimate, no variance factor);
+ *   2  first order: phat from the mean-key logits alone, |b| exp(zbar) normalized over the blocks,
+ *      and score[b] = sum_g phat[g][b] sig2[g][b].
+ * phat receives the mass estimate the score uses. q is [G][d] bf16 bits. Returns 0, or -1 for an
+ * invalid (d, r, layout) or kind.
  */
 int orc_block_scores(const uint16_t* q, int G, const double* kmean, const double* dvar, int n, int d,
-                     int B, int r, int layout, double scale, double* zbar, double* sig2, double* phat,
-                     double* score) {
-    if (orc_group_of(0, d, r, layout) < 0 || B <= 0) return -1;
+                     int B, int r, int layout, double scale, int kind, double* zbar, double* sig2,
+                     double* phat, double* score) {
+    if (orc_group_of(0, d, r, layout) < 0 || B <= 0 || kind < 0 || kind > 2) return -1;
     int X = orc_num_blocks(n, B);
     double* Qg = (double*)calloc((size_t)r, sizeof(double));
     double* logw = (double*)malloc((size_t)(X > 0 ? X : 1) * sizeof(double));
@@ -129,8 +135,8 @@ int orc_block_scores(const uint16_t* q, int G, const double* kmean, const double
             for (int t = 0; t < r; ++t) v += Qg[t] * dvar[(size_t)b * r + t];
             zbar[(size_t)g * X + b] = scale * z;
             sig2[(size_t)g * X + b] = scale * scale * v;
-            logw[b] = log((double)orc_block_len(n, B, b)) + zbar[(size_t)g * X + b] +
-                      0.5 * sig2[(size_t)g * X + b];
+            logw[b] = log((double)orc_block_len(n, B, b)) + zbar[(size_t)g * X + b];
+            if (kind != 2) logw[b] += 0.5 * sig2[(size_t)g * X + b];
         }
         double m = -INFINITY;
         for (int b = 0; b < X; ++b)
@@ -139,7 +145,7 @@ int orc_block_scores(const uint16_t* q, int G, const double* kmean, const double
         for (int b = 0; b < X; ++b) den += exp(logw[b] - m);
         for (int b = 0; b < X; ++b) {
             phat[(size_t)g * X + b] = exp(logw[b] - m) / den;
-            score[b] += phat[(size_t)g * X + b] * sig2[(size_t)g * X + b];
+            score[b] += kind == 1 ? phat[(size_t)g * X + b] : phat[(size_t)g * X + b] * sig2[(size_t)g * X + b];
         }
     }
     free(Qg);
@@ -208,12 +214,14 @@ int orc_select(const double* score, int X, int K, int n_sink, int n_recent, int*
  * Compensated output (Eq. compkv-output): tokens of selected blocks enter with their exact logits
  * z = s q_g . k_j and values v_j; every unselected block enters once with logit log|b| + zbar_b
  * (its |b| tokens all carry the block-mean logit) and value vmean_b. zbar_b is recomputed here from
- * kmean. out is [G][d]; lse[g] is the natural log of the compensated normalizer.
+ * kmean. With compensate == 0 the unselected blocks are left out altogether (Drop: attention
+ * renormalized over the selected tokens, Appendix A.5). out is [G][d]; lse[g] is the natural log of
+ * the normalizer; with no term at all out is 0 and lse is -inf.
  * Returns 0, or -1 if sel holds an out-of-range or repeated id.
  */
 int orc_sparse_decode(const uint16_t* q, int G, const uint16_t* K, const uint16_t* V,
                       const double* kmean, const double* vmean, int n, int d, int B, double scale,
-                      const int* sel, int n_sel, double* out, double* lse) {
+                      const int* sel, int n_sel, int compensate, double* out, double* lse) {
     int X = orc_num_blocks(n, B);
     unsigned char* in_s = (unsigned char*)calloc((size_t)(X > 0 ? X : 1), 1);
     double* logit = (double*)malloc((size_t)(n + X + 1) * sizeof(double));
@@ -242,7 +250,7 @@ int orc_sparse_decode(const uint16_t* q, int G, const uint16_t* K, const uint16_
                     for (int i = 0; i < d; ++i) z += bf16(qg[i]) * bf16(K[(size_t)j * d + i]);
                     logit[m_terms++] = scale * z;
                 }
-            } else {
+            } else if (compensate) {
                 double z = 0.0;
                 for (int i = 0; i < d; ++i) z += bf16(qg[i]) * kmean[(size_t)b * d + i];
                 logit[m_terms++] = log((double)nb) + scale * z;
@@ -264,11 +272,15 @@ int orc_sparse_decode(const uint16_t* q, int G, const uint16_t* K, const uint16_
                     den += w;
                     for (int i = 0; i < d; ++i) o[i] += w * bf16(V[(size_t)j * d + i]);
                 }
-            } else {
+            } else if (compensate) {
                 double w = exp(logit[k++] - m);
                 den += w;
                 for (int i = 0; i < d; ++i) o[i] += w * vmean[(size_t)b * d + i];
             }
+        }
+        if (m_terms == 0) {
+            lse[g] = -INFINITY;
+            continue;
         }
         for (int i = 0; i < d; ++i) o[i] /= den;
         lse[g] = m + log(den);

@@ -454,3 +454,125 @@ def test_completed_blocks_unchanged_by_appends():
         grown = oracle.block_stats(K, V, n + extra, B, 4)
         for a, b in zip(base, grown):
             assert np.array_equal(a[: n // B], b[: n // B])
+
+
+# ---------------------------------------------------------------- ablation variants (Section 5.4, App. A.5)
+
+def test_mass_only_score_block_size_one_is_exact_mass():
+    """B = 1: sigma-hat^2 = 0, so the second-order mass estimate is the exact softmax mass of each token
+    and the mass-only score is sum_g p_{g,b}; its scores sum to G over the blocks."""
+    n, d, G = 40, 16, 3
+    q, K, V = rand_unit(31, n, d, G, qscale=2.0)
+    s = 1 / math.sqrt(d)
+    km, dv, vm = oracle.block_stats(K, V, n, 1, 4)
+    sc = oracle.block_scores(q, km, dv, n, 1, 4, s, kind=oracle.SCORE_MASS)
+    z = dg.exact_logits(q, K, n, s)
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    assert np.allclose(sc["score"], p.sum(axis=0), rtol=1e-12, atol=1e-15)
+    assert sc["score"].sum() == pytest.approx(G, rel=1e-13)
+
+
+def test_first_order_vs_second_order_mass_on_plus_minus_block():
+    """Three blocks with identical keys inside blocks 0 and 2 and a +-a block 1: the first-order
+    estimate weighs block 1 by |b| e^{zbar} alone, the second-order one by |b| e^{zbar + x^2/2}, so the
+    ratio of their block-1-to-block-0 odds is e^{x^2/2} (Section 5.4; a dropped 1/2 fails). With no
+    within-block spread (blocks 0 and 2) both equal the exact mass ratios."""
+    d, B, i, a = 8, 4, 3, 0.5
+    base = np.array([1.0, -0.5, 0.25, 2.0, -1.0, 0.75, 0.125, -2.0], np.float32)
+    rows = []
+    for blk in range(3):
+        for j in range(B):
+            k = (base + blk).copy()
+            if blk == 1:
+                k[i] += a if j % 2 == 0 else -a
+            rows.append(k)
+    K = f32_to_bf16_bits(np.array(rows))
+    V = f32_to_bf16_bits(np.ones((3 * B, d), np.float32))
+    q = f32_to_bf16_bits(np.array([[0.5, 1.0, -1.5, 2.0, 0.25, -0.75, 1.25, 0.5]], np.float32))
+    n, s = 3 * B, 1 / math.sqrt(d)
+    x = s * 2.0 * a
+    km, dv, vm = oracle.block_stats(K, V, n, B, d)
+    p2 = oracle.block_scores(q, km, dv, n, B, d, s)["phat"][0]
+    f = oracle.block_scores(q, km, dv, n, B, d, s, kind=oracle.SCORE_FIRST_ORDER)
+    p1 = f["phat"][0]
+    assert (p2[1] / p2[0]) / (p1[1] / p1[0]) == pytest.approx(math.exp(x * x / 2), rel=1e-12)
+    bx = dg.block_exact(dg.exact_logits(q, K, n, s), n, B)
+    assert p1[2] / p1[0] == pytest.approx(bx["p"][0, 2] / bx["p"][0, 0], rel=1e-12)
+    # first-order score = p-hat^(1) sigma-hat^2: only the spread block scores
+    assert f["score"][0] == 0.0 and f["score"][2] == 0.0
+    assert f["score"][1] == pytest.approx(p1[1] * x * x, rel=1e-12)
+
+
+def test_first_order_equals_exact_mass_for_identical_keys():
+    """Identical keys within every block: Z_b = |b| e^{zbar_b} exactly, so both mass estimates equal the
+    exact block masses and every score kind that carries sigma-hat^2 is zero."""
+    n, d, G, B = 96, 16, 2, 8
+    rng = np.random.default_rng(5)
+    X = n // B
+    K = f32_to_bf16_bits(np.repeat(rng.standard_normal((X, d)).astype(np.float32), B, axis=0))
+    V = f32_to_bf16_bits(rng.standard_normal((n, d)).astype(np.float32))
+    q = f32_to_bf16_bits(2 * rng.standard_normal((G, d)).astype(np.float32))
+    s = 1 / math.sqrt(d)
+    km, dv, vm = oracle.block_stats(K, V, n, B, 4)
+    bx = dg.block_exact(dg.exact_logits(q, K, n, s), n, B)
+    for kind in (oracle.SCORE_COMPKV, oracle.SCORE_FIRST_ORDER):
+        sc = oracle.block_scores(q, km, dv, n, B, 4, s, kind=kind)
+        assert np.allclose(sc["phat"], bx["p"], rtol=1e-11)
+        assert np.all(sc["score"] == 0.0)
+    mass = oracle.block_scores(q, km, dv, n, B, 4, s, kind=oracle.SCORE_MASS)["score"]
+    assert np.allclose(mass, bx["p"].sum(axis=0), rtol=1e-11)
+
+
+def test_drop_decode_is_renormalized_attention_over_selected_tokens():
+    """Drop (Appendix A.5): softmax over the selected tokens only, written out with NumPy; every block
+    selected gives dense attention; lse_dense - lse_drop = -log sum_{b in S} p_b (Eq. app-drop-kl);
+    and lse_drop <= lse_mean <= lse_dense (Eq. app-mean-drop-ordering), strict when a block is omitted."""
+    n, d, G, B = 70, 16, 3, 8
+    q, K, V = blocky_unit(12, n, d, G, B, qscale=3.0)
+    s = 0.3
+    X = -(-n // B)
+    km, dv, vm = oracle.block_stats(K, V, n, B, 4)
+    z = dg.exact_logits(q, K, n, s)
+    bx = dg.block_exact(z, n, B)
+    Vf = bf16_bits_to_f32(V).astype(np.float64)
+    od, ld = oracle.dense_decode(q, K, V, n, s)
+    rng = np.random.default_rng(3)
+    for _ in range(5):
+        sel = np.sort(rng.choice(X, size=rng.integers(1, X), replace=False)).astype(np.int32)
+        o, l = oracle.sparse_decode(q, K, V, km, vm, n, B, s, sel, compensate=False)
+        keep = np.concatenate([np.arange(b * B, min(b * B + B, n)) for b in sel])
+        zs = z[:, keep]
+        w = np.exp(zs - zs.max(axis=1, keepdims=True))
+        ref = (w @ Vf[keep]) / w.sum(axis=1, keepdims=True)
+        assert relerr(o, ref) < 1e-12
+        assert np.allclose(ld - l, -np.log(bx["p"][:, sel].sum(axis=1)), rtol=1e-10, atol=1e-13)
+        om, lm = oracle.sparse_decode(q, K, V, km, vm, n, B, s, sel)
+        assert np.all(l < lm) and np.all(lm < ld + 1e-12)
+    o, l = oracle.sparse_decode(q, K, V, km, vm, n, B, s, np.arange(X, dtype=np.int32), compensate=False)
+    assert relerr(o, od) < 1e-12 and np.allclose(l, ld, rtol=1e-13)
+    # nothing selected: no term at all
+    o, l = oracle.sparse_decode(q, K, V, km, vm, n, B, s, np.zeros(0, np.int32), compensate=False)
+    assert np.all(o == 0.0) and np.all(np.isinf(l)) and np.all(l < 0)
+
+
+def test_llama_workload_offset_blocks_mass_vs_compkv():
+    """The Llama-shaped 32K layer gives 5% of its blocks a shared key offset along the unit's mean query
+    with a small spread: high attention mass, little within-block variation, so Mean compensation
+    already reconstructs them well (Sections 3.2 and 4.1). The mass-only score selects every one of
+    them; the CompKV score (and its first-order variant) spends no exact read on them."""
+    from workloads import WORKLOADS, gen_queries, gen_unit_kv, offset_blocks
+
+    w = WORKLOADS["llama8b_32k"]
+    n, B, G = w.context, w.block_size, w.group
+    K, V = gen_unit_kv(w, 0, 0, 0)
+    q = gen_queries(w, 0, 0, 0)[:G]
+    off = set(offset_blocks(w, 0, 0, 0).tolist())
+    assert len(off) == 51
+    km, dv, vm = oracle.block_stats(K, V, n, B, 4)
+    picked = {}
+    for kind in (oracle.SCORE_COMPKV, oracle.SCORE_MASS, oracle.SCORE_FIRST_ORDER):
+        sc = oracle.block_scores(q, km, dv, n, B, 4, 1 / math.sqrt(w.head_dim), kind=kind)
+        picked[kind] = len(off & set(oracle.select(sc["score"], w.budget_blocks).tolist()))
+    assert picked[oracle.SCORE_MASS] == 51
+    assert picked[oracle.SCORE_COMPKV] == 0 and picked[oracle.SCORE_FIRST_ORDER] == 0

@@ -12,4 +12,5 @@ from .gqa_decode import (  # noqa: F401
     gen_unit_kv,
     gen_queries,
     gen_layer,
+    offset_blocks,
 )

@@ -127,6 +127,17 @@ def gen_queries(w: Workload, layer: int, b: int, step: int = 0) -> np.ndarray:
     return f32_to_bf16_bits(q)
 
 
+def offset_blocks(w: Workload, layer: int, b: int, h: int) -> np.ndarray:
+    """Ids of the blocks of one unit that carry the shared high-mass key offset (none unless
+    ``offset_frac`` > 0); the sink block and the two most recent blocks are never chosen."""
+    if w.offset_frac <= 0:
+        return np.zeros(0, dtype=np.int64)
+    x_ctx = -(-w.context // w.block_size)
+    cand = np.arange(1, max(1, x_ctx - 2))
+    n_off = min(len(cand), int(round(w.offset_frac * x_ctx)))
+    return _rng(w, layer, b, h, _TAG_OFFSET).choice(cand, size=n_off, replace=False)
+
+
 def gen_unit_kv(w: Workload, layer: int, b: int, h: int) -> tuple[np.ndarray, np.ndarray]:
     """bf16 bits of the keys and values of one (layer, batch element, KV head) unit.
 
@@ -145,10 +156,7 @@ def gen_unit_kv(w: Workload, layer: int, b: int, h: int) -> tuple[np.ndarray, np
         qs = bf16_bits_to_f32(gen_queries(w, layer, b, 0))[h * w.group:(h + 1) * w.group]
         qbar = qs.astype(np.float64).mean(axis=0)
         delta = w.offset_logit * math.sqrt(d) * qbar / float(qbar @ qbar)
-        x_ctx = -(-w.context // B)
-        cand = np.arange(1, max(1, x_ctx - 2))  # the sink block and the two most recent stay plain
-        n_off = min(len(cand), int(round(w.offset_frac * x_ctx)))
-        chosen = _rng(w, layer, b, h, _TAG_OFFSET).choice(cand, size=n_off, replace=False)
+        chosen = offset_blocks(w, layer, b, h)
         offset[chosen] = delta.astype(np.float32)
         sigmas[chosen] = np.float32(w.offset_sigma)
     blk = np.arange(cap) // B
