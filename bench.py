@@ -37,6 +37,11 @@ def parse():
     ap.add_argument("--layers", type=int, default=0, help="resident layer copies (0: enough for > 1 GB)")
     ap.add_argument("--select-path", choices=["auto", "chunked", "one_group"], default="auto",
                     help="scoring / selection launch shape (auto: one workgroup per unit where it fits)")
+    ap.add_argument("--score-kind", choices=["compkv", "mass", "first_order"], default="compkv",
+                    help="block score: the CompKV score or an ablation variant (mass only, first-order mass)")
+    ap.add_argument("--compensation", choices=["mean", "drop"], default="mean",
+                    help="decode of the omitted blocks: Mean compensation or Drop")
+    ap.add_argument("--n-var-groups", type=int, default=0, help="override r, the variance groups per block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--only", choices=["all", "sparse", "dense", "fused"], default="all",
@@ -49,13 +54,13 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(w, budget, sel_counts):
+def algorithmic_bytes(w, budget, sel_counts, compensate=True):
     """Bytes the method must move per step (all units), split by kernel.
 
     score_select: mean key (4d) and grouped variances (4r) of every block, the queries (2Gd bytes of
     bf16), and the selected ids written (4K).
     sparse_decode: bf16 keys and values of the selected tokens (4d per token), the fp32 mean value of
-    every omitted block (4d), the queries and the fp32 output (4Gd).
+    every omitted block (4d; none for the Drop decode), the queries and the fp32 output (4Gd).
     append_stats: the new key/value (4d), the cache row written (4d), the active block's summary read
     and written (2 (8d + 4r)).
     """
@@ -67,7 +72,7 @@ def algorithmic_bytes(w, budget, sel_counts):
     dec = 0
     for sel in sel_counts:  # per unit: list of selected ids
         tokens = sum(last_len if b == X - 1 else B for b in sel)
-        dec += tokens * 4 * d + (X - len(sel)) * 4 * d + 2 * G * d + 4 * G * d
+        dec += tokens * 4 * d + (X - len(sel)) * 4 * d * compensate + 2 * G * d + 4 * G * d
     app = units * (8 * d + 2 * (8 * d + 4 * r))
     dense = units * (n * 4 * d + 2 * G * d + 4 * G * d)
     return dict(score_select=score, sparse_decode=dec, append_stats=app, dense_decode=dense)
@@ -294,6 +299,8 @@ def main():
     from workloads import WORKLOADS, gen_layer
 
     w = WORKLOADS[args.workload]
+    if args.n_var_groups:
+        w = w.with_(n_var_groups=args.n_var_groups)
     if w.decode_steps > 0:
         return run_streaming(args, w)
     budget = args.budget or w.budget_blocks
@@ -335,7 +342,10 @@ def main():
             "one_group": P.COMPKV_SELECT_ONE_GROUP}[args.select_path]
     one_group = path == P.COMPKV_SELECT_ONE_GROUP or (
         path == P.COMPKV_SELECT_AUTO and dims.xmax <= 256)
-    params = P.CompkvSelectParams(budget, 1, 2, scale, path)
+    kind = {"compkv": P.COMPKV_SCORE_COMPKV, "mass": P.COMPKV_SCORE_MASS,
+            "first_order": P.COMPKV_SCORE_FIRST_ORDER}[args.score_kind]
+    drop = args.compensation == "drop"
+    params = P.CompkvSelectParams(budget, 1, 2, scale, path, kind, P.COMPKV_COMP_DROP if drop else P.COMPKV_COMP_MEAN)
     torch.cuda.synchronize()
 
     def append(L):
@@ -347,8 +357,8 @@ def main():
         P.compkv_score_select(dims, params, q, s.kmean, s.dvar, seq_after, sel, n_sel, blk_logit, None, ws)
 
     def decode(L):
-        P.compkv_sparse_decode(dims, scale, q, Ks[L], Vs[L], summ[L].vmean, blk_logit, seq_after, sel, n_sel,
-                               out, lse, ws)
+        P.compkv_sparse_decode(dims, scale, q, Ks[L], Vs[L], None if drop else summ[L].vmean,
+                               None if drop else blk_logit, seq_after, sel, n_sel, out, lse, ws)
 
     def fused(L):
         s = summ[L]
@@ -453,11 +463,12 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "context": n, "block_size": w.block_size, "budget_blocks": budget,
                    "n_var_groups": w.n_var_groups, "layer_copies": layers, "parallelism": "single GPU",
-                   "select_path": "one_group" if one_group else "chunked"},
+                   "select_path": "one_group" if one_group else "chunked", "score_kind": args.score_kind,
+                   "compensation": args.compensation},
     }
     if "sparse" in result:
         us, per_k, wall, us_sep = result["sparse"]
-        ab = algorithmic_bytes(w, budget, sel_lists)
+        ab = algorithmic_bytes(w, budget, sel_lists, not drop)
         step_bytes = ab["score_select"] + ab["sparse_decode"] + ab["append_stats"]
         ach = step_bytes / (us * 1e-6) / 1e9
         line.update({

@@ -80,7 +80,28 @@ typedef struct compkv_select_params {
     int32_t n_recent;      /* most recent blocks always selected (the paper uses 2; Section 4.2) */
     float scale;           /* logit scale s; the paper's 1/sqrt(d) (Section 3.1) */
     int32_t select_path;   /* COMPKV_SELECT_*: how the scores are formed and ranked (0 = automatic) */
+    int32_t score_kind;    /* COMPKV_SCORE_*: the block score (0 = the CompKV score) */
+    int32_t compensation;  /* COMPKV_COMP_*: what stands in for the omitted blocks in
+                              compkv_decode_step (0 = Mean compensation) */
 } compkv_select_params;
+
+/*
+ * Block scores (compkv_select_params.score_kind): the paper's score and the variants of its
+ * ablations (Section 5.4). p-hat is normalized per query head over every block in all three.
+ *   COMPKV:      S_b = sum_g p-hat_{g,b} sigma-hat^2_{g,b}, p-hat from log|b| + zbar + sigma-hat^2/2
+ *                (Eqs. compkv-mass-estimate, compkv-score).
+ *   MASS:        S_b = sum_g p-hat_{g,b} (the second-order mass estimate alone).
+ *   FIRST_ORDER: S_b = sum_g p-hat_{g,b} sigma-hat^2_{g,b} with p-hat from log|b| + zbar alone.
+ * Decoding of the omitted blocks (compkv_select_params.compensation):
+ *   MEAN: one pseudo-token per omitted block (Eq. compkv-output).
+ *   DROP: omitted blocks are left out; attention is renormalized over the selected tokens
+ *         (Appendix A.5).
+ */
+#define COMPKV_SCORE_COMPKV 0
+#define COMPKV_SCORE_MASS 1
+#define COMPKV_SCORE_FIRST_ORDER 2
+#define COMPKV_COMP_MEAN 0
+#define COMPKV_COMP_DROP 1
 
 /*
  * Scoring / selection launch shapes (compkv_select_params.select_path). Both compute the same
@@ -150,7 +171,10 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
  * with z_{g,j} = scale q_g . k_j, S = sel[u][0 .. n_sel[u]) (ascending, unique ids below X; entries
  * outside [0, X) are ignored) and zbar read from blk_logit as written by compkv_score_select.
  * sel_stride is the row stride of sel (the budget K). lse (nullable) receives the log of the
- * denominator, i.e. of the compensated normalizer.
+ * denominator, i.e. of the compensated normalizer. With vmean and blk_logit both NULL the omitted
+ * blocks are left out (the Drop decode of Appendix A.5: out_g is attention over the selected
+ * tokens alone); a unit with nothing selected then gets out = 0 and lse = -inf. Exactly one of the
+ * two NULL is COMPKV_EINVAL.
  */
 int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
                          const void* v_cache, const float* vmean, const float* blk_logit,
@@ -177,11 +201,14 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
  *  - sel, n_sel, blk_logit and scores (nullable) are bit-identical to compkv_score_select on the
  *    refreshed summaries (sel has row stride params->budget_blocks).
  *  - out and lse (nullable) follow Eq. compkv-output as in compkv_sparse_decode (same tolerance, not
- *    bitwise: the pseudo-token sum is formed over all blocks while the summaries are streamed, and
- *    the selected blocks' pseudo-terms are then subtracted).
- * Enqueues four kernels. Workspace: compkv_workspace_bytes(dims, budget, COMPKV_WS_DECODE_STEP).
- * Returns COMPKV_EUNSUPPORTED for shapes whose partial count exceeds the merge limit (then use the
- * separate calls), otherwise the statuses of compkv_score_select.
+ *    bitwise: on the chunked path the pseudo-token sum is formed over all blocks while the summaries
+ *    are streamed, and the selected blocks' pseudo-terms are then taken back out). With
+ *    params->compensation == COMPKV_COMP_DROP they are the Drop decode of compkv_sparse_decode.
+ *  - params->score_kind and params->select_path as for compkv_score_select.
+ * Enqueues four kernels on the chunked path, three on the one-group path. Workspace:
+ * compkv_workspace_bytes(dims, budget, COMPKV_WS_DECODE_STEP). Returns COMPKV_EUNSUPPORTED for shapes
+ * whose partial count exceeds the merge limit (then use the separate calls), COMPKV_EINVAL for an
+ * unknown compensation, otherwise the statuses of compkv_score_select.
  */
 int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* params, const void* q,
                        void* k_cache, void* v_cache, const void* k_new, const void* v_new,

@@ -7,10 +7,15 @@ PyTorch only provides device memory and streams. There is no fallback: if the li
 every call raises.
 """
 from .binding import (  # noqa: F401
+    COMPKV_COMP_DROP,
+    COMPKV_COMP_MEAN,
     COMPKV_GROUPS_INTERLEAVED,
     COMPKV_GROUPS_ROTATE_HALF,
     COMPKV_SELECT_AUTO,
     COMPKV_SELECT_CHUNKED,
+    COMPKV_SCORE_COMPKV,
+    COMPKV_SCORE_FIRST_ORDER,
+    COMPKV_SCORE_MASS,
     COMPKV_SELECT_ONE_GROUP,
     COMPKV_WS_ALL,
     COMPKV_WS_DECODE_STEP,

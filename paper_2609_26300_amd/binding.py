@@ -23,6 +23,11 @@ COMPKV_WS_DECODE_STEP = 4
 COMPKV_SELECT_AUTO = 0
 COMPKV_SELECT_CHUNKED = 1
 COMPKV_SELECT_ONE_GROUP = 2
+COMPKV_SCORE_COMPKV = 0
+COMPKV_SCORE_MASS = 1
+COMPKV_SCORE_FIRST_ORDER = 2
+COMPKV_COMP_MEAN = 0
+COMPKV_COMP_DROP = 1
 
 
 class CompkvError(RuntimeError):
@@ -50,7 +55,8 @@ class CompkvDims(ctypes.Structure):
 
 class CompkvSelectParams(ctypes.Structure):
     _fields_ = [("budget_blocks", ctypes.c_int32), ("n_sink", ctypes.c_int32),
-                ("n_recent", ctypes.c_int32), ("scale", ctypes.c_float), ("select_path", ctypes.c_int32)]
+                ("n_recent", ctypes.c_int32), ("scale", ctypes.c_float), ("select_path", ctypes.c_int32),
+                ("score_kind", ctypes.c_int32), ("compensation", ctypes.c_int32)]
 
 
 def make_dims(batch, n_q_heads, n_kv_heads, head_dim, block_size, n_var_groups, capacity_tokens,
@@ -218,6 +224,7 @@ def compkv_score_select(dims, params: CompkvSelectParams, q, kmean, dvar, seq_le
 
 def compkv_sparse_decode(dims, scale, q, k_cache, v_cache, vmean, blk_logit, seq_lens, sel, n_sel, out,
                          lse=None, workspace=None, stream=None):
+    """Compensated sparse decode; vmean = blk_logit = None gives the Drop decode."""
     cache, summ, _, qs = _shapes(dims)
     bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
     units = (dims.batch, dims.n_kv_heads)
@@ -226,8 +233,8 @@ def compkv_sparse_decode(dims, scale, q, k_cache, v_cache, vmean, blk_logit, seq
     ws, ws_bytes = _ws(workspace)
     st = library().compkv_sparse_decode(
         ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _ptr(k_cache, bf, cache, "k_cache"),
-        _ptr(v_cache, bf, cache, "v_cache"), _ptr(vmean, f32, summ, "vmean"),
-        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
+        _ptr(v_cache, bf, cache, "v_cache"), _ptr(vmean, f32, summ, "vmean", nullable=True),
+        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit", nullable=True),
         _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, sel.shape[2]), "sel"),
         _ptr(n_sel, i32, units, "n_sel"), int(sel.shape[2]), _ptr(out, f32, qs, "out"),
         _ptr(lse, f32, qs[:2], "lse", nullable=True), ws, ws_bytes, _stream(stream))

@@ -175,6 +175,7 @@ compkv::ScoreArgs score_args(const Geom& g, const compkv_select_params* params, 
     a.n_sink = params->n_sink;
     a.n_recent = params->n_recent;
     a.scale = params->scale;
+    a.score_kind = params->score_kind;
     return a;
 }
 
@@ -249,6 +250,7 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel || !blk_logit) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
+    if (params->score_kind < COMPKV_SCORE_COMPKV || params->score_kind > COMPKV_SCORE_FIRST_ORDER) return COMPKV_EINVAL;
     const bool one = one_group_path(g, params->select_path, &st);
     if (st != COMPKV_OK) return st;
     if (!one && (score_shape(g).nchunks + 1) * g.G > compkv::select_max_chunk_heads()) return COMPKV_EUNSUPPORTED;
@@ -268,8 +270,8 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     Geom g;
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
-    if (!q || !k_cache || !v_cache || !vmean || !blk_logit || !seq_lens || !sel || !n_sel || !out)
-        return COMPKV_EINVAL;
+    if (!q || !k_cache || !v_cache || !seq_lens || !sel || !n_sel || !out) return COMPKV_EINVAL;
+    if ((vmean == nullptr) != (blk_logit == nullptr)) return COMPKV_EINVAL;  // both null: Drop
     if (sel_stride < 1) return COMPKV_EINVAL;
     const size_t need = ws_bytes(g, sel_stride, COMPKV_WS_SPARSE_DECODE);
     st = check_ws(g, workspace, workspace_bytes, need);
@@ -292,7 +294,7 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     a.sel_stride = sel_stride;
     a.n_exact = sh.n_exact;
     a.eb = sh.eb;
-    a.n_comp = sh.n_comp;
+    a.n_comp = vmean ? sh.n_comp : 0;
     a.cb = sh.cb;
     a.dense = 0;
     a.scale = scale;
@@ -339,6 +341,9 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     if ((k_new == nullptr) != (v_new == nullptr)) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
+    if (params->score_kind < COMPKV_SCORE_COMPKV || params->score_kind > COMPKV_SCORE_FIRST_ORDER) return COMPKV_EINVAL;
+    if (params->compensation != COMPKV_COMP_MEAN && params->compensation != COMPKV_COMP_DROP) return COMPKV_EINVAL;
+    const bool drop = params->compensation == COMPKV_COMP_DROP;
     const int K = params->budget_blocks;
     const bool one = one_group_path(g, params->select_path, &st);
     if (st != COMPKV_OK) return st;
@@ -382,15 +387,17 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.sel_stride = K;
         d.n_exact = sp.n_exact;
         d.eb = sp.eb;
-        d.n_comp = sp.n_comp;
+        d.n_comp = drop ? 0 : sp.n_comp;
         d.cb = sp.cb;
         d.dense = 0;
         d.scale = params->scale;
         return launch_status(compkv::launch_decode(g, d, s));
     }
+    // Mean: the chunks' compensation partials, then the exact items' partials; Drop: exact items only
     float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
-    a.comp_part = dpart;
-    a.part_count = parts;
+    const int nparts = drop ? sp.n_exact : parts;
+    a.comp_part = drop ? nullptr : dpart;
+    a.part_count = nparts;
     hipError_t e = compkv::launch_score_select(g, a, s);
     if (e != hipSuccess) return COMPKV_EHIP;
 
@@ -412,12 +419,12 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.cb = 0;
     d.dense = 0;
     d.scale = params->scale;
-    d.part_count = parts;
-    d.part_base = sc.nchunks + 1;
-    d.neg_pseudo = 1;
+    d.part_count = nparts;
+    d.part_base = drop ? 0 : sc.nchunks + 1;
+    d.neg_pseudo = drop ? 0 : 1;
     e = compkv::launch_decode_items(g, d, sp.n_exact, s);
     if (e != hipSuccess) return COMPKV_EHIP;
-    return launch_status(compkv::launch_decode_merge(g, d, parts, s));
+    return launch_status(compkv::launch_decode_merge(g, d, nparts, s));
 }
 
 }  // extern "C"

@@ -60,6 +60,7 @@ struct ScoreArgs {
     float* comp_part;       // [units][part_count][G][D + 2]: chunk c writes compensation partial c
     int part_count;
     int one_group;          // 1: one workgroup per unit scores and selects (no chunks, no partials)
+    int score_kind;         // COMPKV_SCORE_*: CompKV score, mass only, or first-order mass estimate
 };
 
 struct DecodeArgs {
@@ -67,7 +68,7 @@ struct DecodeArgs {
     const uint16_t* K;
     const uint16_t* V;
     const float* vmean;
-    const float* blk_logit;
+    const float* blk_logit;  // with vmean: null for the Drop decode (no compensation items)
     const int32_t* seq_lens;
     const int32_t* sel;
     const int32_t* n_sel;

@@ -99,6 +99,12 @@ __device__ __forceinline__ void store_query(const QueryPairs<D, G>& qp, float s,
     }
 }
 
+// Score kinds (the ablations of Section 5.4): the log weight of a block is
+// log|b| + zbar + half * sig2 (half = 1/2, or 0 for the first-order mass estimate), and its score
+// term is p-hat * sig2, or p-hat alone for the mass-only score.
+__device__ __forceinline__ float kind_half(int kind) { return kind == 2 ? 0.0f : 0.5f; }
+__device__ __forceinline__ float kind_term(int kind, float sig2) { return kind == 1 ? 1.0f : sig2; }
+
 template <int D, int G>
 struct ChunkShared {
     float q[G][D];   // scaled query
@@ -148,13 +154,14 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* pp = a.ws_part + ((size_t)u * (nc + 1) + nc) * G * 2;
-    float* cp = kStep ? a.comp_part + ((size_t)u * a.part_count + nc) * G * (D + 2) : nullptr;
+    // fused step with Mean compensation: this workgroup's compensation partial
+    float* cp = (kStep && a.comp_part) ? a.comp_part + ((size_t)u * a.part_count + nc) * G * (D + 2) : nullptr;
     if (X == 0) {  // empty sequence: neutral partials
         for (int g = tid; g < G; g += kThreads) {
             pp[2 * g] = -INFINITY;
             pp[2 * g + 1] = 0.0f;
         }
-        if constexpr (kStep)
+        if (cp)
             for (int idx = tid; idx < G * (D + 2); idx += kThreads) cp[idx] = (idx % (D + 2) == 0) ? -INFINITY : 0.0f;
         return;
     }
@@ -195,11 +202,11 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     for (int g = tid; g < G; g += kThreads) {
         const float z = ts.z[g], v = ts.v[g];
         a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
-        pp[2 * g] = lnb + z + 0.5f * v;  // the partial of one block: max a, sum exp(a - a) = 1
+        pp[2 * g] = lnb + z + kind_half(a.score_kind) * v;  // the partial of one block: max a, sum exp(a - a) = 1
         pp[2 * g + 1] = 1.0f;
-        a.ws_w[((size_t)u * geo.xmax() + b) * G + g] = v;
+        a.ws_w[((size_t)u * geo.xmax() + b) * G + g] = kind_term(a.score_kind, v);
     }
-    if constexpr (kStep) {
+    if (cp) {
         for (int idx = tid; idx < G * D; idx += kThreads) {
             const int g = idx / D, i = idx % D;
             float* p = cp + (size_t)g * (D + 2);
@@ -244,6 +251,8 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const int chunk0 = chunk * a.bpc;
     const int li = tid & 7, grp = tid >> 3;
     const int vli = tid % LPB, vslot = tid / LPB;
+    const bool comp = kStep && a.comp_part != nullptr;  // fused step with Mean compensation (uniform)
+    const float half = kind_half(a.score_kind);
 
     // loads in the order of their use: query pairs, then per slot the mean key and first variance
     // group (the mean values follow once the keys are consumed, which halves the registers held).
@@ -323,12 +332,12 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             for (int g = 0; g < G; ++g) {
                 sh.z[g][lb] = z[p][g];
                 sh.v[g][lb] = v[p][g];
-                sh.a[g][lb] = valid ? lnb + z[p][g] + 0.5f * v[p][g] : -INFINITY;
+                sh.a[g][lb] = valid ? lnb + z[p][g] + half * v[p][g] : -INFINITY;
                 if constexpr (kStep) st.cw[g][lb] = valid ? lnb + z[p][g] : -INFINITY;  // pseudo-logit
             }
         }
     }
-    if constexpr (kStep) {  // mean-value rows, requested once the mean keys are consumed
+    if (comp) {  // mean-value rows, requested once the mean keys are consumed
         const float4* vm = reinterpret_cast<const float4*>(a.vmean + (size_t)u * geo.xcap * D) + vli;
 #pragma unroll
         for (int k = 0; k < VROWS; ++k) {
@@ -361,7 +370,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             pp[0] = m;
             pp[1] = ssum;
         }
-        if constexpr (kStep) {
+        if constexpr (kStep) if (comp) {
             float cv[kBpcMax / 64];
             float cm = -INFINITY;
 #pragma unroll
@@ -394,9 +403,10 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     }
     for (int idx = tid; idx < G * nvalid; idx += kThreads) {
         const int lb = idx / G, g = idx % G;
-        a.ws_w[((size_t)u * xmax + chunk0 + lb) * G + g] = expf(sh.a[g][lb] - sh.m[g]) * sh.v[g][lb];
+        a.ws_w[((size_t)u * xmax + chunk0 + lb) * G + g] =
+            expf(sh.a[g][lb] - sh.m[g]) * kind_term(a.score_kind, sh.v[g][lb]);
     }
-    if constexpr (kStep) {
+    if constexpr (kStep) if (comp) {
         // weighted mean values; lane vli of a row slot holds coordinates 4 vli .. 4 vli + 3
         float acc[G][4];
 #pragma unroll
@@ -1005,7 +1015,7 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
                     if (li == 0 && valid) {
                         const int g = g0 + gb;
                         const float lnb = logf((float)min(geo.B, n - b * geo.B));
-                        A[b * G + g] = lnb + z + 0.5f * Vp[b * G + g];
+                        A[b * G + g] = lnb + z + kind_half(a.score_kind) * Vp[b * G + g];
                         a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
                     }
                 }
@@ -1044,7 +1054,7 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
         if (b < X) {
             float S = 0.0f;
 #pragma unroll
-            for (int g = 0; g < G; ++g) S += expf(A[b * G + g] - us.lse[g]) * Vp[b * G + g];
+            for (int g = 0; g < G; ++g) S += expf(A[b * G + g] - us.lse[g]) * kind_term(a.score_kind, Vp[b * G + g]);
             if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
             if (!mandatory(b, X, a.n_sink, a.n_recent)) {
                 ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
@@ -1084,7 +1094,7 @@ hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
             unit_select_kernel<D, G, false><<<dim3(g.units()), kFinThreads, dyn, s>>>(g, a);
         return hipGetLastError();
     }
-    if (a.comp_part)
+    if (a.comp_part || a.k_new)  // fused step: the refresh and / or the compensation partials
         launch_chunks<D, G, true>(g, a, s);
     else
         launch_chunks<D, G, false>(g, a, s);

@@ -96,13 +96,16 @@ class Case:
         self.ws = P.alloc_workspace(self.dims, self.budget)
         self.G = w.group
         self.select_path = P.COMPKV_SELECT_AUTO
+        self.score_kind = P.COMPKV_SCORE_COMPKV
+        self.compensation = P.COMPKV_COMP_MEAN
 
     def one_group_ok(self) -> bool:
         """Whether the one-workgroup-per-unit selection accepts these dims (G * blocks <= 8192)."""
         return self.G * self.dims.xmax <= 8192
 
     def params(self):
-        return P.CompkvSelectParams(self.budget, self.n_sink, self.n_recent, self.scale, self.select_path)
+        return P.CompkvSelectParams(self.budget, self.n_sink, self.n_recent, self.scale, self.select_path,
+                                    self.score_kind, self.compensation)
 
     # ---------------------------------------------------------------- library calls
     def build_stats(self):
@@ -121,10 +124,13 @@ class Case:
                               self.sel, self.n_sel, self.blk_logit, self.scores, self.ws)
 
     def sparse_decode(self, sel=None, n_sel=None):
+        """compkv_sparse_decode; the Drop decode when this case's compensation is COMPKV_COMP_DROP."""
         d = self.dims
         self.out = torch.zeros((d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device="cuda")
         self.lse = torch.zeros((d.batch, d.n_q_heads), dtype=torch.float32, device="cuda")
-        P.compkv_sparse_decode(d, self.scale, self.q, self.K, self.V, self.summ.vmean, self.blk_logit, self.sl,
+        drop = self.compensation == P.COMPKV_COMP_DROP
+        P.compkv_sparse_decode(d, self.scale, self.q, self.K, self.V, None if drop else self.summ.vmean,
+                               None if drop else self.blk_logit, self.sl,
                                self.sel if sel is None else sel, self.n_sel if n_sel is None else n_sel,
                                self.out, self.lse, self.ws)
         return self.out, self.lse
@@ -171,7 +177,8 @@ class Case:
     def oracle_scores(self, b, h, stats=None):
         q, K, V, n = self.unit_inputs(b, h)
         km, dv, vm = stats if stats is not None else self.oracle_stats(b, h)
-        return oracle.block_scores(q, km, dv, n, self.w.block_size, self.r, self.scale, self.layout)
+        return oracle.block_scores(q, km, dv, n, self.w.block_size, self.r, self.scale, self.layout,
+                                   kind=self.score_kind)
 
     def units(self):
         return [(b, h) for b in range(self.w.batch) for h in range(self.w.n_kv_heads)]

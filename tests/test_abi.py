@@ -202,3 +202,25 @@ def test_select_path_validation():
     need = P.compkv_workspace_bytes(fits, 64, P.COMPKV_WS_DECODE_STEP)
     for path in (P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP):
         assert _step(L, fits, P.CompkvSelectParams(64, 1, 2, 0.088, path), ws_bytes=need - 1) == EWS
+
+
+def test_score_kind_and_compensation_validation():
+    """Unknown score kinds and compensation modes are EINVAL; the sparse decode takes vmean and
+    blk_logit together (both NULL: the Drop decode) -- all checked before anything is enqueued."""
+    L = P.library()
+    d = dims()
+    args = [FAKE] * 6 + [FAKE, None]
+    need = P.compkv_workspace_bytes(d, 16, P.COMPKV_WS_SCORE_SELECT)
+    for kind, rc in ((-1, EINVAL), (3, EINVAL), (P.COMPKV_SCORE_MASS, EWS), (P.COMPKV_SCORE_FIRST_ORDER, EWS)):
+        p = P.CompkvSelectParams(16, 1, 2, 0.088, 0, kind)
+        assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), *args, FAKE, need - 1, None) == rc
+        assert _step(L, d, p, ws_bytes=1) == rc
+    for comp, rc in ((-1, EINVAL), (2, EINVAL), (P.COMPKV_COMP_DROP, EWS), (P.COMPKV_COMP_MEAN, EWS)):
+        assert _step(L, d, P.CompkvSelectParams(16, 1, 2, 0.088, 0, 0, comp), ws_bytes=1) == rc
+
+    def sparse(vmean, blk):
+        return L.compkv_sparse_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, vmean, blk, FAKE, FAKE, FAKE, 16,
+                                      FAKE, None, FAKE, 1, None)
+
+    assert sparse(FAKE, None) == EINVAL and sparse(None, FAKE) == EINVAL
+    assert sparse(None, None) == EWS and sparse(FAKE, FAKE) == EWS
