@@ -111,12 +111,19 @@ typedef struct compkv_select_params {
  *              per-chunk normalizers and selects (two launches).
  *   ONE_GROUP: one workgroup per unit scores every block and selects (one launch); needs
  *              G * ceil(max_seq_len / block_size) <= 8192, else COMPKV_EUNSUPPORTED.
+ *   CHUNKED_EXACT: CHUNKED scoring; in compkv_decode_step the selection and the exact attention over
+ *              the selected blocks then run as one launch (each of a unit's workgroups repeats the
+ *              unit's selection and attends over its share of the blocks), when the budget is at most
+ *              1024 blocks and a unit at most 8192 blocks; otherwise, and in compkv_score_select, as
+ *              CHUNKED.
  *   AUTO:      ONE_GROUP when a unit holds at most 256 blocks (one workgroup then reads every summary
- *              in a single round of loads), else CHUNKED.
+ *              in a single round of loads), else CHUNKED_EXACT when all of its workgroups are resident
+ *              at once (at most one per compute unit), else CHUNKED.
  */
 #define COMPKV_SELECT_AUTO 0
 #define COMPKV_SELECT_CHUNKED 1
 #define COMPKV_SELECT_ONE_GROUP 2
+#define COMPKV_SELECT_CHUNKED_EXACT 3
 
 /* Which call a workspace is sized for (compkv_workspace_bytes). */
 #define COMPKV_WS_ALL 0
@@ -205,7 +212,7 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
  *    are streamed, and the selected blocks' pseudo-terms are then taken back out). With
  *    params->compensation == COMPKV_COMP_DROP they are the Drop decode of compkv_sparse_decode.
  *  - params->score_kind and params->select_path as for compkv_score_select.
- * Enqueues four kernels on the chunked path, three on the one-group path. Workspace:
+ * Enqueues four kernels on the chunked path, three on the one-group and chunked-exact paths. Workspace:
  * compkv_workspace_bytes(dims, budget, COMPKV_WS_DECODE_STEP). Returns COMPKV_EUNSUPPORTED for shapes
  * whose partial count exceeds the merge limit (then use the separate calls), COMPKV_EINVAL for an
  * unknown compensation, otherwise the statuses of compkv_score_select.

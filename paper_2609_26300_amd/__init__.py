@@ -13,6 +13,7 @@ from .binding import (  # noqa: F401
     COMPKV_GROUPS_ROTATE_HALF,
     COMPKV_SELECT_AUTO,
     COMPKV_SELECT_CHUNKED,
+    COMPKV_SELECT_CHUNKED_EXACT,
     COMPKV_SCORE_COMPKV,
     COMPKV_SCORE_FIRST_ORDER,
     COMPKV_SCORE_MASS,

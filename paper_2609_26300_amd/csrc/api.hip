@@ -129,7 +129,7 @@ size_t ws_bytes(const Geom& g, int K, int which) {
 // select_path of the call: true for the one-workgroup-per-unit selection; *st receives the status
 bool one_group_path(const Geom& g, int path, int* st) {
     *st = COMPKV_OK;
-    if (path < COMPKV_SELECT_AUTO || path > COMPKV_SELECT_ONE_GROUP) {
+    if (path < COMPKV_SELECT_AUTO || path > COMPKV_SELECT_CHUNKED_EXACT) {
         *st = COMPKV_EINVAL;
         return false;
     }
@@ -138,6 +138,31 @@ bool one_group_path(const Geom& g, int path, int* st) {
     if (path == COMPKV_SELECT_AUTO)  // one workgroup reads at most one batch of summaries per unit
         return fits && g.xmax() <= compkv::select_one_group_auto_blocks();
     return path == COMPKV_SELECT_ONE_GROUP && fits;
+}
+
+// Shape of the fused step's selection + exact launch: items of select_exact_waves() tiles of 16 tokens.
+struct SxShape {
+    int eb, n_exact;
+    bool fits;       // within the kernel's limits
+    bool one_round;  // and every item workgroup resident at once (one workgroup per CU)
+};
+
+SxShape sx_shape(const Geom& g, const compkv::ScoreArgs& a, int K) {
+    const int xmax = g.xmax();
+    const int keff = std::max(1, std::min(K, xmax));
+    int cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 0;
+    // items of 128 tokens (half the waves attend, one tile each) while they fit one workgroup per CU,
+    // else of one tile per wave
+    const int full = 16 * compkv::select_exact_waves();
+    int eb = std::max(1, (full / 2) / g.B);
+    if ((long long)g.units() * ceil_div(keff, eb) > cus) eb = std::max(1, full / g.B);
+    const int n_exact = ceil_div(keff, eb);
+    const size_t dyn = ((size_t)2 * (a.nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
+    const bool fits = K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
+                      eb <= compkv::decode_max_eb() && n_exact <= compkv::decode_max_items();
+    return {eb, n_exact, fits, fits && (long long)g.units() * n_exact <= cus};
 }
 
 int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
@@ -393,11 +418,18 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.scale = params->scale;
         return launch_status(compkv::launch_decode(g, d, s));
     }
+    // chunked scoring; then either the selection and the 128-token exact items as two launches, or
+    // (CHUNKED_EXACT, or AUTO when every item workgroup is resident at once) one fused launch
+    const SxShape sx = sx_shape(g, a, K);
+    const bool use_sx = (params->select_path == COMPKV_SELECT_CHUNKED_EXACT && sx.fits) ||
+                        (params->select_path == COMPKV_SELECT_AUTO && sx.one_round);
+    const int n_ex = use_sx ? sx.n_exact : sp.n_exact;
     // Mean: the chunks' compensation partials, then the exact items' partials; Drop: exact items only
     float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
-    const int nparts = drop ? sp.n_exact : parts;
+    const int nparts = drop ? n_ex : sc.nchunks + 1 + n_ex;
     a.comp_part = drop ? nullptr : dpart;
     a.part_count = nparts;
+    a.chunks_only = use_sx;
     hipError_t e = compkv::launch_score_select(g, a, s);
     if (e != hipSuccess) return COMPKV_EHIP;
 
@@ -413,8 +445,8 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.out = out;
     d.lse = lse;
     d.sel_stride = K;
-    d.n_exact = sp.n_exact;
-    d.eb = sp.eb;
+    d.n_exact = n_ex;
+    d.eb = use_sx ? sx.eb : sp.eb;
     d.n_comp = 0;
     d.cb = 0;
     d.dense = 0;
@@ -422,7 +454,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.part_count = nparts;
     d.part_base = drop ? 0 : sc.nchunks + 1;
     d.neg_pseudo = drop ? 0 : 1;
-    e = compkv::launch_decode_items(g, d, sp.n_exact, s);
+    e = use_sx ? compkv::launch_select_exact(g, a, d, n_ex, s) : compkv::launch_decode_items(g, d, n_ex, s);
     if (e != hipSuccess) return COMPKV_EHIP;
     return launch_status(compkv::launch_decode_merge(g, d, nparts, s));
 }

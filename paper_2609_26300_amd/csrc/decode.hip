@@ -9,262 +9,32 @@
 // A second launch, grid = (units, G), merges each unit's partials in item order, so the result does
 // not depend on scheduling; the kernel boundary makes the partials visible (no cross-workgroup fences).
 //
-// Item workgroups have eight waves (kItemThreads). Exact tokens run on the matrix cores, one 16-token
-// tile per wave and round, so a 128-token item is one round of the eight waves. The logits are formed
-// as S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = 16 key rows, B = the unit's query heads as columns,
-// zero-padded to 16): lane l then holds the logits of head l%16 for tokens 4(l/16)..4(l/16)+3, which is
-// exactly the A-operand layout of v_mfma_f32_16x16x16bf16_1k, so the probabilities feed the P.V product
-// without any data movement. For P.V the value row of each of the lane's 4 tokens is loaded as one
-// contiguous chunk of d/16 coordinates (coordinate (d/16)*(l%16) + j goes to output block j), so every
-// load is a contiguous piece of a row. P.V runs as v_mfma_f32_16x16x16bf16_1k per tile, with P split
-// into three bf16 terms (three MFMAs), which keeps P within 2^-27 of its fp32 value (two terms, 2^-17,
-// are not enough for outputs that cancel to near zero); products with the bf16 values are exact and
-// accumulate in fp32. The softmax max is taken per tile.
-//
-// In the fused step the compensation partials already hold the pseudo-token of every block (logit
-// log|b| + zbar_b, value vmean_b), so an exact item takes its own blocks' pseudo-tokens back out. As
-// |b| e^{zbar_b} vmean_b = sum over the block's tokens of e^{zbar_b} v_j, this is a per-token weight
-// p'_j = e^{zbar_b - m}: the item multiplies V by p_j - p'_j in the same MFMAs, and by Jensen's
-// inequality each block's sum of these weights is non-negative.
+// Item workgroups have eight waves (kItemThreads); an exact item runs the tile loop of exact.h, one
+// 16-token tile per wave and round, so a 128-token item is one round of the eight waves.
 //
 // Compensation items are plain fp32 streaming on the vector ALUs: the mean-value rows (d/4 lanes x
 // float4 per row, 16 rows per thread in flight) are requested first; meanwhile the item marks its
 // selected blocks, forms the pseudo-logits of the others and their per-head max; then the weighted
 // rows are summed.
-#include "internal.h"
+#include "exact.h"
 
 namespace compkv {
 namespace {
 
-typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef __bf16 v8bf16 __attribute__((ext_vector_type(8)));
-typedef float v4f32 __attribute__((ext_vector_type(4)));
-
 constexpr int kMaxItems = 256;     // items per unit and launch, upper bound (checked by the host)
 constexpr int kMaxPartials = 2048;  // partials per unit in a merge, upper bound
 constexpr int kCbMax = 512;     // blocks per compensation item, upper bound
-constexpr int kMaxEb = 128;     // selected blocks per exact item, upper bound
 constexpr int kItemWaves = 8;  // waves of an item workgroup
 constexpr int kItemThreads = 64 * kItemWaves;
 
 template <int D, int G>
 struct DecodeShared {
-    float m[kItemWaves][G], l[kItemWaves][G];
-    float acc[kItemWaves][G][D];
+    ExactLds<D, G, kItemWaves> ex;  // exact items; compensation items use ex.acc for their wave sums
     float w[G][kCbMax];  // compensation weights
-    float zb[G][kMaxEb];  // fused step: the block logits of the exact item's selected blocks
     float M[G], L[G];
     unsigned char flag[kCbMax];
     int sel[kMaxEb];  // the exact item's selected ids
 };
-
-__device__ __forceinline__ short f32_to_bf16_rne(float f) {
-    const uint32_t u = __float_as_uint(f);
-    return (short)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-__device__ __forceinline__ float bf16_bits_to_f32(short h) { return __uint_as_float(uint32_t((unsigned short)h) << 16); }
-
-// floor(v / B) for 0 <= v < 2^23: the float quotient is within one of it, and one step corrects it
-__device__ __forceinline__ int div_small(int v, int B, float invB) {
-    int k = (int)((float)v * invB);
-    const int r = v - k * B;
-    return k + (r >= B ? 1 : 0) - (r < 0 ? 1 : 0);
-}
-
-// virtual token v of an item -> cache row, or -1 if v is past the item's tokens / the block's length
-struct TokenMap {
-    const int32_t* sel;  // sparse: the item's selected ids (first entry of the item)
-    int nblk, B, n, X;   // sparse
-    float invB;
-    int t0, t1;          // dense: row range
-    bool dense;
-    __device__ int row(int v) const {
-        if (dense) {
-            const int r = t0 + v;
-            return r < t1 ? r : -1;
-        }
-        const int k = div_small(v, B, invB);
-        if (k >= nblk) return -1;
-        const int blk = sel[k];
-        const int off = v - k * B;
-        if (blk < 0 || blk >= X || off >= min(B, n - blk * B)) return -1;
-        return blk * B + off;
-    }
-    __device__ int count() const { return dense ? max(0, t1 - t0) : nblk * B; }
-};
-
-// Exact tokens of one item with MFMA. Leaves this wave's (m, l) for head lane%16 (lanes with the same
-// lane%16 agree) and acc[j][i] = sum over the wave's tokens of p * v for head 4(lane/16)+i at
-// coordinate (D/16)*(lane%16) + j. With zt (fused step: zt[g][k] = block logit of head g and the item's
-// k-th block, filled by `mid`) every token's weight is p_j - p'_j with p'_j = e^{zbar_b - m} for its
-// block b. `mid` is workgroup-wide work (every wave calls it once, after its first loads are issued).
-template <int D, int G, typename Mid>
-__device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku, const uint16_t* __restrict__ Vu,
-                             const uint16_t* __restrict__ qh, const float (*zt)[kMaxEb], float scale, float& m,
-                             float& l, v4f32 (&acc)[D / 16], Mid&& mid) {
-    constexpr int KS = D / 32;   // k-steps of the logit MFMA
-    constexpr int CPL = D / 16;  // value coordinates per lane (= output blocks)
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int col = lane & 15, grp = lane >> 4;
-    m = -INFINITY;
-    l = 0.0f;
-#pragma unroll
-    for (int j = 0; j < CPL; ++j) acc[j] = v4f32{0.0f, 0.0f, 0.0f, 0.0f};
-    const int ntiles = (tm.count() + 15) / 16;
-    const bool pseudo = zt != nullptr && col < G;
-    uint4 kreg[KS];
-    uint4 vreg[4];
-    bool vvalid[4];
-    bool kvalid;
-    // every load of a tile is issued first (branch-free: a row past the item's tokens loads row 0 of
-    // the unit and is zeroed after)
-    auto issue = [&](int t) {
-        const int base = t * 16;
-        const int rk = t < ntiles ? tm.row(base + col) : -1;
-        kvalid = rk >= 0;
-        const uint16_t* kp = Ku + (size_t)(rk >= 0 ? rk : 0) * D + 8 * grp;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kreg[ks] = *reinterpret_cast<const uint4*>(kp + 32 * ks);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int rv = t < ntiles ? tm.row(base + 4 * grp + e) : -1;
-            vvalid[e] = rv >= 0;
-            const uint16_t* vp = Vu + (size_t)(rv >= 0 ? rv : 0) * D + CPL * col;
-            if constexpr (CPL == 8) {
-                vreg[e] = *reinterpret_cast<const uint4*>(vp);
-            } else {
-                const uint2 hv = *reinterpret_cast<const uint2*>(vp);
-                vreg[e] = make_uint4(hv.x, hv.y, 0, 0);
-            }
-        }
-    };
-    issue(wave);
-    mid();
-    for (int t = wave; t < ntiles; t += kItemWaves) {
-        if (t != wave) issue(t);
-        // B operand of the logit product: query head `col` (zero for padding heads), requested after the
-        // tile's K/V loads
-        v8bf16 qb[KS];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            uint4 w = make_uint4(0, 0, 0, 0);
-            if (col < G) w = *reinterpret_cast<const uint4*>(qh + col * D + 32 * ks + 8 * grp);
-            qb[ks] = __builtin_bit_cast(v8bf16, w);
-        }
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kreg[ks] = kvalid ? kreg[ks] : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) vreg[e] = vvalid[e] ? vreg[e] : make_uint4(0, 0, 0, 0);
-        // logits: lane holds head `col`, tokens 4*grp + i of the tile; the pseudo-logits join the max so
-        // that both weights stay at most 1
-        auto zpseudo = [&](int i) {
-            return (pseudo && vvalid[i]) ? zt[col][div_small(t * 16 + 4 * grp + i, tm.B, tm.invB)] : -INFINITY;
-        };
-        v4f32 sv = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            sv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf16, kreg[ks]), qb[ks], sv, 0, 0, 0);
-        float z[4], zp[4];
-        float rmax = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            z[i] = vvalid[i] ? scale * sv[i] : -INFINITY;
-            zp[i] = zpseudo(i);
-            rmax = fmaxf(rmax, fmaxf(z[i], zp[i]));
-        }
-        rmax = fmaxf(rmax, __shfl_xor(rmax, 16));
-        rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
-        const float m_new = fmaxf(m, rmax);
-        if (m_new == -INFINITY) continue;  // nothing valid for this head yet (uniform per wave-round)
-        if (m != -INFINITY) {  // a later round: rescale the running state
-            const float c = __expf(m - m_new);
-            l *= c;
-            // accumulator row i holds head 4*grp + i, whose factor lives in lane 4*grp + i
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float ci = __shfl(c, 4 * grp + i);
-#pragma unroll
-                for (int j = 0; j < CPL; ++j) acc[j][i] *= ci;
-            }
-        }
-        m = m_new;
-        // P.V with v_mfma_f32_16x16x16bf16_1k: k-index 4*grp + e is token 4*grp + e in both operands.
-        // The weight is split into three bf16 terms (hi + mid + lo equals it to within 2^-27 relative).
-        v4i16 pa[3];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float p = (z[i] == -INFINITY ? 0.0f : __expf(z[i] - m)) - (zp[i] == -INFINITY ? 0.0f : __expf(zp[i] - m));
-            l += p;
-            const short hi = f32_to_bf16_rne(p);
-            const float r1 = p - bf16_bits_to_f32(hi);
-            const short md = f32_to_bf16_rne(r1);
-            const short lo = f32_to_bf16_rne(r1 - bf16_bits_to_f32(md));
-            pa[0][i] = hi;
-            pa[1][i] = md;
-            pa[2][i] = lo;
-        }
-        const uint32_t* w[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = reinterpret_cast<const uint32_t*>(&vreg[e]);
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-            // B operand for output block j: element 4*grp + e = coordinate CPL*col + j of token 4*grp + e
-            const int wi = j >> 1;
-            uint32_t pk0, pk1;
-            if ((j & 1) == 0) {
-                pk0 = (w[0][wi] & 0xFFFFu) | (w[1][wi] << 16);
-                pk1 = (w[2][wi] & 0xFFFFu) | (w[3][wi] << 16);
-            } else {
-                pk0 = (w[0][wi] >> 16) | (w[1][wi] & 0xFFFF0000u);
-                pk1 = (w[2][wi] >> 16) | (w[3][wi] & 0xFFFF0000u);
-            }
-            const v4i16 bv = __builtin_bit_cast(v4i16, make_uint2(pk0, pk1));
-#pragma unroll
-            for (int k = 0; k < 3; ++k) acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[k], bv, acc[j], 0, 0, 0);
-        }
-    }
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-}
-
-// Combine the waves' exact states in LDS and write the item's partial.
-template <int D, int G>
-__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], DecodeShared<D, G>& sh, float* part) {
-    constexpr int CPL = D / 16;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int col = lane & 15, grp = lane >> 4;
-    if (grp == 0 && col < G) {
-        sh.m[wave][col] = m;
-        sh.l[wave][col] = l;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int g = 4 * grp + i;
-        if (g < G) {
-#pragma unroll
-            for (int j = 0; j < CPL; ++j) sh.acc[wave][g][CPL * col + j] = acc[j][i];
-        }
-    }
-    __syncthreads();
-    for (int idx = tid; idx < G * D; idx += kItemThreads) {
-        const int g = idx / D, i = idx % D;
-        float mm = -INFINITY, ll = 0.0f, aa = 0.0f;
-#pragma unroll
-        for (int w = 0; w < kItemWaves; ++w) {
-            float mn, ca, cb;
-            merge_scales(mm, sh.m[w][g], mn, ca, cb);
-            ll = ll * ca + sh.l[w][g] * cb;
-            aa = aa * ca + sh.acc[w][g][i] * cb;
-            mm = mn;
-        }
-        float* p = part + (size_t)g * (D + 2);
-        if (i == 0) {
-            p[0] = mm;
-            p[1] = ll;
-        }
-        p[2 + i] = aa;
-    }
-}
 
 // Pseudo-tokens of the unselected blocks in [c0, c1).
 template <int D, int G>
@@ -356,7 +126,7 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) sh.acc[wave][g][4 * li + e] = acc[g][e];
+            for (int e = 0; e < 4; ++e) sh.ex.acc[wave][g][4 * li + e] = acc[g][e];
     }
     __syncthreads();
     for (int idx = tid; idx < G * D; idx += kItemThreads) {
@@ -368,7 +138,7 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
         }
         float tot = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kItemWaves; ++w) tot += sh.acc[w][g][i];
+        for (int w = 0; w < kItemWaves; ++w) tot += sh.ex.acc[w][g][i];
         p[2 + i] = tot;
     }
 }
@@ -412,18 +182,18 @@ __global__ __launch_bounds__(kItemThreads) __attribute__((amdgpu_waves_per_eu(4)
         const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
         // fused step: the block logits of the item's blocks, requested once its K/V loads are issued
         const bool pseudo = a.neg_pseudo && !tm.dense;
-        exact_tokens<D, G>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh,
-                           pseudo ? sh.zb : nullptr, a.scale, m, l, acc, [&] {
+        exact_tokens<D, G, kItemWaves>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh,
+                                       pseudo ? sh.ex.zb : nullptr, a.scale, m, l, acc, [&] {
                                if (!pseudo) return;  // workgroup-uniform
                                const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
                                for (int idx = tid; idx < G * tm.nblk; idx += kItemThreads) {
                                    const int g = idx / tm.nblk, k = idx - g * tm.nblk;
                                    const int b = sh.sel[k];
-                                   sh.zb[g][k] = lg[(size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0)];
+                                   sh.ex.zb[g][k] = lg[(size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0)];
                                }
                                __syncthreads();
                            });
-        finish_exact<D, G>(m, l, acc, sh, part);
+        finish_exact<D, G, kItemWaves>(m, l, acc, sh.ex, part);
     } else {
         const int c0 = (item - a.n_exact) * a.cb;
         compensation<D, G>(a, geo, u, n, X, c0, min(c0 + a.cb, X), sh, part);

@@ -61,6 +61,7 @@ struct ScoreArgs {
     int part_count;
     int one_group;          // 1: one workgroup per unit scores and selects (no chunks, no partials)
     int score_kind;         // COMPKV_SCORE_*: CompKV score, mass only, or first-order mass estimate
+    int chunks_only;        // chunked path: launch the chunk scoring without the selection
 };
 
 struct DecodeArgs {
@@ -102,22 +103,37 @@ int decode_max_cb();
 int decode_max_eb();
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s);
+// fused step: the selection (from the chunk partials) and the exact items in one launch, `items`
+// workgroups of select_exact_waves() waves per unit; hipErrorInvalidValue outside its limits
+hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s);
+int select_exact_max_budget();
+int select_exact_waves();
 hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s);
 
-// Resident workgroups of `kern` (kThreads each) on the current device, cached per device.
+// Resident workgroups of `kern` (`threads` each, no dynamic LDS) on the current device, cached per
+// (kernel, device). Not thread-safe on first use per kernel; a race only repeats the same query.
 template <typename Kern>
-int resident_slots(Kern kern) {
-    constexpr int kMaxDev = 64;
-    static int cache[kMaxDev];
+int resident_slots(Kern kern, int threads = kThreads) {
+    constexpr int kSlots = 64;
+    static const void* key_fn[kSlots];
+    static int key_dev[kSlots], value[kSlots];
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) dev = 0;
-    if (cache[dev] > 0) return cache[dev];
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    const void* fn = reinterpret_cast<const void*>(kern);
+    for (int i = 0; i < kSlots; ++i)
+        if (key_fn[i] == fn && key_dev[i] == dev && value[i] > 0) return value[i];
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kThreads, 0) != hipSuccess || per_cu < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, threads, 0) != hipSuccess || per_cu < 1)
         per_cu = 1;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 1;
-    cache[dev] = per_cu * cus;
-    return cache[dev];
+    for (int i = 0; i < kSlots; ++i)
+        if (key_fn[i] == nullptr) {
+            key_fn[i] = fn;
+            key_dev[i] = dev;
+            value[i] = per_cu * cus;
+            break;
+        }
+    return per_cu * cus;
 }
 
 // ------------------------------------------------------------------ device helpers

@@ -32,6 +32,7 @@
 // through a three-pass radix select on the score bits instead. Wave-level reductions and prefix sums
 // use DPP lane moves.
 #include "block_stats.h"
+#include "exact.h"
 
 #include <type_traits>
 
@@ -775,13 +776,14 @@ __device__ void select_radix(const SelectCtx& c, FinalShared& sh) {
     if (tid == 0) *c.n_sel = min(total, K);
 }
 
+// The selection of unit u from the chunk partials (kFinThreads threads): per-head log normalizers,
+// scores (written to a.scores when write_scores) and the stable Top-K into sel_out / nsel_out (global
+// or LDS). dyn: [np][G] partial maxima, then factors; [np][G] sums; [xmax] key bits (keys_in_lds).
 template <int G>
-__global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
+__device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, FinalShared& sh, float* dyn,
+                                int32_t* sel_out, int32_t* nsel_out, bool write_scores) {
     constexpr int FT = kFinThreads, KPT = kKeysPerThread;
-    __shared__ FinalShared sh;
-    extern __shared__ float dyn[];  // [np][G] partial maxima, then factors; [np][G] sums; [xmax] key bits
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int u = blockIdx.x;
     const int bseq = u / geo.hkv;
     const int xmax = geo.xmax();
     const int nc = a.nchunks, np = nc + 1;  // partial nc: the last block's
@@ -837,7 +839,7 @@ __global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, 
     }
     __syncthreads();
 
-    const SelectCtx sc = make_select_ctx(X, a.K, a.n_sink, a.n_recent, a.sel + (size_t)u * a.K, a.n_sel + u,
+    const SelectCtx sc = make_select_ctx(X, a.K, a.n_sink, a.n_recent, sel_out, nsel_out,
                                          a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * np * G)
                                                        : a.ws_key + (size_t)u * xmax);
     auto score_of = [&](int b, const float (&wt)[G]) {
@@ -859,7 +861,7 @@ __global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, 
             ck[k] = 0ull;
             if (b < X) {
                 const float S = score_of(b, w[k]);
-                if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+                if (write_scores && a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
                 if (!mandatory(b, X, a.n_sink, a.n_recent)) {
                     ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
                     mx = max(mx, __float_as_uint(S));
@@ -873,12 +875,20 @@ __global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, 
             float wt[G];
             load_terms<G>(wu, b, wt);
             const float S = score_of(b, wt);
-            if (a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
+            if (write_scores && a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
             sc.keys[b] = __float_as_uint(S);
         }
     }
     __syncthreads();
     select_radix(sc, sh);
+}
+
+template <int G>
+__global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
+    __shared__ FinalShared sh;
+    extern __shared__ float dyn[];
+    const int u = blockIdx.x;
+    finalize_select<G>(geo, a, u, sh, dyn, a.sel + (size_t)u * a.K, a.n_sel + u, true);
 }
 
 
@@ -1070,6 +1080,72 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
     select_radix(sc, sh);
 }
 
+// ---------------------------------------------------------------- selection + exact items, fused
+// The fused step's selection and exact items as one launch, grid = (items, units), kFinThreads threads
+// per workgroup. Every workgroup of a unit repeats the unit's selection from the chunk partials (the
+// same computation as select_finalize_kernel, so all of them hold the same ids) into LDS; item 0 also
+// writes the selection outputs. Then the sixteen waves attend exactly over the item's blocks (exact.h,
+// one 16-token tile per wave and round) and write the item's partial. This saves the launch between
+// selection and exact attention and the round trip of the selected ids through memory; it pays off
+// while the items fit one resident round (one workgroup per CU).
+constexpr int kSxWaves = kFinThreads / 64;
+constexpr int kSelLdsMax = 1024;  // budget limit of the fused kernel (ids held in LDS)
+
+template <int D, int G>
+struct SelExactLds {
+    union {
+        FinalShared fin;
+        ExactLds<D, G, kSxWaves> ex;
+    } u;
+    int32_t sel[kSelLdsMax];
+    int32_t nsel;
+};
+
+template <int D, int G>
+__global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, ScoreArgs a, DecodeArgs d) {
+    __shared__ SelExactLds<D, G> L;
+    extern __shared__ float dyn[];
+    const int tid = threadIdx.x;
+    const int item = blockIdx.x, u = blockIdx.y;
+    finalize_select<G>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
+    __syncthreads();
+    const int bseq = u / geo.hkv, h = u % geo.hkv;
+    const int n = clamp_len(d.seq_lens[bseq], geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
+    const int nsel = L.nsel;
+    if (item == 0) {  // the selection outputs (the ids past n_sel hold -1)
+        for (int k = tid; k < a.K; k += kFinThreads) a.sel[(size_t)u * a.K + k] = L.sel[k];
+        if (tid == 0) a.n_sel[u] = nsel;
+    }
+    TokenMap tm;
+    tm.dense = false;
+    tm.B = geo.B;
+    tm.invB = 1.0f / (float)geo.B;
+    tm.n = n;
+    tm.X = X;
+    const int e0 = item * d.eb;
+    tm.nblk = max(0, min(d.eb, nsel - e0));
+    tm.sel = L.sel + e0;
+    tm.t0 = tm.t1 = 0;
+    float m, l;
+    v4f32 acc[D / 16];
+    const uint16_t* qh = d.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+    const bool pseudo = d.neg_pseudo != 0;  // Mean: the chunks added every block's pseudo-token
+    exact_tokens<D, G, kSxWaves>(tm, d.K + (size_t)u * geo.cap * D, d.V + (size_t)u * geo.cap * D, qh,
+                                 pseudo ? L.u.ex.zb : nullptr, d.scale, m, l, acc, [&] {
+                                     if (!pseudo) return;  // workgroup-uniform
+                                     const float* lg = d.blk_logit + (size_t)u * G * geo.xcap;
+                                     for (int idx = tid; idx < G * tm.nblk; idx += kFinThreads) {
+                                         const int g = idx / tm.nblk, k = idx - g * tm.nblk;
+                                         const int b = tm.sel[k];
+                                         L.u.ex.zb[g][k] = lg[(size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0)];
+                                     }
+                                     __syncthreads();
+                                 });
+    float* part = d.ws_part + ((size_t)u * d.part_count + d.part_base + item) * G * (D + 2);
+    finish_exact<D, G, kSxWaves>(m, l, acc, L.u.ex, part);
+}
+
 size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
     return ((size_t)2 * (a.nchunks + 1) * g.G + (a.keys_in_lds ? (size_t)g.xmax() : 0)) * sizeof(float);
 }
@@ -1099,7 +1175,7 @@ hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
     else
         launch_chunks<D, G, false>(g, a, s);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || a.chunks_only) return e;
     select_finalize_kernel<G><<<dim3(g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a);
     return hipGetLastError();
 }
@@ -1115,9 +1191,37 @@ hipError_t dispatch_g(const Geom& g, const ScoreArgs& a, hipStream_t s) {
     }
 }
 
+template <int D, int G>
+hipError_t launch_sx(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int items, hipStream_t s) {
+    select_exact_kernel<D, G><<<dim3(items, g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a, d);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t sx_g(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int items, hipStream_t s) {
+    switch (g.G) {
+        case 1: return launch_sx<D, 1>(g, a, d, items, s);
+        case 2: return launch_sx<D, 2>(g, a, d, items, s);
+        case 4: return launch_sx<D, 4>(g, a, d, items, s);
+        case 8: return launch_sx<D, 8>(g, a, d, items, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 }  // namespace
 
 int select_max_bpc() { return kBpcMax; }
+int select_exact_max_budget() { return kSelLdsMax; }
+int select_exact_waves() { return kSxWaves; }
+
+hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s) {
+    // the keys of the fast path's tie fallback stay in LDS: no workgroup writes global scratch
+    a.keys_in_lds = 1;
+    if (g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb > kMaxEb ||
+        finalize_dyn_lds(g, a) > kDynBudget)
+        return hipErrorInvalidValue;
+    return g.D == 128 ? sx_g<128>(g, a, d, items, s) : sx_g<64>(g, a, d, items, s);
+}
 int select_one_group_terms() { return kUnitTerms; }
 int select_one_group_auto_blocks() { return kUnitBatch * kFinThreads / 8; }
 int select_max_chunk_heads() { return (int)(kDynBudget / (2 * sizeof(float))); }

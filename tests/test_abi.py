@@ -188,19 +188,20 @@ def test_select_path_validation():
 
     fits = dims(block_size=16, capacity_tokens=2048 * 16, max_seq_len=2048 * 16)  # G = 4: 4 * 2048 = 8192
     over = dims(block_size=16, capacity_tokens=2049 * 16, max_seq_len=2049 * 16)
-    for bad in (-1, 3):
+    for bad in (-1, 4):
         assert score(fits, bad) == EINVAL
         assert _step(L, fits, P.CompkvSelectParams(64, 1, 2, 0.088, bad)) == EINVAL
     assert score(over, P.COMPKV_SELECT_ONE_GROUP) == EUNSUP
     assert _step(L, over, P.CompkvSelectParams(64, 1, 2, 0.088, P.COMPKV_SELECT_ONE_GROUP)) == EUNSUP
     # accepted: the calls get as far as the workspace check
-    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP):
+    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP,
+                 P.COMPKV_SELECT_CHUNKED_EXACT):
         assert score(fits, path) == EWS
-    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED):
+    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_CHUNKED_EXACT):
         assert score(over, path) == EWS
     # one workspace size serves the fused step on either path
     need = P.compkv_workspace_bytes(fits, 64, P.COMPKV_WS_DECODE_STEP)
-    for path in (P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP):
+    for path in (P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP, P.COMPKV_SELECT_CHUNKED_EXACT):
         assert _step(L, fits, P.CompkvSelectParams(64, 1, 2, 0.088, path), ws_bytes=need - 1) == EWS
 
 
