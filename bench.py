@@ -25,6 +25,15 @@ import time
 import numpy as np
 
 HBM_PEAK_GBPS = 8000.0
+PATH_NAMES = {1: "chunked", 2: "one_group", 3: "chunked_exact"}
+
+
+def step_kernels(path: int) -> str:
+    """The dispatches of one compkv_decode_step call on the given launch shape."""
+    return {1: "compkv_decode_step: chunk scoring (append, compensation stream), selection, exact items, merge",
+            2: "compkv_decode_step: one-group scoring and selection (append), exact and compensation items, merge",
+            3: "compkv_decode_step: chunk scoring (append, compensation stream), selection + exact items, merge",
+            }[path]
 
 
 def parse():
@@ -35,7 +44,7 @@ def parse():
     ap.add_argument("--workload", default="llama8b_32k")
     ap.add_argument("--budget", type=int, default=None, help="override the workload's block budget")
     ap.add_argument("--layers", type=int, default=0, help="resident layer copies (0: enough for > 1 GB)")
-    ap.add_argument("--select-path", choices=["auto", "chunked", "one_group"], default="auto",
+    ap.add_argument("--select-path", choices=["auto", "chunked", "one_group", "chunked_exact"], default="auto",
                     help="scoring / selection launch shape (auto: one workgroup per unit where it fits)")
     ap.add_argument("--score-kind", choices=["compkv", "mass", "first_order"], default="compkv",
                     help="block score: the CompKV score or an ablation variant (mass only, first-order mass)")
@@ -263,7 +272,8 @@ def run_streaming(args, w):
         "hbm_gbps": round(ach, 1),
         "hbm_frac": round(ach / HBM_PEAK_GBPS, 4),
         "algorithmic_bytes_per_step": step_bytes,
-        "roofline": {"kernel": "compkv_decode_step (its four dispatches)", "bound": "hbm", "achieved": round(ach, 1),
+        "roofline": {"kernel": step_kernels(P.compkv_decode_step_path(dims, params)), "bound": "hbm",
+                     "achieved": round(ach, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic(w.name, "decode_step"),
                      "algorithmic_bytes_per_launch": step_bytes},
@@ -339,13 +349,12 @@ def main():
     out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
     lse = torch.empty((w.batch, w.n_q_heads), dtype=torch.float32, device=dev)
     path = {"auto": P.COMPKV_SELECT_AUTO, "chunked": P.COMPKV_SELECT_CHUNKED,
-            "one_group": P.COMPKV_SELECT_ONE_GROUP}[args.select_path]
-    one_group = path == P.COMPKV_SELECT_ONE_GROUP or (
-        path == P.COMPKV_SELECT_AUTO and dims.xmax <= 256)
+            "one_group": P.COMPKV_SELECT_ONE_GROUP, "chunked_exact": P.COMPKV_SELECT_CHUNKED_EXACT}[args.select_path]
     kind = {"compkv": P.COMPKV_SCORE_COMPKV, "mass": P.COMPKV_SCORE_MASS,
             "first_order": P.COMPKV_SCORE_FIRST_ORDER}[args.score_kind]
     drop = args.compensation == "drop"
     params = P.CompkvSelectParams(budget, 1, 2, scale, path, kind, P.COMPKV_COMP_DROP if drop else P.COMPKV_COMP_MEAN)
+    step_path = P.compkv_decode_step_path(dims, params)
     torch.cuda.synchronize()
 
     def append(L):
@@ -463,7 +472,7 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "context": n, "block_size": w.block_size, "budget_blocks": budget,
                    "n_var_groups": w.n_var_groups, "layer_copies": layers, "parallelism": "single GPU",
-                   "select_path": "one_group" if one_group else "chunked", "score_kind": args.score_kind,
+                   "select_path": PATH_NAMES[step_path], "score_kind": args.score_kind,
                    "compensation": args.compensation},
     }
     if "sparse" in result:
@@ -479,11 +488,8 @@ def main():
             "algorithmic_bytes_per_step": step_bytes,
             "separate_calls_us_per_step": round(us_sep, 3) if us_sep is not None else None,
             "separate_call_us": {k: round(v, 3) for k, v in per_k.items()},
-            # the timed call: its dispatches are the whole step -- chunked: chunk scoring with the
-            # append and the compensation stream, selection, exact tokens, merge; one group: scoring
-            # with the append and selection, exact and compensation items, merge
-            "roofline": {"kernel": "compkv_decode_step (its %s dispatches)" % ("three" if one_group else "four"),
-                         "bound": "hbm",
+            # the timed call: its dispatches are the whole step
+            "roofline": {"kernel": step_kernels(step_path), "bound": "hbm",
                          "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(w.name, "decode_step"),
                          "algorithmic_bytes_per_launch": step_bytes},

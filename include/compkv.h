@@ -223,6 +223,11 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
                        int32_t* n_sel, float* blk_logit, float* scores, float* out, float* lse,
                        void* workspace, size_t workspace_bytes, void* stream);
 
+/* The launch shape compkv_decode_step takes for these dims and params on the current device:
+ * COMPKV_SELECT_ONE_GROUP, COMPKV_SELECT_CHUNKED or COMPKV_SELECT_CHUNKED_EXACT (params->select_path
+ * resolved), or a negative status (invalid dims or path). Enqueues nothing. */
+int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params* params);
+
 /* Workspace bytes needed by `which` (COMPKV_WS_*; COMPKV_WS_ALL = enough for every call) for these
  * dims and budget. Returns 0 if dims are invalid. */
 size_t compkv_workspace_bytes(const compkv_dims* dims, int32_t budget_blocks, int32_t which);

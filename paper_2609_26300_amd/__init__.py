@@ -32,6 +32,7 @@ from .binding import (  # noqa: F401
     compkv_append_stats,
     compkv_build_stats,
     compkv_decode_step,
+    compkv_decode_step_path,
     compkv_dense_decode,
     compkv_score_select,
     compkv_sparse_decode,

@@ -90,13 +90,15 @@ def library():
                                           ctypes.c_size_t, _vp]
         L.compkv_decode_step.argtypes = [dp, ctypes.POINTER(CompkvSelectParams), _vp, _vp, _vp, _vp, _vp, _vp,
                                          _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+        L.compkv_decode_step_path.argtypes = [dp, ctypes.POINTER(CompkvSelectParams)]
         L.compkv_workspace_bytes.argtypes = [dp, _i32, _i32]
         L.compkv_workspace_bytes.restype = ctypes.c_size_t
         L.compkv_status_string.argtypes = [ctypes.c_int]
         L.compkv_status_string.restype = ctypes.c_char_p
         L.compkv_version.argtypes = []
         for name in ("compkv_build_stats", "compkv_append_stats", "compkv_score_select",
-                     "compkv_sparse_decode", "compkv_dense_decode", "compkv_decode_step", "compkv_version"):
+                     "compkv_sparse_decode", "compkv_dense_decode", "compkv_decode_step", "compkv_decode_step_path",
+                     "compkv_version"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -147,6 +149,13 @@ def _ws(workspace):
     if workspace is None or workspace.device.type != "cuda" or not workspace.is_contiguous():
         raise CompkvError("workspace must be a contiguous CUDA tensor")
     return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def compkv_decode_step_path(dims: CompkvDims, params: CompkvSelectParams) -> int:
+    """The launch shape compkv_decode_step takes (COMPKV_SELECT_ONE_GROUP / _CHUNKED / _CHUNKED_EXACT)."""
+    st = library().compkv_decode_step_path(ctypes.byref(dims), ctypes.byref(params))
+    _check(st if st < 0 else 0, "compkv_decode_step_path")
+    return int(st)
 
 
 def compkv_workspace_bytes(dims: CompkvDims, budget_blocks: int, which: int = COMPKV_WS_ALL) -> int:

@@ -147,7 +147,7 @@ struct SxShape {
     bool one_round;  // and every item workgroup resident at once (one workgroup per CU)
 };
 
-SxShape sx_shape(const Geom& g, const compkv::ScoreArgs& a, int K) {
+SxShape sx_shape(const Geom& g, int nchunks, int K) {
     const int xmax = g.xmax();
     const int keff = std::max(1, std::min(K, xmax));
     int cus = 0, dev = 0;
@@ -159,10 +159,14 @@ SxShape sx_shape(const Geom& g, const compkv::ScoreArgs& a, int K) {
     int eb = std::max(1, (full / 2) / g.B);
     if ((long long)g.units() * ceil_div(keff, eb) > cus) eb = std::max(1, full / g.B);
     const int n_exact = ceil_div(keff, eb);
-    const size_t dyn = ((size_t)2 * (a.nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
+    const size_t dyn = ((size_t)2 * (nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
     const bool fits = K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
                       eb <= compkv::decode_max_eb() && n_exact <= compkv::decode_max_items();
     return {eb, n_exact, fits, fits && (long long)g.units() * n_exact <= cus};
+}
+
+bool use_select_exact(int path, const SxShape& sx) {
+    return (path == COMPKV_SELECT_CHUNKED_EXACT && sx.fits) || (path == COMPKV_SELECT_AUTO && sx.one_round);
 }
 
 int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
@@ -353,6 +357,19 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
     return launch_status(compkv::launch_decode(g, a, static_cast<hipStream_t>(stream)));
 }
 
+int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params* params) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!params) return COMPKV_EINVAL;
+    const bool one = one_group_path(g, params->select_path, &st);
+    if (st != COMPKV_OK) return st;
+    if (one) return COMPKV_SELECT_ONE_GROUP;
+    return use_select_exact(params->select_path, sx_shape(g, score_shape(g).nchunks, params->budget_blocks))
+               ? COMPKV_SELECT_CHUNKED_EXACT
+               : COMPKV_SELECT_CHUNKED;
+}
+
 int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* params, const void* q, void* k_cache,
                        void* v_cache, const void* k_new, const void* v_new, const int32_t* seq_lens, float* kmean,
                        float* dvar, float* vmean, int32_t* sel, int32_t* n_sel, float* blk_logit, float* scores,
@@ -420,9 +437,8 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     }
     // chunked scoring; then either the selection and the 128-token exact items as two launches, or
     // (CHUNKED_EXACT, or AUTO when every item workgroup is resident at once) one fused launch
-    const SxShape sx = sx_shape(g, a, K);
-    const bool use_sx = (params->select_path == COMPKV_SELECT_CHUNKED_EXACT && sx.fits) ||
-                        (params->select_path == COMPKV_SELECT_AUTO && sx.one_round);
+    const SxShape sx = sx_shape(g, sc.nchunks, K);
+    const bool use_sx = use_select_exact(params->select_path, sx);
     const int n_ex = use_sx ? sx.n_exact : sp.n_exact;
     // Mean: the chunks' compensation partials, then the exact items' partials; Drop: exact items only
     float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));

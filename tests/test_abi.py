@@ -225,3 +225,25 @@ def test_score_kind_and_compensation_validation():
 
     assert sparse(FAKE, None) == EINVAL and sparse(None, FAKE) == EINVAL
     assert sparse(None, None) == EWS and sparse(FAKE, FAKE) == EWS
+
+
+def test_decode_step_path_resolution():
+    """compkv_decode_step_path reports the launch shape without enqueuing anything: explicit paths as
+    requested (the fused selection + exact launch whenever its limits hold), AUTO as one group for
+    units of at most 256 blocks, and errors as statuses."""
+    small = dims(block_size=16, capacity_tokens=4096, max_seq_len=4096)  # 256 blocks
+    big = dims(block_size=32, capacity_tokens=32768, max_seq_len=32768)  # 1024 blocks
+    prm = lambda path, K=16: P.CompkvSelectParams(K, 1, 2, 0.088, path)
+    assert P.compkv_decode_step_path(small, prm(P.COMPKV_SELECT_AUTO)) == P.COMPKV_SELECT_ONE_GROUP
+    assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_ONE_GROUP)) == P.COMPKV_SELECT_ONE_GROUP
+    for d in (small, big):
+        assert P.compkv_decode_step_path(d, prm(P.COMPKV_SELECT_CHUNKED)) == P.COMPKV_SELECT_CHUNKED
+        assert P.compkv_decode_step_path(d, prm(P.COMPKV_SELECT_CHUNKED_EXACT)) == P.COMPKV_SELECT_CHUNKED_EXACT
+    # past the fused kernel's budget limit the chunked-exact request runs chunked
+    assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_CHUNKED_EXACT, 1025)) == P.COMPKV_SELECT_CHUNKED
+    assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_AUTO)) in (P.COMPKV_SELECT_CHUNKED,
+                                                                         P.COMPKV_SELECT_CHUNKED_EXACT)
+    with pytest.raises(P.CompkvError):
+        P.compkv_decode_step_path(big, prm(7))
+    with pytest.raises(P.CompkvError):
+        P.compkv_decode_step_path(dims(head_dim=96), prm(0))
