@@ -183,3 +183,27 @@ def spearman(a, b) -> float:
     rb -= rb.mean()
     den = np.sqrt(np.sum(ra * ra) * np.sum(rb * rb))
     return float(np.sum(ra * rb) / den) if den > 0 else 0.0
+
+
+def capture(T, chosen, reference) -> float:
+    """Residual capture of Appendix B.2: sum of T over the chosen blocks / sum over the reference blocks
+    (the exact-residual selection)."""
+    T = np.asarray(T, dtype=np.float64)
+    den = float(np.sum(T[np.asarray(reference, dtype=np.int64)]))
+    return float(np.sum(T[np.asarray(chosen, dtype=np.int64)])) / den if den > 0 else 1.0
+
+
+def top_blocks(score, k: int, exclude=()) -> np.ndarray:
+    """The k blocks of largest score outside `exclude` (ties to the lower id), ascending."""
+    score = np.asarray(score, dtype=np.float64)
+    skip = set(int(b) for b in exclude)
+    cand = [b for b in range(len(score)) if b not in skip]
+    cand.sort(key=lambda b: (-score[b], b))
+    return np.sort(np.array(cand[:k], dtype=np.int64))
+
+
+def output_rel_l2(out, ref) -> np.ndarray:
+    """Per-head relative L2 error ||out_h - ref_h|| / ||ref_h|| (Eq. residual-diagnostic-errors)."""
+    out, ref = np.asarray(out, np.float64), np.asarray(ref, np.float64)
+    return np.linalg.norm(out - ref, axis=-1) / np.linalg.norm(ref, axis=-1)
+

@@ -576,3 +576,37 @@ def test_llama_workload_offset_blocks_mass_vs_compkv():
         picked[kind] = len(off & set(oracle.select(sc["score"], w.budget_blocks).tolist()))
     assert picked[oracle.SCORE_MASS] == 51
     assert picked[oracle.SCORE_COMPKV] == 0 and picked[oracle.SCORE_FIRST_ORDER] == 0
+
+
+# ---------------------------------------------------------------- fidelity diagnostics (Appendix B)
+
+def test_spearman_matches_library_and_closed_form():
+    """Spearman rank correlation: equals scipy's (average ranks for ties) and, without ties, the closed
+    form 1 - 6 sum d^2 / (n (n^2 - 1)); monotone maps give 1, reversal -1."""
+    from scipy.stats import spearmanr
+
+    rng = np.random.default_rng(4)
+    a, b = rng.standard_normal(300), rng.standard_normal(300)
+    assert dg.spearman(a, b) == pytest.approx(spearmanr(a, b).statistic, abs=1e-12)
+    ra, rb = np.argsort(np.argsort(a)), np.argsort(np.argsort(b))
+    n = len(a)
+    assert dg.spearman(a, b) == pytest.approx(1 - 6 * np.sum((ra - rb) ** 2) / (n * (n * n - 1)), abs=1e-12)
+    t = np.round(a * 3)  # many ties
+    assert dg.spearman(t, b) == pytest.approx(spearmanr(t, b).statistic, abs=1e-12)
+    assert dg.spearman(a, np.exp(a)) == pytest.approx(1.0) and dg.spearman(a, -a) == pytest.approx(-1.0)
+
+
+def test_capture_and_top_blocks():
+    """Capture (Appendix B.2) is 1 for the exact-residual selection itself and at most 1 for any other
+    selection of the same size; the top-k helper skips the excluded (mandatory) blocks and breaks ties
+    by the lower id."""
+    rng = np.random.default_rng(6)
+    T = rng.exponential(size=60)
+    ref = dg.top_blocks(T, 10, exclude=[0, 58, 59])
+    assert len(ref) == 10 and not {0, 58, 59} & set(ref.tolist())
+    assert dg.capture(T, ref, ref) == 1.0
+    for _ in range(20):
+        other = rng.choice(np.setdiff1d(np.arange(60), [0, 58, 59]), 10, replace=False)
+        assert dg.capture(T, other, ref) <= 1.0 + 1e-15
+    assert dg.top_blocks([1.0, 2.0, 2.0, 0.5], 2).tolist() == [1, 2]
+    assert dg.top_blocks([3.0, 3.0, 3.0], 1, exclude=[0]).tolist() == [1]

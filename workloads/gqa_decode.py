@@ -75,8 +75,9 @@ def _w(**kw) -> Workload:
     return Workload(**kw)
 
 
-# The five synthetic decode workloads: a tiny case, a Llama-3-8B-shaped 32K layer, a 128K batch-4
-# long-context case, a wide-GQA (64 query heads / 8 KV heads) batch-8 case, and a streaming case.
+# The synthetic decode workloads: a tiny case, a Llama-3-8B-shaped 32K layer, a 128K batch-4
+# long-context case, a wide-GQA (64 query heads / 8 KV heads) batch-8 case, a streaming case, and two
+# score-fidelity cases.
 WORKLOADS = {
     "tiny_4k": _w(name="tiny_4k", batch=1, n_q_heads=8, n_kv_heads=2, head_dim=128, context=4096,
                   block_size=16, budget_blocks=16, seed=1000),
@@ -89,6 +90,13 @@ WORKLOADS = {
     "streaming_128k": _w(name="streaming_128k", batch=2, n_q_heads=32, n_kv_heads=8, head_dim=128,
                          context=131072, block_size=32, budget_blocks=128, layers=4,
                          decode_steps=256, seed=1004),
+    # score fidelity against the exact residual (Appendix B.2 setting: 32 query / 8 KV heads, 16-token
+    # blocks, a 512-token budget = 32 blocks of which 3 mandatory), on two key recipes
+    "fidelity_16k": _w(name="fidelity_16k", batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128, context=16384,
+                       block_size=16, budget_blocks=32, offset_frac=0.05, seed=1005),
+    "fidelity_lognormal_16k": _w(name="fidelity_lognormal_16k", batch=1, n_q_heads=32, n_kv_heads=8,
+                                 head_dim=128, context=16384, block_size=16, budget_blocks=32,
+                                 sigma="lognormal", seed=1006),
 }
 
 
