@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--compensation", choices=["mean", "drop"], default="mean",
                     help="decode of the omitted blocks: Mean compensation or Drop")
     ap.add_argument("--n-var-groups", type=int, default=0, help="override r, the variance groups per block")
+    ap.add_argument("--page-tokens", type=int, default=0,
+                    help="paged K/V cache with pages of this many tokens, randomly permuted (0: contiguous)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--only", choices=["all", "sparse", "dense", "fused"], default="all",
@@ -330,6 +332,25 @@ def main():
     q = to_dev(qb)
     k_new = K0[:, :, n - 1].contiguous()
     v_new = V0[:, :, n - 1].contiguous()
+    page = args.page_tokens
+    if page:  # the same cache scattered over randomly permuted pages
+        pps = -(-w.capacity // page)
+        perm = np.random.default_rng(0).permutation(w.batch * pps).reshape(w.batch, pps).astype(np.int32)
+        table = torch.from_numpy(perm).to(dev)
+        dims = P.make_dims(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.block_size, w.n_var_groups,
+                           pps * page, max_seq_len=n, block_table=table, page_tokens=page, num_pages=w.batch * pps)
+        dest = torch.from_numpy(perm.reshape(-1)).long().to(dev)
+
+        def paged(X):
+            Xc = torch.zeros((w.batch, w.n_kv_heads, pps * page, w.head_dim), dtype=X.dtype, device=dev)
+            Xc[:, :, :X.shape[2]] = X
+            Xv = Xc.view(w.batch, w.n_kv_heads, pps, page, w.head_dim).permute(0, 2, 1, 3, 4)
+            out = torch.empty((w.batch * pps, w.n_kv_heads, page, w.head_dim), dtype=X.dtype, device=dev)
+            out[dest] = Xv.reshape(w.batch * pps, w.n_kv_heads, page, w.head_dim)
+            return out
+
+        K0, V0 = paged(K0), paged(V0)
+        torch.cuda.synchronize()
     seq_before = torch.full((w.batch,), n - 1, dtype=torch.int32, device=dev)
     seq_after = torch.full((w.batch,), n, dtype=torch.int32, device=dev)
     Ks, Vs, summ = [], [], []
@@ -375,8 +396,14 @@ def main():
                              sel, n_sel, blk_logit, None, out, lse, ws)
 
     def row_write(L):
-        Ks[L][:, :, n - 1] = k_new
-        Vs[L][:, :, n - 1] = v_new
+        if page:
+            for b in range(w.batch):
+                pg, r = int(perm[b, (n - 1) // page]), (n - 1) % page
+                Ks[L][pg, :, r] = k_new[b]
+                Vs[L][pg, :, r] = v_new[b]
+        else:
+            Ks[L][:, :, n - 1] = k_new
+            Vs[L][:, :, n - 1] = v_new
 
     def dense(L):
         P.compkv_dense_decode(dims, scale, q, Ks[L], Vs[L], seq_after, out, lse, ws)
@@ -473,7 +500,7 @@ def main():
                    "head_dim": w.head_dim, "context": n, "block_size": w.block_size, "budget_blocks": budget,
                    "n_var_groups": w.n_var_groups, "layer_copies": layers, "parallelism": "single GPU",
                    "select_path": PATH_NAMES[step_path], "score_kind": args.score_kind,
-                   "compensation": args.compensation},
+                   "compensation": args.compensation, "page_tokens": page},
     }
     if "sparse" in result:
         us, per_k, wall, us_sep = result["sparse"]

@@ -16,7 +16,7 @@
  *    validates its host-side arguments and enqueues work on `stream` (a hipStream_t; NULL means the
  *    default stream). Results are ready when the stream reaches that point.
  *  - Layouts (row-major, innermost last). d = head_dim, Xcap = ceil(capacity_tokens / block_size):
- *      k_cache, v_cache  bf16 [batch][n_kv_heads][capacity_tokens][d]
+ *      k_cache, v_cache  bf16 [batch][n_kv_heads][capacity_tokens][d] (or paged, see compkv_dims)
  *      q                 bf16 [batch][n_q_heads][d]; query head hq uses KV head hq / G
  *      kmean, vmean      fp32 [batch][n_kv_heads][Xcap][d]
  *      dvar              fp32 [batch][n_kv_heads][Xcap][n_var_groups]
@@ -72,6 +72,16 @@ typedef struct compkv_dims {
     int32_t group_layout;    /* COMPKV_GROUPS_* */
     int32_t capacity_tokens; /* cache rows per unit (row stride of k_cache / v_cache) */
     int32_t max_seq_len;     /* host-side upper bound of seq_lens, 1..capacity_tokens; sizes grids */
+    /* Paged cache (all zero: the contiguous layout above). With page_tokens > 0, a multiple of
+     * block_size, k_cache and v_cache are bf16 [num_pages][n_kv_heads][page_tokens][d], and token j of
+     * sequence b lives in page block_table[b][j / page_tokens] at row j % page_tokens. block_table is a
+     * device int32 [batch][pages_per_seq] (entries outside [0, num_pages) are clamped, so a bad table
+     * reads the wrong page but never outside the cache); capacity_tokens must equal
+     * pages_per_seq * page_tokens. Summaries, selections and outputs keep their per-sequence layouts. */
+    int32_t page_tokens;
+    int32_t num_pages;
+    int32_t pages_per_seq;
+    const int32_t* block_table;
 } compkv_dims;
 
 typedef struct compkv_select_params {

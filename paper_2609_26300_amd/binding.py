@@ -38,7 +38,12 @@ class CompkvError(RuntimeError):
 class CompkvDims(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "batch", "n_q_heads", "n_kv_heads", "head_dim", "block_size", "n_var_groups", "group_layout",
-        "capacity_tokens", "max_seq_len")]
+        "capacity_tokens", "max_seq_len", "page_tokens", "num_pages", "pages_per_seq")] + [
+        ("block_table", ctypes.c_void_p)]
+
+    @property
+    def paged(self) -> bool:
+        return self.page_tokens > 0
 
     @property
     def group(self) -> int:
@@ -61,9 +66,22 @@ class CompkvSelectParams(ctypes.Structure):
 
 
 def make_dims(batch, n_q_heads, n_kv_heads, head_dim, block_size, n_var_groups, capacity_tokens,
-              max_seq_len=None, group_layout=COMPKV_GROUPS_ROTATE_HALF) -> CompkvDims:
-    return CompkvDims(batch, n_q_heads, n_kv_heads, head_dim, block_size, n_var_groups, group_layout,
-                      capacity_tokens, capacity_tokens if max_seq_len is None else max_seq_len)
+              max_seq_len=None, group_layout=COMPKV_GROUPS_ROTATE_HALF, block_table=None, page_tokens=0,
+              num_pages=0) -> CompkvDims:
+    """Call geometry. For a paged cache pass block_table (int32 [batch][pages_per_seq] on the device;
+    the dims keep a reference to it), page_tokens and num_pages; capacity_tokens is then
+    pages_per_seq * page_tokens."""
+    d = CompkvDims(batch, n_q_heads, n_kv_heads, head_dim, block_size, n_var_groups, group_layout,
+                   capacity_tokens, capacity_tokens if max_seq_len is None else max_seq_len)
+    if block_table is not None:
+        if block_table.dtype != torch.int32 or block_table.dim() != 2 or block_table.shape[0] != batch:
+            raise CompkvError("block_table must be int32 [batch][pages_per_seq]")
+        if not block_table.is_contiguous():
+            raise CompkvError("block_table must be contiguous")
+        d.page_tokens, d.num_pages, d.pages_per_seq = int(page_tokens), int(num_pages), int(block_table.shape[1])
+        d.block_table = block_table.data_ptr()
+        d._table = block_table  # keep the device memory alive as long as the dims
+    return d
 
 
 _lib = None
@@ -187,7 +205,8 @@ def alloc_summaries(dims: CompkvDims, device="cuda") -> Summaries:
 
 
 def _shapes(d: CompkvDims):
-    cache = (d.batch, d.n_kv_heads, d.capacity_tokens, d.head_dim)
+    cache = ((d.num_pages, d.n_kv_heads, d.page_tokens, d.head_dim) if d.paged
+             else (d.batch, d.n_kv_heads, d.capacity_tokens, d.head_dim))
     summ = (d.batch, d.n_kv_heads, d.xcap, d.head_dim)
     dvar = (d.batch, d.n_kv_heads, d.xcap, d.n_var_groups)
     q = (d.batch, d.n_q_heads, d.head_dim)

@@ -32,6 +32,24 @@ int check_dims(const compkv_dims* dm, Geom* g) {
         return COMPKV_EUNSUPPORTED;
     const long long units = (long long)dm->batch * dm->n_kv_heads;
     if (units > 65535) return COMPKV_EUNSUPPORTED;  // grid.y limit
+    // cache rows are addressed with 32-bit indices
+    if (dm->page_tokens < 0) return COMPKV_EINVAL;
+    if (dm->page_tokens == 0) {
+        if (units * dm->capacity_tokens >= (1LL << 31)) return COMPKV_EUNSUPPORTED;
+        g->bpp = g->pps = g->npages = 0;
+        g->inv_bpp = 0.0f;
+        g->table = nullptr;
+    } else {
+        if (dm->num_pages < 1 || dm->pages_per_seq < 1 || !dm->block_table) return COMPKV_EINVAL;
+        if ((long long)dm->pages_per_seq * dm->page_tokens != dm->capacity_tokens) return COMPKV_EINVAL;
+        if (dm->page_tokens % dm->block_size != 0) return COMPKV_EUNSUPPORTED;
+        if ((long long)dm->num_pages * dm->n_kv_heads * dm->page_tokens >= (1LL << 31)) return COMPKV_EUNSUPPORTED;
+        g->bpp = dm->page_tokens / dm->block_size;
+        g->pps = dm->pages_per_seq;
+        g->npages = dm->num_pages;
+        g->inv_bpp = 1.0f / (float)g->bpp;
+        g->table = dm->block_table;
+    }
     g->batch = dm->batch;
     g->hq = dm->n_q_heads;
     g->hkv = dm->n_kv_heads;
@@ -341,6 +359,7 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
     const DenseShape sh = dense_shape(g);
+    if (g.bpp > 0 && sh.te / (g.bpp * g.B) + 2 > compkv::decode_max_row_bases()) return COMPKV_EUNSUPPORTED;
     char* base = static_cast<char*>(workspace);
     compkv::DecodeArgs a{};
     a.ws_part = reinterpret_cast<float*>(base);

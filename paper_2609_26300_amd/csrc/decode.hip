@@ -24,6 +24,7 @@ namespace {
 constexpr int kMaxItems = 256;     // items per unit and launch, upper bound (checked by the host)
 constexpr int kMaxPartials = 2048;  // partials per unit in a merge, upper bound
 constexpr int kCbMax = 512;     // blocks per compensation item, upper bound
+constexpr int kMaxRowBase = 1024;  // row bases per item: selected blocks, or pages of a dense item
 constexpr int kItemWaves = 8;  // waves of an item workgroup
 constexpr int kItemThreads = 64 * kItemWaves;
 
@@ -34,6 +35,7 @@ struct DecodeShared {
     float M[G], L[G];
     unsigned char flag[kCbMax];
     int sel[kMaxEb];  // the exact item's selected ids
+    int rowbase[kMaxRowBase];  // cache row of token 0 of each selected block (sparse) or page (dense)
 };
 
 // Pseudo-tokens of the unselected blocks in [c0, c1).
@@ -162,17 +164,35 @@ __global__ __launch_bounds__(kItemThreads) __attribute__((amdgpu_waves_per_eu(4)
         tm.invB = 1.0f / (float)geo.B;
         tm.n = n;
         tm.X = X;
+        tm.rowbase = sh.rowbase;
+        tm.page = 0;
+        tm.pg0 = 0;
+        tm.invP = 0.0f;
         if (tm.dense) {
             tm.t0 = item * a.eb;
             tm.t1 = min(tm.t0 + a.eb, n);
             tm.sel = nullptr;
             tm.nblk = 0;
+            if (geo.bpp == 0) {
+                if (tid == 0) sh.rowbase[0] = u * geo.cap + tm.t0;
+            } else {  // the item's logical pages (the host bounds their count by kMaxRowBase)
+                tm.page = geo.bpp * geo.B;
+                tm.invP = 1.0f / (float)tm.page;
+                tm.pg0 = tm.t0 / tm.page;
+                const int npg = tm.t1 > tm.t0 ? (tm.t1 - 1) / tm.page - tm.pg0 + 1 : 0;
+                for (int i = tid; i < npg; i += kItemThreads) sh.rowbase[i] = block_row0(geo, u, (tm.pg0 + i) * geo.bpp);
+            }
+            __syncthreads();
         } else {
             const int nsel = min(a.n_sel[u], a.sel_stride);
             const int e0 = item * a.eb;
             tm.nblk = max(0, min(a.eb, nsel - e0));
             const int32_t* selu = a.sel + (size_t)u * a.sel_stride + e0;
-            for (int k = tid; k < tm.nblk; k += kItemThreads) sh.sel[k] = selu[k];
+            for (int k = tid; k < tm.nblk; k += kItemThreads) {
+                const int b = selu[k];
+                sh.sel[k] = b;
+                sh.rowbase[k] = block_row0(geo, u, b >= 0 && b < X ? b : 0);
+            }
             __syncthreads();
             tm.sel = sh.sel;
             tm.t0 = tm.t1 = 0;
@@ -182,7 +202,7 @@ __global__ __launch_bounds__(kItemThreads) __attribute__((amdgpu_waves_per_eu(4)
         const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
         // fused step: the block logits of the item's blocks, requested once its K/V loads are issued
         const bool pseudo = a.neg_pseudo && !tm.dense;
-        exact_tokens<D, G, kItemWaves>(tm, a.K + (size_t)u * geo.cap * D, a.V + (size_t)u * geo.cap * D, qh,
+        exact_tokens<D, G, kItemWaves>(tm, a.K, a.V, qh,
                                        pseudo ? sh.ex.zb : nullptr, a.scale, m, l, acc, [&] {
                                if (!pseudo) return;  // workgroup-uniform
                                const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
@@ -325,10 +345,12 @@ int decode_max_items() { return kMaxItems; }
 int decode_max_partials() { return kMaxPartials; }
 int decode_max_cb() { return kCbMax; }
 int decode_max_eb() { return kMaxEb; }
+int decode_max_row_bases() { return kMaxRowBase; }
 
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
     if (items < 1 || a.part_base + items > a.part_count || a.part_count > kMaxPartials ||
-        (!a.dense && (a.cb > kCbMax || a.eb > kMaxEb)))
+        (!a.dense && (a.cb > kCbMax || a.eb > kMaxEb)) ||
+        (a.dense && g.bpp > 0 && a.eb / (g.bpp * g.B) + 2 > kMaxRowBase))
         return hipErrorInvalidValue;
     return g.D == 128 ? items_d<128>(g, a, items, s) : items_d<64>(g, a, items, s);
 }

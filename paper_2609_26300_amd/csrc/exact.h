@@ -46,31 +46,33 @@ __device__ __forceinline__ short f32_to_bf16_rne(float f) {
 }
 __device__ __forceinline__ float bf16_bits_to_f32(short h) { return __uint_as_float(uint32_t((unsigned short)h) << 16); }
 
-// floor(v / B) for 0 <= v < 2^23: the float quotient is within one of it, and one step corrects it
-__device__ __forceinline__ int div_small(int v, int B, float invB) {
-    int k = (int)((float)v * invB);
-    const int r = v - k * B;
-    return k + (r >= B ? 1 : 0) - (r < 0 ? 1 : 0);
-}
-
-// virtual token v of an item -> cache row, or -1 if v is past the item's tokens / the block's length
+// Virtual token v of an item -> absolute cache row, or -1 if v is past the item's tokens / the block's
+// length. Sparse items: rowbase[k] is the row of token 0 of the item's k-th selected block. Dense
+// items (tokens t0 .. t1 - 1): contiguous caches give rowbase[0] = the row of token t0; paged caches
+// (page tokens per page) give rowbase[i] = the row of token 0 of logical page pg0 + i.
 struct TokenMap {
-    const int32_t* sel;  // sparse: the item's selected ids (first entry of the item)
-    int nblk, B, n, X;   // sparse
+    const int32_t* sel;      // sparse: the item's selected ids (first entry of the item)
+    const int32_t* rowbase;  // see above (LDS)
+    int nblk, B, n, X;       // sparse
     float invB;
-    int t0, t1;          // dense: row range
+    int t0, t1;              // dense: token range
+    int page, pg0;           // dense, paged: tokens per page, first logical page of the item
+    float invP;
     bool dense;
     __device__ int row(int v) const {
         if (dense) {
-            const int r = t0 + v;
-            return r < t1 ? r : -1;
+            const int j = t0 + v;
+            if (j >= t1) return -1;
+            if (page == 0) return rowbase[0] + v;
+            const int lp = div_small(j, page, invP);
+            return rowbase[lp - pg0] + (j - lp * page);
         }
         const int k = div_small(v, B, invB);
         if (k >= nblk) return -1;
         const int blk = sel[k];
         const int off = v - k * B;
         if (blk < 0 || blk >= X || off >= min(B, n - blk * B)) return -1;
-        return blk * B + off;
+        return rowbase[k] + off;
     }
     __device__ int count() const { return dense ? max(0, t1 - t0) : nblk * B; }
 };
@@ -80,6 +82,7 @@ struct TokenMap {
 // coordinate (D/16)*(lane%16) + j. With zt (fused step: zt[g][k] = block logit of head g and the item's
 // k-th block, filled by `mid`) every token's weight is p_j - p'_j with p'_j = e^{zbar_b - m} for its
 // block b. `mid` is workgroup-wide work (every wave calls it once, after its first loads are issued).
+// Ku / Vu are the cache bases (tm.row gives absolute rows).
 template <int D, int G, int NW, typename Mid>
 __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku, const uint16_t* __restrict__ Vu,
                              const uint16_t* __restrict__ qh, const float (*zt)[kMaxEb], float scale, float& m,

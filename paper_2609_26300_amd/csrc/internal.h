@@ -10,9 +10,15 @@ namespace compkv {
 
 constexpr int kThreads = 256;  // every kernel runs 256-thread workgroups (4 wave64)
 
-// Shape of one call after host validation.
+// Shape of one call after host validation. The K/V cache is either contiguous per unit
+// ([units][cap][D], bpp == 0) or paged: [npages][hkv][bpp * B][D] with table[bseq][pps] mapping a
+// sequence's logical page to a physical page (bpp blocks per page). Row indices below are absolute
+// rows of the cache (the host checks that every row index fits in int32).
 struct Geom {
     int batch, hq, hkv, G, D, B, r, layout, cap, xcap, max_seq;
+    int bpp, pps, npages;  // paged cache (bpp == 0: contiguous)
+    float inv_bpp;
+    const int32_t* table;
     __host__ __device__ int units() const { return batch * hkv; }
     __host__ __device__ int xmax() const { return (max_seq + B - 1) / B; }
 };
@@ -101,6 +107,7 @@ int decode_max_items();
 int decode_max_partials();
 int decode_max_cb();
 int decode_max_eb();
+int decode_max_row_bases();  // row bases an item holds (dense items of a paged cache: their pages)
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s);
 // fused step: the selection (from the chunk partials) and the exact items in one launch, `items`
@@ -154,6 +161,25 @@ __device__ __forceinline__ void unpack_bf16x8(const uint4 w, float f[8]) {
 }
 
 __device__ __forceinline__ int clamp_len(int n, int cap) { return n < 0 ? 0 : (n > cap ? cap : n); }
+
+// floor(v / B) for 0 <= v < 2^23: the float quotient is within one of it, and one step corrects it
+__device__ __forceinline__ int div_small(int v, int B, float invB) {
+    int k = (int)((float)v * invB);
+    const int r = v - k * B;
+    return k + (r >= B ? 1 : 0) - (r < 0 ? 1 : 0);
+}
+
+// Absolute cache row of the first token of logical block blk (0 <= blk < xcap) of unit u; a block's
+// rows are consecutive. Paged: one table read; a page id outside [0, npages) is clamped, so a bad table
+// entry reads the wrong page but never outside the cache.
+__device__ __forceinline__ int block_row0(const Geom& g, int u, int blk) {
+    if (g.bpp == 0) return u * g.cap + blk * g.B;
+    const int bseq = u / g.hkv, h = u - bseq * g.hkv;
+    const int lp = div_small(blk, g.bpp, g.inv_bpp);
+    int pg = g.table[(size_t)bseq * g.pps + lp];
+    pg = pg < 0 ? 0 : (pg >= g.npages ? g.npages - 1 : pg);
+    return ((pg * g.hkv + h) * g.bpp + (blk - lp * g.bpp)) * g.B;
+}
 
 // Cross-lane moves with DPP (data-parallel primitives): `old` is kept by lanes whose source is outside
 // the row or whose row/bank is masked off.

@@ -170,7 +170,7 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     const size_t blk = (size_t)u * geo.xcap + b;
     const bool append = kStep && a.k_new;
     if (append) {  // the summary reads row n - 1 from k_new / v_new; the cache row is stored at the end
-        const size_t row0 = (size_t)u * geo.cap + (size_t)b * geo.B;
+        const size_t row0 = (size_t)block_row0(geo, u, b);
         const BlockSrc src{a.Kc + row0 * D, a.Vc + row0 * D, a.k_new + (size_t)u * D, a.v_new + (size_t)u * D, nb,
                            nb - 1};
         BlockRows rows;
@@ -219,7 +219,7 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
         }
     }
     if (append && wave == 0) {  // the new token's cache row
-        const size_t row = (size_t)u * geo.cap + (n - 1);
+        const size_t row = (size_t)block_row0(geo, u, b) + (n - 1 - b * geo.B);
         const uint4* kn = reinterpret_cast<const uint4*>(a.k_new + (size_t)u * D);
         const uint4* vn = reinterpret_cast<const uint4*>(a.v_new + (size_t)u * D);
         for (int i = lane; i < D / 8; i += 64) {
@@ -937,7 +937,7 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
     BlockSrc src{};
     BlockRows rows;
     if (refresh) {
-        const size_t row0 = (size_t)u * geo.cap + (size_t)lastb * geo.B;
+        const size_t row0 = (size_t)block_row0(geo, u, lastb);
         const int nb = n - lastb * geo.B;
         src = BlockSrc{a.Kc + row0 * D, a.Vc + row0 * D, a.k_new + (size_t)u * D, a.v_new + (size_t)u * D, nb, nb - 1};
         if (wave < 4) load_block_rows<D>(src, 0, rows);
@@ -1033,7 +1033,7 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
         }
     }
     if (refresh && wave == 4) {  // the new token's cache row (the refresh read it from k_new / v_new)
-        const size_t row = (size_t)u * geo.cap + (n - 1);
+        const size_t row = (size_t)block_row0(geo, u, lastb) + (n - 1 - lastb * geo.B);
         const uint4* kn = reinterpret_cast<const uint4*>(a.k_new + (size_t)u * D);
         const uint4* vn = reinterpret_cast<const uint4*>(a.v_new + (size_t)u * D);
         for (int i = lane; i < D / 8; i += 64) {
@@ -1098,6 +1098,7 @@ struct SelExactLds {
         ExactLds<D, G, kSxWaves> ex;
     } u;
     int32_t sel[kSelLdsMax];
+    int32_t rowbase[kMaxEb];  // cache row of token 0 of each of the item's blocks
     int32_t nsel;
 };
 
@@ -1127,11 +1128,19 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
     tm.nblk = max(0, min(d.eb, nsel - e0));
     tm.sel = L.sel + e0;
     tm.t0 = tm.t1 = 0;
+    tm.page = tm.pg0 = 0;
+    tm.invP = 0.0f;
+    tm.rowbase = L.rowbase;
+    for (int k = tid; k < tm.nblk; k += kFinThreads) {
+        const int b = tm.sel[k];
+        L.rowbase[k] = block_row0(geo, u, b >= 0 && b < X ? b : 0);
+    }
+    __syncthreads();
     float m, l;
     v4f32 acc[D / 16];
     const uint16_t* qh = d.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     const bool pseudo = d.neg_pseudo != 0;  // Mean: the chunks added every block's pseudo-token
-    exact_tokens<D, G, kSxWaves>(tm, d.K + (size_t)u * geo.cap * D, d.V + (size_t)u * geo.cap * D, qh,
+    exact_tokens<D, G, kSxWaves>(tm, d.K, d.V, qh,
                                  pseudo ? L.u.ex.zb : nullptr, d.scale, m, l, acc, [&] {
                                      if (!pseudo) return;  // workgroup-uniform
                                      const float* lg = d.blk_logit + (size_t)u * G * geo.xcap;

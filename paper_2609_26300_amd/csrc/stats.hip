@@ -28,7 +28,7 @@ __global__ __launch_bounds__(kThreads) void build_stats_kernel(Geom g, StatsArgs
         const int u = flat / xmax, b = flat % xmax;
         const int n = clamp_len(a.seq_lens[u / g.hkv], g.max_seq);
         if (b >= (n + g.B - 1) / g.B) return it;
-        const size_t row0 = (size_t)u * g.cap + (size_t)b * g.B;
+        const size_t row0 = (size_t)block_row0(g, u, b);
         it.src = BlockSrc{a.K + row0 * D, a.V + row0 * D, nullptr, nullptr, min(g.B, n - b * g.B), -1};
         it.blk = (size_t)u * g.xcap + b;
         it.valid = true;
@@ -65,12 +65,12 @@ __global__ __launch_bounds__(kThreads) void append_stats_kernel(Geom g, StatsArg
     const int nb = n - blk_id * g.B + 1;
     const uint16_t* kn = a.k_new + (size_t)u * D;
     const uint16_t* vn = a.v_new + (size_t)u * D;
-    const size_t row0 = (size_t)u * g.cap + (size_t)blk_id * g.B;
+    const size_t row0 = (size_t)block_row0(g, u, blk_id);
     const size_t blk = (size_t)u * g.xcap + blk_id;
     wg_block_stats<D>(a.K + row0 * D, a.V + row0 * D, nb, kn, vn, nb - 1, g.r, g.layout, a.kmean + blk * D,
                       a.dvar + blk * g.r, a.vmean + blk * D, L);
     if (wave == 0) {  // the cache row (the summary above read it from k_new / v_new)
-        const size_t row = (size_t)u * g.cap + n;
+        const size_t row = row0 + (n - blk_id * g.B);
         for (int i = lane; i < D / 8; i += 64) {
             reinterpret_cast<uint4*>(a.K_out + row * D)[i] = reinterpret_cast<const uint4*>(kn)[i];
             reinterpret_cast<uint4*>(a.V_out + row * D)[i] = reinterpret_cast<const uint4*>(vn)[i];

@@ -247,3 +247,30 @@ def test_decode_step_path_resolution():
         P.compkv_decode_step_path(big, prm(7))
     with pytest.raises(P.CompkvError):
         P.compkv_decode_step_path(dims(head_dim=96), prm(0))
+
+
+def test_paged_dims_validation():
+    """Paged caches: the page size must be a multiple of the block size (else EUNSUPPORTED), and
+    num_pages, pages_per_seq and the table must be given with capacity = pages_per_seq * page_tokens
+    (else EINVAL) -- checked before anything is enqueued."""
+    import torch
+
+    L = P.library()
+    table = torch.zeros((1, 4), dtype=torch.int32)  # never read: every case fails validation or the ws check
+    need = lambda d: P.compkv_workspace_bytes(d, 16, P.COMPKV_WS_ALL)
+
+    def dense(d):
+        return L.compkv_dense_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1, None)
+
+    ok = dims(capacity_tokens=128, max_seq_len=128, block_table=table, page_tokens=32, num_pages=9)
+    assert need(ok) > 0 and dense(ok) == EWS
+    bad = dims(capacity_tokens=96, max_seq_len=96, block_table=table, page_tokens=24, num_pages=9)
+    assert dense(bad) == EUNSUP  # 24 is not a multiple of block_size 16
+    assert dense(dims(capacity_tokens=100, max_seq_len=100, block_table=table, page_tokens=32, num_pages=9)) == EINVAL
+    assert dense(dims(capacity_tokens=128, max_seq_len=128, block_table=table, page_tokens=32, num_pages=0)) == EINVAL
+    nul = dims(capacity_tokens=128, max_seq_len=128, block_table=table, page_tokens=32, num_pages=9)
+    nul.block_table = None
+    assert dense(nul) == EINVAL
+    neg = dims()
+    neg.page_tokens = -1
+    assert dense(neg) == EINVAL
