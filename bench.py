@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--compensation", choices=["mean", "drop"], default="mean",
                     help="decode of the omitted blocks: Mean compensation or Drop")
     ap.add_argument("--n-var-groups", type=int, default=0, help="override r, the variance groups per block")
+    ap.add_argument("--host-kv", action="store_true",
+                    help="offload tier: K/V caches in pinned host memory, read across the host link")
     ap.add_argument("--page-tokens", type=int, default=0,
                     help="paged K/V cache with pages of this many tokens, randomly permuted (0: contiguous)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -359,9 +361,15 @@ def main():
         V = V0 if layer == 0 else V0.clone()
         s = P.alloc_summaries(dims)
         P.compkv_build_stats(dims, K, V, seq_after, s.kmean, s.dvar, s.vmean)
+        if args.host_kv:  # the layer's cache moves to pinned host memory
+            K = torch.empty(K.shape, dtype=K.dtype, pin_memory=True).copy_(K)
+            V = torch.empty(V.shape, dtype=V.dtype, pin_memory=True).copy_(V)
         Ks.append(K)
         Vs.append(V)
         summ.append(s)
+    if args.host_kv:
+        K0 = V0 = None
+        torch.cuda.empty_cache()
     units = (w.batch, w.n_kv_heads)
     ws = P.alloc_workspace(dims, budget)
     sel = torch.empty((*units, budget), dtype=torch.int32, device=dev)
@@ -396,6 +404,8 @@ def main():
                              sel, n_sel, blk_logit, None, out, lse, ws)
 
     def row_write(L):
+        if args.host_kv:  # (a host cache row is not written inside torch's captured graphs)
+            return
         if page:
             for b in range(w.batch):
                 pg, r = int(perm[b, (n - 1) // page]), (n - 1) % page
@@ -500,7 +510,8 @@ def main():
                    "head_dim": w.head_dim, "context": n, "block_size": w.block_size, "budget_blocks": budget,
                    "n_var_groups": w.n_var_groups, "layer_copies": layers, "parallelism": "single GPU",
                    "select_path": PATH_NAMES[step_path], "score_kind": args.score_kind,
-                   "compensation": args.compensation, "page_tokens": page},
+                   "compensation": args.compensation, "page_tokens": page,
+                   "kv_memory": "pinned host" if args.host_kv else "device"},
     }
     if "sparse" in result:
         us, per_k, wall, us_sep = result["sparse"]

@@ -238,6 +238,16 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
  * resolved), or a negative status (invalid dims or path). Enqueues nothing. */
 int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params* params);
 
+/*
+ * Offload tier (Appendix E.1 keeps the cache in host memory): k_cache and v_cache may live in pinned,
+ * device-mapped host memory (hipHostMalloc). This returns the device address of such an allocation in
+ * *device_ptr, to be passed as k_cache / v_cache to any call; the kernels then read the rows they need
+ * (the selected blocks, the active block) and write appended rows across the host link, with no
+ * staging copy. The summaries, selections, outputs and workspace stay in device memory. Returns
+ * COMPKV_EINVAL for null arguments or memory that is not pinned and mapped.
+ */
+int compkv_host_cache_pointer(const void* host_ptr, void** device_ptr);
+
 /* Workspace bytes needed by `which` (COMPKV_WS_*; COMPKV_WS_ALL = enough for every call) for these
  * dims and budget. Returns 0 if dims are invalid. */
 size_t compkv_workspace_bytes(const compkv_dims* dims, int32_t budget_blocks, int32_t which);

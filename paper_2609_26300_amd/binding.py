@@ -109,6 +109,8 @@ def library():
         L.compkv_decode_step.argtypes = [dp, ctypes.POINTER(CompkvSelectParams), _vp, _vp, _vp, _vp, _vp, _vp,
                                          _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.compkv_decode_step_path.argtypes = [dp, ctypes.POINTER(CompkvSelectParams)]
+        L.compkv_host_cache_pointer.argtypes = [_vp, ctypes.POINTER(ctypes.c_void_p)]
+        L.compkv_host_cache_pointer.restype = ctypes.c_int
         L.compkv_workspace_bytes.argtypes = [dp, _i32, _i32]
         L.compkv_workspace_bytes.restype = ctypes.c_size_t
         L.compkv_status_string.argtypes = [ctypes.c_int]
@@ -155,6 +157,20 @@ def _ptr(t, dtype, shape, name, nullable=False):
     if shape is not None and tuple(t.shape) != tuple(shape):
         raise CompkvError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
     return t.data_ptr()
+
+
+def _kv_ptr(t, shape, name):
+    """Device address of a K/V cache: a CUDA tensor, or a pinned host tensor (the offload tier)."""
+    if isinstance(t, torch.Tensor) and t.device.type == "cpu":
+        if not t.is_pinned():
+            raise CompkvError(f"{name} in host memory must be pinned")
+        if t.dtype != torch.bfloat16 or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+            raise CompkvError(f"{name} must be a contiguous bf16 tensor of shape {tuple(shape)}")
+        dev = ctypes.c_void_p()
+        _check(library().compkv_host_cache_pointer(ctypes.c_void_p(t.data_ptr()), ctypes.byref(dev)),
+               "compkv_host_cache_pointer")
+        return dev.value
+    return _ptr(t, torch.bfloat16, shape, name)
 
 
 def _stream(stream):
@@ -217,7 +233,7 @@ def compkv_build_stats(dims, k_cache, v_cache, seq_lens, kmean, dvar, vmean, str
     cache, summ, dv, _ = _shapes(dims)
     bf, f32 = torch.bfloat16, torch.float32
     st = library().compkv_build_stats(
-        ctypes.byref(dims), _ptr(k_cache, bf, cache, "k_cache"), _ptr(v_cache, bf, cache, "v_cache"),
+        ctypes.byref(dims), _kv_ptr(k_cache, cache, "k_cache"), _kv_ptr(v_cache, cache, "v_cache"),
         _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _ptr(kmean, f32, summ, "kmean"),
         _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"), _stream(stream))
     _check(st, "compkv_build_stats")
@@ -228,7 +244,7 @@ def compkv_append_stats(dims, k_cache, v_cache, k_new, v_new, seq_lens, kmean, d
     bf, f32 = torch.bfloat16, torch.float32
     new = (dims.batch, dims.n_kv_heads, dims.head_dim)
     st = library().compkv_append_stats(
-        ctypes.byref(dims), _ptr(k_cache, bf, cache, "k_cache"), _ptr(v_cache, bf, cache, "v_cache"),
+        ctypes.byref(dims), _kv_ptr(k_cache, cache, "k_cache"), _kv_ptr(v_cache, cache, "v_cache"),
         _ptr(k_new, bf, new, "k_new"), _ptr(v_new, bf, new, "v_new"),
         _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _ptr(kmean, f32, summ, "kmean"),
         _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"), _stream(stream))
@@ -261,8 +277,8 @@ def compkv_sparse_decode(dims, scale, q, k_cache, v_cache, vmean, blk_logit, seq
         raise CompkvError("sel must be int32 [batch][n_kv_heads][budget]")
     ws, ws_bytes = _ws(workspace)
     st = library().compkv_sparse_decode(
-        ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _ptr(k_cache, bf, cache, "k_cache"),
-        _ptr(v_cache, bf, cache, "v_cache"), _ptr(vmean, f32, summ, "vmean", nullable=True),
+        ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _kv_ptr(k_cache, cache, "k_cache"),
+        _kv_ptr(v_cache, cache, "v_cache"), _ptr(vmean, f32, summ, "vmean", nullable=True),
         _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit", nullable=True),
         _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, sel.shape[2]), "sel"),
         _ptr(n_sel, i32, units, "n_sel"), int(sel.shape[2]), _ptr(out, f32, qs, "out"),
@@ -275,8 +291,8 @@ def compkv_dense_decode(dims, scale, q, k_cache, v_cache, seq_lens, out, lse=Non
     bf, f32 = torch.bfloat16, torch.float32
     ws, ws_bytes = _ws(workspace)
     st = library().compkv_dense_decode(
-        ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _ptr(k_cache, bf, cache, "k_cache"),
-        _ptr(v_cache, bf, cache, "v_cache"), _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"),
+        ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _kv_ptr(k_cache, cache, "k_cache"),
+        _kv_ptr(v_cache, cache, "v_cache"), _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"),
         _ptr(out, f32, qs, "out"), _ptr(lse, f32, qs[:2], "lse", nullable=True), ws, ws_bytes,
         _stream(stream))
     _check(st, "compkv_dense_decode")
@@ -293,8 +309,8 @@ def compkv_decode_step(dims, params: CompkvSelectParams, q, k_cache, v_cache, k_
         raise CompkvError("k_new and v_new must be given together")
     ws, ws_bytes = _ws(workspace)
     st = library().compkv_decode_step(
-        ctypes.byref(dims), ctypes.byref(params), _ptr(q, bf, qs, "q"), _ptr(k_cache, bf, cache, "k_cache"),
-        _ptr(v_cache, bf, cache, "v_cache"), _ptr(k_new, bf, new, "k_new", nullable=True),
+        ctypes.byref(dims), ctypes.byref(params), _ptr(q, bf, qs, "q"), _kv_ptr(k_cache, cache, "k_cache"),
+        _kv_ptr(v_cache, cache, "v_cache"), _ptr(k_new, bf, new, "k_new", nullable=True),
         _ptr(v_new, bf, new, "v_new", nullable=True), _ptr(seq_lens, i32, (dims.batch,), "seq_lens"),
         _ptr(kmean, f32, summ, "kmean"), _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"),
         _ptr(sel, i32, (*units, params.budget_blocks), "sel"), _ptr(n_sel, i32, units, "n_sel"),

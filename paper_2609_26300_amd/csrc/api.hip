@@ -376,6 +376,18 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
     return launch_status(compkv::launch_decode(g, a, static_cast<hipStream_t>(stream)));
 }
 
+int compkv_host_cache_pointer(const void* host_ptr, void** device_ptr) {
+    if (!host_ptr || !device_ptr) return COMPKV_EINVAL;
+    *device_ptr = nullptr;
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, const_cast<void*>(host_ptr), 0) != hipSuccess || !d) {
+        (void)hipGetLastError();  // clear the sticky error of the failed query
+        return COMPKV_EINVAL;
+    }
+    *device_ptr = d;
+    return COMPKV_OK;
+}
+
 int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params* params) {
     Geom g;
     int st = check_dims(dims, &g);

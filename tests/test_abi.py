@@ -274,3 +274,21 @@ def test_paged_dims_validation():
     neg = dims()
     neg.page_tokens = -1
     assert dense(neg) == EINVAL
+
+
+def test_host_cache_pointer_rejects_unmapped_memory():
+    """The offload tier's pointer query refuses null arguments and memory that is not pinned and mapped
+    (a plain host buffer), so such a cache never reaches a kernel."""
+    L = P.library()
+    out = ctypes.c_void_p()
+    assert L.compkv_host_cache_pointer(None, ctypes.byref(out)) == EINVAL
+    buf = ctypes.create_string_buffer(4096)
+    assert L.compkv_host_cache_pointer(ctypes.cast(buf, ctypes.c_void_p), None) == EINVAL
+    assert L.compkv_host_cache_pointer(ctypes.cast(buf, ctypes.c_void_p), ctypes.byref(out)) == EINVAL
+    assert not out.value
+    import torch
+
+    with pytest.raises(P.CompkvError):  # unpinned host tensors are refused by the binding
+        d = dims()
+        K = torch.zeros((1, 2, 4096, 128), dtype=torch.bfloat16)
+        P.compkv_dense_decode(d, 0.1, K, K, K, K, K, None, K)
