@@ -464,6 +464,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.cb = sp.cb;
         d.dense = 0;
         d.scale = params->scale;
+        d.sel_padded = 1;
         return launch_status(compkv::launch_decode(g, d, s));
     }
     // chunked scoring; then either the selection and the 128-token exact items as two launches, or
@@ -501,6 +502,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.part_count = nparts;
     d.part_base = drop ? 0 : sc.nchunks + 1;
     d.neg_pseudo = drop ? 0 : 1;
+    d.sel_padded = 1;
     e = use_sx ? compkv::launch_select_exact(g, a, d, n_ex, s) : compkv::launch_decode_items(g, d, n_ex, s);
     if (e != hipSuccess) return COMPKV_EHIP;
     return launch_status(compkv::launch_decode_merge(g, d, nparts, s));

@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kItemThreads) __attribute__((amdgpu_waves_per_eu(4)
             }
             __syncthreads();
         } else {
-            const int nsel = min(a.n_sel[u], a.sel_stride);
+            const int nsel = a.sel_padded ? a.sel_stride : min(a.n_sel[u], a.sel_stride);
             const int e0 = item * a.eb;
             tm.nblk = max(0, min(a.eb, nsel - e0));
             const int32_t* selu = a.sel + (size_t)u * a.sel_stride + e0;

@@ -68,6 +68,7 @@ struct ScoreArgs {
     int one_group;          // 1: one workgroup per unit scores and selects (no chunks, no partials)
     int score_kind;         // COMPKV_SCORE_*: CompKV score, mass only, or first-order mass estimate
     int chunks_only;        // chunked path: launch the chunk scoring without the selection
+    int tail_first;         // set by the launcher: the last-block workgroups lead the grid (else trail)
 };
 
 struct DecodeArgs {
@@ -92,6 +93,8 @@ struct DecodeArgs {
     int part_count;  // partials per unit in ws_part (row stride of the partial array)
     int part_base;   // partial index of this launch's item 0
     int neg_pseudo;  // exact items subtract the pseudo-terms of their selected blocks (fused step)
+    int sel_padded;  // the id slots past n_sel hold -1 (written by this library's selection): exact
+                     // items read their ids without waiting for n_sel
 };
 
 // ------------------------------------------------------------------ launchers (one per kernel family)

@@ -11,8 +11,10 @@
 // chunk's per-head (max m_c of a, sum of exp(a - m_c)), and per block the G terms
 // w_g = exp(a_g - m_c) sig2_g, stored contiguously so one vector load fetches a block's terms.
 // The last block of each unit (the one a decode step appends to) is scored by one extra workgroup per
-// unit, which writes its own partial; the chunks skip it. The grid is one-dimensional with these
-// workgroups first (ids 0 .. units-1), so they are dispatched before any chunk.
+// unit, which writes its own partial; the chunks skip it. The grid is one-dimensional. When every
+// workgroup is resident at once these lead it (ids 0 .. units-1: dispatched first, they are no longer
+// the last to finish); otherwise they trail it, so that the chunks (the long pole) all start at once and
+// the short extra workgroups take the first slots that free up.
 //
 // Fused decode step (kStep): the extra workgroup first stores the new row and recomputes the last
 // block's summary with the append's routine (bit-identical), so no chunk waits for it; every workgroup
@@ -111,8 +113,7 @@ struct ChunkShared {
     float q[G][D];   // scaled query
     float Qv[G][D];  // s^2 * sum of q^2 over each group (first r entries)
     float z[G][kBpcMax];
-    float v[G][kBpcMax];
-    float a[G][kBpcMax];
+    float v[G][kBpcMax];  // (a block's log weight is formed from z and v where it is needed)
     float m[G];
 };
 
@@ -234,10 +235,12 @@ template <int D, int G, bool kStep, int PMAX>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
     __shared__ ChunkLds<D, G, kStep> lds;
     const int units = geo.units();
-    if ((int)blockIdx.x < units) {
-        score_tail<D, G, kStep>(geo, a, blockIdx.x, lds.t);
+    const int tail = a.tail_first ? (int)blockIdx.x : (int)blockIdx.x - units * a.nchunks;
+    if (tail >= 0 && tail < units) {
+        score_tail<D, G, kStep>(geo, a, tail, lds.t);
         return;
     }
+    const int ck = a.tail_first ? (int)blockIdx.x - units : (int)blockIdx.x;
     constexpr int NF4 = D / 32;           // float4 of the mean-key row per lane
     constexpr int LPB = D / 4;            // compensation: lanes per mean-value row (one float4 each)
     constexpr int RPS = kThreads / LPB;   // mean-value rows per workgroup step
@@ -245,7 +248,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     ChunkShared<D, G>& sh = lds.c.sh;
     auto& st = lds.c.st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int u = (blockIdx.x - units) / a.nchunks, chunk = (blockIdx.x - units) % a.nchunks;
+    const int u = ck / a.nchunks, chunk = ck % a.nchunks;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int xmax = geo.xmax();
     const float s = a.scale;
@@ -281,11 +284,39 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const int xs = X - 1;  // blocks [0, X - 1) are scored here; the last one by the extra workgroup
     __syncthreads();
 
-    // block-mean logits: the query slice a lane needs is the same for all its slots, so it is read
-    // from LDS once per pair of heads (and the slots' sums are formed in the order the loads arrive)
-    constexpr int GB = G < 2 ? G : 2;
-    float z[PMAX][G], v[PMAX][G];
+    // projected variances first (the lead lane of each block keeps them in LDS), then the block-mean
+    // logits one pair of heads at a time: the query slice a lane needs is the same for all its slots,
+    // so it is read from LDS once per pair, and only one pair's sums are held (fewer registers, more
+    // resident workgroups)
+    float qv[G];
 #pragma unroll
+    for (int g = 0; g < G; ++g) qv[g] = li < geo.r ? sh.Qv[g][li] : 0.0f;
+    float lnb[PMAX];
+#pragma unroll
+    for (int p = 0; p < PMAX; ++p) {
+        const int lb = p * 32 + grp;
+        const int b = chunk0 + lb;
+        const bool valid = b < xs;
+        lnb[p] = valid ? logf((float)min(geo.B, n - b * geo.B)) : 0.0f;
+        float v[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) v[g] = qv[g] * dv0[p];
+        if (geo.r > 8 && valid) {
+            const size_t blk = (size_t)u * geo.xcap + b;
+            for (int t = li + 8; t < geo.r; t += 8) {
+                const float dv = a.dvar[blk * geo.r + t];
+#pragma unroll
+                for (int g = 0; g < G; ++g) v[g] += sh.Qv[g][t] * dv;
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            v[g] = sum8_lead(v[g]);
+            if (li == 0) sh.v[g][lb] = v[g];
+        }
+    }
+    constexpr int GB = G < 2 ? G : 2;
+#pragma unroll 1
     for (int g0 = 0; g0 < G; g0 += GB) {
         float4 qq[GB][NF4];
 #pragma unroll
@@ -293,48 +324,22 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
 #pragma unroll
             for (int m = 0; m < NF4; ++m) qq[gb][m] = *reinterpret_cast<const float4*>(&sh.q[g0 + gb][4 * (li + 8 * m)]);
 #pragma unroll
-        for (int p = 0; p < PMAX; ++p)
+        for (int p = 0; p < PMAX; ++p) {
+            const int lb = p * 32 + grp;
+            const bool valid = chunk0 + lb < xs;
 #pragma unroll
             for (int gb = 0; gb < GB; ++gb) {
-                float acc = 0.0f;
+                float z = 0.0f;
 #pragma unroll
                 for (int m = 0; m < NF4; ++m)
-                    acc += qq[gb][m].x * kv[p][m].x + qq[gb][m].y * kv[p][m].y + qq[gb][m].z * kv[p][m].z +
-                           qq[gb][m].w * kv[p][m].w;
-                z[p][g0 + gb] = acc;
-            }
-    }
-    float qv[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) qv[g] = li < geo.r ? sh.Qv[g][li] : 0.0f;
-#pragma unroll
-    for (int p = 0; p < PMAX; ++p) {
-        const int lb = p * 32 + grp;
-        const int b = chunk0 + lb;
-        const bool valid = b < xs;
-#pragma unroll
-        for (int g = 0; g < G; ++g) v[p][g] = qv[g] * dv0[p];
-        if (geo.r > 8 && valid) {
-            const size_t blk = (size_t)u * geo.xcap + b;
-            for (int t = li + 8; t < geo.r; t += 8) {
-                const float dv = a.dvar[blk * geo.r + t];
-#pragma unroll
-                for (int g = 0; g < G; ++g) v[p][g] += sh.Qv[g][t] * dv;
-            }
-        }
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            z[p][g] = sum8_lead(z[p][g]);
-            v[p][g] = sum8_lead(v[p][g]);
-        }
-        if (li == 0) {
-            const float lnb = valid ? logf((float)min(geo.B, n - b * geo.B)) : 0.0f;
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                sh.z[g][lb] = z[p][g];
-                sh.v[g][lb] = v[p][g];
-                sh.a[g][lb] = valid ? lnb + z[p][g] + half * v[p][g] : -INFINITY;
-                if constexpr (kStep) st.cw[g][lb] = valid ? lnb + z[p][g] : -INFINITY;  // pseudo-logit
+                    z += qq[gb][m].x * kv[p][m].x + qq[gb][m].y * kv[p][m].y + qq[gb][m].z * kv[p][m].z +
+                         qq[gb][m].w * kv[p][m].w;
+                z = sum8_lead(z);
+                if (li == 0) {
+                    const int g = g0 + gb;
+                    sh.z[g][lb] = z;
+                    if constexpr (kStep) st.cw[g][lb] = valid ? lnb[p] + z : -INFINITY;  // pseudo-logit
+                }
             }
         }
     }
@@ -347,6 +352,10 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         }
     }
     __syncthreads();
+    // log weight a = log|b| + zbar + half * sig2 of valid block lb of the chunk
+    auto logw = [&](int g, int lb) {
+        return logf((float)min(geo.B, n - (chunk0 + lb) * geo.B)) + sh.z[g][lb] + half * sh.v[g][lb];
+    };
     // the chunk's per-head max and sum of exp(a - max) (and, fused, of the pseudo-logits)
     const int nvalid = max(0, min(a.bpc, xs - chunk0));
     for (int g = wave; g < G; g += 4) {
@@ -355,7 +364,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
 #pragma unroll
         for (int k = 0; k < kBpcMax / 64; ++k) {
             const int lb = lane + 64 * k;
-            av[k] = lb < nvalid ? sh.a[g][lb] : -INFINITY;
+            av[k] = lb < nvalid ? logw(g, lb) : -INFINITY;
             m = fmaxf(m, av[k]);
         }
         m = wave_max(m);
@@ -405,7 +414,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     for (int idx = tid; idx < G * nvalid; idx += kThreads) {
         const int lb = idx / G, g = idx % G;
         a.ws_w[((size_t)u * xmax + chunk0 + lb) * G + g] =
-            expf(sh.a[g][lb] - sh.m[g]) * kind_term(a.score_kind, sh.v[g][lb]);
+            expf(logw(g, lb) - sh.m[g]) * kind_term(a.score_kind, sh.v[g][lb]);
     }
     if constexpr (kStep) if (comp) {
         // weighted mean values; lane vli of a row slot holds coordinates 4 vli .. 4 vli + 3
@@ -1159,13 +1168,19 @@ size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
     return ((size_t)2 * (a.nchunks + 1) * g.G + (a.keys_in_lds ? (size_t)g.xmax() : 0)) * sizeof(float);
 }
 
+template <int D, int G, bool kStep, int PMAX>
+void launch_chunks_p(const Geom& g, ScoreArgs a, hipStream_t s) {
+    const int grid = (a.nchunks + 1) * g.units();
+    a.tail_first = grid <= resident_slots(score_chunks_kernel<D, G, kStep, PMAX>);
+    score_chunks_kernel<D, G, kStep, PMAX><<<dim3(grid), kThreads, 0, s>>>(g, a);
+}
+
 template <int D, int G, bool kStep>
 void launch_chunks(const Geom& g, const ScoreArgs& a, hipStream_t s) {
-    const dim3 grid((a.nchunks + 1) * g.units());
     switch (a.bpc / 32) {
-        case 1: score_chunks_kernel<D, G, kStep, 1><<<grid, kThreads, 0, s>>>(g, a); break;
-        case 2: score_chunks_kernel<D, G, kStep, 2><<<grid, kThreads, 0, s>>>(g, a); break;
-        default: score_chunks_kernel<D, G, kStep, 4><<<grid, kThreads, 0, s>>>(g, a); break;
+        case 1: launch_chunks_p<D, G, kStep, 1>(g, a, s); break;
+        case 2: launch_chunks_p<D, G, kStep, 2>(g, a, s); break;
+        default: launch_chunks_p<D, G, kStep, 4>(g, a, s); break;
     }
 }
 
