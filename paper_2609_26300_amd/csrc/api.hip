@@ -87,6 +87,10 @@ SparseShape sparse_shape(const Geom& g, int K) {
     const int keff = std::max(1, std::min(K, xmax));
     int eb = std::max(1, 128 / g.B);         // one round of 128 exact tokens per item
     eb = std::max(eb, ceil_div(keff, 128));  // at most 128 exact items
+    // when the items would take more than one resident round, items of two rounds each (one
+    // workgroup's prologue and merge of its waves instead of two)
+    if ((long long)g.units() * ceil_div(keff, eb) > compkv::decode_item_slots(g))
+        eb = std::max(eb, std::min(compkv::decode_max_eb(), std::max(1, 256 / g.B)));
     const int n_exact = ceil_div(keff, eb);
     int cb = 128;                            // mean-value rows per compensation item
     cb = std::max(cb, ceil_div(xmax, compkv::decode_max_items() - n_exact));

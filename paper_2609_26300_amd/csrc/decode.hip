@@ -347,6 +347,17 @@ int decode_max_cb() { return kCbMax; }
 int decode_max_eb() { return kMaxEb; }
 int decode_max_row_bases() { return kMaxRowBase; }
 
+template <int D>
+int item_slots_d(const Geom& g) {
+    switch (g.G) {
+        case 1: return resident_slots(decode_items_kernel<D, 1>, kItemThreads);
+        case 2: return resident_slots(decode_items_kernel<D, 2>, kItemThreads);
+        case 4: return resident_slots(decode_items_kernel<D, 4>, kItemThreads);
+        default: return resident_slots(decode_items_kernel<D, 8>, kItemThreads);
+    }
+}
+int decode_item_slots(const Geom& g) { return g.D == 128 ? item_slots_d<128>(g) : item_slots_d<64>(g); }
+
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
     if (items < 1 || a.part_base + items > a.part_count || a.part_count > kMaxPartials ||
         (!a.dense && (a.cb > kCbMax || a.eb > kMaxEb)) ||

@@ -110,6 +110,7 @@ int decode_max_items();
 int decode_max_partials();
 int decode_max_cb();
 int decode_max_eb();
+int decode_item_slots(const Geom& g);  // item workgroups resident at once on the current device
 int decode_max_row_bases();  // row bases an item holds (dense items of a paged cache: their pages)
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s);
