@@ -248,7 +248,14 @@ __device__ __forceinline__ float xor_add(float x, int off) {
         case 2: return x + dpp_f<0x4E>(x);
         case 4: return x + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x101F));
         case 8: return x + dpp_f<0x128>(x);
-        case 16: return x + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F));
+        case 16: {  // gfx950 lane swaps (VALU, no LDS crossbar): the lower and upper rows of each half
+            const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+            return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+        }
+        case 32: {  // the two halves of the wave
+            const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+            return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+        }
         default: return x + __shfl_xor(x, off);
     }
 }
