@@ -10,7 +10,7 @@
  * Arithmetic is fp64 throughout; loops follow the paper's definitions in the order the paper
  * states them, with no blocking, fusion or reordering.
  *
- * Readings of points the paper leaves open (shared with the HIP path, listed in the design doc):
+ * Readings of points the paper leaves open (the HIP path takes the same readings):
  *  - coordinate groups (Appendix A.4): the d coordinates form d/2 RoPE frequency pairs; with the
  *    rotate-half layout pair f is (f, f + d/2), with the interleaved layout it is (2f, 2f+1). For r
  *    dividing d/2 the pairs are cut into r equal consecutive groups; for r = d each coordinate is
