@@ -471,7 +471,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.sel_padded = 1;
         return launch_status(compkv::launch_decode(g, d, s));
     }
-    // chunked scoring; then either the selection and the 128-token exact items as two launches, or
+    // chunked scoring; then either the selection and the exact items as two launches, or
     // (CHUNKED_EXACT, or AUTO when every item workgroup is resident at once) one fused launch
     const SxShape sx = sx_shape(g, sc.nchunks, K);
     const bool use_sx = use_select_exact(params->select_path, sx);

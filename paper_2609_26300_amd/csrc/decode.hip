@@ -10,7 +10,8 @@
 // not depend on scheduling; the kernel boundary makes the partials visible (no cross-workgroup fences).
 //
 // Item workgroups have eight waves (kItemThreads); an exact item runs the tile loop of exact.h, one
-// 16-token tile per wave and round, so a 128-token item is one round of the eight waves.
+// 16-token tile per wave and round, so a 128-token item is one round of the eight waves (256-token
+// items, two rounds, when the 128-token items would not all be resident at once).
 //
 // Compensation items are plain fp32 streaming on the vector ALUs: the mean-value rows (d/4 lanes x
 // float4 per row, 16 rows per thread in flight) are requested first; meanwhile the item marks its
