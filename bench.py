@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=40)
     ap.add_argument("--workload", default="llama8b_32k")
     ap.add_argument("--budget", type=int, default=None, help="override the workload's block budget")
+    ap.add_argument("--context", type=int, default=0,
+                    help="override the workload's tokens per sequence (a context sweep of one layer shape)")
     ap.add_argument("--layers", type=int, default=0, help="resident layer copies (0: enough for > 1 GB)")
     ap.add_argument("--select-path", choices=["auto", "chunked", "one_group", "chunked_exact"], default="auto",
                     help="scoring / selection launch shape (auto: one workgroup per unit where it fits)")
@@ -315,6 +317,8 @@ def main():
     w = WORKLOADS[args.workload]
     if args.n_var_groups:
         w = w.with_(n_var_groups=args.n_var_groups)
+    if args.context:
+        w = w.with_(context=args.context, name=f"{w.name} at {args.context} tokens")
     if w.decode_steps > 0:
         return run_streaming(args, w)
     budget = args.budget or w.budget_blocks

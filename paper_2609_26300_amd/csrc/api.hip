@@ -191,6 +191,15 @@ bool use_select_exact(int path, const SxShape& sx) {
     return (path == COMPKV_SELECT_CHUNKED_EXACT && sx.fits) || (path == COMPKV_SELECT_AUTO && sx.one_round);
 }
 
+// The fused step's choice of the one-group path: as for the scoring call, except that AUTO prefers the
+// fused selection/exact launch whenever all of its workgroups are resident at once (one launch fewer
+// than the one-group decode; measured faster at 4K-8K on 2 and 8 units)
+bool step_one_group(const Geom& g, const compkv_select_params* params, int* st) {
+    const bool one = one_group_path(g, params->select_path, st);
+    if (!one || params->select_path != COMPKV_SELECT_AUTO) return one;
+    return !sx_shape(g, score_shape(g).nchunks, params->budget_blocks).one_round;
+}
+
 int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
     if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || bytes < need) return COMPKV_EWORKSPACE;
     (void)g;
@@ -397,7 +406,7 @@ int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params*
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!params) return COMPKV_EINVAL;
-    const bool one = one_group_path(g, params->select_path, &st);
+    const bool one = step_one_group(g, params, &st);
     if (st != COMPKV_OK) return st;
     if (one) return COMPKV_SELECT_ONE_GROUP;
     return use_select_exact(params->select_path, sx_shape(g, score_shape(g).nchunks, params->budget_blocks))
@@ -422,7 +431,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     if (params->compensation != COMPKV_COMP_MEAN && params->compensation != COMPKV_COMP_DROP) return COMPKV_EINVAL;
     const bool drop = params->compensation == COMPKV_COMP_DROP;
     const int K = params->budget_blocks;
-    const bool one = one_group_path(g, params->select_path, &st);
+    const bool one = step_one_group(g, params, &st);
     if (st != COMPKV_OK) return st;
     const SparseShape sp = sparse_shape(g, K);
     const ScoreShape sc = score_shape(g);
