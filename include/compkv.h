@@ -126,9 +126,11 @@ typedef struct compkv_select_params {
  *              unit's selection and attends over its share of the blocks), when the budget is at most
  *              1024 blocks and a unit at most 8192 blocks; otherwise, and in compkv_score_select, as
  *              CHUNKED.
- *   AUTO:      ONE_GROUP when a unit holds at most 256 blocks (one workgroup then reads every summary
- *              in a single round of loads), else CHUNKED_EXACT when all of its workgroups are resident
- *              at once (at most one per compute unit), else CHUNKED.
+ *   AUTO:      in compkv_score_select, ONE_GROUP when a unit holds at most 256 blocks (one workgroup
+ *              then reads every summary in a single round of loads), else CHUNKED. In
+ *              compkv_decode_step, CHUNKED_EXACT when all of its workgroups are resident at once (at
+ *              most one per compute unit), else ONE_GROUP when a unit holds at most 256 blocks, else
+ *              CHUNKED.
  */
 #define COMPKV_SELECT_AUTO 0
 #define COMPKV_SELECT_CHUNKED 1
