@@ -81,3 +81,45 @@ def test_fullsize_fused_step(name, budget):
         o, l = oracle.sparse_decode(q, K, V, km, vm, nn, c.w.block_size, c.scale, s)
         assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL, (name, b, h)
         assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, float(np.max(np.abs(l)))), (name, b, h)
+
+
+@pytest.mark.parametrize("name", ["long_128k", "wide_gqa_64k"])
+def test_fullsize_graph_replays_match_eager(name):
+    """At full size the chunk grid exceeds one resident round (the last-block workgroups then trail the
+    grid) and the exact items are sized to one round: a captured step reproduces the eager step bit for
+    bit on every replay."""
+    c = _case(name)
+    c.budget = c.w.budget_blocks
+    c.select_path = P.COMPKV_SELECT_AUTO
+    d = c.dims
+    n = int(c.seq_lens[0])
+    k_new = c.K[:, :, n - 1].contiguous()
+    v_new = c.V[:, :, n - 1].contiguous()
+    ws = P.alloc_workspace(d, c.budget)
+    ref = c.decode_step(k_new, v_new, ws=ws)
+    torch.cuda.synchronize()
+    outs = {k: torch.empty_like(v) for k, v in ref.items()}
+    params = c.params()
+
+    def call():
+        P.compkv_decode_step(d, params, c.q, c.K, c.V, k_new, v_new, c.sl, c.summ.kmean, c.summ.dvar, c.summ.vmean,
+                             outs["sel"], outs["n_sel"], outs["blk_logit"], outs["scores"], outs["out"], outs["lse"],
+                             ws)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call()
+    for rep in range(3):
+        for t in outs.values():
+            t.fill_(-3)
+        g.replay()
+        torch.cuda.synchronize()
+        for k in ref:
+            assert torch.equal(outs[k], ref[k]), f"{name} replay {rep}: {k} differs"
+    print(f"[full-size {name}] {rep + 1} graph replays match the eager step", flush=True)
