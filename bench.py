@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--n-var-groups", type=int, default=0, help="override r, the variance groups per block")
     ap.add_argument("--host-kv", action="store_true",
                     help="offload tier: K/V caches in pinned host memory, read across the host link")
+    ap.add_argument("--host-summaries", action="store_true",
+                    help="with --host-kv: the fp32 summaries in pinned host memory too (the paper's layout)")
     ap.add_argument("--page-tokens", type=int, default=0,
                     help="paged K/V cache with pages of this many tokens, randomly permuted (0: contiguous)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -368,6 +370,10 @@ def main():
         if args.host_kv:  # the layer's cache moves to pinned host memory
             K = torch.empty(K.shape, dtype=K.dtype, pin_memory=True).copy_(K)
             V = torch.empty(V.shape, dtype=V.dtype, pin_memory=True).copy_(V)
+            if args.host_summaries:  # and its summaries
+                for f in ("kmean", "dvar", "vmean"):
+                    x = getattr(s, f)
+                    setattr(s, f, torch.empty(x.shape, dtype=x.dtype, pin_memory=True).copy_(x))
         Ks.append(K)
         Vs.append(V)
         summ.append(s)
@@ -515,7 +521,8 @@ def main():
                    "n_var_groups": w.n_var_groups, "layer_copies": layers, "parallelism": "single GPU",
                    "select_path": PATH_NAMES[step_path], "score_kind": args.score_kind,
                    "compensation": args.compensation, "page_tokens": page,
-                   "kv_memory": "pinned host" if args.host_kv else "device"},
+                   "kv_memory": "pinned host" if args.host_kv else "device",
+                   "summary_memory": "pinned host" if args.host_kv and args.host_summaries else "device"},
     }
     if "sparse" in result:
         us, per_k, wall, us_sep = result["sparse"]

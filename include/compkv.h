@@ -245,8 +245,10 @@ int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params*
  * device-mapped host memory (hipHostMalloc). This returns the device address of such an allocation in
  * *device_ptr, to be passed as k_cache / v_cache to any call; the kernels then read the rows they need
  * (the selected blocks, the active block) and write appended rows across the host link, with no
- * staging copy. The summaries, selections, outputs and workspace stay in device memory. Returns
- * COMPKV_EINVAL for null arguments or memory that is not pinned and mapped.
+ * staging copy. The summaries (kmean, dvar, vmean) may be placed there the same way (the paper keeps
+ * both in host memory); every step then also streams them across the link. Selections, outputs and
+ * workspace stay in device memory. Returns COMPKV_EINVAL for null arguments or memory that is not
+ * pinned and mapped.
  */
 int compkv_host_cache_pointer(const void* host_ptr, void** device_ptr);
 

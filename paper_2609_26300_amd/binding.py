@@ -159,18 +159,23 @@ def _ptr(t, dtype, shape, name, nullable=False):
     return t.data_ptr()
 
 
-def _kv_ptr(t, shape, name):
-    """Device address of a K/V cache: a CUDA tensor, or a pinned host tensor (the offload tier)."""
+def _mem_ptr(t, dtype, shape, name, nullable=False):
+    """Device address of a cache or summary array: a CUDA tensor, or a pinned host tensor (the offload
+    tier, mapped into the device address space by compkv_host_cache_pointer)."""
     if isinstance(t, torch.Tensor) and t.device.type == "cpu":
         if not t.is_pinned():
             raise CompkvError(f"{name} in host memory must be pinned")
-        if t.dtype != torch.bfloat16 or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
-            raise CompkvError(f"{name} must be a contiguous bf16 tensor of shape {tuple(shape)}")
+        if t.dtype != dtype or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+            raise CompkvError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)}")
         dev = ctypes.c_void_p()
         _check(library().compkv_host_cache_pointer(ctypes.c_void_p(t.data_ptr()), ctypes.byref(dev)),
                "compkv_host_cache_pointer")
         return dev.value
-    return _ptr(t, torch.bfloat16, shape, name)
+    return _ptr(t, dtype, shape, name, nullable)
+
+
+def _kv_ptr(t, shape, name):
+    return _mem_ptr(t, torch.bfloat16, shape, name)
 
 
 def _stream(stream):
@@ -234,8 +239,8 @@ def compkv_build_stats(dims, k_cache, v_cache, seq_lens, kmean, dvar, vmean, str
     bf, f32 = torch.bfloat16, torch.float32
     st = library().compkv_build_stats(
         ctypes.byref(dims), _kv_ptr(k_cache, cache, "k_cache"), _kv_ptr(v_cache, cache, "v_cache"),
-        _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _ptr(kmean, f32, summ, "kmean"),
-        _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"), _stream(stream))
+        _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _mem_ptr(kmean, f32, summ, "kmean"),
+        _mem_ptr(dvar, f32, dv, "dvar"), _mem_ptr(vmean, f32, summ, "vmean"), _stream(stream))
     _check(st, "compkv_build_stats")
 
 
@@ -246,8 +251,8 @@ def compkv_append_stats(dims, k_cache, v_cache, k_new, v_new, seq_lens, kmean, d
     st = library().compkv_append_stats(
         ctypes.byref(dims), _kv_ptr(k_cache, cache, "k_cache"), _kv_ptr(v_cache, cache, "v_cache"),
         _ptr(k_new, bf, new, "k_new"), _ptr(v_new, bf, new, "v_new"),
-        _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _ptr(kmean, f32, summ, "kmean"),
-        _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"), _stream(stream))
+        _ptr(seq_lens, torch.int32, (dims.batch,), "seq_lens"), _mem_ptr(kmean, f32, summ, "kmean"),
+        _mem_ptr(dvar, f32, dv, "dvar"), _mem_ptr(vmean, f32, summ, "vmean"), _stream(stream))
     _check(st, "compkv_append_stats")
 
 
@@ -259,7 +264,7 @@ def compkv_score_select(dims, params: CompkvSelectParams, q, kmean, dvar, seq_le
     ws, ws_bytes = _ws(workspace)
     st = library().compkv_score_select(
         ctypes.byref(dims), ctypes.byref(params), _ptr(q, torch.bfloat16, qs, "q"),
-        _ptr(kmean, f32, summ, "kmean"), _ptr(dvar, f32, dv, "dvar"),
+        _mem_ptr(kmean, f32, summ, "kmean"), _mem_ptr(dvar, f32, dv, "dvar"),
         _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, params.budget_blocks), "sel"),
         _ptr(n_sel, i32, units, "n_sel"),
         _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
@@ -278,7 +283,7 @@ def compkv_sparse_decode(dims, scale, q, k_cache, v_cache, vmean, blk_logit, seq
     ws, ws_bytes = _ws(workspace)
     st = library().compkv_sparse_decode(
         ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _kv_ptr(k_cache, cache, "k_cache"),
-        _kv_ptr(v_cache, cache, "v_cache"), _ptr(vmean, f32, summ, "vmean", nullable=True),
+        _kv_ptr(v_cache, cache, "v_cache"), _mem_ptr(vmean, f32, summ, "vmean", nullable=True),
         _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit", nullable=True),
         _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, sel.shape[2]), "sel"),
         _ptr(n_sel, i32, units, "n_sel"), int(sel.shape[2]), _ptr(out, f32, qs, "out"),
@@ -312,7 +317,7 @@ def compkv_decode_step(dims, params: CompkvSelectParams, q, k_cache, v_cache, k_
         ctypes.byref(dims), ctypes.byref(params), _ptr(q, bf, qs, "q"), _kv_ptr(k_cache, cache, "k_cache"),
         _kv_ptr(v_cache, cache, "v_cache"), _ptr(k_new, bf, new, "k_new", nullable=True),
         _ptr(v_new, bf, new, "v_new", nullable=True), _ptr(seq_lens, i32, (dims.batch,), "seq_lens"),
-        _ptr(kmean, f32, summ, "kmean"), _ptr(dvar, f32, dv, "dvar"), _ptr(vmean, f32, summ, "vmean"),
+        _mem_ptr(kmean, f32, summ, "kmean"), _mem_ptr(dvar, f32, dv, "dvar"), _mem_ptr(vmean, f32, summ, "vmean"),
         _ptr(sel, i32, (*units, params.budget_blocks), "sel"), _ptr(n_sel, i32, units, "n_sel"),
         _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
         _ptr(scores, f32, (*units, dims.xcap), "scores", nullable=True), _ptr(out, f32, qs, "out"),
