@@ -147,7 +147,7 @@ __device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int lay
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const float dev = kf[e] - mk[e];
-                m2[e] += ok ? dev * dev : 0.0f;
+                m2[e] += ok ? __fmul_rn(dev, dev) : 0.0f;  // (no fused multiply-add: same bits everywhere)
             }
         }
     }
@@ -184,6 +184,144 @@ __device__ void block_stats_from(const BlockSrc& b, BlockRows& R, int r, int lay
         }
     }
     __syncthreads();
+}
+
+// The same summary computed by ONE wave (no barrier, no LDS), for blocks of at most two workgroup load
+// steps (nb <= 2 * 4 * 64/(d/8): 32 rows at d = 128, 64 at d = 64). The wave plays the four waves of the
+// workgroup routine in turn (virtual wave v takes the rows the real wave v takes there) and adds in
+// exactly the same order: per lane over the steps, the butterflies over the row groups, the four waves'
+// sums as (w0 + w1) + (w2 + w3), the pair sums and the group butterflies over lanes = pairs. So its
+// results are bit-identical to block_stats_from's, which the append and the fused step keep using.
+template <int D>
+constexpr int wave_stats_max_rows() {
+    return 2 * 4 * (64 / (D / 8));
+}
+
+template <int D>
+__device__ void wave_block_stats(const BlockSrc& b, int r, int layout, float* __restrict__ km_out,
+                                 float* __restrict__ dv_out, float* __restrict__ vm_out) {
+    constexpr int LPR = D / 8;     // lanes per row
+    constexpr int RPW = 64 / LPR;  // rows per wave step
+    constexpr int RPG = 4 * RPW;   // rows per workgroup step
+    const int lane = threadIdx.x & 63, ro = lane / LPR, li = lane % LPR;
+    const int nb = b.nb;
+    // every row of the block (two workgroup steps x four virtual waves), requested at once
+    uint4 kw[2][4], vw[2][4];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = st * RPG + v * RPW + ro;
+            const int jj = j < nb ? j : 0;
+            kw[st][v] = *reinterpret_cast<const uint4*>(stats_krow<D>(b, jj) + li * 8);
+            vw[st][v] = *reinterpret_cast<const uint4*>(stats_vrow<D>(b, jj) + li * 8);
+        }
+    // per virtual wave: the lane's sums over its rows (step order), then over the row groups
+    float tk[8], tv[8], ak[8], av[8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        float sk[8] = {0, 0, 0, 0, 0, 0, 0, 0}, sv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+            const bool ok = st * RPG + v * RPW + ro < nb;
+            float kf[8], vf[8];
+            unpack_bf16x8(kw[st][v], kf);
+            unpack_bf16x8(vw[st][v], vf);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                sk[e] += ok ? kf[e] : 0.0f;
+                sv[e] += ok ? vf[e] : 0.0f;
+            }
+        }
+        // (the workgroup routine's later steps add +0 for rows past the block: no change)
+#pragma unroll
+        for (int off = LPR; off < 64; off <<= 1)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                sk[e] = xor_add(sk[e], off);
+                sv[e] = xor_add(sv[e], off);
+            }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            if (v == 0 || v == 2) {
+                tk[e] = sk[e];
+                tv[e] = sv[e];
+            } else if (v == 1) {
+                ak[e] = tk[e] + sk[e];
+                av[e] = tv[e] + sv[e];
+            } else {
+                ak[e] = ak[e] + (tk[e] + sk[e]);
+                av[e] = av[e] + (tv[e] + sv[e]);
+            }
+        }
+    }
+    const float fn = (float)nb;
+    float mk[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        mk[e] = ak[e] / fn;
+        av[e] = av[e] / fn;
+    }
+    if (ro == 0) {
+        float4* ko = reinterpret_cast<float4*>(km_out + li * 8);
+        float4* vo = reinterpret_cast<float4*>(vm_out + li * 8);
+        ko[0] = make_float4(mk[0], mk[1], mk[2], mk[3]);
+        ko[1] = make_float4(mk[4], mk[5], mk[6], mk[7]);
+        vo[0] = make_float4(av[0], av[1], av[2], av[3]);
+        vo[1] = make_float4(av[4], av[5], av[6], av[7]);
+    }
+    // squared deviations, the same way
+    float m2[8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        float s2[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+            const bool ok = st * RPG + v * RPW + ro < nb;
+            float kf[8];
+            unpack_bf16x8(kw[st][v], kf);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float dev = kf[e] - mk[e];
+                s2[e] += ok ? __fmul_rn(dev, dev) : 0.0f;
+            }
+        }
+#pragma unroll
+        for (int off = LPR; off < 64; off <<= 1)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s2[e] = xor_add(s2[e], off);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            if (v == 0 || v == 2) tk[e] = s2[e];
+            else if (v == 1) m2[e] = tk[e] + s2[e];
+            else m2[e] = m2[e] + (tk[e] + s2[e]);
+        }
+    }
+    if (r == D) {
+        if (ro == 0) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dv_out[li * 8 + e] = m2[e] / fn;
+        }
+        return;
+    }
+    // lane f = pair f: its two coordinates' totals, fetched from the lanes that hold them
+    auto coord = [&](int c) {  // every lane active; the value of coordinate c (lane c / 8, element c % 8)
+        float x = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float y = __shfl(m2[e], c / 8);
+            x = (c % 8 == e) ? y : x;
+        }
+        return x;
+    };
+    const bool in = lane < D / 2;
+    const int f = in ? lane : 0;
+    const int ia = layout == 0 ? f : 2 * f, ib = layout == 0 ? f + D / 2 : 2 * f + 1;
+    const float xa = coord(ia), xb = coord(ib);
+    float e2 = in ? xa + xb : 0.0f;
+    const int w = (D / 2) / r;
+    for (int off = 1; off < w; off <<= 1) e2 = xor_add(e2, off);
+    if (in && lane % w == 0) dv_out[lane / w] = e2 / (fn * (float)(D / r));
 }
 
 template <int D>

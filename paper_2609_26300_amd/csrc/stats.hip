@@ -1,7 +1,8 @@
 // stats.hip -- block summaries: prefill build and streaming append (Sections 4.1, 4.2; Appendix E.1).
 //
 // One workgroup computes one block's summary with wg_block_stats (block_stats.h): the prefill strides
-// over every (unit, block), the append recomputes each unit's active block after storing the new row.
+// over every (unit, block) (blocks of up to 32 rows at d = 128: one wave per block, same arithmetic),
+// the append recomputes each unit's active block after storing the new row.
 // Build, append and the fused decode step share that routine, so an appended block's summary is
 // bit-identical to the prefill one.
 #include "block_stats.h"
@@ -52,6 +53,26 @@ __global__ __launch_bounds__(kThreads) void build_stats_kernel(Geom g, StatsArgs
     }
 }
 
+// Blocks of at most wave_stats_max_rows<D>() rows: each wave summarizes whole blocks on its own (no
+// barrier, no LDS; bit-identical to the workgroup routine), consecutive waves taking consecutive
+// blocks, every row of a block requested at once.
+template <int D>
+__global__ __launch_bounds__(kThreads) void build_stats_wave_kernel(Geom g, StatsArgs a) {
+    constexpr int WPG = kThreads / 64;
+    const int xmax = g.xmax();
+    const int total = xmax * g.units();
+    const int nwaves = gridDim.x * WPG;
+    for (int flat = blockIdx.x * WPG + (threadIdx.x >> 6); flat < total; flat += nwaves) {  // wave-uniform
+        const int u = flat / xmax, b = flat % xmax;
+        const int n = clamp_len(a.seq_lens[u / g.hkv], g.max_seq);
+        if (b >= (n + g.B - 1) / g.B) continue;
+        const size_t row0 = (size_t)block_row0(g, u, b);
+        const BlockSrc src{a.K + row0 * D, a.V + row0 * D, nullptr, nullptr, min(g.B, n - b * g.B), -1};
+        const size_t blk = (size_t)u * g.xcap + b;
+        wave_block_stats<D>(src, g.r, g.layout, a.kmean + blk * D, a.dvar + blk * g.r, a.vmean + blk * D);
+    }
+}
+
 // grid = (units): workgroup u recomputes block n / B with the new row n = seq_lens (before the append)
 // taken from k_new / v_new, then stores that row in the cache.
 template <int D>
@@ -83,6 +104,12 @@ __global__ __launch_bounds__(kThreads) void append_stats_kernel(Geom g, StatsArg
 template <int D>
 void launch_build_d(const Geom& g, const StatsArgs& a, hipStream_t s) {
     const long long total = (long long)g.xmax() * g.units();
+    if (g.B <= wave_stats_max_rows<D>()) {  // one wave per block
+        const long long wgs = (total + kThreads / 64 - 1) / (kThreads / 64);
+        const long long slots = resident_slots(build_stats_wave_kernel<D>);  // one resident round
+        build_stats_wave_kernel<D><<<dim3((unsigned)(wgs < slots ? wgs : slots)), kThreads, 0, s>>>(g, a);
+        return;
+    }
     const long long slots = resident_slots(build_stats_kernel<D>);  // one resident round, grid-stride
     build_stats_kernel<D><<<dim3((unsigned)(total < slots ? total : slots)), kThreads, 0, s>>>(g, a);
 }
