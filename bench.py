@@ -551,6 +551,21 @@ def main():
             line["speedup_vs_dense"] = round(us_d / line["value"], 3)
             ab_d = algorithmic_bytes(w, budget, sel_lists)["dense_decode"]
             line["dense_hbm_gbps"] = round(ab_d / (per_kd["dense_decode"] * 1e-6) / 1e9, 1)
+    if not args.host_kv and not page:  # the prefill (compkv_build_stats) of one layer, outside the step
+        for _ in range(2):
+            P.compkv_build_stats(dims, Ks[0], Vs[0], seq_after, summ[0].kmean, summ[0].dvar, summ[0].vmean)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            P.compkv_build_stats(dims, Ks[0], Vs[0], seq_after, summ[0].kmean, summ[0].dvar, summ[0].vmean)
+        e1.record()
+        torch.cuda.synchronize()
+        us_b = e0.elapsed_time(e1) * 1e3 / 5
+        X = -(-n // w.block_size)
+        b_bytes = (w.batch * w.n_kv_heads * (n * w.head_dim * 2 * 2 + X * (2 * w.head_dim + w.n_var_groups) * 4))
+        line["prefill_build_us"] = round(us_b, 1)
+        line["prefill_hbm_gbps"] = round(b_bytes / (us_b * 1e-6) / 1e9, 1)
     line["paper_context"] = ("paper: up to 6.85x self-attention speedup over full attention, CPU-offload "
                              "pipeline on one NVIDIA H100 80GB + 4 host threads, PCIe-bound (128K, 512-token "
                              "budget); not comparable with an HBM-resident MI355X step")
