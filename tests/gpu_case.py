@@ -211,6 +211,9 @@ CASES = {
     "block1": lambda: Case(TINY.with_(context=300, block_size=1, budget_blocks=40, seed=8)),
     "r_eq_d": lambda: Case(TINY.with_(n_var_groups=128, seed=9)),
     "interleaved_r8": lambda: Case(TINY.with_(n_var_groups=8, seed=10), layout=1),
+    # variance groups of every width: one group of all 64 pairs, and 64 groups of one pair
+    "r1": lambda: Case(TINY.with_(n_var_groups=1, seed=28)),
+    "interleaved_r64": lambda: Case(TINY.with_(n_var_groups=64, seed=29), layout=1),
     "d64": lambda: Case(TINY.with_(head_dim=64, seed=11)),
     "g1": lambda: Case(TINY.with_(n_q_heads=2, seed=12)),
     "g2_b32": lambda: Case(TINY.with_(n_q_heads=4, block_size=32, budget_blocks=9, seed=13)),
