@@ -215,6 +215,7 @@ CASES = {
     "r1": lambda: Case(TINY.with_(n_var_groups=1, seed=28)),
     "interleaved_r64": lambda: Case(TINY.with_(n_var_groups=64, seed=29), layout=1),
     "d64": lambda: Case(TINY.with_(head_dim=64, seed=11)),
+    "d64_b64": lambda: Case(TINY.with_(head_dim=64, block_size=64, context=4000, budget_blocks=8, seed=30)),
     "g1": lambda: Case(TINY.with_(n_q_heads=2, seed=12)),
     "g2_b32": lambda: Case(TINY.with_(n_q_heads=4, block_size=32, budget_blocks=9, seed=13)),
     "g8_b64": lambda: Case(TINY.with_(n_q_heads=16, block_size=64, context=8000, budget_blocks=12, seed=14)),
