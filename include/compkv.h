@@ -253,7 +253,9 @@ int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params*
 int compkv_host_cache_pointer(const void* host_ptr, void** device_ptr);
 
 /* Workspace bytes needed by `which` (COMPKV_WS_*; COMPKV_WS_ALL = enough for every call) for these
- * dims and budget. Returns 0 if dims are invalid. */
+ * dims and budget. The fused step's launch shape follows the compute-unit count of the current device:
+ * query with the device that runs the calls current (a call given too small a workspace returns
+ * COMPKV_EWORKSPACE). Returns 0 if dims are invalid. */
 size_t compkv_workspace_bytes(const compkv_dims* dims, int32_t budget_blocks, int32_t which);
 
 /* Static string naming a status code. */

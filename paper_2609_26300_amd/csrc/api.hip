@@ -132,15 +132,27 @@ size_t dense_ws(const Geom& g) {
     return align_up((size_t)g.units() * sh.items * g.G * (g.D + 2) * sizeof(float));
 }
 
-// fused step: the score region, then [units][nchunks + 1 + n_exact][G][D + 2] decode partials:
-// compensation of each chunk and of the last block, then each exact item's partial
-int step_partials(const Geom& g, int K) {
-    return score_shape(g).nchunks + 1 + sparse_shape(g, K).n_exact;
+struct SxShape {  // the fused step's selection + exact launch (sx_shape below)
+    int eb, n_exact;
+    bool fits;       // within the kernel's limits
+    bool one_round;  // and every item workgroup resident at once (one workgroup per CU)
+};
+SxShape sx_shape(const Geom& g, int nchunks, int K);
+
+size_t step_part_bytes(const Geom& g, int parts) {
+    return align_up((size_t)g.units() * parts * g.G * (g.D + 2) * sizeof(float));
 }
 
-size_t step_ws(const Geom& g, int K) {
-    return score_ws(g) + align_up((size_t)g.units() * step_partials(g, K) * g.G * (g.D + 2) * sizeof(float));
+// fused step: the score region, then [units][nchunks + 1 + n_exact][G][D + 2] decode partials:
+// compensation of each chunk and of the last block, then each exact item's partial. The exact items
+// are those of the separate decode or of the fused selection/exact launch, whichever are more.
+int step_partials(const Geom& g, int K) {
+    const int nchunks = score_shape(g).nchunks;
+    const SxShape sx = sx_shape(g, nchunks, K);
+    return nchunks + 1 + std::max(sparse_shape(g, K).n_exact, sx.fits ? sx.n_exact : 0);
 }
+
+size_t step_ws(const Geom& g, int K) { return score_ws(g) + step_part_bytes(g, step_partials(g, K)); }
 
 size_t ws_bytes(const Geom& g, int K, int which) {
     size_t body = 0;
@@ -166,24 +178,21 @@ bool one_group_path(const Geom& g, int path, int* st) {
     return path == COMPKV_SELECT_ONE_GROUP && fits;
 }
 
-// Shape of the fused step's selection + exact launch: items of select_exact_waves() tiles of 16 tokens.
-struct SxShape {
-    int eb, n_exact;
-    bool fits;       // within the kernel's limits
-    bool one_round;  // and every item workgroup resident at once (one workgroup per CU)
-};
-
+// Shape of the fused step's selection + exact launch: items of up to select_exact_waves() tiles of 16
+// tokens.
 SxShape sx_shape(const Geom& g, int nchunks, int K) {
     const int xmax = g.xmax();
     const int keff = std::max(1, std::min(K, xmax));
     int cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 0;
-    // items of 128 tokens (half the waves attend, one tile each) while they fit one workgroup per CU,
-    // else of one tile per wave
+    // the smallest items of at least 64 tokens (four tiles) whose workgroups fit one per CU, up to one
+    // tile per wave (fewer attending waves per workgroup finish sooner: at 32K, 96-token items gave
+    // 24.0 us against 24.2 with 128-token ones and 25.7 with 256-token ones)
     const int full = 16 * compkv::select_exact_waves();
-    int eb = std::max(1, (full / 2) / g.B);
-    if ((long long)g.units() * ceil_div(keff, eb) > cus) eb = std::max(1, full / g.B);
+    const int eb_full = std::max(1, full / g.B);
+    int eb = std::min(eb_full, std::max(1, 64 / g.B));
+    while (eb < eb_full && (long long)g.units() * ceil_div(keff, eb) > cus) ++eb;
     const int n_exact = ceil_div(keff, eb);
     const size_t dyn = ((size_t)2 * (nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
     const bool fits = K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
@@ -492,6 +501,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     // Mean: the chunks' compensation partials, then the exact items' partials; Drop: exact items only
     float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
     const int nparts = drop ? n_ex : sc.nchunks + 1 + n_ex;
+    if (score_ws(g) + step_part_bytes(g, nparts) > workspace_bytes) return COMPKV_EWORKSPACE;  // sizing invariant
     a.comp_part = drop ? nullptr : dpart;
     a.part_count = nparts;
     a.chunks_only = use_sx;

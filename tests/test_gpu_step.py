@@ -201,3 +201,23 @@ def test_empty_sequence_in_batch(path):
             check_selection(s, sc["score"], c.budget, c.n_sink, c.n_recent)
             o, _ = oracle.sparse_decode(q, K, V, st[0], st[2], n, c.w.block_size, c.scale, s)
             assert rel_err(_gpu(out)[b, h * G:(h + 1) * G], o, axis=1) <= TOL
+
+
+@pytest.mark.parametrize("path", sorted(PATHS))
+@pytest.mark.parametrize("name", ["tiny_4k", "llama8b_32k", "wide_gqa_8k", "block1", "budget300_x2000"])
+def test_step_stays_within_workspace(name, path):
+    """Given exactly compkv_workspace_bytes(..., COMPKV_WS_DECODE_STEP) bytes, the fused step writes
+    nothing past them (a guard region after the workspace keeps its pattern) and gives the outputs of a
+    step on an oversized workspace."""
+    c = make_case(name, path)
+    c.build_stats()
+    d = c.dims
+    need = P.compkv_workspace_bytes(d, c.budget, P.COMPKV_WS_DECODE_STEP)
+    guard = 1 << 16
+    buf = torch.full((need + guard,), 0xA5, dtype=torch.uint8, device="cuda")
+    r = c.decode_step(ws=buf[:need])
+    ref = c.decode_step(ws=P.alloc_workspace(d, c.budget))
+    torch.cuda.synchronize()
+    assert bool((buf[need:] == 0xA5).all()), "the step wrote past its workspace"
+    for k in ref:
+        assert torch.equal(r[k], ref[k]), k
