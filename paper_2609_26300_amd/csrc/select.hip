@@ -1098,6 +1098,7 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
 // selection and exact attention and the round trip of the selected ids through memory; it pays off
 // while the items fit one resident round (one workgroup per CU).
 constexpr int kSxWaves = kFinThreads / 64;
+constexpr int kXcds = 8;  // accelerator complex dies of an MI355X, each with its own L2
 constexpr int kSelLdsMax = 1024;  // budget limit of the fused kernel (ids held in LDS)
 
 template <int D, int G>
@@ -1116,7 +1117,19 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
     __shared__ SelExactLds<D, G> L;
     extern __shared__ float dyn[];
     const int tid = threadIdx.x;
-    const int item = blockIdx.x, u = blockIdx.y;
+    // one-dimensional grid of items x units workgroups, which the dispatcher deals to the XCDs in turn
+    // by linear id: when the units fill whole rounds of kXcds, the items of unit u all run on XCD
+    // u % kXcds, so the unit's selection inputs are fetched once into that XCD's L2
+    const int units = geo.units(), items = (int)gridDim.x / units, lin = blockIdx.x;
+    int item, u;
+    if (units % kXcds == 0) {
+        const int s = lin / kXcds;
+        u = lin % kXcds + kXcds * (s / items);
+        item = s % items;
+    } else {
+        u = lin / items;
+        item = lin % items;
+    }
     finalize_select<G>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
     __syncthreads();
     const int bseq = u / geo.hkv, h = u % geo.hkv;
@@ -1217,7 +1230,7 @@ hipError_t dispatch_g(const Geom& g, const ScoreArgs& a, hipStream_t s) {
 
 template <int D, int G>
 hipError_t launch_sx(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int items, hipStream_t s) {
-    select_exact_kernel<D, G><<<dim3(items, g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a, d);
+    select_exact_kernel<D, G><<<dim3(items * g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a, d);
     return hipGetLastError();
 }
 
