@@ -108,19 +108,27 @@ __device__ __forceinline__ void store_query(const QueryPairs<D, G>& qp, float s,
 __device__ __forceinline__ float kind_half(int kind) { return kind == 2 ? 0.0f : 0.5f; }
 __device__ __forceinline__ float kind_term(int kind, float sig2) { return kind == 1 ? 1.0f : sig2; }
 
-template <int D, int G>
+// Per-block LDS rows of a chunk of 32 PMAX blocks: at least one wave's width, since the per-head passes
+// give every lane of a wave a slot. Sizing them by the chunk (not the largest one) keeps the 64-block
+// chunks of G = 8 at five workgroups per CU.
+template <int PMAX>
+constexpr int chunk_slots() {
+    return 32 * PMAX < 64 ? 64 : 32 * PMAX;
+}
+
+template <int D, int G, int NB>
 struct ChunkShared {
     float q[G][D];   // scaled query
     float Qv[G][D];  // s^2 * sum of q^2 over each group (first r entries)
-    float z[G][kBpcMax];
-    float v[G][kBpcMax];  // (a block's log weight is formed from z and v where it is needed)
+    float z[G][NB];
+    float v[G][NB];  // (a block's log weight is formed from z and v where it is needed)
     float m[G];
 };
 
 // Compensation state of the fused decode step.
-template <int D, int G>
+template <int D, int G, int NB>
 struct CompShared {
-    float cw[G][kBpcMax];
+    float cw[G][NB];
     float cm[G], cl[G];
     alignas(16) float acc[4][G][D];
 };
@@ -135,11 +143,11 @@ struct TailShared {
 };
 
 // A chunk workgroup and a last-block workgroup share one LDS allocation.
-template <int D, int G, bool kStep>
+template <int D, int G, bool kStep, int NB>
 union ChunkLds {
     struct {
-        ChunkShared<D, G> sh;
-        std::conditional_t<kStep, CompShared<D, G>, NoComp> st;
+        ChunkShared<D, G, NB> sh;
+        std::conditional_t<kStep, CompShared<D, G, NB>, NoComp> st;
     } c;
     TailShared<D, G> t;
 };
@@ -233,7 +241,9 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
 // PMAX = bpc / 32: block slots per thread (the chunk is 32 PMAX blocks).
 template <int D, int G, bool kStep, int PMAX>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
-    __shared__ ChunkLds<D, G, kStep> lds;
+    constexpr int NB = chunk_slots<PMAX>();
+    static_assert(NB % 64 == 0 && NB >= 32 * PMAX, "per-block rows must cover the chunk and whole waves");
+    __shared__ ChunkLds<D, G, kStep, NB> lds;
     const int units = geo.units();
     const int tail = a.tail_first ? (int)blockIdx.x : (int)blockIdx.x - units * a.nchunks;
     if (tail >= 0 && tail < units) {
@@ -245,7 +255,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     constexpr int LPB = D / 4;            // compensation: lanes per mean-value row (one float4 each)
     constexpr int RPS = kThreads / LPB;   // mean-value rows per workgroup step
     constexpr int VROWS = kStep ? 32 * PMAX / RPS : 1;
-    ChunkShared<D, G>& sh = lds.c.sh;
+    ChunkShared<D, G, NB>& sh = lds.c.sh;
     auto& st = lds.c.st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int u = ck / a.nchunks, chunk = ck % a.nchunks;
@@ -359,10 +369,10 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     // the chunk's per-head max and sum of exp(a - max) (and, fused, of the pseudo-logits)
     const int nvalid = max(0, min(a.bpc, xs - chunk0));
     for (int g = wave; g < G; g += 4) {
-        float av[kBpcMax / 64];
+        float av[NB / 64];
         float m = -INFINITY;
 #pragma unroll
-        for (int k = 0; k < kBpcMax / 64; ++k) {
+        for (int k = 0; k < NB / 64; ++k) {
             const int lb = lane + 64 * k;
             av[k] = lb < nvalid ? logw(g, lb) : -INFINITY;
             m = fmaxf(m, av[k]);
@@ -371,7 +381,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         float ssum = 0.0f;
         if (m != -INFINITY) {
 #pragma unroll
-            for (int k = 0; k < kBpcMax / 64; ++k) ssum += (av[k] == -INFINITY) ? 0.0f : expf(av[k] - m);
+            for (int k = 0; k < NB / 64; ++k) ssum += (av[k] == -INFINITY) ? 0.0f : expf(av[k] - m);
         }
         ssum = wave_sum(ssum);
         if (lane == 0) {
@@ -381,10 +391,10 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             pp[1] = ssum;
         }
         if constexpr (kStep) if (comp) {
-            float cv[kBpcMax / 64];
+            float cv[NB / 64];
             float cm = -INFINITY;
 #pragma unroll
-            for (int k = 0; k < kBpcMax / 64; ++k) {
+            for (int k = 0; k < NB / 64; ++k) {
                 const int lb = lane + 64 * k;
                 cv[k] = lb < nvalid ? st.cw[g][lb] : -INFINITY;
                 cm = fmaxf(cm, cv[k]);
@@ -392,7 +402,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             cm = wave_max(cm);
             float csum = 0.0f;
 #pragma unroll
-            for (int k = 0; k < kBpcMax / 64; ++k) {
+            for (int k = 0; k < NB / 64; ++k) {
                 const int lb = lane + 64 * k;
                 const float wv = (cv[k] == -INFINITY) ? 0.0f : __expf(cv[k] - cm);
                 st.cw[g][lb] = wv;
