@@ -42,6 +42,7 @@ namespace compkv {
 namespace {
 
 constexpr int kBpcMax = 128;  // blocks per chunk, upper bound
+constexpr int kXcds = 8;       // accelerator complex dies of an MI355X, each with its own L2
 constexpr int kHistBins = 2048;
 constexpr size_t kDynBudget = 32768;  // dynamic LDS of the finalize launch
 constexpr int kUnitTerms = 8192;      // G * xmax bound of the one-workgroup-per-unit path (64 KB of LDS)
@@ -258,7 +259,18 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     ChunkShared<D, G, NB>& sh = lds.c.sh;
     auto& st = lds.c.st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int u = ck / a.nchunks, chunk = ck % a.nchunks;
+    // workgroups go to the XCDs in turn by linear id: when the units fill whole rounds of kXcds, every
+    // chunk of unit u (like its last-block workgroup) runs on XCD u % kXcds, the XCD whose L2 the unit's
+    // selection then reads the chunks' outputs through
+    int u, chunk;
+    if (units % kXcds == 0) {
+        const int s = ck / kXcds;
+        u = ck % kXcds + kXcds * (s / a.nchunks);
+        chunk = s % a.nchunks;
+    } else {
+        u = ck / a.nchunks;
+        chunk = ck % a.nchunks;
+    }
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int xmax = geo.xmax();
     const float s = a.scale;
@@ -1108,7 +1120,6 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
 // selection and exact attention and the round trip of the selected ids through memory; it pays off
 // while the items fit one resident round (one workgroup per CU).
 constexpr int kSxWaves = kFinThreads / 64;
-constexpr int kXcds = 8;  // accelerator complex dies of an MI355X, each with its own L2
 constexpr int kSelLdsMax = 1024;  // budget limit of the fused kernel (ids held in LDS)
 
 template <int D, int G>
