@@ -152,7 +152,9 @@ __global__ __launch_bounds__(kItemThreads) __attribute__((amdgpu_waves_per_eu(4)
     Geom geo, DecodeArgs a, int nitems) {
     __shared__ DecodeShared<D, G> sh;
     const int tid = threadIdx.x;
-    const int u = blockIdx.y, item = blockIdx.x;
+    // the items of unit u all on XCD u % kXcds, like the unit's selection before and merge after them
+    int u, item;
+    xcd_unit_work(blockIdx.x, geo.units(), nitems, u, item);
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
@@ -308,7 +310,7 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(Geom geo, Decode
 
 template <int D, int G>
 hipError_t items_g(const Geom& g, const DecodeArgs& a, int items, hipStream_t s) {
-    decode_items_kernel<D, G><<<dim3(items, g.units()), kItemThreads, 0, s>>>(g, a, items);
+    decode_items_kernel<D, G><<<dim3(items * g.units()), kItemThreads, 0, s>>>(g, a, items);
     return hipGetLastError();
 }
 

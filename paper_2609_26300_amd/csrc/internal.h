@@ -166,6 +166,23 @@ __device__ __forceinline__ void unpack_bf16x8(const uint4 w, float f[8]) {
 
 __device__ __forceinline__ int clamp_len(int n, int cap) { return n < 0 ? 0 : (n > cap ? cap : n); }
 
+// The dispatcher deals the workgroups of a launch to the XCDs (accelerator complex dies, each with its
+// own L2) in turn by linear id. For a one-dimensional grid of units x per workgroups, work item w of
+// unit u is given linear id kXcds * (per * (u / kXcds) + w) + u % kXcds when the units fill whole
+// rounds of kXcds, so all of a unit's workgroups run on XCD u % kXcds (where the workgroups before
+// and after it for that unit run too); otherwise unit-major order. A bijection either way.
+constexpr int kXcds = 8;
+__device__ __forceinline__ void xcd_unit_work(int lin, int units, int per, int& u, int& w) {
+    if (units % kXcds == 0) {
+        const int s = lin / kXcds;
+        u = lin % kXcds + kXcds * (s / per);
+        w = s % per;
+    } else {
+        u = lin / per;
+        w = lin % per;
+    }
+}
+
 // floor(v / B) for 0 <= v < 2^23: the float quotient is within one of it, and one step corrects it
 __device__ __forceinline__ int div_small(int v, int B, float invB) {
     int k = (int)((float)v * invB);

@@ -42,7 +42,6 @@ namespace compkv {
 namespace {
 
 constexpr int kBpcMax = 128;  // blocks per chunk, upper bound
-constexpr int kXcds = 8;       // accelerator complex dies of an MI355X, each with its own L2
 constexpr int kHistBins = 2048;
 constexpr size_t kDynBudget = 32768;  // dynamic LDS of the finalize launch
 constexpr int kUnitTerms = 8192;      // G * xmax bound of the one-workgroup-per-unit path (64 KB of LDS)
@@ -259,18 +258,11 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     ChunkShared<D, G, NB>& sh = lds.c.sh;
     auto& st = lds.c.st;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // workgroups go to the XCDs in turn by linear id: when the units fill whole rounds of kXcds, every
-    // chunk of unit u (like its last-block workgroup) runs on XCD u % kXcds, the XCD whose L2 the unit's
-    // selection then reads the chunks' outputs through
+    // every chunk of unit u (like its last-block workgroup) on XCD u % kXcds, the XCD whose L2 the
+    // unit's selection then reads the chunks' outputs through (the chunks' linear ids start at 0 or at
+    // units, a multiple of kXcds whenever the mapping applies)
     int u, chunk;
-    if (units % kXcds == 0) {
-        const int s = ck / kXcds;
-        u = ck % kXcds + kXcds * (s / a.nchunks);
-        chunk = s % a.nchunks;
-    } else {
-        u = ck / a.nchunks;
-        chunk = ck % a.nchunks;
-    }
+    xcd_unit_work(ck, units, a.nchunks, u, chunk);
     const int bseq = u / geo.hkv, h = u % geo.hkv;
     const int xmax = geo.xmax();
     const float s = a.scale;
@@ -1138,19 +1130,11 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
     __shared__ SelExactLds<D, G> L;
     extern __shared__ float dyn[];
     const int tid = threadIdx.x;
-    // one-dimensional grid of items x units workgroups, which the dispatcher deals to the XCDs in turn
-    // by linear id: when the units fill whole rounds of kXcds, the items of unit u all run on XCD
-    // u % kXcds, so the unit's selection inputs are fetched once into that XCD's L2
-    const int units = geo.units(), items = (int)gridDim.x / units, lin = blockIdx.x;
-    int item, u;
-    if (units % kXcds == 0) {
-        const int s = lin / kXcds;
-        u = lin % kXcds + kXcds * (s / items);
-        item = s % items;
-    } else {
-        u = lin / items;
-        item = lin % items;
-    }
+    // the items of unit u all on XCD u % kXcds: the unit's selection inputs are fetched once into
+    // that XCD's L2
+    const int units = geo.units();
+    int u, item;
+    xcd_unit_work(blockIdx.x, units, (int)gridDim.x / units, u, item);
     finalize_select<G>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
     __syncthreads();
     const int bseq = u / geo.hkv, h = u % geo.hkv;
