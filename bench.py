@@ -26,6 +26,8 @@ import numpy as np
 
 HBM_PEAK_GBPS = 8000.0
 PATH_NAMES = {1: "chunked", 2: "one_group", 3: "chunked_exact"}
+# extra budgets timed beside a workload's own (the long-context layer's budget sweep)
+BUDGET_SWEEPS = {"long_128k": (32, 64, 128)}
 
 
 def step_kernels(path: int) -> str:
@@ -41,7 +43,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=400)
     ap.add_argument("--warmup", type=int, default=40)
-    ap.add_argument("--workload", default="llama8b_32k")
+    ap.add_argument("--workload", default="long_128k")
     ap.add_argument("--budget", type=int, default=None, help="override the workload's block budget")
     ap.add_argument("--context", type=int, default=0,
                     help="override the workload's tokens per sequence (a context sweep of one layer shape)")
@@ -60,7 +62,9 @@ def parse():
     ap.add_argument("--page-tokens", type=int, default=0,
                     help="paged K/V cache with pages of this many tokens, randomly permuted (0: contiguous)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="oracle time budget of each CPU-baseline leg (one thread, then all host threads)")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the extra budgets of the workload's sweep")
     ap.add_argument("--only", choices=["all", "sparse", "dense", "fused"], default="all",
                     help="limit the timed work (for profiler runs): sparse = fused step and separate calls, "
                          "fused = the fused step alone")
@@ -114,29 +118,66 @@ def measured_traffic(workload: str, call: str):
     return rec.get("traffic_bytes", {}).get(workload, {}).get(call)
 
 
+def host_cpu():
+    """(model name, logical CPUs visible, threads the all-core oracle run may use) of this host."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    visible = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    # at most 16 threads: the CPU share of one GPU on a shared box, whatever the machine shows
+    return model, os.cpu_count() or 1, max(1, min(16, visible))
+
+
 def cpu_baseline(w, budget, Kb, Vb, qb, seconds):
-    """The oracle (plain C, fp64, one thread) on the same step: score, select, compensated decode."""
+    """The oracle (plain C, fp64) on the same step: score, select, compensated decode of every unit,
+    from prebuilt fp64 summaries. Timed once on one thread and once on all host threads (one unit per
+    thread at a time; the C calls release the interpreter lock)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import oracle
 
     scale = 1.0 / math.sqrt(w.head_dim)
     B, r, G, n = w.block_size, w.n_var_groups, w.group, w.context
     units = [(b, h) for b in range(w.batch) for h in range(w.n_kv_heads)]
-    stats = {u: oracle.block_stats(Kb[u[0], u[1]], Vb[u[0], u[1]], n, B, r) for u in units}
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        for b, h in units:
-            km, dv, vm = stats[b, h]
-            q = qb[b, h * G:(h + 1) * G]
-            sc = oracle.block_scores(q, km, dv, n, B, r, scale)
-            sel = oracle.select(sc["score"], budget)
-            oracle.sparse_decode(q, Kb[b, h], Vb[b, h], km, vm, n, B, scale, sel)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    return dict(value=el / reps * 1e6, unit="us/decode-step/layer", cores=1, kind="oracle",
-                sample=f"{reps} full decode steps of the {w.name} layer ({len(units)} units): block scores, "
-                       f"selection and compensated decode from prebuilt fp64 summaries")
+    model, nproc, threads = host_cpu()
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        built = list(ex.map(lambda u: oracle.block_stats(Kb[u[0], u[1]], Vb[u[0], u[1]], n, B, r), units))
+    stats = dict(zip(units, built))
+
+    def unit(u):
+        b, h = u
+        km, dv, vm = stats[b, h]
+        q = qb[b, h * G:(h + 1) * G]
+        sc = oracle.block_scores(q, km, dv, n, B, r, scale)
+        sel = oracle.select(sc["score"], budget)
+        oracle.sparse_decode(q, Kb[b, h], Vb[b, h], km, vm, n, B, scale, sel)
+
+    def timed(nthreads):
+        reps, t0 = 0, time.perf_counter()
+        with ThreadPoolExecutor(max_workers=nthreads) as ex:
+            while True:
+                if nthreads == 1:
+                    for u in units:
+                        unit(u)
+                else:
+                    list(ex.map(unit, units))
+                reps += 1
+                el = time.perf_counter() - t0
+                if el >= seconds:
+                    return el / reps * 1e6, reps
+
+    one_us, one_reps = timed(1)
+    all_us, all_reps = timed(threads)
+    return dict(value=round(all_us, 1), unit="us/decode-step/layer", cores=threads, kind="oracle",
+                sample=f"{all_reps} full decode steps of the {w.name} layer ({len(units)} units) on {threads} "
+                       f"threads, and {one_reps} on one thread: block scores, selection and compensated decode "
+                       f"from prebuilt fp64 summaries",
+                one_core_value=round(one_us, 1), host_cpu=model, nproc=nproc)
 
 
 def run_streaming(args, w):
@@ -484,9 +525,37 @@ def main():
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) * 1e3 / steps, time.perf_counter() - wall0
 
+    def step_samples(fns, steps):
+        """Per-step times (us): one captured graph per layer, each replay followed by an event on the
+        launch stream, so consecutive events bracket exactly one step."""
+        graphs = [capture(fns, [L]) for L in range(layers)]
+        for i in range(min(steps, 2 * layers)):
+            graphs[i % layers].replay()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        ev[0].record()
+        for i in range(steps):
+            graphs[i % layers].replay()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        return np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(steps)])
+
+    def fused_at(K):
+        """The fused step at budget K with its own selection outputs and workspace."""
+        pk = P.CompkvSelectParams(K, 1, 2, scale, path, kind, params.compensation)
+        wk = P.alloc_workspace(dims, K)
+        sk = torch.empty((*units, K), dtype=torch.int32, device=dev)
+
+        def f(L):
+            s = summ[L]
+            P.compkv_decode_step(dims, pk, q, Ks[L], Vs[L], k_new, v_new, seq_after, s.kmean, s.dvar, s.vmean,
+                                 sk, n_sel, blk_logit, None, out, lse, wk)
+        return f, pk, sk
+
     result = {}
     if args.only in ("all", "sparse", "fused"):
         us, wall = run_steps([fused], args.steps, args.warmup)
+        samples = None if args.eager else step_samples([fused], args.steps)
         us_sep, per_k = None, {}
         if args.only != "fused":
             us_sep, _ = run_steps([append, score, decode], args.steps, args.warmup)
@@ -495,11 +564,29 @@ def main():
         # leave the outputs of a complete step for the checks below
         fused(0)
         torch.cuda.synchronize()
-        result["sparse"] = (us, per_k, wall, us_sep)
+        result["sparse"] = (us, per_k, wall, us_sep, samples)
         sel_host = sel.cpu().numpy().reshape(-1, budget)
         nsel_host = n_sel.cpu().numpy().reshape(-1)
         sel_lists = [list(sel_host[u, :nsel_host[u]]) for u in range(w.units)]
         assert all(len(s) == min(budget, -(-n // w.block_size)) for s in sel_lists), "selection count mismatch"
+        sweep = []
+        if args.only == "all" and not args.no_sweep and args.budget is None:
+            for K in BUDGET_SWEEPS.get(w.name, ()):
+                if K == budget:
+                    continue
+                f, pk, sk = fused_at(K)
+                us_k, _ = run_steps([f], args.steps, args.warmup)
+                f(0)
+                torch.cuda.synchronize()
+                sh, nh = sk.cpu().numpy().reshape(-1, K), n_sel.cpu().numpy().reshape(-1)
+                lists = [list(sh[u, :nh[u]]) for u in range(w.units)]
+                ab_k = algorithmic_bytes(w, K, lists, not drop)
+                b_k = ab_k["score_select"] + ab_k["sparse_decode"] + ab_k["append_stats"]
+                sweep.append(dict(budget_blocks=K, us=round(us_k, 3), algorithmic_bytes=b_k,
+                                  hbm_frac=round(b_k / (us_k * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                                  select_path=PATH_NAMES[P.compkv_decode_step_path(dims, pk)]))
+            fused(0)
+            torch.cuda.synchronize()
     if args.only in ("all", "dense"):
         us_d, wall_d = run_steps([row_write, dense], args.steps, args.warmup)
         per_kd = {"dense_decode": run_steps([dense], args.steps, args.warmup)[0]}
@@ -525,7 +612,7 @@ def main():
                    "summary_memory": "pinned host" if args.host_kv and args.host_summaries else "device"},
     }
     if "sparse" in result:
-        us, per_k, wall, us_sep = result["sparse"]
+        us, per_k, wall, us_sep, samples = result["sparse"]
         ab = algorithmic_bytes(w, budget, sel_lists, not drop)
         step_bytes = ab["score_select"] + ab["sparse_decode"] + ab["append_stats"]
         ach = step_bytes / (us * 1e-6) / 1e9
@@ -535,6 +622,9 @@ def main():
             "hbm_gbps": round(ach, 1),
             "hbm_frac": round(ach / HBM_PEAK_GBPS, 4),
             "algorithmic_bytes_per_step": step_bytes,
+            # mean and sample SD over individually timed steps (one graph replay per step)
+            "step_us_mean": round(float(samples.mean()), 3) if samples is not None else None,
+            "step_us_sd": round(float(samples.std(ddof=1)), 3) if samples is not None else None,
             "separate_calls_us_per_step": round(us_sep, 3) if us_sep is not None else None,
             "separate_call_us": {k: round(v, 3) for k, v in per_k.items()},
             # the timed call: its dispatches are the whole step
@@ -543,12 +633,19 @@ def main():
                          "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(w.name, "decode_step"),
                          "algorithmic_bytes_per_launch": step_bytes},
         })
+    if "sparse" in result and sweep:
+        line["budget_sweep"] = sweep + [dict(budget_blocks=budget, us=line["value"],
+                                             algorithmic_bytes=line["algorithmic_bytes_per_step"],
+                                             hbm_frac=line["hbm_frac"], select_path=PATH_NAMES[step_path])]
+        line["budget_sweep"].sort(key=lambda e: e["budget_blocks"])
     if "dense" in result:
         us_d, per_kd, _ = result["dense"]
         line["dense_us_per_step"] = round(us_d, 3)
         line["dense_kernel_us"] = {k: round(v, 3) for k, v in per_kd.items()}
         if "sparse" in result:
             line["speedup_vs_dense"] = round(us_d / line["value"], 3)
+            for e in line.get("budget_sweep", []):
+                e["speedup_vs_dense"] = round(us_d / e["us"], 3)
             ab_d = algorithmic_bytes(w, budget, sel_lists)["dense_decode"]
             line["dense_hbm_gbps"] = round(ab_d / (per_kd["dense_decode"] * 1e-6) / 1e9, 1)
     if not args.host_kv and not page:  # the prefill (compkv_build_stats) of one layer, outside the step

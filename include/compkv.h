@@ -173,8 +173,8 @@ int compkv_append_stats(const compkv_dims* dims, void* k_cache, void* v_cache, c
  * then S = F u TopK_{K-|F|}{S_b : b not in F}, F = first n_sink and last n_recent blocks (overlap
  * counted once). Ties rank the lower block id first; sel lists the ids in ascending order and
  * n_sel[u] = min(K, X); slots past n_sel are set to -1. If K >= X every block is selected.
- * blk_logit receives zbar (needed by compkv_sparse_decode); scores (nullable) receives S_b for every
- * block. q is bf16 [batch][n_q_heads][d]. Returns COMPKV_EBUDGET if K < n_sink + n_recent and
+ * blk_logit (nullable) receives zbar, which compkv_sparse_decode can take instead of recomputing it;
+ * scores (nullable) receives S_b for every block. q is bf16 [batch][n_q_heads][d]. Returns COMPKV_EBUDGET if K < n_sink + n_recent and
  * COMPKV_EUNSUPPORTED when a unit can hold more than 128 * (4096 / G - 1) blocks
  * (ceil(max_seq_len / block_size)).
  */
@@ -188,15 +188,16 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
  *   out_g = [ sum_{b in S} sum_{j in b} e^{z_{g,j}} v_j + sum_{b not in S} |b| e^{zbar_{g,b}} vmean_b ]
  *         / [ sum_{b in S} sum_{j in b} e^{z_{g,j}}     + sum_{b not in S} |b| e^{zbar_{g,b}} ]
  * with z_{g,j} = scale q_g . k_j, S = sel[u][0 .. n_sel[u]) (ascending, unique ids below X; entries
- * outside [0, X) are ignored) and zbar read from blk_logit as written by compkv_score_select.
- * sel_stride is the row stride of sel (the budget K). lse (nullable) receives the log of the
- * denominator, i.e. of the compensated normalizer. With vmean and blk_logit both NULL the omitted
- * blocks are left out (the Drop decode of Appendix A.5: out_g is attention over the selected
- * tokens alone); a unit with nothing selected then gets out = 0 and lse = -inf. Exactly one of the
- * two NULL is COMPKV_EINVAL.
+ * outside [0, X) are ignored) and zbar_{g,b} = scale q_g . kmean_b. zbar is read from blk_logit as
+ * written by compkv_score_select when blk_logit is given; with blk_logit NULL it is recomputed from
+ * kmean (then required). sel_stride is the row stride of sel (the budget K). lse (nullable) receives
+ * the log of the denominator, i.e. of the compensated normalizer. With vmean and blk_logit both NULL
+ * the omitted blocks are left out (the Drop decode of Appendix A.5: out_g is attention over the
+ * selected tokens alone; kmean is ignored); a unit with nothing selected then gets out = 0 and
+ * lse = -inf. COMPKV_EINVAL: vmean given without blk_logit or kmean, or blk_logit without vmean.
  */
 int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
-                         const void* v_cache, const float* vmean, const float* blk_logit,
+                         const void* v_cache, const float* kmean, const float* vmean, const float* blk_logit,
                          const int32_t* seq_lens, const int32_t* sel, const int32_t* n_sel,
                          int32_t sel_stride, float* out, float* lse, void* workspace,
                          size_t workspace_bytes, void* stream);
@@ -216,7 +217,9 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
  *  - seq_lens holds the lengths AFTER the new token (n = seq_lens[b] >= 1 per sequence). If k_new and
  *    v_new are given (bf16 [batch][n_kv_heads][d], both or neither), row n - 1 of every unit is
  *    stored from them and the summary of its block (n - 1) / B is refreshed, bit-identical to
- *    compkv_append_stats with length n - 1. Units with n == 0 append nothing.
+ *    compkv_append_stats with length n - 1. Units with n == 0 append nothing, and so do units with
+ *    n > max_seq_len (their cache rows and summaries are left untouched; like every call, the step
+ *    then scores and decodes them over max_seq_len tokens).
  *  - sel, n_sel, blk_logit and scores (nullable) are bit-identical to compkv_score_select on the
  *    refreshed summaries (sel has row stride params->budget_blocks).
  *  - out and lse (nullable) follow Eq. compkv-output as in compkv_sparse_decode (same tolerance, not

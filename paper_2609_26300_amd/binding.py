@@ -102,7 +102,7 @@ def library():
         L.compkv_append_stats.argtypes = [dp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
         L.compkv_score_select.argtypes = [dp, ctypes.POINTER(CompkvSelectParams), _vp, _vp, _vp, _vp, _vp,
                                           _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
-        L.compkv_sparse_decode.argtypes = [dp, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+        L.compkv_sparse_decode.argtypes = [dp, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                            _i32, _vp, _vp, _vp, ctypes.c_size_t, _vp]
         L.compkv_dense_decode.argtypes = [dp, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                           ctypes.c_size_t, _vp]
@@ -267,14 +267,15 @@ def compkv_score_select(dims, params: CompkvSelectParams, q, kmean, dvar, seq_le
         _mem_ptr(kmean, f32, summ, "kmean"), _mem_ptr(dvar, f32, dv, "dvar"),
         _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, params.budget_blocks), "sel"),
         _ptr(n_sel, i32, units, "n_sel"),
-        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
+        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit", nullable=True),
         _ptr(scores, f32, (*units, dims.xcap), "scores", nullable=True), ws, ws_bytes, _stream(stream))
     _check(st, "compkv_score_select")
 
 
 def compkv_sparse_decode(dims, scale, q, k_cache, v_cache, vmean, blk_logit, seq_lens, sel, n_sel, out,
-                         lse=None, workspace=None, stream=None):
-    """Compensated sparse decode; vmean = blk_logit = None gives the Drop decode."""
+                         lse=None, workspace=None, stream=None, kmean=None):
+    """Compensated sparse decode; vmean = blk_logit = None gives the Drop decode. With blk_logit None
+    and vmean given, the block-mean logits are recomputed from kmean."""
     cache, summ, _, qs = _shapes(dims)
     bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
     units = (dims.batch, dims.n_kv_heads)
@@ -283,7 +284,8 @@ def compkv_sparse_decode(dims, scale, q, k_cache, v_cache, vmean, blk_logit, seq
     ws, ws_bytes = _ws(workspace)
     st = library().compkv_sparse_decode(
         ctypes.byref(dims), float(scale), _ptr(q, bf, qs, "q"), _kv_ptr(k_cache, cache, "k_cache"),
-        _kv_ptr(v_cache, cache, "v_cache"), _mem_ptr(vmean, f32, summ, "vmean", nullable=True),
+        _kv_ptr(v_cache, cache, "v_cache"), _mem_ptr(kmean, f32, summ, "kmean", nullable=True),
+        _mem_ptr(vmean, f32, summ, "vmean", nullable=True),
         _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit", nullable=True),
         _ptr(seq_lens, i32, (dims.batch,), "seq_lens"), _ptr(sel, i32, (*units, sel.shape[2]), "sel"),
         _ptr(n_sel, i32, units, "n_sel"), int(sel.shape[2]), _ptr(out, f32, qs, "out"),

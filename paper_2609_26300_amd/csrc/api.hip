@@ -320,7 +320,7 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     Geom g;
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
-    if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel || !blk_logit) return COMPKV_EINVAL;
+    if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
     if (params->score_kind < COMPKV_SCORE_COMPKV || params->score_kind > COMPKV_SCORE_FIRST_ORDER) return COMPKV_EINVAL;
@@ -336,7 +336,7 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
 }
 
 int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, const void* k_cache,
-                         const void* v_cache, const float* vmean, const float* blk_logit,
+                         const void* v_cache, const float* kmean, const float* vmean, const float* blk_logit,
                          const int32_t* seq_lens, const int32_t* sel, const int32_t* n_sel,
                          int32_t sel_stride, float* out, float* lse, void* workspace,
                          size_t workspace_bytes, void* stream) {
@@ -344,7 +344,8 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!q || !k_cache || !v_cache || !seq_lens || !sel || !n_sel || !out) return COMPKV_EINVAL;
-    if ((vmean == nullptr) != (blk_logit == nullptr)) return COMPKV_EINVAL;  // both null: Drop
+    // Mean: vmean with blk_logit or kmean (zbar recomputed); Drop: vmean and blk_logit both null
+    if (vmean ? (!blk_logit && !kmean) : blk_logit != nullptr) return COMPKV_EINVAL;
     if (sel_stride < 1) return COMPKV_EINVAL;
     const size_t need = ws_bytes(g, sel_stride, COMPKV_WS_SPARSE_DECODE);
     st = check_ws(g, workspace, workspace_bytes, need);
@@ -359,6 +360,7 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     a.V = static_cast<const uint16_t*>(v_cache);
     a.vmean = vmean;
     a.blk_logit = blk_logit;
+    a.kmean = kmean;
     a.seq_lens = seq_lens;
     a.sel = sel;
     a.n_sel = n_sel;

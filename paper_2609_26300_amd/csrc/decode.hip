@@ -1,6 +1,8 @@
 // decode.hip -- compensated sparse decode and dense decode (Eq. compkv-output; Section 3.1).
 //
-// grid = (items, units). Every item produces one softmax partial per query head of its unit: the
+// One-dimensional grid of items * units workgroups, mapped by xcd_unit_work so that (when the units
+// fill whole rounds of eight) all items of unit u run on XCD u % 8. Every item produces one softmax
+// partial per query head of its unit: the
 // max m, the sum of weights l and the weighted value sum acc[d] (flash-decoding split-K).
 //   * exact items (sparse): the tokens of up to `eb` consecutive entries of the selected-id list;
 //   * compensation items (sparse): the unselected blocks among `cb` consecutive block ids, each
@@ -39,6 +41,53 @@ struct DecodeShared {
     int rowbase[kMaxRowBase];  // cache row of token 0 of each selected block (sparse) or page (dense)
 };
 
+// Pseudo-logits log|b| + zbar of the unselected blocks in [c0, c0 + nb) recomputed from the mean keys
+// (no block logits given): zbar_g = s q_g . kmean_b. The scaled query goes to LDS (in the exact items'
+// accumulator area, unused here); each wave then takes blocks in turn, four mean-key rows in flight per
+// lane, the G dot products summed over the wave. Selected blocks (sh.flag) get -inf.
+template <int D, int G>
+__device__ void block_logits_from_kmean(const DecodeArgs& a, const Geom& geo, int u, int n, int c0, int nb,
+                                        DecodeShared<D, G>& sh) {
+    constexpr int CPL = D / 64;  // mean-key coordinates per lane
+    constexpr int RIF = 4;       // rows in flight per wave
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bseq = u / geo.hkv, h = u % geo.hkv;
+    float (*qs)[D] = sh.ex.acc[0];  // [G][D] scaled query
+    const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+    for (int idx = tid; idx < G * D; idx += kItemThreads) qs[idx / D][idx % D] = a.scale * bf16_at(qh + idx);
+    __syncthreads();
+    float qv[G][CPL];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) qv[g][c] = qs[g][lane * CPL + c];
+    const float* km = a.kmean + ((size_t)u * geo.xcap + c0) * D + lane * CPL;
+    for (int lb0 = wave * RIF; lb0 < nb; lb0 += kItemWaves * RIF) {  // wave-uniform
+        float k[RIF][CPL];
+#pragma unroll
+        for (int e = 0; e < RIF; ++e) {  // branch-free: rows past the range reload row 0, unused
+            const int lb = lb0 + e < nb ? lb0 + e : 0;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) k[e][c] = km[(size_t)lb * D + c];
+        }
+#pragma unroll
+        for (int e = 0; e < RIF; ++e) {
+            const int lb = lb0 + e;
+            if (lb >= nb) break;  // wave-uniform
+            const int b = c0 + lb;
+            const float lnb = logf((float)min(geo.B, n - b * geo.B));
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                float z = 0.0f;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) z += qv[g][c] * k[e][c];
+                z = wave_sum(z);
+                if (lane == 0) sh.w[g][lb] = sh.flag[lb] ? -INFINITY : lnb + z;
+            }
+        }
+    }
+}
+
 // Pseudo-tokens of the unselected blocks in [c0, c1).
 template <int D, int G>
 __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n, int X, int c0, int c1,
@@ -68,11 +117,15 @@ __device__ void compensation(const DecodeArgs& a, const Geom& geo, int u, int n,
     }
     __syncthreads();
     // pseudo-logits log|b| + zbar and their per-head max
-    const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
-    for (int idx = tid; idx < G * nb; idx += kItemThreads) {
-        const int g = idx / nb, lb = idx % nb, b = c0 + lb;
-        sh.w[g][lb] = sh.flag[lb] ? -INFINITY
-                                  : logf((float)min(geo.B, n - b * geo.B)) + lg[(size_t)g * geo.xcap + b];
+    if (a.blk_logit) {  // workgroup-uniform: zbar as written by the scoring call
+        const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
+        for (int idx = tid; idx < G * nb; idx += kItemThreads) {
+            const int g = idx / nb, lb = idx % nb, b = c0 + lb;
+            sh.w[g][lb] = sh.flag[lb] ? -INFINITY
+                                      : logf((float)min(geo.B, n - b * geo.B)) + lg[(size_t)g * geo.xcap + b];
+        }
+    } else {
+        block_logits_from_kmean<D, G>(a, geo, u, n, c0, nb, sh);
     }
     __syncthreads();
     for (int g = wave; g < G; g += kItemWaves) {

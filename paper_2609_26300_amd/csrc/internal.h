@@ -77,6 +77,7 @@ struct DecodeArgs {
     const uint16_t* V;
     const float* vmean;
     const float* blk_logit;  // with vmean: null for the Drop decode (no compensation items)
+    const float* kmean;      // Mean decode without blk_logit: the block-mean logits are recomputed
     const int32_t* seq_lens;
     const int32_t* sel;
     const int32_t* n_sel;

@@ -161,7 +161,8 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     QueryPairs<D, G> qp;
     load_query_pairs<D, G>(qh, geo.layout, qp);  // consumed only after the block's own loads are issued
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int n_raw = a.seq_lens[bseq];
+    const int n = clamp_len(n_raw, geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* pp = a.ws_part + ((size_t)u * (nc + 1) + nc) * G * 2;
     // fused step with Mean compensation: this workgroup's compensation partial
@@ -177,7 +178,9 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     }
     const int b = X - 1, nb = n - b * geo.B;
     const size_t blk = (size_t)u * geo.xcap + b;
-    const bool append = kStep && a.k_new;
+    // a length beyond max_seq_len appends nothing (row n - 1 would lie past the sized range): the unit
+    // is scored over max_seq_len tokens from its stored summaries, as in the separate calls
+    const bool append = kStep && a.k_new && n_raw <= geo.max_seq;
     if (append) {  // the summary reads row n - 1 from k_new / v_new; the cache row is stored at the end
         const size_t row0 = (size_t)block_row0(geo, u, b);
         const BlockSrc src{a.Kc + row0 * D, a.Vc + row0 * D, a.k_new + (size_t)u * D, a.v_new + (size_t)u * D, nb,
@@ -211,7 +214,7 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     const float lnb = logf((float)nb);
     for (int g = tid; g < G; g += kThreads) {
         const float z = ts.z[g], v = ts.v[g];
-        a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
+        if (a.blk_logit) a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
         pp[2 * g] = lnb + z + kind_half(a.score_kind) * v;  // the partial of one block: max a, sum exp(a - a) = 1
         pp[2 * g + 1] = 1.0f;
         a.ws_w[((size_t)u * geo.xmax() + b) * G + g] = kind_term(a.score_kind, v);
@@ -420,8 +423,8 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         }
     }
     __syncthreads();
-    // coalesced stores: block logits [g][b] and score terms [b][g]
-    for (int idx = tid; idx < G * nvalid; idx += kThreads) {
+    // coalesced stores: block logits [g][b] (when requested) and score terms [b][g]
+    for (int idx = tid; a.blk_logit && idx < G * nvalid; idx += kThreads) {
         const int g = idx / nvalid, lb = idx % nvalid;
         a.blk_logit[((size_t)u * G + g) * geo.xcap + chunk0 + lb] = sh.z[g][lb];
     }
@@ -951,10 +954,12 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
     QueryPairs<D, G> qp;
     if (wave < 4) load_query_pairs<D, G>(qh, geo.layout, qp);
     __asm__ volatile("" ::: "memory");
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
+    const int n_raw = a.seq_lens[bseq];
+    const int n = clamp_len(n_raw, geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     const int npass = (X + GPP - 1) / GPP;
-    const bool refresh = kStep && a.k_new && X >= 1;  // workgroup-uniform
+    // workgroup-uniform; a length beyond max_seq_len appends nothing (as in the chunked path)
+    const bool refresh = kStep && a.k_new && X >= 1 && n_raw <= geo.max_seq;
     const int lastb = X - 1;
     const size_t blk_last = (size_t)u * geo.xcap + (lastb >= 0 ? lastb : 0);
     BlockSrc src{};
@@ -1049,7 +1054,7 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
                         const int g = g0 + gb;
                         const float lnb = logf((float)min(geo.B, n - b * geo.B));
                         A[b * G + g] = lnb + z + kind_half(a.score_kind) * Vp[b * G + g];
-                        a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
+                        if (a.blk_logit) a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
                     }
                 }
             }
@@ -1104,8 +1109,9 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
 }
 
 // ---------------------------------------------------------------- selection + exact items, fused
-// The fused step's selection and exact items as one launch, grid = (items, units), kFinThreads threads
-// per workgroup. Every workgroup of a unit repeats the unit's selection from the chunk partials (the
+// The fused step's selection and exact items as one launch: a one-dimensional grid of items * units
+// workgroups of kFinThreads threads, mapped by xcd_unit_work so that (when the units fill whole rounds
+// of eight) all items of unit u run on XCD u % 8. Every workgroup of a unit repeats the unit's selection from the chunk partials (the
 // same computation as select_finalize_kernel, so all of them hold the same ids) into LDS; item 0 also
 // writes the selection outputs. Then the sixteen waves attend exactly over the item's blocks (exact.h,
 // one 16-token tile per wave and round) and write the item's partial. This saves the launch between

@@ -123,16 +123,17 @@ class Case:
         P.compkv_score_select(d, self.params(), self.q if q is None else q, self.summ.kmean, self.summ.dvar, self.sl,
                               self.sel, self.n_sel, self.blk_logit, self.scores, self.ws)
 
-    def sparse_decode(self, sel=None, n_sel=None):
-        """compkv_sparse_decode; the Drop decode when this case's compensation is COMPKV_COMP_DROP."""
+    def sparse_decode(self, sel=None, n_sel=None, from_kmean=False):
+        """compkv_sparse_decode; the Drop decode when this case's compensation is COMPKV_COMP_DROP. With
+        from_kmean the block logits are not passed: the library recomputes them from the mean keys."""
         d = self.dims
         self.out = torch.zeros((d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device="cuda")
         self.lse = torch.zeros((d.batch, d.n_q_heads), dtype=torch.float32, device="cuda")
         drop = self.compensation == P.COMPKV_COMP_DROP
         P.compkv_sparse_decode(d, self.scale, self.q, self.K, self.V, None if drop else self.summ.vmean,
-                               None if drop else self.blk_logit, self.sl,
+                               None if drop or from_kmean else self.blk_logit, self.sl,
                                self.sel if sel is None else sel, self.n_sel if n_sel is None else n_sel,
-                               self.out, self.lse, self.ws)
+                               self.out, self.lse, self.ws, kmean=self.summ.kmean if from_kmean else None)
         return self.out, self.lse
 
     def decode_step(self, k_new=None, v_new=None, sl=None, summ=None, K=None, V=None, ws=None):

@@ -81,10 +81,13 @@ def test_null_pointers_rejected():
     assert L.compkv_build_stats(ctypes.byref(d), None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == EINVAL
     assert L.compkv_append_stats(ctypes.byref(d), FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == EINVAL
     p = P.CompkvSelectParams(16, 1, 2, 0.088)
+    assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                 None, FAKE, 1 << 30, None) == EINVAL  # n_sel required
+    # blk_logit is optional: a NULL one gets past the pointer checks (to the workspace check)
     assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
-                                 None, FAKE, 1 << 30, None) == EINVAL  # blk_logit required
-    assert L.compkv_sparse_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 16,
-                                  FAKE, None, FAKE, 1 << 30, None) == EINVAL
+                                 None, FAKE, 1, None) == EWS
+    assert L.compkv_sparse_decode(ctypes.byref(d), 0.1, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE,
+                                  16, FAKE, None, FAKE, 1 << 30, None) == EINVAL  # q required
 
 
 def test_budget_below_mandatory_set_rejected():
@@ -219,12 +222,14 @@ def test_score_kind_and_compensation_validation():
     for comp, rc in ((-1, EINVAL), (2, EINVAL), (P.COMPKV_COMP_DROP, EWS), (P.COMPKV_COMP_MEAN, EWS)):
         assert _step(L, d, P.CompkvSelectParams(16, 1, 2, 0.088, 0, 0, comp), ws_bytes=1) == rc
 
-    def sparse(vmean, blk):
-        return L.compkv_sparse_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, vmean, blk, FAKE, FAKE, FAKE, 16,
-                                      FAKE, None, FAKE, 1, None)
+    def sparse(vmean, blk, kmean=None):
+        return L.compkv_sparse_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, kmean, vmean, blk, FAKE, FAKE, FAKE,
+                                      16, FAKE, None, FAKE, 1, None)
 
-    assert sparse(FAKE, None) == EINVAL and sparse(None, FAKE) == EINVAL
+    # Mean needs the block logits or the mean keys to form them; Drop takes neither vmean nor blk_logit
+    assert sparse(FAKE, None) == EINVAL and sparse(None, FAKE) == EINVAL and sparse(None, FAKE, FAKE) == EINVAL
     assert sparse(None, None) == EWS and sparse(FAKE, FAKE) == EWS
+    assert sparse(FAKE, None, FAKE) == EWS and sparse(None, None, FAKE) == EWS
 
 
 def test_decode_step_path_resolution():

@@ -67,8 +67,10 @@ def test_score_select_parity(case_p):
         assert np.all(sel[b, h, nsel[b, h]:] == -1)
 
 
-def test_sparse_decode_with_oracle_selection(case):
-    """Eq. compkv-output on the oracle's own selected set (decode tested apart from selection)."""
+@pytest.mark.parametrize("from_kmean", [False, True], ids=["blk_logit", "kmean"])
+def test_sparse_decode_with_oracle_selection(case, from_kmean):
+    """Eq. compkv-output on the oracle's own selected set (decode tested apart from selection), with the
+    block-mean logits passed in (blk_logit) or recomputed by the library from the mean keys."""
     d = case.dims
     sel = np.full((d.batch, d.n_kv_heads, case.budget), -1, np.int32)
     nsel = np.zeros((d.batch, d.n_kv_heads), np.int32)
@@ -78,7 +80,7 @@ def test_sparse_decode_with_oracle_selection(case):
         s = oracle.select(case.oracle_scores(b, h, stats[b, h])["score"], case.budget, case.n_sink, case.n_recent)
         sel[b, h, :len(s)] = s
         nsel[b, h] = len(s)
-    out, lse = case.sparse_decode(torch.from_numpy(sel).cuda(), torch.from_numpy(nsel).cuda())
+    out, lse = case.sparse_decode(torch.from_numpy(sel).cuda(), torch.from_numpy(nsel).cuda(), from_kmean)
     out, lse = _gpu(out), _gpu(lse)
     G = case.G
     for b, h in case.units():
@@ -88,6 +90,19 @@ def test_sparse_decode_with_oracle_selection(case):
         assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL
         assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, np.max(np.abs(l)))
     case.sparse_decode()  # restore the pipeline's own output
+
+
+def test_score_select_without_block_logits(case_p):
+    """blk_logit is optional: without it the selection outputs are the same, bit for bit."""
+    case = case_p
+    import paper_2609_26300_amd as P
+    sel = torch.full_like(case.sel, -7)
+    n_sel = torch.zeros_like(case.n_sel)
+    scores = torch.zeros_like(case.scores)
+    P.compkv_score_select(case.dims, case.params(), case.q, case.summ.kmean, case.summ.dvar, case.sl, sel, n_sel,
+                          None, scores, case.ws)
+    torch.cuda.synchronize()
+    assert torch.equal(sel, case.sel) and torch.equal(n_sel, case.n_sel) and torch.equal(scores, case.scores)
 
 
 def test_end_to_end_parity(case_p):

@@ -176,6 +176,32 @@ def test_step_graph_replays_match_eager(path):
 
 
 @pytest.mark.parametrize("path", sorted(PATHS))
+def test_step_length_beyond_max_seq_appends_nothing(path):
+    """A sequence whose length exceeds max_seq_len appends nothing: its cache rows and every block
+    summary stay bit-identical, and the step's outputs equal a step without an append (the unit is
+    decoded over max_seq_len tokens, like in every other call)."""
+    w = TINY.with_(batch=2, context=1000, decode_steps=8, seed=34)
+    c = Case(w, seq_lens=[1001, 700], max_seq_len=1000)
+    c.select_path = PATHS[path]
+    c.build_stats()
+    K0, V0 = c.K.clone(), c.V.clone()
+    summ0 = {k: getattr(c.summ, k).clone() for k in ("kmean", "dvar", "vmean")}
+    ref = c.decode_step()
+    kn = dev_bf16(c.K_bits[:, :, 1003])
+    vn = dev_bf16(c.V_bits[:, :, 1004])
+    r = c.decode_step(kn.contiguous(), vn.contiguous())
+    torch.cuda.synchronize()
+    # sequence 0 (1001 > max_seq_len): nothing stored, no summary touched
+    assert torch.equal(c.K[0], K0[0]) and torch.equal(c.V[0], V0[0])
+    for k, v in summ0.items():
+        assert torch.equal(getattr(c.summ, k)[0], v[0]), k
+    for k in ("sel", "n_sel", "out", "lse"):
+        assert torch.equal(r[k][0], ref[k][0]), k
+    # sequence 1 (700 tokens) did append row 699
+    assert torch.equal(c.K[1, :, 699], kn[1]) and torch.equal(c.V[1, :, 699], vn[1])
+
+
+@pytest.mark.parametrize("path", sorted(PATHS))
 def test_empty_sequence_in_batch(path):
     """A sequence with no tokens has no blocks: nothing is selected, its output is zero and its lse is
     -inf, in the separate calls and in the fused step (which appends nothing for it); the other
