@@ -54,6 +54,7 @@ extern "C" {
 #define COMPKV_EBUDGET (-3)     /* budget smaller than the mandatory set n_sink + n_recent */
 #define COMPKV_EWORKSPACE (-4)  /* workspace null, misaligned or too small */
 #define COMPKV_EHIP (-5)        /* a kernel launch failed */
+#define COMPKV_ESCRATCH (-6)    /* compkv_decode_step_noalloc: the step needs more than its fixed scratch */
 
 /* Coordinate groups of the grouped key variance (Appendix A.4): the d coordinates form d/2 RoPE
  * frequency pairs, cut into r equal consecutive groups with both coordinates of a pair together.
@@ -237,6 +238,27 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
                        const int32_t* seq_lens, float* kmean, float* dvar, float* vmean, int32_t* sel,
                        int32_t* n_sel, float* blk_logit, float* scores, float* out, float* lse,
                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * compkv_decode_step for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same step, arguments and results, with
+ * no workspace argument. Its scratch is a fixed device array of compkv_decode_step_noalloc_limit()
+ * bytes (32 MiB) inside the library, one per GPU, held until the process ends; the call allocates and
+ * frees nothing. Returns COMPKV_ESCRATCH when compkv_workspace_bytes(dims, budget,
+ * COMPKV_WS_DECODE_STEP) exceeds that size (use compkv_decode_step with a workspace then), and
+ * COMPKV_EHIP when the scratch's device address cannot be obtained. The scratch needs no initial
+ * contents and keeps whatever the last call left; every call on one GPU uses the same scratch, so
+ * calls that may overlap on one GPU (concurrent streams or threads) race and must be serialized by
+ * the caller.
+ */
+int compkv_decode_step_noalloc(const compkv_dims* dims, const compkv_select_params* params, const void* q,
+                               void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                               const int32_t* seq_lens, float* kmean, float* dvar, float* vmean, int32_t* sel,
+                               int32_t* n_sel, float* blk_logit, float* scores, float* out, float* lse,
+                               void* stream);
+
+/* Bytes of the fixed scratch behind compkv_decode_step_noalloc. */
+size_t compkv_decode_step_noalloc_limit(void);
 
 /* The launch shape compkv_decode_step takes for these dims and params on the current device:
  * COMPKV_SELECT_ONE_GROUP, COMPKV_SELECT_CHUNKED or COMPKV_SELECT_CHUNKED_EXACT (params->select_path

@@ -32,6 +32,8 @@ from .binding import (  # noqa: F401
     compkv_append_stats,
     compkv_build_stats,
     compkv_decode_step,
+    compkv_decode_step_noalloc,
+    compkv_decode_step_noalloc_limit,
     compkv_decode_step_path,
     compkv_dense_decode,
     compkv_score_select,

@@ -108,6 +108,9 @@ def library():
                                           ctypes.c_size_t, _vp]
         L.compkv_decode_step.argtypes = [dp, ctypes.POINTER(CompkvSelectParams), _vp, _vp, _vp, _vp, _vp, _vp,
                                          _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+        L.compkv_decode_step_noalloc.argtypes = [dp, ctypes.POINTER(CompkvSelectParams)] + [_vp] * 16
+        L.compkv_decode_step_noalloc_limit.argtypes = []
+        L.compkv_decode_step_noalloc_limit.restype = ctypes.c_size_t
         L.compkv_decode_step_path.argtypes = [dp, ctypes.POINTER(CompkvSelectParams)]
         L.compkv_host_cache_pointer.argtypes = [_vp, ctypes.POINTER(ctypes.c_void_p)]
         L.compkv_host_cache_pointer.restype = ctypes.c_int
@@ -118,6 +121,7 @@ def library():
         L.compkv_version.argtypes = []
         for name in ("compkv_build_stats", "compkv_append_stats", "compkv_score_select",
                      "compkv_sparse_decode", "compkv_dense_decode", "compkv_decode_step", "compkv_decode_step_path",
+                     "compkv_decode_step_noalloc",
                      "compkv_version"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -325,6 +329,32 @@ def compkv_decode_step(dims, params: CompkvSelectParams, q, k_cache, v_cache, k_
         _ptr(scores, f32, (*units, dims.xcap), "scores", nullable=True), _ptr(out, f32, qs, "out"),
         _ptr(lse, f32, qs[:2], "lse", nullable=True), ws, ws_bytes, _stream(stream))
     _check(st, "compkv_decode_step")
+
+
+def compkv_decode_step_noalloc(dims, params: CompkvSelectParams, q, k_cache, v_cache, k_new, v_new, seq_lens,
+                               kmean, dvar, vmean, sel, n_sel, blk_logit, scores, out, lse=None, stream=None):
+    """compkv_decode_step without a workspace: the library's fixed per-GPU scratch is used instead
+    (nothing is allocated; overlapping calls on one GPU race)."""
+    cache, summ, dv, qs = _shapes(dims)
+    bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+    units = (dims.batch, dims.n_kv_heads)
+    new = (*units, dims.head_dim)
+    if (k_new is None) != (v_new is None):
+        raise CompkvError("k_new and v_new must be given together")
+    st = library().compkv_decode_step_noalloc(
+        ctypes.byref(dims), ctypes.byref(params), _ptr(q, bf, qs, "q"), _kv_ptr(k_cache, cache, "k_cache"),
+        _kv_ptr(v_cache, cache, "v_cache"), _ptr(k_new, bf, new, "k_new", nullable=True),
+        _ptr(v_new, bf, new, "v_new", nullable=True), _ptr(seq_lens, i32, (dims.batch,), "seq_lens"),
+        _mem_ptr(kmean, f32, summ, "kmean"), _mem_ptr(dvar, f32, dv, "dvar"), _mem_ptr(vmean, f32, summ, "vmean"),
+        _ptr(sel, i32, (*units, params.budget_blocks), "sel"), _ptr(n_sel, i32, units, "n_sel"),
+        _ptr(blk_logit, f32, (*units, dims.group, dims.xcap), "blk_logit"),
+        _ptr(scores, f32, (*units, dims.xcap), "scores", nullable=True), _ptr(out, f32, qs, "out"),
+        _ptr(lse, f32, qs[:2], "lse", nullable=True), _stream(stream))
+    _check(st, "compkv_decode_step_noalloc")
+
+
+def compkv_decode_step_noalloc_limit() -> int:
+    return int(library().compkv_decode_step_noalloc_limit())
 
 
 def default_scale(head_dim: int) -> float:

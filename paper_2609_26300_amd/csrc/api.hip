@@ -4,8 +4,16 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <mutex>
 
 using compkv::Geom;
+
+// Scratch of the allocation-free decode step: a fixed device array in place of the caller's
+// workspace. Every GPU the library runs on holds its own copy until the process ends. In host code
+// `scratch` names a host-side stand-in, never a device address: its device address is looked up per
+// device (hipGetSymbolAddress with that device current) and only that address reaches the kernels.
+static constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -252,6 +260,26 @@ compkv::ScoreArgs score_args(const Geom& g, const compkv_select_params* params, 
     return a;
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mutex;
+void* scratch_ptr[kMaxDevices];
+
+// The current device's scratch address (nullptr: no device, too many devices, or the lookup failed).
+void* device_scratch() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(scratch_mutex);
+    if (!scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        scratch_ptr[dev] = ptr;
+    }
+    return scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -266,6 +294,9 @@ const char* compkv_status_string(int status) {
         case COMPKV_EBUDGET: return "COMPKV_EBUDGET: budget smaller than the mandatory set";
         case COMPKV_EWORKSPACE: return "COMPKV_EWORKSPACE: workspace null, misaligned or too small";
         case COMPKV_EHIP: return "COMPKV_EHIP: kernel launch failed";
+        case COMPKV_ESCRATCH:
+            return "COMPKV_ESCRATCH: the step needs more scratch than compkv_decode_step_noalloc holds "
+                   "(use compkv_decode_step with a workspace)";
         default: return "unknown compkv status";
     }
 }
@@ -535,6 +566,24 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     e = use_sx ? compkv::launch_select_exact(g, a, d, n_ex, s) : compkv::launch_decode_items(g, d, n_ex, s);
     if (e != hipSuccess) return COMPKV_EHIP;
     return launch_status(compkv::launch_decode_merge(g, d, nparts, s));
+}
+
+size_t compkv_decode_step_noalloc_limit(void) { return kScratchBytes; }
+
+int compkv_decode_step_noalloc(const compkv_dims* dims, const compkv_select_params* params, const void* q,
+                               void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                               const int32_t* seq_lens, float* kmean, float* dvar, float* vmean, int32_t* sel,
+                               int32_t* n_sel, float* blk_logit, float* scores, float* out, float* lse,
+                               void* stream) {
+    Geom g;
+    int st = check_dims(dims, &g);
+    if (st != COMPKV_OK) return st;
+    if (!params || params->budget_blocks < 1) return COMPKV_EINVAL;
+    if (ws_bytes(g, params->budget_blocks, COMPKV_WS_DECODE_STEP) > kScratchBytes) return COMPKV_ESCRATCH;
+    void* ws = device_scratch();
+    if (!ws) return COMPKV_EHIP;
+    return compkv_decode_step(dims, params, q, k_cache, v_cache, k_new, v_new, seq_lens, kmean, dvar, vmean, sel,
+                              n_sel, blk_logit, scores, out, lse, ws, kScratchBytes, stream);
 }
 
 }  // extern "C"

@@ -297,3 +297,16 @@ def test_host_cache_pointer_rejects_unmapped_memory():
         d = dims()
         K = torch.zeros((1, 2, 4096, 128), dtype=torch.bfloat16)
         P.compkv_dense_decode(d, 0.1, K, K, K, K, K, None, K)
+
+
+def test_noalloc_step_rejects_oversized_workspace():
+    """The allocation-free step refuses, before enqueuing anything, a step whose workspace would exceed
+    its fixed scratch (here 256 units of 65536 blocks: over 1 GiB of score terms)."""
+    L = P.library()
+    limit = P.compkv_decode_step_noalloc_limit()
+    assert limit == 32 << 20
+    d = dims(batch=16, n_q_heads=128, n_kv_heads=16, block_size=16, capacity_tokens=1 << 20, max_seq_len=1 << 20)
+    assert P.compkv_workspace_bytes(d, 64, P.COMPKV_WS_DECODE_STEP) > limit
+    p = P.CompkvSelectParams(64, 1, 2, 0.088)
+    assert L.compkv_decode_step_noalloc(ctypes.byref(d), ctypes.byref(p), *([FAKE] * 15), None) == -6
+    assert "scratch" in P.compkv_status_string(-6)
