@@ -142,8 +142,9 @@ size_t dense_ws(const Geom& g) {
 
 struct SxShape {  // the fused step's selection + exact launch (sx_shape below)
     int eb, n_exact;
+    int cb, n_comp;  // its compensation workgroups: blocks each, workgroups per unit
     bool fits;       // within the kernel's limits
-    bool one_round;  // and every item workgroup resident at once (one workgroup per CU)
+    bool one_round;  // and every workgroup resident at once (one per CU)
 };
 SxShape sx_shape(const Geom& g, int nchunks, int K);
 
@@ -151,13 +152,14 @@ size_t step_part_bytes(const Geom& g, int parts) {
     return align_up((size_t)g.units() * parts * g.G * (g.D + 2) * sizeof(float));
 }
 
-// fused step: the score region, then [units][nchunks + 1 + n_exact][G][D + 2] decode partials:
-// compensation of each chunk and of the last block, then each exact item's partial. The exact items
-// are those of the separate decode or of the fused selection/exact launch, whichever are more.
+// fused step: the score region, then [units][parts][G][D + 2] decode partials. Chunked path: the
+// compensation of each chunk and of the last block, then each exact item's (nchunks + 1 + n_exact);
+// fused selection/exact launch: each compensation workgroup's, then each exact item's (n_comp +
+// n_exact). Sized for the larger of the two.
 int step_partials(const Geom& g, int K) {
     const int nchunks = score_shape(g).nchunks;
     const SxShape sx = sx_shape(g, nchunks, K);
-    return nchunks + 1 + std::max(sparse_shape(g, K).n_exact, sx.fits ? sx.n_exact : 0);
+    return std::max(nchunks + 1 + sparse_shape(g, K).n_exact, sx.fits ? sx.n_comp + sx.n_exact : 0);
 }
 
 size_t step_ws(const Geom& g, int K) { return score_ws(g) + step_part_bytes(g, step_partials(g, K)); }
@@ -194,18 +196,24 @@ SxShape sx_shape(const Geom& g, int nchunks, int K) {
     int cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 0;
-    // the smallest items of at least 64 tokens (four tiles) whose workgroups fit one per CU, up to one
-    // tile per wave (fewer attending waves per workgroup finish sooner: at 32K, 96-token items gave
-    // 24.0 us against 24.2 with 128-token ones and 25.7 with 256-token ones)
-    const int full = 16 * compkv::select_exact_waves();
-    const int eb_full = std::max(1, full / g.B);
-    int eb = std::min(eb_full, std::max(1, 64 / g.B));
-    while (eb < eb_full && (long long)g.units() * ceil_div(keff, eb) > cus) ++eb;
+    // one workgroup per CU: a unit's share of the CUs goes half to compensation workgroups (of at least
+    // 64 and at most select_exact_max_cb() blocks each) and the rest to exact items, the smallest of
+    // at least 64 tokens that fit it (an item of more than 16 tiles takes several rounds of its waves)
+    const int per = std::max(1, cus / std::max(1, g.units()));
+    const int cbmax = compkv::select_exact_max_cb();
+    int n_comp = std::max(1, std::min(per / 2, ceil_div(xmax, 64)));
+    n_comp = std::max(n_comp, ceil_div(xmax, cbmax));
+    const int cb = ceil_div(xmax, n_comp);
+    const int slots = std::max(1, per - n_comp);
+    const int eb = std::max(std::max(1, 64 / g.B), ceil_div(keff, slots));
     const int n_exact = ceil_div(keff, eb);
     const size_t dyn = ((size_t)2 * (nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
     const bool fits = K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
-                      eb <= compkv::decode_max_eb() && n_exact <= compkv::decode_max_items();
-    return {eb, n_exact, fits, fits && (long long)g.units() * n_exact <= cus};
+                      eb <= compkv::decode_max_eb() && n_exact <= compkv::decode_max_items() && cb <= cbmax &&
+                      n_comp + n_exact <= compkv::decode_max_partials();
+    const bool one_round = fits && (long long)g.units() * (n_exact + n_comp) <= cus &&
+                           compkv::select_exact_slots(g, dyn) >= cus;
+    return {eb, n_exact, cb, n_comp, fits, one_round};
 }
 
 bool use_select_exact(int path, const SxShape& sx) {
@@ -530,14 +538,53 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     // (CHUNKED_EXACT, or AUTO when every item workgroup is resident at once) one fused launch
     const SxShape sx = sx_shape(g, sc.nchunks, K);
     const bool use_sx = use_select_exact(params->select_path, sx);
-    const int n_ex = use_sx ? sx.n_exact : sp.n_exact;
-    // Mean: the chunks' compensation partials, then the exact items' partials; Drop: exact items only
+    if (use_sx) {
+        // the chunks score from the mean keys and variances alone; the fused launch's compensation
+        // workgroups stream the mean values while its item workgroups select, then the merge
+        float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
+        const int n_comp = drop ? 0 : sx.n_comp;
+        const int nparts = n_comp + sx.n_exact;
+        if (score_ws(g) + step_part_bytes(g, nparts) > workspace_bytes) return COMPKV_EWORKSPACE;  // sizing invariant
+        a.comp_part = nullptr;
+        a.part_count = nparts;
+        a.chunks_only = 1;
+        hipError_t e = compkv::launch_score_select(g, a, s);
+        if (e != hipSuccess) return COMPKV_EHIP;
+        d.ws_part = dpart;
+        d.q = static_cast<const uint16_t*>(q);
+        d.K = static_cast<const uint16_t*>(k_cache);
+        d.V = static_cast<const uint16_t*>(v_cache);
+        d.vmean = vmean;
+        d.blk_logit = blk_logit;
+        d.seq_lens = seq_lens;
+        d.sel = sel;
+        d.n_sel = n_sel;
+        d.out = out;
+        d.lse = lse;
+        d.sel_stride = K;
+        d.n_exact = sx.n_exact;
+        d.eb = sx.eb;
+        d.n_comp = n_comp;
+        d.cb = sx.cb;
+        d.dense = 0;
+        d.scale = params->scale;
+        d.part_count = nparts;
+        d.part_base = n_comp;
+        d.neg_pseudo = drop ? 0 : 1;
+        d.sel_padded = 1;
+        e = compkv::launch_select_exact(g, a, d, sx.n_exact, s);
+        if (e != hipSuccess) return COMPKV_EHIP;
+        return launch_status(compkv::launch_decode_merge(g, d, nparts, s));
+    }
+    // separate selection and exact items. Mean: the chunks' compensation partials, then the exact
+    // items' partials; Drop: exact items only
+    const int n_ex = sp.n_exact;
     float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
     const int nparts = drop ? n_ex : sc.nchunks + 1 + n_ex;
     if (score_ws(g) + step_part_bytes(g, nparts) > workspace_bytes) return COMPKV_EWORKSPACE;  // sizing invariant
     a.comp_part = drop ? nullptr : dpart;
     a.part_count = nparts;
-    a.chunks_only = use_sx;
+    a.chunks_only = 0;
     hipError_t e = compkv::launch_score_select(g, a, s);
     if (e != hipSuccess) return COMPKV_EHIP;
 
@@ -554,7 +601,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.lse = lse;
     d.sel_stride = K;
     d.n_exact = n_ex;
-    d.eb = use_sx ? sx.eb : sp.eb;
+    d.eb = sp.eb;
     d.n_comp = 0;
     d.cb = 0;
     d.dense = 0;
@@ -563,7 +610,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     d.part_base = drop ? 0 : sc.nchunks + 1;
     d.neg_pseudo = drop ? 0 : 1;
     d.sel_padded = 1;
-    e = use_sx ? compkv::launch_select_exact(g, a, d, n_ex, s) : compkv::launch_decode_items(g, d, n_ex, s);
+    e = compkv::launch_decode_items(g, d, n_ex, s);
     if (e != hipSuccess) return COMPKV_EHIP;
     return launch_status(compkv::launch_decode_merge(g, d, nparts, s));
 }

@@ -116,10 +116,14 @@ int decode_max_row_bases();  // row bases an item holds (dense items of a paged 
 hipError_t launch_decode(const Geom& g, const DecodeArgs& a, hipStream_t s);
 hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hipStream_t s);
 // fused step: the selection (from the chunk partials) and the exact items in one launch, `items`
-// workgroups of select_exact_waves() waves per unit; hipErrorInvalidValue outside its limits
+// workgroups of select_exact_waves() waves per unit, plus d.n_comp compensation workgroups per unit of
+// d.cb blocks each (partials 0 .. n_comp - 1; the items' from d.part_base); hipErrorInvalidValue outside
+// its limits
 hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s);
 int select_exact_max_budget();
 int select_exact_waves();
+int select_exact_max_cb();  // blocks per compensation workgroup of the fused launch
+int select_exact_slots(const Geom& g, size_t dyn);  // its workgroups resident at once on the current device
 hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s);
 
 // Resident workgroups of `kern` (`threads` each, no dynamic LDS) on the current device, cached per

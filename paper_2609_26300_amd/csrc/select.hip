@@ -1117,30 +1117,150 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
 // one 16-token tile per wave and round) and write the item's partial. This saves the launch between
 // selection and exact attention and the round trip of the selected ids through memory; it pays off
 // while the items fit one resident round (one workgroup per CU).
+//
+// Compensation workgroups (the fused step with Mean compensation and the chunk launch scoring only):
+// the same launch also holds n_comp workgroups per unit, after the item workgroups in the grid, that
+// stream the mean values of every block while the item workgroups select. Workgroup c of unit u takes
+// blocks [c cb, (c + 1) cb): the pseudo-token of each (logit log|b| + zbar_b from the block logits the
+// chunk launch wrote, value vmean_b), reduced to one softmax partial per head (max, sum of weights,
+// weighted mean values). The exact items take their selected blocks' pseudo-tokens back out, so the
+// compensation needs no selection and the mean values stream while the HBM would otherwise idle.
 constexpr int kSxWaves = kFinThreads / 64;
 constexpr int kSelLdsMax = 1024;  // budget limit of the fused kernel (ids held in LDS)
+constexpr int kStepCbMax = 1024;  // blocks per compensation workgroup of the fused launch
 
 template <int D, int G>
 struct SelExactLds {
     union {
         FinalShared fin;
-        ExactLds<D, G, kSxWaves> ex;
+        ExactLds<D, G, kSxWaves> ex;  // (compensation workgroups: their wave sums in ex.acc)
     } u;
     int32_t sel[kSelLdsMax];
     int32_t rowbase[kMaxEb];  // cache row of token 0 of each of the item's blocks
     int32_t nsel;
+    float cw[G][kStepCbMax];  // compensation workgroups: pseudo-logits, then their weights
+    float cm[G], cl[G];
 };
 
+// One compensation workgroup of the fused launch (see above): blocks [c0, c1) of unit u with n tokens.
 template <int D, int G>
-__global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, ScoreArgs a, DecodeArgs d) {
+__device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, int n, int c0, int c1,
+                                  SelExactLds<D, G>& L, float* part) {
+    constexpr int NT = kFinThreads;
+    constexpr int LPB = D / 4;               // lanes per mean-value row (one float4 each)
+    constexpr int RPS = NT / LPB;            // rows per workgroup step
+    constexpr int ROWS = G <= 4 ? 16 : 8;    // rows in flight per thread
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nb = max(0, c1 - c0);
+    const int li = tid % LPB, slot = tid / LPB;
+    // this thread's first rows before anything else (branch-free: a slot past the range reloads the
+    // range's first row, weighted by zero)
+    const float4* vm = reinterpret_cast<const float4*>(d.vmean + ((size_t)u * geo.xcap + c0) * D) + li;
+    float4 v[ROWS];
+#pragma unroll
+    for (int k = 0; k < ROWS; ++k) {
+        const int lb = slot + k * RPS;
+        v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
+    }
+    // pseudo-logits log|b| + zbar, then per head (wave g) their max and the weights exp(. - max)
+    const float* lg = d.blk_logit + (size_t)u * G * geo.xcap;
+    for (int idx = tid; idx < G * nb; idx += NT) {
+        const int g = idx / nb, lb = idx - g * nb, b = c0 + lb;
+        L.cw[g][lb] = logf((float)min(geo.B, n - b * geo.B)) + lg[(size_t)g * geo.xcap + b];
+    }
+    __syncthreads();
+    if (wave < G) {
+        const int g = wave;
+        float mx = -INFINITY;
+        for (int lb = lane; lb < nb; lb += 64) mx = fmaxf(mx, L.cw[g][lb]);
+        mx = wave_max(mx);
+        float sum = 0.0f;
+        for (int lb = lane; lb < nb; lb += 64) {
+            const float wv = __expf(L.cw[g][lb] - mx);
+            L.cw[g][lb] = wv;
+            sum += wv;
+        }
+        sum = wave_sum(sum);
+        if (lane == 0) {
+            L.cm[g] = mx;
+            L.cl[g] = sum;
+        }
+    }
+    __syncthreads();
+    // weighted mean values; lane li of a row slot holds coordinates 4 li .. 4 li + 3
+    float acc[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
+    for (int lb0 = slot; lb0 < nb; lb0 += RPS * ROWS) {
+        if (lb0 != slot) {
+#pragma unroll
+            for (int k = 0; k < ROWS; ++k) {
+                const int lb = lb0 + k * RPS;
+                v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < ROWS; ++k) {
+            const int lb = lb0 + k * RPS;
+            if (lb < nb) {
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const float wv = L.cw[g][lb];
+                    acc[g][0] += wv * v[k].x;
+                    acc[g][1] += wv * v[k].y;
+                    acc[g][2] += wv * v[k].z;
+                    acc[g][3] += wv * v[k].w;
+                }
+            }
+        }
+    }
+    // the row slots of a wave (lanes li, li + LPB, ...), then the waves in order
+#pragma unroll
+    for (int off = LPB; off < 64; off <<= 1)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[g][e] = xor_add(acc[g][e], off);
+    if (lane < LPB) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+            *reinterpret_cast<float4*>(&L.u.ex.acc[wave][g][4 * li]) = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+    }
+    __syncthreads();
+    for (int idx = tid; idx < G * D; idx += NT) {
+        const int g = idx / D, i = idx - g * D;
+        float* p = part + (size_t)g * (D + 2);
+        if (i == 0) {
+            p[0] = L.cm[g];
+            p[1] = L.cl[g];
+        }
+        float tot = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kSxWaves; ++w) tot += L.u.ex.acc[w][g][i];
+        p[2 + i] = tot;
+    }
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int items) {
     __shared__ SelExactLds<D, G> L;
     extern __shared__ float dyn[];
     const int tid = threadIdx.x;
-    // the items of unit u all on XCD u % kXcds: the unit's selection inputs are fetched once into
-    // that XCD's L2
     const int units = geo.units();
     int u, item;
-    xcd_unit_work(blockIdx.x, units, (int)gridDim.x / units, u, item);
+    if ((int)blockIdx.x >= items * units) {  // a compensation workgroup (workgroup-uniform)
+        int c;
+        xcd_unit_work((int)blockIdx.x - items * units, units, d.n_comp, u, c);
+        const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
+        const int X = (n + geo.B - 1) / geo.B;
+        const int c0 = min(c * d.cb, X), c1 = min(c0 + d.cb, X);
+        step_compensation<D, G>(geo, d, u, n, c0, c1, L,
+                                d.ws_part + ((size_t)u * d.part_count + c) * G * (D + 2));
+        return;
+    }
+    // the items of unit u all on XCD u % kXcds: the unit's selection inputs are fetched once into
+    // that XCD's L2
+    xcd_unit_work(blockIdx.x, units, items, u, item);
     finalize_select<G>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
     __syncthreads();
     const int bseq = u / geo.hkv, h = u % geo.hkv;
@@ -1241,7 +1361,8 @@ hipError_t dispatch_g(const Geom& g, const ScoreArgs& a, hipStream_t s) {
 
 template <int D, int G>
 hipError_t launch_sx(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int items, hipStream_t s) {
-    select_exact_kernel<D, G><<<dim3(items * g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a, d);
+    const int grid = (items + d.n_comp) * g.units();
+    select_exact_kernel<D, G><<<dim3(grid), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a, d, items);
     return hipGetLastError();
 }
 
@@ -1261,12 +1382,36 @@ hipError_t sx_g(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int item
 int select_max_bpc() { return kBpcMax; }
 int select_exact_max_budget() { return kSelLdsMax; }
 int select_exact_waves() { return kSxWaves; }
+int select_exact_max_cb() { return kStepCbMax; }
+
+// Resident workgroups of the fused selection/exact launch on the current device with `dyn` bytes of
+// dynamic LDS each.
+template <int D, int G>
+int sx_slots(size_t dyn) {
+    int per_cu = 0, cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_exact_kernel<D, G>, kFinThreads, dyn) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    return per_cu * cus;
+}
+template <int D>
+int sx_slots_d(const Geom& g, size_t dyn) {
+    switch (g.G) {
+        case 1: return sx_slots<D, 1>(dyn);
+        case 2: return sx_slots<D, 2>(dyn);
+        case 4: return sx_slots<D, 4>(dyn);
+        default: return sx_slots<D, 8>(dyn);
+    }
+}
+int select_exact_slots(const Geom& g, size_t dyn) { return g.D == 128 ? sx_slots_d<128>(g, dyn) : sx_slots_d<64>(g, dyn); }
 
 hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s) {
     // the keys of the fast path's tie fallback stay in LDS: no workgroup writes global scratch
     a.keys_in_lds = 1;
     if (g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb > kMaxEb ||
-        finalize_dyn_lds(g, a) > kDynBudget)
+        finalize_dyn_lds(g, a) > kDynBudget || (d.n_comp > 0 && (d.cb < 1 || d.cb > kStepCbMax)) ||
+        (long long)d.n_comp * d.cb < (d.n_comp > 0 ? g.xmax() : 0) || d.part_base + items > d.part_count)
         return hipErrorInvalidValue;
     return g.D == 128 ? sx_g<128>(g, a, d, items, s) : sx_g<64>(g, a, d, items, s);
 }
