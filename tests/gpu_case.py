@@ -95,6 +95,7 @@ class Case:
         self.sl = torch.from_numpy(self.seq_lens).to("cuda")
         self.ws = P.alloc_workspace(self.dims, self.budget)
         self.G = w.group
+        self._orc = {}  # oracle results per (kind, unit, length)
         self.select_path = P.COMPKV_SELECT_AUTO
         self.score_kind = P.COMPKV_SCORE_COMPKV
         self.compensation = P.COMPKV_COMP_MEAN
@@ -173,13 +174,75 @@ class Case:
 
     def oracle_stats(self, b, h):
         q, K, V, n = self.unit_inputs(b, h)
-        return oracle.block_stats(K, V, n, self.w.block_size, self.r, self.layout)
+        key = ("stats", b, h, n)
+        if key not in self._orc:
+            self._orc[key] = oracle.block_stats(K, V, n, self.w.block_size, self.r, self.layout)
+        return self._orc[key]
 
     def oracle_scores(self, b, h, stats=None):
         q, K, V, n = self.unit_inputs(b, h)
-        km, dv, vm = stats if stats is not None else self.oracle_stats(b, h)
-        return oracle.block_scores(q, km, dv, n, self.w.block_size, self.r, self.scale, self.layout,
-                                   kind=self.score_kind)
+        if stats is not None:
+            km, dv, vm = stats
+            return oracle.block_scores(q, km, dv, n, self.w.block_size, self.r, self.scale, self.layout,
+                                       kind=self.score_kind)
+        key = ("scores", b, h, n, self.score_kind)
+        if key not in self._orc:
+            km, dv, vm = self.oracle_stats(b, h)
+            self._orc[key] = oracle.block_scores(q, km, dv, n, self.w.block_size, self.r, self.scale,
+                                                 self.layout, kind=self.score_kind)
+        return self._orc[key]
+
+    def prefetch_oracle(self, units=None, threads=8):
+        """Oracle summaries and scores of the given units (all by default), computed on a thread pool (the C
+        oracle releases the interpreter lock)."""
+        from concurrent.futures import ThreadPoolExecutor
+
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(lambda u: self.oracle_scores(*u), units or self.units()))
+
+    def check_stats(self, kmean, dvar, vmean, units=None):
+        """Summaries (device tensors) against the oracle's, unit by unit."""
+        km_g, dv_g, vm_g = (x.cpu().numpy() for x in (kmean, dvar, vmean))
+        for b, h in units or self.units():
+            okm, odv, ovm = self.oracle_stats(b, h)
+            X = okm.shape[0]
+            assert rel_err(km_g[b, h, :X], okm, axis=1) <= TOL, ("kmean", b, h)
+            assert rel_err(vm_g[b, h, :X], ovm, axis=1) <= TOL, ("vmean", b, h)
+            assert rel_err(dv_g[b, h, :X], odv) <= TOL, ("dvar", b, h)
+
+    def check_step(self, sel, n_sel, out, lse=None, units=None):
+        """Selection (tie band) and compensated output / lse against the oracle recomputed on the GPU's
+        selection, unit by unit."""
+        sel, nsel, out = (x.cpu().numpy() for x in (sel, n_sel, out))
+        lse = None if lse is None else lse.cpu().numpy()
+        G = self.G
+        compensate = self.compensation != P.COMPKV_COMP_DROP
+        for b, h in units or self.units():
+            q, K, V, n = self.unit_inputs(b, h)
+            km, dv, vm = self.oracle_stats(b, h)
+            sc = self.oracle_scores(b, h)
+            s = sel[b, h, :nsel[b, h]]
+            check_selection(s, sc["score"], self.budget, self.n_sink, self.n_recent)
+            assert np.all(sel[b, h, nsel[b, h]:] == -1)
+            o, l = oracle.sparse_decode(q, K, V, km, vm, n, self.w.block_size, self.scale, s, compensate)
+            assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL, ("out", b, h)
+            if lse is not None:
+                got = lse[b, h * G:(h + 1) * G]
+                fin = np.isfinite(l)
+                assert np.array_equal(fin, np.isfinite(got)), ("lse finiteness", b, h)
+                if fin.any():
+                    assert np.max(np.abs(got[fin] - l[fin])) <= TOL * max(1.0, float(np.max(np.abs(l[fin])))), \
+                        ("lse", b, h)
+
+    def check_dense(self, out, lse, units=None):
+        out, lse = out.cpu().numpy(), lse.cpu().numpy()
+        G = self.G
+        for b, h in units or self.units():
+            q, K, V, n = self.unit_inputs(b, h)
+            o, l = oracle.dense_decode(q, K, V, n, self.scale)
+            assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL, ("dense out", b, h)
+            assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, np.max(np.abs(l))), \
+                ("dense lse", b, h)
 
     def units(self):
         return [(b, h) for b in range(self.w.batch) for h in range(self.w.n_kv_heads)]
@@ -231,4 +294,24 @@ CASES = {
     "block1_9000": lambda: Case(TINY.with_(context=9000, block_size=1, budget_blocks=40, seed=25)),
     "budget300_x1000": lambda: Case(TINY.with_(context=16000, budget_blocks=300, seed=26)),
     "budget300_x2000": lambda: Case(TINY.with_(context=32000, budget_blocks=300, seed=27)),
+    # high logit spread: 8 of 32 query heads scaled by 16 and offset blocks 8 nats up along the unit's mean
+    # query, so that in most units the selected blocks hold most of the attention mass; and a 4K layer with
+    # 4 query heads scaled by 128, whose units' log weights span up to 98 nats (seeds chosen so the cut
+    # is at least 2.5e-4 relative away from the next candidate: the case tests the arithmetic at large
+    # spreads, not ties)
+    "high_spread_8k": lambda: Case(LLAMA.with_(context=8192, offset_frac=0.05, offset_logit=8.0, peaky_frac=0.25,
+                                               peaky_scale=16.0, seed=69)),
+    "span_98nats": lambda: Case(LLAMA.with_(context=4096, offset_frac=0.05, offset_logit=8.0, peaky_frac=0.125,
+                                            peaky_scale=128.0, budget_blocks=20, seed=55)),
+    # mandatory sets other than (1, 2): none, (2, 1) and (3, 3), on long contexts and on contexts of a few
+    # blocks where the sink and recent ranges overlap or cover every block
+    "sink0_recent0": lambda: Case(TINY.with_(context=2000, seed=50), n_sink=0, n_recent=0),
+    "sink2_recent1": lambda: Case(TINY.with_(context=3000, seed=51), n_sink=2, n_recent=1),
+    "sink3_recent3": lambda: Case(TINY.with_(context=4000, seed=52), n_sink=3, n_recent=3),
+    "sink3_recent3_short": lambda: Case(TINY.with_(batch=4, seed=53), seq_lens=[16, 48, 80, 100], budget=6,
+                                        n_sink=3, n_recent=3),
+    "sink2_recent1_short": lambda: Case(TINY.with_(batch=4, seed=54), seq_lens=[1, 20, 33, 64], budget=3,
+                                        n_sink=2, n_recent=1),
+    "sink0_recent0_short": lambda: Case(TINY.with_(batch=3, seed=56), seq_lens=[5, 40, 70], budget=2,
+                                        n_sink=0, n_recent=0),
 }

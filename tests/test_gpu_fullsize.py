@@ -4,17 +4,17 @@ The long-context 128K layer (batch 4; budgets 32, 64 and 128 blocks), the wide-G
 G = 8) and the streaming layer's first appending step (131072 + 1 tokens, so the last block holds one
 token), each run exactly as bench.py times them: summaries built over n tokens, then one
 compkv_decode_step on the automatic launch shape that appends row n - 1 (rewriting it with the same
-values, which also refreshes the active block's summary). The oracle is too slow for every unit at these
-sizes, so three units per workload (first, middle, last) are checked one by one: their summaries, the
-selection (bit-exact outside the tie band), the compensated output and lse.
+values, which also refreshes the active block's summary). Every unit is checked against the oracle: its
+summaries, the selection (bit-exact outside the tie band), the compensated output and lse. The streaming
+layer is also run through 40 appending steps from its 131072-token prefill (a block completes and the
+next one starts), and the last step is checked the same way.
 """
 import numpy as np
 import pytest
 import torch
 
-import oracle
 import paper_2609_26300_amd as P
-from gpu_case import TOL, Case, check_selection, rel_err
+from gpu_case import Case
 from workloads import WORKLOADS
 
 pytestmark = pytest.mark.gpu
@@ -44,9 +44,6 @@ def _case(name):
     return _cases[name]
 
 
-def _sample_units(c):
-    units = c.units()
-    return [units[0], units[len(units) // 2], units[-1]]
 
 
 @pytest.mark.parametrize("name,budget", [(n, k) for n, (_, _, ks) in FULL.items() for k in ks],
@@ -64,23 +61,10 @@ def test_fullsize_fused_step(name, budget):
     ws = P.alloc_workspace(d, c.budget)
     r = c.decode_step(k_new, v_new, ws=ws)
     torch.cuda.synchronize()
-    sel, nsel = r["sel"].cpu().numpy(), r["n_sel"].cpu().numpy()
-    out, lse = r["out"].cpu().numpy(), r["lse"].cpu().numpy()
-    G = c.G
-    for b, h in _sample_units(c):
-        q, K, V, nn = c.unit_inputs(b, h)
-        km, dv, vm = c.oracle_stats(b, h)
-        X = km.shape[0]
-        for got, ref, what in ((c.summ.kmean, km, "kmean"), (c.summ.dvar, dv, "dvar"), (c.summ.vmean, vm, "vmean")):
-            g = got[b, h, :X].cpu().numpy()
-            err = rel_err(g, ref, axis=None if what == "dvar" else 1)
-            assert err <= TOL, (name, b, h, what, err)
-        sc = c.oracle_scores(b, h, (km, dv, vm))
-        s = sel[b, h, :nsel[b, h]]
-        check_selection(s, sc["score"], c.budget, c.n_sink, c.n_recent)
-        o, l = oracle.sparse_decode(q, K, V, km, vm, nn, c.w.block_size, c.scale, s)
-        assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL, (name, b, h)
-        assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, float(np.max(np.abs(l)))), (name, b, h)
+    print(f"[full-size {name} K={c.budget}] oracle over all {len(c.units())} units", flush=True)
+    c.prefetch_oracle()
+    c.check_stats(c.summ.kmean, c.summ.dvar, c.summ.vmean)
+    c.check_step(r["sel"], r["n_sel"], r["out"], r["lse"])
 
 
 @pytest.mark.parametrize("name", ["long_128k", "wide_gqa_64k"])
@@ -123,3 +107,45 @@ def test_fullsize_graph_replays_match_eager(name):
         for k in ref:
             assert torch.equal(outs[k], ref[k]), f"{name} replay {rep}: {k} differs"
     print(f"[full-size {name}] {rep + 1} graph replays match the eager step", flush=True)
+
+
+def test_fullsize_streaming_forty_appends():
+    """The streaming layer (batch 2, 8 KV heads, K = 128) prefilled with 131072 tokens, then 40 fused steps
+    that each append the next token and score / select / decode with fresh queries (Appendix E.2's
+    decode phase). Block 4096 fills and block 4097 opens on the way. After the last step every summary
+    equals a prefill build over the final cache bit for bit, and every unit's summaries, selection and
+    output match the oracle over 131112 tokens."""
+    from workloads import gen_queries
+    from gpu_case import dev_bf16
+
+    _cases.clear()
+    torch.cuda.empty_cache()
+    w = WORKLOADS["streaming_128k"]
+    n0, T = w.context, 40
+    c = Case(w, seq_lens=[n0 + T] * w.batch, max_seq_len=w.capacity)
+    c.select_path = P.COMPKV_SELECT_AUTO
+    d = c.dims
+    c.K[:, :, n0:] = 0
+    c.V[:, :, n0:] = 0
+    summ = P.alloc_summaries(d)
+    P.compkv_build_stats(d, c.K, c.V, torch.full((w.batch,), n0, dtype=torch.int32, device="cuda"), summ.kmean,
+                         summ.dvar, summ.vmean)
+    Kn = dev_bf16(c.K_bits[:, :, n0:n0 + T])
+    Vn = dev_bf16(c.V_bits[:, :, n0:n0 + T])
+    ws = P.alloc_workspace(d, c.budget)
+    path = P.compkv_decode_step_path(d, c.params())
+    print(f"[full-size streaming] 40 appending steps, launch shape {PATH_NAMES.get(path, path)}", flush=True)
+    for t in range(T):
+        c.q = dev_bf16(np.stack([gen_queries(w, 0, b, t) for b in range(w.batch)]))
+        sl = torch.full((w.batch,), n0 + t + 1, dtype=torch.int32, device="cuda")
+        r = c.decode_step(Kn[:, :, t].contiguous(), Vn[:, :, t].contiguous(), sl=sl, summ=summ, ws=ws)
+    torch.cuda.synchronize()
+    c.q_bits = np.stack([gen_queries(w, 0, b, T - 1) for b in range(w.batch)])
+    ref = P.alloc_summaries(d)
+    P.compkv_build_stats(d, c.K, c.V, sl, ref.kmean, ref.dvar, ref.vmean)
+    for f in ("kmean", "dvar", "vmean"):
+        assert torch.equal(getattr(ref, f), getattr(summ, f)), f
+    assert np.array_equal(c.K.view(torch.int16).cpu().numpy().view(np.uint16)[:, :, :n0 + T], c.K_bits[:, :, :n0 + T])
+    c.prefetch_oracle()
+    c.check_stats(summ.kmean, summ.dvar, summ.vmean)
+    c.check_step(r["sel"], r["n_sel"], r["out"], r["lse"])

@@ -1,6 +1,7 @@
 """Offload tier: K/V caches in pinned host memory read and written by the kernels across the host link
 (needs an MI355X). Every call gives bit-identical results to a device-memory cache, and the fused step's
-append lands in the host cache."""
+append lands in the host cache. The host-memory results are also checked against the CPU oracle directly
+(summaries, selection under the tie band, compensated and dense outputs)."""
 import pytest
 import torch
 
@@ -41,6 +42,9 @@ def test_host_cache_bitwise(name, path):
     torch.cuda.synchronize()
     assert torch.equal(out, c.out) and torch.equal(lse, c.lse)
     assert torch.equal(dout, ref_dense[0]) and torch.equal(dlse, ref_dense[1])
+    c.check_stats(summ.kmean, summ.dvar, summ.vmean)
+    c.check_step(c.sel, c.n_sel, out, lse)
+    c.check_dense(dout, dlse)
     # the fused step with an append, from n - 1 cached tokens
     K2, V2, kn, vn, summ2 = _prefix_state(c)
     ref = c.decode_step(kn, vn, summ=summ2, K=K2, V=V2)
@@ -53,6 +57,8 @@ def test_host_cache_bitwise(name, path):
     assert torch.equal(K3h, K2.cpu()) and torch.equal(V3h, V2.cpu())
     for f in ("kmean", "dvar", "vmean"):
         assert torch.equal(getattr(summ3, f), getattr(summ2, f)), f
+    c.check_stats(summ3.kmean, summ3.dvar, summ3.vmean)
+    c.check_step(r["sel"], r["n_sel"], r["out"], r["lse"])
 
 
 @pytest.mark.parametrize("path", sorted(PATHS))
@@ -96,3 +102,5 @@ def test_host_summaries_bitwise(name, path):
         assert torch.equal(r[k], ref[k]), k
     for f in ("kmean", "dvar", "vmean"):
         assert torch.equal(getattr(hs3, f), getattr(summ2, f).cpu()), f
+    c.check_stats(hs3.kmean, hs3.dvar, hs3.vmean)
+    c.check_step(r["sel"], r["n_sel"], r["out"], r["lse"])

@@ -3,7 +3,9 @@
 Every case's cache is scattered over randomly permuted physical pages; every call then runs on the
 paged cache and must give bit-identical results to the contiguous cache: the summaries of the prefill
 build, the selection and outputs of score_select / sparse_decode / dense_decode, and the fused step on
-every launch shape with an append whose row lands in the right page.
+every launch shape with an append whose row lands in the right page. The paged results are also
+checked against the CPU oracle directly (summaries, the selection under the tie band, the compensated
+and dense outputs), so they do not rest on the contiguous path alone.
 """
 import numpy as np
 import pytest
@@ -90,6 +92,9 @@ def test_paged_separate_calls_bitwise(name):
         if k in ("blk", "scores"):
             a, b = a[..., :X], b[..., :X]
         assert torch.equal(a, b), k
+    c.check_stats(s1.kmean, s1.dvar, s1.vmean)
+    c.check_step(r1["sel"], r1["n_sel"], r1["out"], r1["lse"])
+    c.check_dense(r1["dout"], r1["dlse"])
 
 
 @pytest.mark.parametrize("path", sorted(PATHS))
@@ -122,3 +127,5 @@ def test_paged_decode_step_with_append_bitwise(name, path):
     for f in ("kmean", "dvar", "vmean"):
         assert torch.equal(getattr(summ, f)[:, :, :X], getattr(summ2, f)), f
     assert torch.equal(unpack(Kp), K2) and torch.equal(unpack(Vp), V2)  # the appended rows, in their pages
+    c.check_stats(summ.kmean, summ.dvar, summ.vmean)
+    c.check_step(r["sel"], r["n_sel"], r["out"], r["lse"])

@@ -66,17 +66,7 @@ def _selection_equal(c: Case, r):
 
 
 def _oracle_end_to_end(c: Case, r):
-    sel, nsel, out, lse = _gpu(r["sel"]), _gpu(r["n_sel"]), _gpu(r["out"]), _gpu(r["lse"])
-    G = c.G
-    for b, h in c.units():
-        q, K, V, n = c.unit_inputs(b, h)
-        st = c.oracle_stats(b, h)
-        sc = c.oracle_scores(b, h, st)
-        s = sel[b, h, :nsel[b, h]]
-        check_selection(s, sc["score"], c.budget, c.n_sink, c.n_recent)
-        o, l = oracle.sparse_decode(q, K, V, st[0], st[2], n, c.w.block_size, c.scale, s)
-        assert rel_err(out[b, h * G:(h + 1) * G], o, axis=1) <= TOL
-        assert np.max(np.abs(lse[b, h * G:(h + 1) * G] - l)) <= TOL * max(1.0, np.max(np.abs(l)))
+    c.check_step(r["sel"], r["n_sel"], r["out"], r["lse"])
 
 
 def test_step_selection_matches_separate_calls(step):

@@ -20,7 +20,8 @@ from workloads import offset_blocks
 pytestmark = pytest.mark.gpu
 
 KINDS = {"mass": P.COMPKV_SCORE_MASS, "first_order": P.COMPKV_SCORE_FIRST_ORDER}
-VARIANT_CASES = ["tiny_4k", "llama8b_32k", "partial_tail", "g8_b64", "short", "budget_ge_x", "interleaved_r8"]
+VARIANT_CASES = ["tiny_4k", "llama8b_32k", "partial_tail", "g8_b64", "short", "budget_ge_x", "interleaved_r8",
+                 "high_spread_8k", "span_98nats", "sink0_recent0", "sink2_recent1_short"]
 
 
 def _gpu(t):
