@@ -162,7 +162,11 @@ int step_partials(const Geom& g, int K) {
     return std::max(nchunks + 1 + sparse_shape(g, K).n_exact, sx.fits ? sx.n_comp + sx.n_exact : 0);
 }
 
-size_t step_ws(const Geom& g, int K) { return score_ws(g) + step_part_bytes(g, step_partials(g, K)); }
+// fused step: the arrival counters of the fused selection/exact launch's in-launch merge (one per unit)
+// follow the partials
+size_t step_ws(const Geom& g, int K) {
+    return score_ws(g) + step_part_bytes(g, step_partials(g, K)) + align_up((size_t)g.units() * sizeof(uint32_t));
+}
 
 size_t ws_bytes(const Geom& g, int K, int which) {
     size_t body = 0;
@@ -210,7 +214,8 @@ SxShape sx_shape(const Geom& g, int nchunks, int K) {
     const size_t dyn = ((size_t)2 * (nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
     const bool fits = K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
                       eb <= compkv::decode_max_eb() && n_exact <= compkv::decode_max_items() && cb <= cbmax &&
-                      n_comp + n_exact <= compkv::decode_max_partials();
+                      n_comp + n_exact <= compkv::decode_max_partials() &&
+                      (n_comp + n_exact) * g.G <= compkv::select_exact_merge_terms();
     const bool one_round = fits && (long long)g.units() * (n_exact + n_comp) <= cus &&
                            compkv::select_exact_slots(g, dyn) >= cus;
     return {eb, n_exact, cb, n_comp, fits, one_round};
@@ -540,11 +545,16 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     const bool use_sx = use_select_exact(params->select_path, sx);
     if (use_sx) {
         // the chunks score from the mean keys and variances alone; the fused launch's compensation
-        // workgroups stream the mean values while its item workgroups select, then the merge
+        // workgroups stream the mean values while its item workgroups select, and the last of each
+        // unit's workgroups merges the unit's partials
         float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
         const int n_comp = drop ? 0 : sx.n_comp;
         const int nparts = n_comp + sx.n_exact;
-        if (score_ws(g) + step_part_bytes(g, nparts) > workspace_bytes) return COMPKV_EWORKSPACE;  // sizing invariant
+        const size_t part_bytes = step_part_bytes(g, step_partials(g, K));
+        uint32_t* arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + score_ws(g) + part_bytes);
+        if (step_part_bytes(g, nparts) > part_bytes || step_ws(g, K) > workspace_bytes)
+            return COMPKV_EWORKSPACE;  // sizing invariant
+        a.arrive_zero = arrive;
         a.comp_part = nullptr;
         a.part_count = nparts;
         a.chunks_only = 1;
@@ -572,9 +582,8 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.part_base = n_comp;
         d.neg_pseudo = drop ? 0 : 1;
         d.sel_padded = 1;
-        e = compkv::launch_select_exact(g, a, d, sx.n_exact, s);
-        if (e != hipSuccess) return COMPKV_EHIP;
-        return launch_status(compkv::launch_decode_merge(g, d, nparts, s));
+        d.arrive = arrive;
+        return launch_status(compkv::launch_select_exact(g, a, d, sx.n_exact, s));
     }
     // separate selection and exact items. Mean: the chunks' compensation partials, then the exact
     // items' partials; Drop: exact items only

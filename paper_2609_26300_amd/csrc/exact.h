@@ -40,6 +40,15 @@ struct ExactLds {
     float zb[G][kMaxEb];  // fused step: the block logits of the item's selected blocks
 };
 
+// Stores and loads coherent across the device (relaxed atomics at agent scope: they bypass the
+// non-coherent cached copies), for partials that another workgroup of the same launch merges.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ short f32_to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
     return (short)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
@@ -215,8 +224,9 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
 
 // Combine the NW waves' exact states in LDS and write the item's partial: the per-head maximum M
 // over the waves and each wave's factor exp(m_w - M) first, then every coordinate as a plain sum of
-// the waves' scaled accumulators in wave order.
-template <int D, int G, int NW>
+// the waves' scaled accumulators in wave order. kCoherent: the partial is stored with device-coherent
+// stores (merged by another workgroup of the same launch).
+template <int D, int G, int NW, bool kCoherent = false>
 __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], ExactLds<D, G, NW>& sh, float* part) {
     constexpr int CPL = D / 16;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -258,11 +268,19 @@ __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], Exact
 #pragma unroll
         for (int w = 0; w < NW; ++w) aa += sh.f[w][g] * sh.acc[w][g][i];
         float* p = part + (size_t)g * (D + 2);
-        if (i == 0) {
-            p[0] = sh.M[g];
-            p[1] = sh.L[g];
+        if constexpr (kCoherent) {
+            if (i == 0) {
+                st_agent(p, sh.M[g]);
+                st_agent(p + 1, sh.L[g]);
+            }
+            st_agent(p + 2 + i, aa);
+        } else {
+            if (i == 0) {
+                p[0] = sh.M[g];
+                p[1] = sh.L[g];
+            }
+            p[2 + i] = aa;
         }
-        p[2 + i] = aa;
     }
 }
 

@@ -69,6 +69,7 @@ struct ScoreArgs {
     int score_kind;         // COMPKV_SCORE_*: CompKV score, mass only, or first-order mass estimate
     int chunks_only;        // chunked path: launch the chunk scoring without the selection
     int tail_first;         // set by the launcher: the last-block workgroups lead the grid (else trail)
+    uint32_t* arrive_zero;  // nullable: per-unit counters the last-block workgroups set to zero
 };
 
 struct DecodeArgs {
@@ -96,6 +97,9 @@ struct DecodeArgs {
     int neg_pseudo;  // exact items subtract the pseudo-terms of their selected blocks (fused step)
     int sel_padded;  // the id slots past n_sel hold -1 (written by this library's selection): exact
                      // items read their ids without waiting for n_sel
+    uint32_t* arrive;  // fused selection/exact launch: per-unit arrival counters (zeroed by the chunk
+                       // launch); the unit's last workgroup merges its partials (null: a merge launch
+                       // follows)
 };
 
 // ------------------------------------------------------------------ launchers (one per kernel family)
@@ -124,6 +128,7 @@ int select_exact_max_budget();
 int select_exact_waves();
 int select_exact_max_cb();  // blocks per compensation workgroup of the fused launch
 int select_exact_slots(const Geom& g, size_t dyn);  // its workgroups resident at once on the current device
+int select_exact_merge_terms();  // partials x heads limit of its in-launch merge
 hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s);
 
 // Resident workgroups of `kern` (`threads` each, no dynamic LDS) on the current device, cached per

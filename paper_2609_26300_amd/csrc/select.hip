@@ -165,6 +165,7 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     const int n = clamp_len(n_raw, geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* pp = a.ws_part + ((size_t)u * (nc + 1) + nc) * G * 2;
+    if (a.arrive_zero && tid == 0) a.arrive_zero[u] = 0u;  // for the launch that merges after this one
     // fused step with Mean compensation: this workgroup's compensation partial
     float* cp = (kStep && a.comp_part) ? a.comp_part + ((size_t)u * a.part_count + nc) * G * (D + 2) : nullptr;
     if (X == 0) {  // empty sequence: neutral partials
@@ -1140,7 +1141,80 @@ struct SelExactLds {
     int32_t nsel;
     float cw[G][kStepCbMax];  // compensation workgroups: pseudo-logits, then their weights
     float cm[G], cl[G];
+    int32_t last;             // this workgroup arrived last for its unit (it merges the partials)
 };
+
+// Partials per unit that the in-launch merge handles (their maxima and factors live in the selection's
+// LDS area).
+constexpr int kMergeMaxTerms = (int)(sizeof(FinalShared) / (2 * sizeof(float)));
+
+// After a workgroup of the fused launch has stored its partial (device-coherent stores): count the
+// arrival on the unit's counter; the unit's last workgroup merges every partial in index order (so the
+// result does not depend on which workgroup is last): per head the maximum M, the sum L of
+// exp(m_p - M) l_p and of exp(m_p - M) acc_p, then out = acc / L and lse = M + log L.
+template <int D, int G>
+__device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, SelExactLds<D, G>& L) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int np = d.part_count;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's partial stores are complete
+    __syncthreads();
+    if (tid == 0)
+        L.last = __hip_atomic_fetch_add(d.arrive + u, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                 (uint32_t)(np - 1);
+    __syncthreads();
+    if (!L.last) return;  // workgroup-uniform
+    constexpr int RB = 8;  // partial values requested per round
+    const float* pu = d.ws_part + (size_t)u * np * G * (D + 2);
+    float* pm = reinterpret_cast<float*>(&L.u.fin);  // [np][G] maxima, then factors
+    float* pl = pm + np * G;                         // [np][G] sums
+    const int g = tid / D, i = tid - g * D;
+    const bool mine = tid < G * D;
+    const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
+    float x[RB];
+#pragma unroll
+    for (int k = 0; k < RB; ++k) x[k] = (mine && k < np) ? ld_agent(pi + (size_t)k * G * (D + 2)) : 0.0f;
+    for (int t = tid; t < np * G; t += kFinThreads) {
+        const float* q = pu + (size_t)t * (D + 2);
+        pm[t] = ld_agent(q);
+        pl[t] = ld_agent(q + 1);
+    }
+    __syncthreads();
+    if (wave < G) {
+        float M = -INFINITY;
+        for (int p = lane; p < np; p += 64) M = fmaxf(M, pm[p * G + wave]);
+        M = wave_max(M);
+        float S = 0.0f;
+        for (int p = lane; p < np; p += 64) {
+            const float mp = pm[p * G + wave];
+            const float f = mp == -INFINITY ? 0.0f : __expf(mp - M);
+            S += f * pl[p * G + wave];
+            pm[p * G + wave] = f;
+        }
+        S = wave_sum(S);
+        if (lane == 0) {
+            L.cm[wave] = M;
+            L.cl[wave] = S;
+        }
+    }
+    __syncthreads();
+    if (mine) {
+        float A = 0.0f;
+        for (int p0 = 0; p0 < np; p0 += RB) {
+            if (p0 > 0) {
+#pragma unroll
+                for (int k = 0; k < RB; ++k) x[k] = p0 + k < np ? ld_agent(pi + (size_t)(p0 + k) * G * (D + 2)) : 0.0f;
+            }
+#pragma unroll
+            for (int k = 0; k < RB; ++k)
+                if (p0 + k < np) A += pm[(p0 + k) * G + g] * x[k];
+        }
+        const int bseq = u / geo.hkv, h = u - bseq * geo.hkv;
+        const size_t o = (size_t)bseq * geo.hq + (size_t)h * G + g;
+        const float S = L.cl[g];
+        d.out[o * D + i] = S > 0.0f ? A / S : 0.0f;
+        if (i == 0 && d.lse) d.lse[o] = S > 0.0f ? L.cm[g] + logf(S) : -INFINITY;
+    }
+}
 
 // One compensation workgroup of the fused launch (see above): blocks [c0, c1) of unit u with n tokens.
 template <int D, int G>
@@ -1231,13 +1305,13 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
         const int g = idx / D, i = idx - g * D;
         float* p = part + (size_t)g * (D + 2);
         if (i == 0) {
-            p[0] = L.cm[g];
-            p[1] = L.cl[g];
+            st_agent(p, L.cm[g]);
+            st_agent(p + 1, L.cl[g]);
         }
         float tot = 0.0f;
 #pragma unroll
         for (int w = 0; w < kSxWaves; ++w) tot += L.u.ex.acc[w][g][i];
-        p[2 + i] = tot;
+        st_agent(p + 2 + i, tot);
     }
 }
 
@@ -1256,6 +1330,7 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
         const int c0 = min(c * d.cb, X), c1 = min(c0 + d.cb, X);
         step_compensation<D, G>(geo, d, u, n, c0, c1, L,
                                 d.ws_part + ((size_t)u * d.part_count + c) * G * (D + 2));
+        if (d.arrive) arrive_and_merge<D, G>(geo, d, u, L);
         return;
     }
     // the items of unit u all on XCD u % kXcds: the unit's selection inputs are fetched once into
@@ -1305,7 +1380,8 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
                                      __syncthreads();
                                  });
     float* part = d.ws_part + ((size_t)u * d.part_count + d.part_base + item) * G * (D + 2);
-    finish_exact<D, G, kSxWaves>(m, l, acc, L.u.ex, part);
+    finish_exact<D, G, kSxWaves, true>(m, l, acc, L.u.ex, part);
+    if (d.arrive) arrive_and_merge<D, G>(geo, d, u, L);
 }
 
 size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
@@ -1383,6 +1459,7 @@ int select_max_bpc() { return kBpcMax; }
 int select_exact_max_budget() { return kSelLdsMax; }
 int select_exact_waves() { return kSxWaves; }
 int select_exact_max_cb() { return kStepCbMax; }
+int select_exact_merge_terms() { return kMergeMaxTerms; }
 
 // Resident workgroups of the fused selection/exact launch on the current device with `dyn` bytes of
 // dynamic LDS each.
@@ -1411,7 +1488,8 @@ hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, 
     a.keys_in_lds = 1;
     if (g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb > kMaxEb ||
         finalize_dyn_lds(g, a) > kDynBudget || (d.n_comp > 0 && (d.cb < 1 || d.cb > kStepCbMax)) ||
-        (long long)d.n_comp * d.cb < (d.n_comp > 0 ? g.xmax() : 0) || d.part_base + items > d.part_count)
+        (long long)d.n_comp * d.cb < (d.n_comp > 0 ? g.xmax() : 0) || d.part_base + items > d.part_count ||
+        (d.arrive && (d.part_count != d.n_comp + items || d.part_count * g.G > kMergeMaxTerms)))
         return hipErrorInvalidValue;
     return g.D == 128 ? sx_g<128>(g, a, d, items, s) : sx_g<64>(g, a, d, items, s);
 }

@@ -109,6 +109,50 @@ def test_fullsize_graph_replays_match_eager(name):
     print(f"[full-size {name}] {rep + 1} graph replays match the eager step", flush=True)
 
 
+@pytest.mark.parametrize("name", ["long_128k", "wide_gqa_64k"])
+def test_fullsize_repeated_steps_bit_identical(name):
+    """The fused launch's last workgroup of each unit merges the unit's partials in index order, whichever
+    workgroup arrives last: 200 eager steps and 200 graph replays of the same full-size step (no append)
+    all give the same output and lse bits."""
+    c = _case(name)
+    c.budget = c.w.budget_blocks
+    c.select_path = P.COMPKV_SELECT_AUTO
+    d = c.dims
+    ws = P.alloc_workspace(d, c.budget)
+    ref = c.decode_step(ws=ws)
+    torch.cuda.synchronize()
+    outs = {k: torch.empty_like(v) for k, v in ref.items()}
+    params = c.params()
+
+    def call():
+        P.compkv_decode_step(d, params, c.q, c.K, c.V, None, None, c.sl, c.summ.kmean, c.summ.dvar, c.summ.vmean,
+                             outs["sel"], outs["n_sel"], outs["blk_logit"], outs["scores"], outs["out"], outs["lse"],
+                             ws)
+
+    bad = 0
+    for rep in range(200):
+        call()
+        if rep % 20 == 19:
+            torch.cuda.synchronize()
+            bad += int(not (torch.equal(outs["out"], ref["out"]) and torch.equal(outs["lse"], ref["lse"])))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(20):
+            call()
+    for rep in range(10):
+        outs["out"].fill_(-3)
+        g.replay()
+        torch.cuda.synchronize()
+        bad += int(not (torch.equal(outs["out"], ref["out"]) and torch.equal(outs["lse"], ref["lse"])))
+    assert bad == 0, f"{bad} of 20 checks differ"
+
+
 def test_fullsize_streaming_forty_appends():
     """The streaming layer (batch 2, 8 KV heads, K = 128) prefilled with 131072 tokens, then 40 fused steps
     that each append the next token and score / select / decode with fresh queries (Appendix E.2's
