@@ -200,12 +200,13 @@ SxShape sx_shape(const Geom& g, int nchunks, int K) {
     int cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 0;
-    // one workgroup per CU: a unit's share of the CUs goes half to compensation workgroups (of at least
-    // 64 and at most select_exact_max_cb() blocks each) and the rest to exact items, the smallest of
-    // at least 64 tokens that fit it (an item of more than 16 tiles takes several rounds of its waves)
+    // one workgroup per CU: up to half of a unit's share of the CUs goes to compensation workgroups (of
+    // at least 128 and at most select_exact_max_cb() blocks each: few partials to merge) and the rest to
+    // exact items, the smallest of at least 64 tokens that fit it (an item of more than 16 tiles takes
+    // several rounds of its waves)
     const int per = std::max(1, cus / std::max(1, g.units()));
     const int cbmax = compkv::select_exact_max_cb();
-    int n_comp = std::max(1, std::min(per / 2, ceil_div(xmax, 64)));
+    int n_comp = std::max(1, std::min(per / 2, ceil_div(xmax, 128)));
     n_comp = std::max(n_comp, ceil_div(xmax, cbmax));
     const int cb = ceil_div(xmax, n_comp);
     const int slots = std::max(1, per - n_comp);

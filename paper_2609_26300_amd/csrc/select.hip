@@ -1163,7 +1163,7 @@ __device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, Se
                  (uint32_t)(np - 1);
     __syncthreads();
     if (!L.last) return;  // workgroup-uniform
-    constexpr int RB = 8;  // partial values requested per round
+    constexpr int RB = 16;  // partial values requested per round
     const float* pu = d.ws_part + (size_t)u * np * G * (D + 2);
     float* pm = reinterpret_cast<float*>(&L.u.fin);  // [np][G] maxima, then factors
     float* pl = pm + np * G;                         // [np][G] sums
