@@ -25,7 +25,7 @@ import time
 import numpy as np
 
 HBM_PEAK_GBPS = 8000.0
-PATH_NAMES = {1: "chunked", 2: "one_group", 3: "chunked_exact"}
+PATH_NAMES = {1: "chunked", 2: "one_group", 3: "chunked_exact", 4: "stream"}
 # extra budgets timed beside a workload's own (the long-context layer's budget sweep)
 BUDGET_SWEEPS = {"long_128k": (32, 64, 128)}
 
@@ -35,6 +35,8 @@ def step_kernels(path: int) -> str:
     return {1: "compkv_decode_step: chunk scoring (append, compensation stream), selection, exact items, merge",
             2: "compkv_decode_step: one-group scoring and selection (append), exact and compensation items, merge",
             3: "compkv_decode_step: chunk scoring (append, compensation stream), selection + exact items, merge",
+            4: "compkv_decode_step: one launch (append, chunk scoring, selection, compensation stream, exact "
+               "items, merge)",
             }[path]
 
 
@@ -48,7 +50,8 @@ def parse():
     ap.add_argument("--context", type=int, default=0,
                     help="override the workload's tokens per sequence (a context sweep of one layer shape)")
     ap.add_argument("--layers", type=int, default=0, help="resident layer copies (0: enough for > 1 GB)")
-    ap.add_argument("--select-path", choices=["auto", "chunked", "one_group", "chunked_exact"], default="auto",
+    ap.add_argument("--select-path", choices=["auto", "chunked", "one_group", "chunked_exact", "stream"],
+                    default="auto",
                     help="scoring / selection launch shape (auto: one workgroup per unit where it fits)")
     ap.add_argument("--score-kind", choices=["compkv", "mass", "first_order"], default="compkv",
                     help="block score: the CompKV score or an ablation variant (mass only, first-order mass)")
@@ -429,7 +432,8 @@ def main():
     out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
     lse = torch.empty((w.batch, w.n_q_heads), dtype=torch.float32, device=dev)
     path = {"auto": P.COMPKV_SELECT_AUTO, "chunked": P.COMPKV_SELECT_CHUNKED,
-            "one_group": P.COMPKV_SELECT_ONE_GROUP, "chunked_exact": P.COMPKV_SELECT_CHUNKED_EXACT}[args.select_path]
+            "one_group": P.COMPKV_SELECT_ONE_GROUP, "chunked_exact": P.COMPKV_SELECT_CHUNKED_EXACT,
+            "stream": P.COMPKV_SELECT_STREAM}[args.select_path]
     kind = {"compkv": P.COMPKV_SCORE_COMPKV, "mass": P.COMPKV_SCORE_MASS,
             "first_order": P.COMPKV_SCORE_FIRST_ORDER}[args.score_kind]
     drop = args.compensation == "drop"

@@ -28,10 +28,13 @@
  *      scores            fp32 [batch][n_kv_heads][Xcap]
  *      out               fp32 [batch][n_q_heads][d]; lse fp32 [batch][n_q_heads] (natural log)
  *  - bf16 values are passed as their 16-bit patterns. Inputs must be finite.
- *  - workspace: device scratch of at least compkv_workspace_bytes(...) bytes, 256-byte aligned, with
- *    no initial contents required. Each call that takes one enqueues two kernels (compkv_decode_step:
- *    four), each reading what the previous one wrote there. Calls that may run concurrently need
- *    distinct workspaces.
+ *  - workspace: device scratch of at least compkv_workspace_bytes(...) bytes, 256-byte aligned. Its
+ *    first 16 * batch * n_kv_heads bytes, rounded up to 256, are per-unit words of the STREAM step
+ *    (below): they must be zero before a workspace's first compkv_decode_step on that path (zero the
+ *    whole workspace once after allocating it); every such step leaves them zero, and no other call
+ *    writes them. The rest needs no initial contents. Each call that takes one enqueues two kernels
+ *    (compkv_decode_step: up to four), each reading what the previous one wrote there. Calls that may
+ *    run concurrently need distinct workspaces.
  *  - Return value: COMPKV_OK (0) or a negative status; compkv_status_string() names it. On error
  *    nothing has been enqueued, except for COMPKV_EHIP (a launch failed).
  *
@@ -127,6 +130,13 @@ typedef struct compkv_select_params {
  *              unit's selection and attends over its share of the blocks), when the budget is at most
  *              1024 blocks and a unit at most 8192 blocks; otherwise, and in compkv_score_select, as
  *              CHUNKED.
+ *   STREAM:    in compkv_decode_step, two launches: the scoring of every completed block (the
+ *              CHUNKED chunks, bit-identical scores) with the refreshed last block, then one launch in
+ *              which one selector per unit ranks the blocks while compensation workgroups stream the
+ *              mean values, and exact workgroups wait for their unit's ids (a bounded wait on a
+ *              per-unit word of the workspace; a wait that times out makes the unit's outputs NaN);
+ *              the unit's last workgroup merges. When the budget is at most 1024 blocks and a unit at
+ *              most 8192 blocks; otherwise, and in compkv_score_select, as CHUNKED.
  *   AUTO:      in compkv_score_select, ONE_GROUP when a unit holds at most 256 blocks (one workgroup
  *              then reads every summary in a single round of loads), else CHUNKED. In
  *              compkv_decode_step, CHUNKED_EXACT when all of its workgroups are resident at once (at
@@ -137,6 +147,7 @@ typedef struct compkv_select_params {
 #define COMPKV_SELECT_CHUNKED 1
 #define COMPKV_SELECT_ONE_GROUP 2
 #define COMPKV_SELECT_CHUNKED_EXACT 3
+#define COMPKV_SELECT_STREAM 4
 
 /* Which call a workspace is sized for (compkv_workspace_bytes). */
 #define COMPKV_WS_ALL 0

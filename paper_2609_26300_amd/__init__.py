@@ -18,6 +18,7 @@ from .binding import (  # noqa: F401
     COMPKV_SCORE_FIRST_ORDER,
     COMPKV_SCORE_MASS,
     COMPKV_SELECT_ONE_GROUP,
+    COMPKV_SELECT_STREAM,
     COMPKV_WS_ALL,
     COMPKV_WS_DECODE_STEP,
     COMPKV_WS_DENSE_DECODE,

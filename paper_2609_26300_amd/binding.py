@@ -24,6 +24,7 @@ COMPKV_SELECT_AUTO = 0
 COMPKV_SELECT_CHUNKED = 1
 COMPKV_SELECT_ONE_GROUP = 2
 COMPKV_SELECT_CHUNKED_EXACT = 3
+COMPKV_SELECT_STREAM = 4
 COMPKV_SCORE_COMPKV = 0
 COMPKV_SCORE_MASS = 1
 COMPKV_SCORE_FIRST_ORDER = 2

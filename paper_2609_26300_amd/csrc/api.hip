@@ -148,6 +148,13 @@ struct SxShape {  // the fused step's selection + exact launch (sx_shape below)
 };
 SxShape sx_shape(const Geom& g, int nchunks, int K);
 
+struct StreamShape {  // the two-launch step (stream_shape below)
+    int n_comp, cb;    // compensation workgroups per unit, blocks each (0 under Drop)
+    int n_exact, eb;   // exact workgroups per unit, selected blocks each
+    int parts;         // decode partials per unit
+    bool fits;         // within the kernel's limits
+};
+
 size_t step_part_bytes(const Geom& g, int parts) {
     return align_up((size_t)g.units() * parts * g.G * (g.D + 2) * sizeof(float));
 }
@@ -168,6 +175,14 @@ size_t step_ws(const Geom& g, int K) {
     return score_ws(g) + step_part_bytes(g, step_partials(g, K)) + align_up((size_t)g.units() * sizeof(uint32_t));
 }
 
+StreamShape stream_shape(const Geom& g, int K, bool mean);
+size_t stream_ws(const Geom& g, int K);
+
+// Every workspace starts with the per-unit words of the two-launch step (final
+// arrivals, phase bits, timeouts): zero before a workspace's first compkv_decode_step call, returned to
+// zero by every step (the timeout count aside), never written by the other calls.
+size_t state_bytes(const Geom& g) { return align_up((size_t)g.units() * 4 * sizeof(uint32_t)); }
+
 size_t ws_bytes(const Geom& g, int K, int which) {
     size_t body = 0;
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_DECODE_STEP)  // either selection path
@@ -175,13 +190,14 @@ size_t ws_bytes(const Geom& g, int K, int which) {
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SCORE_SELECT) body = std::max(body, score_ws(g));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_SPARSE_DECODE) body = std::max(body, sparse_ws(g, K));
     if (which == COMPKV_WS_ALL || which == COMPKV_WS_DENSE_DECODE) body = std::max(body, dense_ws(g));
-    return body;
+    if (which == COMPKV_WS_ALL || which == COMPKV_WS_DECODE_STEP) body = std::max(body, stream_ws(g, K));
+    return state_bytes(g) + body;
 }
 
 // select_path of the call: true for the one-workgroup-per-unit selection; *st receives the status
 bool one_group_path(const Geom& g, int path, int* st) {
     *st = COMPKV_OK;
-    if (path < COMPKV_SELECT_AUTO || path > COMPKV_SELECT_CHUNKED_EXACT) {
+    if (path < COMPKV_SELECT_AUTO || path > COMPKV_SELECT_STREAM) {
         *st = COMPKV_EINVAL;
         return false;
     }
@@ -222,6 +238,41 @@ SxShape sx_shape(const Geom& g, int nchunks, int K) {
     return {eb, n_exact, cb, n_comp, fits, one_round};
 }
 
+// Shape of the two-launch step: the chunked path's scoring chunks; one round of selectors and
+// compensation workgroups (one per compute unit, at least 32 and at most step_stream_max_cb() blocks
+// each) so that the mean values stream while the selections run; exact workgroups of one round of the
+// sixteen waves (256 tokens).
+StreamShape stream_shape(const Geom& g, int K, bool mean) {
+    const int xmax = g.xmax();
+    const int keff = std::max(1, std::min(K, xmax));
+    int cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 256;
+    const int units = g.units();
+    int n_comp = 0, cb = 0;
+    if (mean) {
+        n_comp = std::max(1, (cus - units) / units);
+        n_comp = std::min(n_comp, std::max(1, ceil_div(xmax, 32)));
+        n_comp = std::max(n_comp, ceil_div(xmax, compkv::step_stream_max_cb()));
+        cb = ceil_div(xmax, n_comp);
+    }
+    const int eb = std::max(1, std::min(keff, 256 / g.B));
+    const int n_exact = ceil_div(keff, eb);
+    const int parts = (mean ? 1 + n_comp : 0) + n_exact;
+    const ScoreShape sc = score_shape(g);
+    const bool fits = K <= compkv::step_stream_max_budget() && xmax <= 8192 && eb <= compkv::decode_max_eb() &&
+                      (long long)parts * g.G <= compkv::step_stream_merge_terms() &&
+                      compkv::step_stream_dyn_lds(g, sc.nchunks) <= 32768;
+    return {n_comp, cb, n_exact, eb, parts, fits};
+}
+
+// the two-launch step: the score region, then [units][parts][G][D + 2] decode partials (Mean's shape,
+// the larger)
+size_t stream_ws(const Geom& g, int K) {
+    const StreamShape sh = stream_shape(g, K, true);
+    return score_ws(g) + step_part_bytes(g, sh.parts);
+}
+
 bool use_select_exact(int path, const SxShape& sx) {
     return (path == COMPKV_SELECT_CHUNKED_EXACT && sx.fits) || (path == COMPKV_SELECT_AUTO && sx.one_round);
 }
@@ -233,6 +284,22 @@ bool step_one_group(const Geom& g, const compkv_select_params* params, int* st) 
     const bool one = one_group_path(g, params->select_path, st);
     if (!one || params->select_path != COMPKV_SELECT_AUTO) return one;
     return !sx_shape(g, score_shape(g).nchunks, params->budget_blocks).one_round;
+}
+
+// The launch shape of compkv_decode_step (a COMPKV_SELECT_* value other than AUTO); *st receives the
+// status. STREAM takes the two-launch step whenever it fits (AUTO does not: it measured slower);
+// otherwise as CHUNKED.
+int step_path(const Geom& g, const compkv_select_params* params, int* st) {
+    const bool one = step_one_group(g, params, st);
+    if (*st != COMPKV_OK) return 0;
+    const int path = params->select_path;
+    if (path == COMPKV_SELECT_STREAM &&
+        stream_shape(g, params->budget_blocks, params->compensation == COMPKV_COMP_MEAN).fits)
+        return COMPKV_SELECT_STREAM;
+    if (one) return COMPKV_SELECT_ONE_GROUP;
+    return use_select_exact(path, sx_shape(g, score_shape(g).nchunks, params->budget_blocks))
+               ? COMPKV_SELECT_CHUNKED_EXACT
+               : COMPKV_SELECT_CHUNKED;
 }
 
 int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
@@ -375,7 +442,8 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     const size_t need = ws_bytes(g, params->budget_blocks, COMPKV_WS_SCORE_SELECT);
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
-    compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, workspace);
+    void* body = static_cast<char*>(workspace) + state_bytes(g);
+    compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, body);
     a.one_group = one;
     return launch_status(compkv::launch_score_select(g, a, static_cast<hipStream_t>(stream)));
 }
@@ -397,7 +465,7 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     if (st != COMPKV_OK) return st;
     const SparseShape sh = sparse_shape(g, sel_stride);
     if (sh.cb > compkv::decode_max_cb() || sh.eb > compkv::decode_max_eb()) return COMPKV_EUNSUPPORTED;
-    char* base = static_cast<char*>(workspace);
+    char* base = static_cast<char*>(workspace) + state_bytes(g);
     compkv::DecodeArgs a{};
     a.ws_part = reinterpret_cast<float*>(base);
     a.q = static_cast<const uint16_t*>(q);
@@ -433,7 +501,7 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
     if (st != COMPKV_OK) return st;
     const DenseShape sh = dense_shape(g);
     if (g.bpp > 0 && sh.te / (g.bpp * g.B) + 2 > compkv::decode_max_row_bases()) return COMPKV_EUNSUPPORTED;
-    char* base = static_cast<char*>(workspace);
+    char* base = static_cast<char*>(workspace) + state_bytes(g);
     compkv::DecodeArgs a{};
     a.ws_part = reinterpret_cast<float*>(base);
     a.q = static_cast<const uint16_t*>(q);
@@ -466,12 +534,8 @@ int compkv_decode_step_path(const compkv_dims* dims, const compkv_select_params*
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!params) return COMPKV_EINVAL;
-    const bool one = step_one_group(g, params, &st);
-    if (st != COMPKV_OK) return st;
-    if (one) return COMPKV_SELECT_ONE_GROUP;
-    return use_select_exact(params->select_path, sx_shape(g, score_shape(g).nchunks, params->budget_blocks))
-               ? COMPKV_SELECT_CHUNKED_EXACT
-               : COMPKV_SELECT_CHUNKED;
+    const int path = step_path(g, params, &st);
+    return st != COMPKV_OK ? st : path;
 }
 
 int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* params, const void* q, void* k_cache,
@@ -491,20 +555,26 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     if (params->compensation != COMPKV_COMP_MEAN && params->compensation != COMPKV_COMP_DROP) return COMPKV_EINVAL;
     const bool drop = params->compensation == COMPKV_COMP_DROP;
     const int K = params->budget_blocks;
-    const bool one = step_one_group(g, params, &st);
+    const int path = step_path(g, params, &st);
     if (st != COMPKV_OK) return st;
+    const bool one = path == COMPKV_SELECT_ONE_GROUP;
     const SparseShape sp = sparse_shape(g, K);
     const ScoreShape sc = score_shape(g);
     const int parts = step_partials(g, K);
-    if (sp.eb > compkv::decode_max_eb() || sp.n_exact > compkv::decode_max_items()) return COMPKV_EUNSUPPORTED;
-    if (one ? sp.cb > compkv::decode_max_cb()
-            : (parts > compkv::decode_max_partials() || (sc.nchunks + 1) * g.G > compkv::select_max_chunk_heads()))
-        return COMPKV_EUNSUPPORTED;
+    if (path != COMPKV_SELECT_STREAM) {
+        if (sp.eb > compkv::decode_max_eb() || sp.n_exact > compkv::decode_max_items()) return COMPKV_EUNSUPPORTED;
+        if (one ? sp.cb > compkv::decode_max_cb()
+                : (parts > compkv::decode_max_partials() || (sc.nchunks + 1) * g.G > compkv::select_max_chunk_heads()))
+            return COMPKV_EUNSUPPORTED;
+    }
     st = check_ws(g, workspace, workspace_bytes, ws_bytes(g, K, COMPKV_WS_DECODE_STEP));
     if (st != COMPKV_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* state = static_cast<uint32_t*>(workspace);
+    void* wsb = static_cast<char*>(workspace) + state_bytes(g);
+    const size_t wsb_bytes = workspace_bytes - state_bytes(g);
 
-    compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, workspace);
+    compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, wsb);
     a.k_new = static_cast<const uint16_t*>(k_new);
     a.v_new = static_cast<const uint16_t*>(v_new);
     a.Kc = static_cast<uint16_t*>(k_cache);
@@ -514,12 +584,40 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     a.vmean = vmean;
     a.one_group = one;
     compkv::DecodeArgs d{};
+    d.q = static_cast<const uint16_t*>(q);
+    d.K = static_cast<const uint16_t*>(k_cache);
+    d.V = static_cast<const uint16_t*>(v_cache);
+    d.vmean = vmean;
+    d.blk_logit = blk_logit;
+    d.seq_lens = seq_lens;
+    d.sel = sel;
+    d.n_sel = n_sel;
+    d.out = out;
+    d.lse = lse;
+    d.sel_stride = K;
+    d.scale = params->scale;
+    d.sel_padded = 1;
+    if (path == COMPKV_SELECT_STREAM) {
+        // everything in one launch: scoring (with the append), selection, compensation stream, exact
+        // items and merge, ordered by the per-unit words at the start of the workspace
+        const StreamShape sh = stream_shape(g, K, !drop);
+        if (!sh.fits || score_ws(g) + step_part_bytes(g, sh.parts) > wsb_bytes) return COMPKV_EWORKSPACE;  // sizing invariant
+        d.ws_part = reinterpret_cast<float*>(static_cast<char*>(wsb) + score_ws(g));
+        d.n_exact = sh.n_exact;
+        d.eb = sh.eb;
+        d.n_comp = sh.n_comp;
+        d.cb = sh.cb;
+        d.part_count = sh.parts;
+        d.part_base = drop ? 0 : 1 + sh.n_comp;
+        d.neg_pseudo = drop ? 0 : 1;
+        return launch_status(compkv::launch_step_stream(g, a, d, state, s));
+    }
     if (one) {
         // one workgroup per unit refreshes, scores and selects; then the compensated sparse decode
         // (exact and compensation items, merge) with its partials at the start of the workspace
         hipError_t e = compkv::launch_score_select(g, a, s);
         if (e != hipSuccess) return COMPKV_EHIP;
-        d.ws_part = static_cast<float*>(workspace);
+        d.ws_part = static_cast<float*>(wsb);
         d.q = static_cast<const uint16_t*>(q);
         d.K = static_cast<const uint16_t*>(k_cache);
         d.V = static_cast<const uint16_t*>(v_cache);
@@ -548,12 +646,12 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         // the chunks score from the mean keys and variances alone; the fused launch's compensation
         // workgroups stream the mean values while its item workgroups select, and the last of each
         // unit's workgroups merges the unit's partials
-        float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
+        float* dpart = reinterpret_cast<float*>(static_cast<char*>(wsb) + score_ws(g));
         const int n_comp = drop ? 0 : sx.n_comp;
         const int nparts = n_comp + sx.n_exact;
         const size_t part_bytes = step_part_bytes(g, step_partials(g, K));
-        uint32_t* arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + score_ws(g) + part_bytes);
-        if (step_part_bytes(g, nparts) > part_bytes || step_ws(g, K) > workspace_bytes)
+        uint32_t* arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(wsb) + score_ws(g) + part_bytes);
+        if (step_part_bytes(g, nparts) > part_bytes || step_ws(g, K) > wsb_bytes)
             return COMPKV_EWORKSPACE;  // sizing invariant
         a.arrive_zero = arrive;
         a.comp_part = nullptr;
@@ -589,9 +687,9 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     // separate selection and exact items. Mean: the chunks' compensation partials, then the exact
     // items' partials; Drop: exact items only
     const int n_ex = sp.n_exact;
-    float* dpart = reinterpret_cast<float*>(static_cast<char*>(workspace) + score_ws(g));
+    float* dpart = reinterpret_cast<float*>(static_cast<char*>(wsb) + score_ws(g));
     const int nparts = drop ? n_ex : sc.nchunks + 1 + n_ex;
-    if (score_ws(g) + step_part_bytes(g, nparts) > workspace_bytes) return COMPKV_EWORKSPACE;  // sizing invariant
+    if (score_ws(g) + step_part_bytes(g, nparts) > wsb_bytes) return COMPKV_EWORKSPACE;  // sizing invariant
     a.comp_part = drop ? nullptr : dpart;
     a.part_count = nparts;
     a.chunks_only = 0;

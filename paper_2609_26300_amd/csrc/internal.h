@@ -131,6 +131,19 @@ int select_exact_slots(const Geom& g, size_t dyn);  // its workgroups resident a
 int select_exact_merge_terms();  // partials x heads limit of its in-launch merge
 hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s);
 
+// The decode step in two launches (step.hip): the scores of every completed block (the chunked path's
+// chunks of a.bpc blocks), then per unit one selector (the last block, the selection), d.n_comp
+// compensation workgroups of d.cb blocks and d.n_exact exact workgroups of d.eb selected blocks,
+// ordered through `state` ([units][4] words: unused, final arrivals, phase bits, timeouts; zero on
+// entry, returned to zero except the timeout count). The decode partials are [last block's
+// compensation][n_comp compensation][n_exact exact] (Mean) or the exact ones alone (Drop);
+// d.part_base is the first exact partial. hipErrorInvalidValue outside its limits.
+hipError_t launch_step_stream(const Geom& g, ScoreArgs a, const DecodeArgs& d, uint32_t* state, hipStream_t s);
+int step_stream_max_cb();  // blocks per compensation workgroup, upper bound
+int step_stream_max_budget();
+int step_stream_merge_terms();  // partials x heads limit of the in-launch merge
+size_t step_stream_dyn_lds(const Geom& g, int nchunks);
+
 // Resident workgroups of `kern` (`threads` each, no dynamic LDS) on the current device, cached per
 // (kernel, device). Not thread-safe on first use per kernel; a race only repeats the same query.
 template <typename Kern>

@@ -33,80 +33,10 @@
 // into ascending ids. Larger inputs, or ties that leave too many keys at or above the cut's bin, go
 // through a three-pass radix select on the score bits instead. Wave-level reductions and prefix sums
 // use DPP lane moves.
-#include "block_stats.h"
-#include "exact.h"
-
-#include <type_traits>
+#include "select_core.h"
 
 namespace compkv {
 namespace {
-
-constexpr int kBpcMax = 128;  // blocks per chunk, upper bound
-constexpr int kHistBins = 2048;
-constexpr size_t kDynBudget = 32768;  // dynamic LDS of the finalize launch
-constexpr int kUnitTerms = 8192;      // G * xmax bound of the one-workgroup-per-unit path (64 KB of LDS)
-
-// The query enters through frequency pairs (Appendix A.4): lane f of wave w holds pair f of heads
-// g = w, w + 4, ... (coordinates f, f + d/2 for rotate-half; 2f, 2f + 1 interleaved). The loads are
-// issued before the summaries' so that waiting for them never waits for the summaries.
-template <int D, int G>
-struct QueryPairs {
-    static constexpr int J = (G + 3) / 4;
-    uint16_t xa[J], xb[J];
-};
-
-__device__ __forceinline__ int pair_a(int f, int layout) { return layout == 0 ? f : 2 * f; }
-__device__ __forceinline__ int pair_b(int f, int layout, int D) { return layout == 0 ? f + D / 2 : 2 * f + 1; }
-
-template <int D, int G>
-__device__ __forceinline__ void load_query_pairs(const uint16_t* qh, int layout, QueryPairs<D, G>& qp) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int f = lane < D / 2 ? lane : 0;
-#pragma unroll
-    for (int j = 0; j < QueryPairs<D, G>::J; ++j) {
-        const int g = wave + 4 * j < G ? wave + 4 * j : 0;  // branch-free: unused when past G
-        qp.xa[j] = qh[g * D + pair_a(f, layout)];
-        qp.xb[j] = qh[g * D + pair_b(f, layout, D)];
-    }
-}
-
-// From the loaded pairs: the scaled query s q into q (nullable) and s^2 Q_{g,t} -- the squared scaled
-// coordinates summed over group t -- into Qv[g][t]. A group is a run of (d/2)/r consecutive pairs,
-// summed by butterflies; with r == d every coordinate is its own group.
-template <int D, int G>
-__device__ __forceinline__ void store_query(const QueryPairs<D, G>& qp, float s, int r, int layout, float (*q)[D],
-                                            float (*Qv)[D]) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const bool in = lane < D / 2;
-    const int ia = pair_a(in ? lane : 0, layout), ib = pair_b(in ? lane : 0, layout, D);
-#pragma unroll
-    for (int j = 0; j < QueryPairs<D, G>::J; ++j) {
-        const int g = wave + 4 * j;
-        if (g >= G) break;  // wave-uniform
-        const float xa = s * bf16_at(&qp.xa[j]), xb = s * bf16_at(&qp.xb[j]);
-        if (q && in) {
-            q[g][ia] = xa;
-            q[g][ib] = xb;
-        }
-        if (r == D) {
-            if (in) {
-                Qv[g][ia] = xa * xa;
-                Qv[g][ib] = xb * xb;
-            }
-            continue;
-        }
-        float e = in ? xa * xa + xb * xb : 0.0f;
-        const int w = (D / 2) / r;
-        for (int off = 1; off < w; off <<= 1) e = xor_add(e, off);
-        if (in && lane % w == 0) Qv[g][lane / w] = e;
-    }
-}
-
-// Score kinds (the ablations of Section 5.4): the log weight of a block is
-// log|b| + zbar + half * sig2 (half = 1/2, or 0 for the first-order mass estimate), and its score
-// term is p-hat * sig2, or p-hat alone for the mass-only score.
-__device__ __forceinline__ float kind_half(int kind) { return kind == 2 ? 0.0f : 0.5f; }
-__device__ __forceinline__ float kind_term(int kind, float sig2) { return kind == 1 ? 1.0f : sig2; }
 
 // Per-block LDS rows of a chunk of 32 PMAX blocks: at least one wave's width, since the per-head passes
 // give every lane of a wave a slot. Sizing them by the chunk (not the largest one) keeps the 64-block
@@ -276,49 +206,54 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const bool comp = kStep && a.comp_part != nullptr;  // fused step with Mean compensation (uniform)
     const float half = kind_half(a.score_kind);
 
-    // loads in the order of their use: query pairs, then per slot the mean key and first variance
-    // group (the mean values follow once the keys are consumed, which halves the registers held).
-    // Block ids past the allocated range load block 0 of the unit; values of blocks that turn out
-    // invalid are never used (every result below is selected by validity).
+    // The sequence length and the query pairs first, on their own: loads return in order per compute
+    // unit, so requesting the mean keys only once the query is in LDS keeps the query (and the first
+    // slots' keys) from queueing behind the mean keys of the other workgroups on the CU. Then per slot
+    // the mean key and first variance group (the mean values follow once the keys are consumed, which
+    // halves the registers held). Block ids past the allocated range load block 0 of the unit; values
+    // of blocks that turn out invalid are never used (every result below is selected by validity).
+    const int n_raw = a.seq_lens[bseq];
     const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     QueryPairs<D, G> qp;
     load_query_pairs<D, G>(qh, geo.layout, qp);
-    __asm__ volatile("" ::: "memory");  // keep the query loads ahead of the summary loads
-    float4 kv[PMAX][NF4];
-    float dv0[PMAX];
-#pragma unroll
-    for (int p = 0; p < PMAX; ++p) {
+    store_query<D, G>(qp, s, geo.r, geo.layout, sh.q, sh.Qv);
+    const int n = clamp_len(n_raw, geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
+    const int xs = X - 1;  // blocks [0, X - 1) are scored here (all full); the last one by the extra workgroup
+    const float logB = logf((float)geo.B);
+    __syncthreads();
+    // a rolling window of two slots: slot p + 2 is requested once slot p is computed
+    float4 kv[2][NF4];
+    float dv0[2];
+    auto issue = [&](int p, int w) {
         const int b = chunk0 + p * 32 + grp;
         const size_t blk = (size_t)u * geo.xcap + (b < xmax ? b : 0);
         const float4* kp = reinterpret_cast<const float4*>(a.kmean + blk * D);
 #pragma unroll
-        for (int m = 0; m < NF4; ++m) kv[p][m] = kp[li + 8 * m];
-        dv0[p] = a.dvar[blk * geo.r + min(li, geo.r - 1)];
-    }
+        for (int m = 0; m < NF4; ++m) kv[w][m] = kp[li + 8 * m];
+        dv0[w] = a.dvar[blk * geo.r + min(li, geo.r - 1)];
+    };
+    issue(0, 0);
+    if (PMAX > 1) issue(1, 1);
     float4 vrow[VROWS];
-    store_query<D, G>(qp, s, geo.r, geo.layout, sh.q, sh.Qv);
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
-    const int xs = X - 1;  // blocks [0, X - 1) are scored here; the last one by the extra workgroup
-    __syncthreads();
 
-    // projected variances first (the lead lane of each block keeps them in LDS), then the block-mean
-    // logits one pair of heads at a time: the query slice a lane needs is the same for all its slots,
-    // so it is read from LDS once per pair, and only one pair's sums are held (fewer registers, more
-    // resident workgroups)
+    // slot by slot, in the order the slots' loads return: the projected variances (the lead lane of
+    // each block keeps them in LDS), then the block-mean logits one pair of heads at a time, the pair's
+    // query slice read from LDS into registers
     float qv[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) qv[g] = li < geo.r ? sh.Qv[g][li] : 0.0f;
-    float lnb[PMAX];
+    constexpr int GB = G < 2 ? G : 2;
 #pragma unroll
     for (int p = 0; p < PMAX; ++p) {
+        const int w = p & 1;
         const int lb = p * 32 + grp;
         const int b = chunk0 + lb;
         const bool valid = b < xs;
-        lnb[p] = valid ? logf((float)min(geo.B, n - b * geo.B)) : 0.0f;
+        const float lnb = valid ? logB : 0.0f;
         float v[G];
 #pragma unroll
-        for (int g = 0; g < G; ++g) v[g] = qv[g] * dv0[p];
+        for (int g = 0; g < G; ++g) v[g] = qv[g] * dv0[w];
         if (geo.r > 8 && valid) {
             const size_t blk = (size_t)u * geo.xcap + b;
             for (int t = li + 8; t < geo.r; t += 8) {
@@ -332,34 +267,29 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             v[g] = sum8_lead(v[g]);
             if (li == 0) sh.v[g][lb] = v[g];
         }
-    }
-    constexpr int GB = G < 2 ? G : 2;
 #pragma unroll 1
-    for (int g0 = 0; g0 < G; g0 += GB) {
-        float4 qq[GB][NF4];
+        for (int g0 = 0; g0 < G; g0 += GB) {
+            float4 qq[GB][NF4];
 #pragma unroll
-        for (int gb = 0; gb < GB; ++gb)
+            for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
-            for (int m = 0; m < NF4; ++m) qq[gb][m] = *reinterpret_cast<const float4*>(&sh.q[g0 + gb][4 * (li + 8 * m)]);
-#pragma unroll
-        for (int p = 0; p < PMAX; ++p) {
-            const int lb = p * 32 + grp;
-            const bool valid = chunk0 + lb < xs;
+                for (int m = 0; m < NF4; ++m) qq[gb][m] = *reinterpret_cast<const float4*>(&sh.q[g0 + gb][4 * (li + 8 * m)]);
 #pragma unroll
             for (int gb = 0; gb < GB; ++gb) {
                 float z = 0.0f;
 #pragma unroll
                 for (int m = 0; m < NF4; ++m)
-                    z += qq[gb][m].x * kv[p][m].x + qq[gb][m].y * kv[p][m].y + qq[gb][m].z * kv[p][m].z +
-                         qq[gb][m].w * kv[p][m].w;
+                    z += qq[gb][m].x * kv[w][m].x + qq[gb][m].y * kv[w][m].y + qq[gb][m].z * kv[w][m].z +
+                         qq[gb][m].w * kv[w][m].w;
                 z = sum8_lead(z);
                 if (li == 0) {
                     const int g = g0 + gb;
                     sh.z[g][lb] = z;
-                    if constexpr (kStep) st.cw[g][lb] = valid ? lnb[p] + z : -INFINITY;  // pseudo-logit
+                    if constexpr (kStep) st.cw[g][lb] = valid ? lnb + z : -INFINITY;  // pseudo-logit
                 }
             }
         }
+        if (p + 2 < PMAX) issue(p + 2, w);
     }
     if (comp) {  // mean-value rows, requested once the mean keys are consumed
         const float4* vm = reinterpret_cast<const float4*>(a.vmean + (size_t)u * geo.xcap * D) + vli;
@@ -371,8 +301,8 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     }
     __syncthreads();
     // log weight a = log|b| + zbar + half * sig2 of valid block lb of the chunk
-    auto logw = [&](int g, int lb) {
-        return logf((float)min(geo.B, n - (chunk0 + lb) * geo.B)) + sh.z[g][lb] + half * sh.v[g][lb];
+    auto logw = [&](int g, int lb) {  // (every block of a chunk is full: |b| = B)
+        return logB + sh.z[g][lb] + half * sh.v[g][lb];
     };
     // the chunk's per-head max and sum of exp(a - max) (and, fused, of the pseudo-logits)
     const int nvalid = max(0, min(a.bpc, xs - chunk0));
@@ -477,437 +407,6 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             p[2 + i] = st.acc[0][g][i] + st.acc[1][g][i] + st.acc[2][g][i] + st.acc[3][g][i];
         }
     }
-}
-
-constexpr int kFinThreads = 1024;  // threads of the selection workgroup (one per unit)
-constexpr int kFinWaves = kFinThreads / 64;
-constexpr int kKeysPerThread = 8;  // fast path: up to 8192 keys in registers
-constexpr int kBitmapWords = kKeysPerThread * kFinThreads / 32;
-constexpr int kCandCap = 1024;     // candidates ranked by brute force on the fast path
-constexpr int kHistTail = 255;     // distance bins counted on the fast path (bin 255 = everything farther)
-
-struct FinalShared {
-    int hist[kHistBins];
-    uint32_t wmax[kFinWaves];
-    int cnt[kFinWaves], cnt2[kFinWaves];
-    int digit, above, beta, ncand;
-    unsigned long long cand[kCandCap];
-    uint32_t bitmap[kBitmapWords];
-};
-
-// bits [lo, hi) of the 32-bit word holding ids base .. base + 31
-__device__ __forceinline__ uint32_t range_bits(int lo, int hi, int base) {
-    const int l = max(lo - base, 0), r = min(hi - base, 32);
-    if (l >= r) return 0u;
-    const uint32_t upto = r == 32 ? 0xFFFFFFFFu : ((1u << r) - 1u);
-    return upto & ~((1u << l) - 1u);
-}
-
-// score terms of block b (G floats, contiguous)
-template <int G>
-__device__ __forceinline__ void load_terms(const float* wu, int b, float (&w)[G]) {
-    if constexpr (G % 4 == 0) {
-#pragma unroll
-        for (int g4 = 0; g4 < G; g4 += 4) {
-            const float4 t4 = *reinterpret_cast<const float4*>(wu + (size_t)b * G + g4);
-            w[g4] = t4.x;
-            w[g4 + 1] = t4.y;
-            w[g4 + 2] = t4.z;
-            w[g4 + 3] = t4.w;
-        }
-    } else {
-#pragma unroll
-        for (int g = 0; g < G; ++g) w[g] = wu[(size_t)b * G + g];
-    }
-}
-
-// Selection shared by the workgroups that rank one unit's blocks (kFinThreads threads, keys as in
-// select_finalize_kernel).
-struct SelectCtx {
-    int X, K, kk, sink, rec_lo, n_sink, n_recent;
-    bool take_all, ranked;
-    int32_t* sel;    // this unit's row of selected ids
-    int32_t* n_sel;  // this unit's count
-    uint32_t* keys;  // [X] score bits, for the radix path
-};
-
-__device__ inline SelectCtx make_select_ctx(int X, int K, int n_sink, int n_recent, int32_t* sel, int32_t* n_sel,
-                                            uint32_t* keys) {
-    SelectCtx c;
-    c.X = X;
-    c.K = K;
-    c.n_sink = n_sink;
-    c.n_recent = n_recent;
-    c.take_all = K >= X;
-    c.sink = min(n_sink, X);
-    c.rec_lo = max(X - n_recent, 0);
-    const int n_mand = c.sink + (X - c.rec_lo) - max(0, c.sink - c.rec_lo);
-    c.kk = c.take_all ? 0 : K - n_mand;  // >= 0: the host checks K >= n_sink + n_recent
-    c.ranked = !c.take_all && c.kk > 0;
-    c.sel = sel;
-    c.n_sel = n_sel;
-    c.keys = keys;
-    return c;
-}
-
-// before the first barrier that precedes select_fast
-__device__ inline void select_init(FinalShared& sh) {
-    const int tid = threadIdx.x;
-    if (tid < kBitmapWords) sh.bitmap[tid] = 0u;
-    if (tid <= kHistTail) sh.hist[tid] = 0;
-    if (tid == 0) {
-        sh.beta = kHistTail;
-        sh.ncand = 0;
-    }
-}
-
-// Fast path: the keys ck (each non-zero key held by exactly one thread; zero = no key) and this
-// thread's largest score bits mx. Returns false when too many keys tie around the cut: their bits are
-// then in c.keys and select_radix finishes.
-template <int KPT>
-__device__ bool select_fast(const SelectCtx& ctx, const unsigned long long (&ck)[KPT], uint32_t mx, FinalShared& sh) {
-    constexpr int FT = kFinThreads, NW = kFinWaves;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int X = ctx.X, K = ctx.K, kk = ctx.kk, sink = ctx.sink, rec_lo = ctx.rec_lo;
-    const bool take_all = ctx.take_all, ranked = ctx.ranked;
-    int32_t* sel = ctx.sel;
-    uint32_t* keys = ctx.keys;
-    int m = 0;  // candidates ranked exactly
-    if (ranked) {
-        mx = wave_max_u32(mx);
-        if (lane == 0) sh.wmax[wave] = mx;
-        __syncthreads();
-        uint32_t smax = 0u;
-#pragma unroll
-        for (int w2 = 0; w2 < NW; ++w2) smax = max(smax, sh.wmax[w2]);
-        // histogram of the keys' distance below the largest score, in bins of 2^19 float ulps (1/16
-        // of an octave); keys more than 255 bins below are not counted
-        uint32_t bin[KPT];
-#pragma unroll
-        for (int k = 0; k < KPT; ++k) {
-            const uint32_t bits = (uint32_t)(ck[k] >> 32);
-            bin[k] = ck[k] ? min((smax - bits) >> 19, (uint32_t)kHistTail) : 0xFFFFFFFFu;
-            if (bin[k] < (uint32_t)kHistTail) atomicAdd(&sh.hist[bin[k]], 1);
-        }
-        __syncthreads();
-        // wave 0: prefix over the counted bins (four per lane); the bin reaching kk holds the cut
-        if (wave == 0) {
-            int c[4], tot = 0;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int bi = 4 * lane + e;
-                c[e] = bi < kHistTail ? sh.hist[bi] : 0;
-                tot += c[e];
-            }
-            int run = wave_incl_scan(tot) - tot;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (run < kk && run + c[e] >= kk) sh.beta = 4 * lane + e;
-                run += c[e];
-            }
-        }
-        __syncthreads();
-        const uint32_t beta = (uint32_t)sh.beta;  // kHistTail: the cut lies below the counted range
-        // candidates: keys in the cut's bin or above; each wave reserves its slots with one atomic
-        int mine = 0;
-#pragma unroll
-        for (int k = 0; k < KPT; ++k) mine += bin[k] <= beta;
-        const int incl = wave_incl_scan(mine);
-        int base = 0;
-        if (lane == 63) base = atomicAdd(&sh.ncand, incl);
-        int off = __builtin_amdgcn_readlane(base, 63) + incl - mine;
-#pragma unroll
-        for (int k = 0; k < KPT; ++k) {
-            if (bin[k] <= beta) {
-                if (off < kCandCap) sh.cand[off] = ck[k];
-                ++off;
-            }
-        }
-        __syncthreads();
-        m = sh.ncand;
-        if (m <= kCandCap) {
-            // exact rank among the candidates (order-independent); the kk best are selected. With
-            // few candidates the four lanes of a quad share one.
-            const int share = m <= FT / 4 ? 4 : 1;
-            const int i = tid / share, part = tid % share;
-            if (i < m) {  // quad-uniform
-                const unsigned long long ci = sh.cand[i];
-                int r = 0;
-                int j = part;
-                for (; j + 7 * share < m; j += 8 * share) {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) r += sh.cand[j + e * share] > ci;
-                }
-                for (; j < m; j += share) r += sh.cand[j] > ci;
-                if (share == 4) {
-                    r += dpp_i<0xB1>(r, r);
-                    r += dpp_i<0x4E>(r, r);
-                }
-                if (part == 0 && r < kk) {
-                    const uint32_t b = 0xFFFFFFFFu - (uint32_t)(ci & 0xFFFFFFFFull);
-                    atomicOr(&sh.bitmap[b >> 5], 1u << (b & 31));
-                }
-            }
-        } else {
-            // too many ties around the threshold: keep the bits for the radix path below
-#pragma unroll
-            for (int k = 0; k < KPT; ++k)
-                if (ck[k]) keys[0xFFFFFFFFu - (uint32_t)(ck[k] & 0xFFFFFFFFull)] = (uint32_t)(ck[k] >> 32);
-        }
-        __syncthreads();
-    }
-    if (m <= kCandCap) {  // block-uniform
-        // thread t < 256 owns ids 32t .. 32t+31: selected, mandatory (or every block when K >= X)
-        uint32_t word = 0u;
-        if (tid < kBitmapWords) {
-            word = take_all ? range_bits(0, X, 32 * tid)
-                            : (sh.bitmap[tid] | range_bits(0, sink, 32 * tid) | range_bits(rec_lo, X, 32 * tid));
-        }
-        const int c = __popc(word);
-        const int incl = wave_incl_scan(c);
-        if (lane == 63) sh.cnt[wave] = incl;
-        __syncthreads();
-        int pos = incl - c, total = 0;
-#pragma unroll
-        for (int w2 = 0; w2 < kBitmapWords / 64; ++w2) {
-            pos += w2 < wave ? sh.cnt[w2] : 0;
-            total += sh.cnt[w2];
-        }
-        while (word) {
-            const int bit = __ffs(word) - 1;
-            word &= word - 1;
-            if (pos < K) sel[pos] = 32 * tid + bit;
-            ++pos;
-        }
-        for (int k = total + tid; k < K; k += FT) sel[k] = -1;
-        if (tid == 0) *ctx.n_sel = min(total, K);
-        return true;
-    }
-    return false;
-}
-
-// General path: radix select on the key bits of blocks [0, X), then ascending compaction.
-__device__ void select_radix(const SelectCtx& c, FinalShared& sh) {
-    constexpr int FT = kFinThreads, NW = kFinWaves;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int X = c.X, K = c.K, kk = c.kk;
-    const bool take_all = c.take_all, ranked = c.ranked;
-    int32_t* sel = c.sel;
-    const uint32_t* keys = c.keys;
-    struct {
-        int n_sink, n_recent;
-    } a{c.n_sink, c.n_recent};
-    __syncthreads();
-
-    // ---- threshold of the Top-(K-|F|) among non-mandatory blocks (radix select on the score bits)
-    uint32_t thr = 0xFFFFFFFFu;  // keys above thr are taken; keys equal to thr up to need_eq
-    int need_eq = 0;
-    if (ranked) {
-        uint32_t prefix = 0, pmask = 0;
-        int remaining = kk;
-#pragma unroll
-        for (int pass = 0; pass < 3; ++pass) {
-            const int shft = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
-            const uint32_t dmask = pass == 2 ? 0x3FFu : 0x7FFu;
-            for (int i = tid; i < kHistBins; i += FT) sh.hist[i] = 0;
-            __syncthreads();
-            for (int b = tid; b < X; b += FT) {
-                if (mandatory(b, X, a.n_sink, a.n_recent)) continue;
-                const uint32_t key = keys[b];
-                if ((key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shft) & dmask], 1);
-            }
-            __syncthreads();
-            // suffix counts: thread t < 256 owns bins [8t, 8t + 8)
-            int local = 0;
-            if (tid < kHistBins / 8) {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) local += sh.hist[tid * 8 + e];
-            }
-            const int pre = wave_incl_scan(local);
-            const int wtot = __builtin_amdgcn_readlane(pre, 63);
-            const int incl = wtot - pre + local;  // over this lane and the higher ones (higher bins)
-            if (lane == 0) sh.cnt[wave] = wtot;
-            __syncthreads();
-            if (tid < kHistBins / 8) {
-                int cum = incl - local;
-                for (int w2 = wave + 1; w2 < kHistBins / 8 / 64; ++w2) cum += sh.cnt[w2];
-                for (int e = 7; e >= 0; --e) {
-                    const int c = sh.hist[tid * 8 + e];
-                    if (cum < remaining && cum + c >= remaining) {
-                        sh.digit = tid * 8 + e;
-                        sh.above = cum;
-                    }
-                    cum += c;
-                }
-            }
-            __syncthreads();
-            remaining -= sh.above;
-            prefix |= (uint32_t)sh.digit << shft;
-            pmask |= dmask << shft;
-            __syncthreads();
-        }
-        thr = prefix;
-        need_eq = remaining;
-    }
-
-    // ---- mark and compact in ascending id order; wave w scans its own id segment
-    const int seg = ((X + NW - 1) / NW + 63) / 64 * 64;
-    const int s0 = min(X, wave * seg), s1 = min(X, s0 + seg);
-    int cnt_eq = 0;
-    for (int base = s0; base < s1; base += 64) {
-        const int b = base + lane;
-        const bool eq = ranked && b < s1 && !mandatory(b, X, a.n_sink, a.n_recent) && keys[b] == thr;
-        cnt_eq += __popcll(__ballot(eq));
-    }
-    if (lane == 0) sh.cnt[wave] = cnt_eq;
-    __syncthreads();
-    int eq_run = 0;
-    for (int w2 = 0; w2 < wave; ++w2) eq_run += sh.cnt[w2];
-    const int eq_before = eq_run;
-    int cnt_take = 0;
-    for (int base = s0; base < s1; base += 64) {
-        const int b = base + lane;
-        const bool in = b < s1;
-        const bool mand = in && mandatory(b, X, a.n_sink, a.n_recent);
-        const uint32_t key = in ? keys[b] : 0u;
-        const bool cand = in && !mand && ranked;
-        const bool eq = cand && key == thr;
-        const unsigned long long em = __ballot(eq);
-        const bool take = in && (take_all || mand || (cand && (key > thr || (eq && eq_run + lanes_below(em) < need_eq))));
-        eq_run += __popcll(em);
-        cnt_take += __popcll(__ballot(take));
-    }
-    if (lane == 0) sh.cnt2[wave] = cnt_take;
-    __syncthreads();
-    int pos = 0;
-    for (int w2 = 0; w2 < wave; ++w2) pos += sh.cnt2[w2];
-    int total = 0;
-    for (int w2 = 0; w2 < NW; ++w2) total += sh.cnt2[w2];
-    eq_run = eq_before;
-    for (int base = s0; base < s1; base += 64) {
-        const int b = base + lane;
-        const bool in = b < s1;
-        const bool mand = in && mandatory(b, X, a.n_sink, a.n_recent);
-        const uint32_t key = in ? keys[b] : 0u;
-        const bool cand = in && !mand && ranked;
-        const bool eq = cand && key == thr;
-        const unsigned long long em = __ballot(eq);
-        const bool take = in && (take_all || mand || (cand && (key > thr || (eq && eq_run + lanes_below(em) < need_eq))));
-        eq_run += __popcll(em);
-        const unsigned long long tm = __ballot(take);
-        const int p = pos + lanes_below(tm);
-        if (take && p < K) sel[p] = b;
-        pos += __popcll(tm);
-    }
-    for (int k = total + tid; k < K; k += FT) sel[k] = -1;
-    if (tid == 0) *c.n_sel = min(total, K);
-}
-
-// The selection of unit u from the chunk partials (kFinThreads threads): per-head log normalizers,
-// scores (written to a.scores when write_scores) and the stable Top-K into sel_out / nsel_out (global
-// or LDS). dyn: [np][G] partial maxima, then factors; [np][G] sums; [xmax] key bits (keys_in_lds).
-template <int G>
-__device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, FinalShared& sh, float* dyn,
-                                int32_t* sel_out, int32_t* nsel_out, bool write_scores) {
-    constexpr int FT = kFinThreads, KPT = kKeysPerThread;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bseq = u / geo.hkv;
-    const int xmax = geo.xmax();
-    const int nc = a.nchunks, np = nc + 1;  // partial nc: the last block's
-    const float* wu = a.ws_w + (size_t)u * xmax * G;
-    const bool fast = xmax <= KPT * FT;
-
-    // ---- loads in the order of their use: the length, the partials, this thread's score terms
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
-    float* fac = dyn;
-    float* sums = dyn + np * G;
-    const float2* pu = reinterpret_cast<const float2*>(a.ws_part + (size_t)u * np * G * 2);
-    const bool one_pass = np * G <= FT;  // usual case: one partial per thread
-    float2 pv = make_float2(0.0f, 0.0f);
-    if (one_pass && tid < np * G) pv = pu[tid];
-    __asm__ volatile("" ::: "memory");
-    float w[KPT][G];
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {  // branch-free: ids past xmax load block 0, unused
-        const int b = tid + k * FT;
-        load_terms<G>(wu, b < xmax ? b : 0, w[k]);
-    }
-    if (one_pass && tid < np * G) {
-        fac[tid] = pv.x;
-        sums[tid] = pv.y;
-    }
-    if (!one_pass) {
-        for (int idx = tid; idx < np * G; idx += FT) {
-            const float2 t = pu[idx];
-            fac[idx] = t.x;
-            sums[idx] = t.y;
-        }
-    }
-    select_init(sh);
-    __syncthreads();
-    // ---- wave g: head g's log normalizer over every block, then each partial's factor exp(m_c - lse)
-    if (wave < G) {
-        const int g = wave;
-        float m = -INFINITY;
-        for (int c = lane; c < np; c += 64) m = fmaxf(m, fac[c * G + g]);
-        m = wave_max(m);
-        float l = 0.0f;
-        for (int c = lane; c < np; c += 64) {
-            const float pm = fac[c * G + g];
-            if (pm != -INFINITY) l += sums[c * G + g] * expf(pm - m);
-        }
-        l = wave_sum(l);  // (every lane's reads above are complete)
-        const float lse = m + logf(l);
-        for (int c = lane; c < np; c += 64) {
-            const float pm = fac[c * G + g];
-            fac[c * G + g] = pm == -INFINITY ? 0.0f : expf(pm - lse);
-        }
-    }
-    __syncthreads();
-
-    const SelectCtx sc = make_select_ctx(X, a.K, a.n_sink, a.n_recent, sel_out, nsel_out,
-                                         a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * np * G)
-                                                       : a.ws_key + (size_t)u * xmax);
-    auto score_of = [&](int b, const float (&wt)[G]) {
-        const float* f = fac + (b == X - 1 ? nc : b / a.bpc) * G;
-        float S = 0.0f;
-#pragma unroll
-        for (int g = 0; g < G; ++g) S += f[g] * wt[g];
-        return S;
-    };
-
-    // ---- fast path. Block b's key is (bits of S_b) << 32 | ~b: unique, and ordered exactly like
-    // (S_b descending, b ascending). Thread t keeps the keys of blocks t + 1024k in registers.
-    if (fast) {
-        unsigned long long ck[KPT];
-        uint32_t mx = 0u;
-#pragma unroll
-        for (int k = 0; k < KPT; ++k) {
-            const int b = tid + k * FT;
-            ck[k] = 0ull;
-            if (b < X) {
-                const float S = score_of(b, w[k]);
-                if (write_scores && a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
-                if (!mandatory(b, X, a.n_sink, a.n_recent)) {
-                    ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
-                    mx = max(mx, __float_as_uint(S));
-                }
-            }
-        }
-        if (select_fast<KPT>(sc, ck, mx, sh)) return;
-    } else {
-        // ---- general path (more than 8192 blocks): scores and their bits into the key array
-        for (int b = tid; b < X; b += FT) {
-            float wt[G];
-            load_terms<G>(wu, b, wt);
-            const float S = score_of(b, wt);
-            if (write_scores && a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
-            sc.keys[b] = __float_as_uint(S);
-        }
-    }
-    __syncthreads();
-    select_radix(sc, sh);
 }
 
 template <int G>
@@ -1126,195 +625,6 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
 // chunk launch wrote, value vmean_b), reduced to one softmax partial per head (max, sum of weights,
 // weighted mean values). The exact items take their selected blocks' pseudo-tokens back out, so the
 // compensation needs no selection and the mean values stream while the HBM would otherwise idle.
-constexpr int kSxWaves = kFinThreads / 64;
-constexpr int kSelLdsMax = 1024;  // budget limit of the fused kernel (ids held in LDS)
-constexpr int kStepCbMax = 1024;  // blocks per compensation workgroup of the fused launch
-
-template <int D, int G>
-struct SelExactLds {
-    union {
-        FinalShared fin;
-        ExactLds<D, G, kSxWaves> ex;  // (compensation workgroups: their wave sums in ex.acc)
-    } u;
-    int32_t sel[kSelLdsMax];
-    int32_t rowbase[kMaxEb];  // cache row of token 0 of each of the item's blocks
-    int32_t nsel;
-    float cw[G][kStepCbMax];  // compensation workgroups: pseudo-logits, then their weights
-    float cm[G], cl[G];
-    int32_t last;             // this workgroup arrived last for its unit (it merges the partials)
-};
-
-// Partials per unit that the in-launch merge handles (their maxima and factors live in the selection's
-// LDS area).
-constexpr int kMergeMaxTerms = (int)(sizeof(FinalShared) / (2 * sizeof(float)));
-
-// After a workgroup of the fused launch has stored its partial (device-coherent stores): count the
-// arrival on the unit's counter; the unit's last workgroup merges every partial in index order (so the
-// result does not depend on which workgroup is last): per head the maximum M, the sum L of
-// exp(m_p - M) l_p and of exp(m_p - M) acc_p, then out = acc / L and lse = M + log L.
-template <int D, int G>
-__device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, SelExactLds<D, G>& L) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int np = d.part_count;
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's partial stores are complete
-    __syncthreads();
-    if (tid == 0)
-        L.last = __hip_atomic_fetch_add(d.arrive + u, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                 (uint32_t)(np - 1);
-    __syncthreads();
-    if (!L.last) return;  // workgroup-uniform
-    constexpr int RB = 16;  // partial values requested per round
-    const float* pu = d.ws_part + (size_t)u * np * G * (D + 2);
-    float* pm = reinterpret_cast<float*>(&L.u.fin);  // [np][G] maxima, then factors
-    float* pl = pm + np * G;                         // [np][G] sums
-    const int g = tid / D, i = tid - g * D;
-    const bool mine = tid < G * D;
-    const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
-    float x[RB];
-#pragma unroll
-    for (int k = 0; k < RB; ++k) x[k] = (mine && k < np) ? ld_agent(pi + (size_t)k * G * (D + 2)) : 0.0f;
-    for (int t = tid; t < np * G; t += kFinThreads) {
-        const float* q = pu + (size_t)t * (D + 2);
-        pm[t] = ld_agent(q);
-        pl[t] = ld_agent(q + 1);
-    }
-    __syncthreads();
-    if (wave < G) {
-        float M = -INFINITY;
-        for (int p = lane; p < np; p += 64) M = fmaxf(M, pm[p * G + wave]);
-        M = wave_max(M);
-        float S = 0.0f;
-        for (int p = lane; p < np; p += 64) {
-            const float mp = pm[p * G + wave];
-            const float f = mp == -INFINITY ? 0.0f : __expf(mp - M);
-            S += f * pl[p * G + wave];
-            pm[p * G + wave] = f;
-        }
-        S = wave_sum(S);
-        if (lane == 0) {
-            L.cm[wave] = M;
-            L.cl[wave] = S;
-        }
-    }
-    __syncthreads();
-    if (mine) {
-        float A = 0.0f;
-        for (int p0 = 0; p0 < np; p0 += RB) {
-            if (p0 > 0) {
-#pragma unroll
-                for (int k = 0; k < RB; ++k) x[k] = p0 + k < np ? ld_agent(pi + (size_t)(p0 + k) * G * (D + 2)) : 0.0f;
-            }
-#pragma unroll
-            for (int k = 0; k < RB; ++k)
-                if (p0 + k < np) A += pm[(p0 + k) * G + g] * x[k];
-        }
-        const int bseq = u / geo.hkv, h = u - bseq * geo.hkv;
-        const size_t o = (size_t)bseq * geo.hq + (size_t)h * G + g;
-        const float S = L.cl[g];
-        d.out[o * D + i] = S > 0.0f ? A / S : 0.0f;
-        if (i == 0 && d.lse) d.lse[o] = S > 0.0f ? L.cm[g] + logf(S) : -INFINITY;
-    }
-}
-
-// One compensation workgroup of the fused launch (see above): blocks [c0, c1) of unit u with n tokens.
-template <int D, int G>
-__device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, int n, int c0, int c1,
-                                  SelExactLds<D, G>& L, float* part) {
-    constexpr int NT = kFinThreads;
-    constexpr int LPB = D / 4;               // lanes per mean-value row (one float4 each)
-    constexpr int RPS = NT / LPB;            // rows per workgroup step
-    constexpr int ROWS = G <= 4 ? 16 : 8;    // rows in flight per thread
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nb = max(0, c1 - c0);
-    const int li = tid % LPB, slot = tid / LPB;
-    // this thread's first rows before anything else (branch-free: a slot past the range reloads the
-    // range's first row, weighted by zero)
-    const float4* vm = reinterpret_cast<const float4*>(d.vmean + ((size_t)u * geo.xcap + c0) * D) + li;
-    float4 v[ROWS];
-#pragma unroll
-    for (int k = 0; k < ROWS; ++k) {
-        const int lb = slot + k * RPS;
-        v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
-    }
-    // pseudo-logits log|b| + zbar, then per head (wave g) their max and the weights exp(. - max)
-    const float* lg = d.blk_logit + (size_t)u * G * geo.xcap;
-    for (int idx = tid; idx < G * nb; idx += NT) {
-        const int g = idx / nb, lb = idx - g * nb, b = c0 + lb;
-        L.cw[g][lb] = logf((float)min(geo.B, n - b * geo.B)) + lg[(size_t)g * geo.xcap + b];
-    }
-    __syncthreads();
-    if (wave < G) {
-        const int g = wave;
-        float mx = -INFINITY;
-        for (int lb = lane; lb < nb; lb += 64) mx = fmaxf(mx, L.cw[g][lb]);
-        mx = wave_max(mx);
-        float sum = 0.0f;
-        for (int lb = lane; lb < nb; lb += 64) {
-            const float wv = __expf(L.cw[g][lb] - mx);
-            L.cw[g][lb] = wv;
-            sum += wv;
-        }
-        sum = wave_sum(sum);
-        if (lane == 0) {
-            L.cm[g] = mx;
-            L.cl[g] = sum;
-        }
-    }
-    __syncthreads();
-    // weighted mean values; lane li of a row slot holds coordinates 4 li .. 4 li + 3
-    float acc[G][4];
-#pragma unroll
-    for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
-    for (int lb0 = slot; lb0 < nb; lb0 += RPS * ROWS) {
-        if (lb0 != slot) {
-#pragma unroll
-            for (int k = 0; k < ROWS; ++k) {
-                const int lb = lb0 + k * RPS;
-                v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < ROWS; ++k) {
-            const int lb = lb0 + k * RPS;
-            if (lb < nb) {
-#pragma unroll
-                for (int g = 0; g < G; ++g) {
-                    const float wv = L.cw[g][lb];
-                    acc[g][0] += wv * v[k].x;
-                    acc[g][1] += wv * v[k].y;
-                    acc[g][2] += wv * v[k].z;
-                    acc[g][3] += wv * v[k].w;
-                }
-            }
-        }
-    }
-    // the row slots of a wave (lanes li, li + LPB, ...), then the waves in order
-#pragma unroll
-    for (int off = LPB; off < 64; off <<= 1)
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[g][e] = xor_add(acc[g][e], off);
-    if (lane < LPB) {
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-            *reinterpret_cast<float4*>(&L.u.ex.acc[wave][g][4 * li]) = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
-    }
-    __syncthreads();
-    for (int idx = tid; idx < G * D; idx += NT) {
-        const int g = idx / D, i = idx - g * D;
-        float* p = part + (size_t)g * (D + 2);
-        if (i == 0) {
-            st_agent(p, L.cm[g]);
-            st_agent(p + 1, L.cl[g]);
-        }
-        float tot = 0.0f;
-#pragma unroll
-        for (int w = 0; w < kSxWaves; ++w) tot += L.u.ex.acc[w][g][i];
-        st_agent(p + 2 + i, tot);
-    }
-}
-
 template <int D, int G>
 __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int items) {
     __shared__ SelExactLds<D, G> L;
@@ -1328,8 +638,9 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
         const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
         const int X = (n + geo.B - 1) / geo.B;
         const int c0 = min(c * d.cb, X), c1 = min(c0 + d.cb, X);
-        step_compensation<D, G>(geo, d, u, n, c0, c1, L,
-                                d.ws_part + ((size_t)u * d.part_count + c) * G * (D + 2));
+        step_compensation<D, G, (G <= 4 ? 16 : 8), false>(geo, d, u, n, c0, c1, L,
+                                                          d.ws_part + ((size_t)u * d.part_count + c) * G * (D + 2),
+                                                          [] {});
         if (d.arrive) arrive_and_merge<D, G>(geo, d, u, L);
         return;
     }
@@ -1382,10 +693,6 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
     float* part = d.ws_part + ((size_t)u * d.part_count + d.part_base + item) * G * (D + 2);
     finish_exact<D, G, kSxWaves, true>(m, l, acc, L.u.ex, part);
     if (d.arrive) arrive_and_merge<D, G>(geo, d, u, L);
-}
-
-size_t finalize_dyn_lds(const Geom& g, const ScoreArgs& a) {
-    return ((size_t)2 * (a.nchunks + 1) * g.G + (a.keys_in_lds ? (size_t)g.xmax() : 0)) * sizeof(float);
 }
 
 template <int D, int G, bool kStep, int PMAX>

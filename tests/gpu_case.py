@@ -250,7 +250,7 @@ class Case:
 
 # selection paths under test; a case the one-group path does not accept runs on the chunked path only
 PATHS = {"chunked": P.COMPKV_SELECT_CHUNKED, "one_group": P.COMPKV_SELECT_ONE_GROUP,
-         "chunked_exact": P.COMPKV_SELECT_CHUNKED_EXACT}
+         "chunked_exact": P.COMPKV_SELECT_CHUNKED_EXACT, "stream": P.COMPKV_SELECT_STREAM}
 
 
 def make_case(name: str, path: str) -> Case:

@@ -179,7 +179,8 @@ def test_score_select_block_count_limit():
 
 def test_select_path_validation():
     """select_path: an unknown value is EINVAL; the one-group path is refused (before anything is
-    enqueued) when G * blocks exceeds 8192, and accepted up to that bound."""
+    enqueued) when G * blocks exceeds 8192, and accepted up to that bound; the one-launch step is
+    accepted by both calls (the scoring call runs it chunked)."""
     L = P.library()
     args = [FAKE] * 6 + [FAKE, None]
 
@@ -191,20 +192,22 @@ def test_select_path_validation():
 
     fits = dims(block_size=16, capacity_tokens=2048 * 16, max_seq_len=2048 * 16)  # G = 4: 4 * 2048 = 8192
     over = dims(block_size=16, capacity_tokens=2049 * 16, max_seq_len=2049 * 16)
-    for bad in (-1, 4):
+    for bad in (-1, 5):
         assert score(fits, bad) == EINVAL
         assert _step(L, fits, P.CompkvSelectParams(64, 1, 2, 0.088, bad)) == EINVAL
     assert score(over, P.COMPKV_SELECT_ONE_GROUP) == EUNSUP
     assert _step(L, over, P.CompkvSelectParams(64, 1, 2, 0.088, P.COMPKV_SELECT_ONE_GROUP)) == EUNSUP
     # accepted: the calls get as far as the workspace check
     for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP,
-                 P.COMPKV_SELECT_CHUNKED_EXACT):
+                 P.COMPKV_SELECT_CHUNKED_EXACT, P.COMPKV_SELECT_STREAM):
         assert score(fits, path) == EWS
-    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_CHUNKED_EXACT):
+    for path in (P.COMPKV_SELECT_AUTO, P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_CHUNKED_EXACT,
+                 P.COMPKV_SELECT_STREAM):
         assert score(over, path) == EWS
-    # one workspace size serves the fused step on either path
+    # one workspace size serves the fused step on every path
     need = P.compkv_workspace_bytes(fits, 64, P.COMPKV_WS_DECODE_STEP)
-    for path in (P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP, P.COMPKV_SELECT_CHUNKED_EXACT):
+    for path in (P.COMPKV_SELECT_CHUNKED, P.COMPKV_SELECT_ONE_GROUP, P.COMPKV_SELECT_CHUNKED_EXACT,
+                 P.COMPKV_SELECT_STREAM):
         assert _step(L, fits, P.CompkvSelectParams(64, 1, 2, 0.088, path), ws_bytes=need - 1) == EWS
 
 
@@ -234,20 +237,27 @@ def test_score_kind_and_compensation_validation():
 
 def test_decode_step_path_resolution():
     """compkv_decode_step_path reports the launch shape without enqueuing anything: explicit paths as
-    requested (the fused selection + exact launch whenever its limits hold), AUTO as one group for
-    units of at most 256 blocks, and errors as statuses."""
+    requested (the fused selection + exact launch and the two-launch step whenever their limits
+    hold), AUTO as one group or the chunked launches, and errors as statuses."""
     small = dims(block_size=16, capacity_tokens=4096, max_seq_len=4096)  # 256 blocks
     big = dims(block_size=32, capacity_tokens=32768, max_seq_len=32768)  # 1024 blocks
     prm = lambda path, K=16: P.CompkvSelectParams(K, 1, 2, 0.088, path)
-    assert P.compkv_decode_step_path(small, prm(P.COMPKV_SELECT_AUTO)) == P.COMPKV_SELECT_ONE_GROUP
     assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_ONE_GROUP)) == P.COMPKV_SELECT_ONE_GROUP
     for d in (small, big):
         assert P.compkv_decode_step_path(d, prm(P.COMPKV_SELECT_CHUNKED)) == P.COMPKV_SELECT_CHUNKED
         assert P.compkv_decode_step_path(d, prm(P.COMPKV_SELECT_CHUNKED_EXACT)) == P.COMPKV_SELECT_CHUNKED_EXACT
-    # past the fused kernel's budget limit the chunked-exact request runs chunked
-    assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_CHUNKED_EXACT, 1025)) == P.COMPKV_SELECT_CHUNKED
+        assert P.compkv_decode_step_path(d, prm(P.COMPKV_SELECT_STREAM)) == P.COMPKV_SELECT_STREAM
+    assert P.compkv_decode_step_path(small, prm(P.COMPKV_SELECT_AUTO)) in (P.COMPKV_SELECT_ONE_GROUP,
+                                                                           P.COMPKV_SELECT_CHUNKED_EXACT)
     assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_AUTO)) in (P.COMPKV_SELECT_CHUNKED,
                                                                          P.COMPKV_SELECT_CHUNKED_EXACT)
+    # past the fused kernels' budget limit the chunked-exact and one-launch requests run chunked
+    assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_CHUNKED_EXACT, 1025)) == P.COMPKV_SELECT_CHUNKED
+    assert P.compkv_decode_step_path(big, prm(P.COMPKV_SELECT_STREAM, 1025)) == P.COMPKV_SELECT_CHUNKED
+    # past 8192 blocks per unit AUTO falls back to the chunked launches
+    long_ = dims(block_size=16, capacity_tokens=8193 * 16, max_seq_len=8193 * 16)
+    assert P.compkv_decode_step_path(long_, prm(P.COMPKV_SELECT_AUTO)) in (P.COMPKV_SELECT_CHUNKED,
+                                                                           P.COMPKV_SELECT_CHUNKED_EXACT)
     with pytest.raises(P.CompkvError):
         P.compkv_decode_step_path(big, prm(7))
     with pytest.raises(P.CompkvError):

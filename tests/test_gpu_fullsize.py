@@ -26,7 +26,8 @@ FULL = {
     "streaming_128k": (WORKLOADS["streaming_128k"], WORKLOADS["streaming_128k"].context + 1, (None,)),
 }
 PATH_NAMES = {P.COMPKV_SELECT_CHUNKED: "chunked", P.COMPKV_SELECT_ONE_GROUP: "one group",
-              P.COMPKV_SELECT_CHUNKED_EXACT: "chunked + fused selection/exact"}
+              P.COMPKV_SELECT_CHUNKED_EXACT: "chunked + fused selection/exact",
+              P.COMPKV_SELECT_STREAM: "one launch"}
 
 _cases = {}
 
