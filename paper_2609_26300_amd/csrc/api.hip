@@ -144,7 +144,10 @@ struct SxShape {  // the fused step's selection + exact launch (sx_shape below)
     int eb, n_exact;
     int cb, n_comp;  // its compensation workgroups: blocks each, workgroups per unit
     bool fits;       // within the kernel's limits
-    bool one_round;  // and every workgroup resident at once (one per CU)
+    bool one_round;  // every workgroup of the chosen form resident at once (one per CU)
+    bool work;       // the one-selector form (below) is chosen
+    int P, web, wcb;  // one-selector form: workgroups per unit, exact blocks each, compensation blocks
+                      // per worker
 };
 SxShape sx_shape(const Geom& g, int nchunks, int K);
 
@@ -166,13 +169,16 @@ size_t step_part_bytes(const Geom& g, int parts) {
 int step_partials(const Geom& g, int K) {
     const int nchunks = score_shape(g).nchunks;
     const SxShape sx = sx_shape(g, nchunks, K);
-    return std::max(nchunks + 1 + sparse_shape(g, K).n_exact, sx.fits ? sx.n_comp + sx.n_exact : 0);
+    return std::max(std::max(nchunks + 1 + sparse_shape(g, K).n_exact, sx.fits ? sx.n_comp + sx.n_exact : 0),
+                    sx.work ? 2 * sx.P - 1 : 0);
 }
 
-// fused step: the arrival counters of the fused selection/exact launch's in-launch merge (one per unit)
-// follow the partials
+// fused step: the arrival counters of the fused selection/exact launch's in-launch merge and the
+// selection words of its one-selector form (one each per unit), then that form's mailbox of posted ids
+// ([units][K]), follow the partials
 size_t step_ws(const Geom& g, int K) {
-    return score_ws(g) + step_part_bytes(g, step_partials(g, K)) + align_up((size_t)g.units() * sizeof(uint32_t));
+    return score_ws(g) + step_part_bytes(g, step_partials(g, K)) +
+           align_up((size_t)g.units() * (2 + (size_t)K) * sizeof(uint32_t));
 }
 
 StreamShape stream_shape(const Geom& g, int K, bool mean);
@@ -216,11 +222,14 @@ SxShape sx_shape(const Geom& g, int nchunks, int K) {
     int cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 0;
-    // one workgroup per CU: up to half of a unit's share of the CUs goes to compensation workgroups (of
-    // at least 128 and at most select_exact_max_cb() blocks each: few partials to merge) and the rest to
-    // exact items, the smallest of at least 64 tokens that fit it (an item of more than 16 tiles takes
-    // several rounds of its waves)
-    const int per = std::max(1, cus / std::max(1, g.units()));
+    // one resident round of workgroups (two per CU): up to half of a unit's share goes to compensation
+    // workgroups (of at least 128 and at most select_exact_max_cb() blocks each: few partials to merge)
+    // and the rest to exact items, the smallest of at least 64 tokens that fit it (an item of more
+    // tiles than the workgroup has waves takes several rounds of its waves), so that each CU streams
+    // mean values while its item workgroup selects
+    const size_t dyn = ((size_t)2 * (nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
+    const int resident = compkv::select_exact_slots(g, dyn);
+    const int per = std::max(1, resident / std::max(1, g.units()));
     const int cbmax = compkv::select_exact_max_cb();
     int n_comp = std::max(1, std::min(per / 2, ceil_div(xmax, 128)));
     n_comp = std::max(n_comp, ceil_div(xmax, cbmax));
@@ -228,14 +237,29 @@ SxShape sx_shape(const Geom& g, int nchunks, int K) {
     const int slots = std::max(1, per - n_comp);
     const int eb = std::max(std::max(1, 64 / g.B), ceil_div(keff, slots));
     const int n_exact = ceil_div(keff, eb);
-    const size_t dyn = ((size_t)2 * (nchunks + 1) * g.G + (size_t)xmax) * sizeof(float);
     const bool fits = K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
                       eb <= compkv::decode_max_eb() && n_exact <= compkv::decode_max_items() && cb <= cbmax &&
                       n_comp + n_exact <= compkv::decode_max_partials() &&
                       (n_comp + n_exact) * g.G <= compkv::select_exact_merge_terms();
-    const bool one_round = fits && (long long)g.units() * (n_exact + n_comp) <= cus &&
-                           compkv::select_exact_slots(g, dyn) >= cus;
-    return {eb, n_exact, cb, n_comp, fits, one_round};
+    // one-selector launch: per unit one selector and P - 1 workers, compensation shares of at least 128
+    // blocks, every workgroup resident at once
+    int P = std::min(per, 1 + ceil_div(xmax, 128));
+    P = std::max(P, 1 + ceil_div(xmax, cbmax));
+    P = std::max(P, ceil_div(keff, compkv::decode_max_eb()));
+    const int wcb = ceil_div(xmax, std::max(1, P - 1));
+    const int web = ceil_div(keff, P);
+    const bool work_fits = cus > 0 && P >= 2 && (long long)g.units() * P <= resident &&
+                           K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
+                           web <= compkv::decode_max_eb() && wcb <= cbmax &&
+                           (2 * P - 1) * g.G <= compkv::select_exact_merge_terms();
+    const bool items_round = fits && cus > 0 && (long long)g.units() * (n_exact + n_comp) <= resident;
+    // the one-selector form where a unit's selected tokens are at least its mean-value rows (both 4 d
+    // bytes each): spread over all of the unit's workgroups, the exact share then outweighs the repeated
+    // selections it saves. Where the mean values dominate, the form with compensation workgroups that
+    // stream from the start while the item workgroups select is faster (measured: 128K layer 26.9 vs
+    // 28.6 us; wide GQA 33.3 vs 29.9 us; 32K layer 18.3 vs 18.5 us)
+    const bool work = work_fits && ((long long)xmax <= (long long)keff * g.B || !items_round);
+    return {eb, n_exact, cb, n_comp, fits, work || items_round, work, P, web, wcb};
 }
 
 // Shape of the two-launch step: the chunked path's scoring chunks; one round of selectors and
@@ -274,7 +298,7 @@ size_t stream_ws(const Geom& g, int K) {
 }
 
 bool use_select_exact(int path, const SxShape& sx) {
-    return (path == COMPKV_SELECT_CHUNKED_EXACT && sx.fits) || (path == COMPKV_SELECT_AUTO && sx.one_round);
+    return (path == COMPKV_SELECT_CHUNKED_EXACT && (sx.fits || sx.work)) || (path == COMPKV_SELECT_AUTO && sx.one_round);
 }
 
 // The fused step's choice of the one-group path: as for the scoring call, except that AUTO prefers the
@@ -646,9 +670,12 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         // the chunks score from the mean keys and variances alone; the fused launch's compensation
         // workgroups stream the mean values while its item workgroups select, and the last of each
         // unit's workgroups merges the unit's partials
+        // (all workgroups resident at once: one selector per unit, the others stream the mean values
+        // and then attend over their share of its ids)
         float* dpart = reinterpret_cast<float*>(static_cast<char*>(wsb) + score_ws(g));
-        const int n_comp = drop ? 0 : sx.n_comp;
-        const int nparts = n_comp + sx.n_exact;
+        const bool work = sx.work;
+        const int n_comp = drop ? 0 : (work ? sx.P - 1 : sx.n_comp);
+        const int nparts = n_comp + (work ? sx.P : sx.n_exact);
         const size_t part_bytes = step_part_bytes(g, step_partials(g, K));
         uint32_t* arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(wsb) + score_ws(g) + part_bytes);
         if (step_part_bytes(g, nparts) > part_bytes || step_ws(g, K) > wsb_bytes)
@@ -671,10 +698,10 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.out = out;
         d.lse = lse;
         d.sel_stride = K;
-        d.n_exact = sx.n_exact;
-        d.eb = sx.eb;
+        d.n_exact = work ? sx.P : sx.n_exact;
+        d.eb = work ? sx.web : sx.eb;
         d.n_comp = n_comp;
-        d.cb = sx.cb;
+        d.cb = work ? sx.wcb : sx.cb;
         d.dense = 0;
         d.scale = params->scale;
         d.part_count = nparts;
@@ -682,6 +709,10 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.neg_pseudo = drop ? 0 : 1;
         d.sel_padded = 1;
         d.arrive = arrive;
+        d.sel_word = arrive + g.units();
+        d.mailbox = arrive + 2 * (size_t)g.units();
+        d.timeouts = state;
+        if (work) return launch_status(compkv::launch_select_work(g, a, d, sx.P, s));
         return launch_status(compkv::launch_select_exact(g, a, d, sx.n_exact, s));
     }
     // separate selection and exact items. Mean: the chunks' compensation partials, then the exact

@@ -256,19 +256,10 @@ __global__ __launch_bounds__(kItemThreads) __attribute__((amdgpu_waves_per_eu(4)
         float m, l;
         v4f32 acc[D / 16];
         const uint16_t* qh = a.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
-        // fused step: the block logits of the item's blocks, requested once its K/V loads are issued
+        // fused step: the block logits of the item's blocks (their pseudo-terms are taken back out)
         const bool pseudo = a.neg_pseudo && !tm.dense;
-        exact_tokens<D, G, kItemWaves>(tm, a.K, a.V, qh,
-                                       pseudo ? sh.ex.zb : nullptr, a.scale, m, l, acc, [&] {
-                               if (!pseudo) return;  // workgroup-uniform
-                               const float* lg = a.blk_logit + (size_t)u * G * geo.xcap;
-                               for (int idx = tid; idx < G * tm.nblk; idx += kItemThreads) {
-                                   const int g = idx / tm.nblk, k = idx - g * tm.nblk;
-                                   const int b = sh.sel[k];
-                                   sh.ex.zb[g][k] = lg[(size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0)];
-                               }
-                               __syncthreads();
-                           });
+        exact_tokens<D, G, kItemWaves>(tm, a.K, a.V, qh, pseudo ? a.blk_logit + (size_t)u * G * geo.xcap : nullptr,
+                                       geo.xcap, sh.ex.zb, a.scale, m, l, acc);
         finish_exact<D, G, kItemWaves>(m, l, acc, sh.ex, part);
     } else {
         const int c0 = (item - a.n_exact) * a.cb;

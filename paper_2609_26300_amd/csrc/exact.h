@@ -54,6 +54,9 @@ __device__ __forceinline__ void st_agent_i32(int32_t* p, int32_t v) {
 __device__ __forceinline__ int32_t ld_agent_i32(const int32_t* p) {
     return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void st_agent_u32(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ uint32_t ld_agent_u32(const uint32_t* p) {
     return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -111,24 +114,43 @@ struct TokenMap {
 
 // Exact tokens of one item with MFMA. Leaves this wave's (m, l) for head lane%16 (lanes with the same
 // lane%16 agree) and acc[j][i] = sum over the wave's tokens of p * v for head 4(lane/16)+i at
-// coordinate (D/16)*(lane%16) + j. With zt (fused step: zt[g][k] = block logit of head g and the item's
-// k-th block, filled by `mid`) every token's weight is p_j - p'_j with p'_j = e^{zbar_b - m} for its
-// block b. `mid` is workgroup-wide work (every wave calls it once, after its first loads are issued).
-// Ku / Vu are the cache bases (tm.row gives absolute rows).
-template <int D, int G, int NW, typename Mid>
+// coordinate (D/16)*(lane%16) + j. With lg (the fused step: the unit's block logits, lg[g * lstride +
+// b] for head g and block b; sparse items only) every token's weight is p_j - p'_j with
+// p'_j = e^{zbar_b - m} for its block b; the item's block logits are staged in zt (LDS, [G][kMaxEb]).
+// Ku / Vu are the cache bases (tm.row gives absolute rows). Loads are requested in the order of their
+// use (they return in that order): the block logits, the query, then the first tiles' keys and values.
+template <int D, int G, int NW>
 __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku, const uint16_t* __restrict__ Vu,
-                             const uint16_t* __restrict__ qh, const float (*zt)[kMaxEb], float scale, float& m,
-                             float& l, v4f32 (&acc)[D / 16], Mid&& mid) {
+                             const uint16_t* __restrict__ qh, const float* lg, size_t lstride, float (*zt)[kMaxEb],
+                             float scale, float& m, float& l, v4f32 (&acc)[D / 16]) {
+    static_assert(NW * 64 >= kMaxEb, "one block logit per thread and head");
     constexpr int KS = D / 32;   // k-steps of the logit MFMA
     constexpr int CPL = D / 16;  // value coordinates per lane (= output blocks)
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
     m = -INFINITY;
     l = 0.0f;
 #pragma unroll
     for (int j = 0; j < CPL; ++j) acc[j] = v4f32{0.0f, 0.0f, 0.0f, 0.0f};
+    // the block logits of the item's blocks (thread k < nblk: block k, every head)
+    const bool stage = lg != nullptr && !tm.dense;  // (workgroup-uniform)
+    float zv[G];
+    if (stage && tid < tm.nblk) {
+        const int b = tm.sel[tid];
+        const int bb = b >= 0 && b < tm.X ? b : 0;
+#pragma unroll
+        for (int g = 0; g < G; ++g) zv[g] = lg[(size_t)g * lstride + bb];
+    }
+    // B operand of the logit product: query head `col` (zero for padding heads)
+    v8bf16 qb[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        uint4 w = make_uint4(0, 0, 0, 0);
+        if (col < G) w = *reinterpret_cast<const uint4*>(qh + col * D + 32 * ks + 8 * grp);
+        qb[ks] = __builtin_bit_cast(v8bf16, w);
+    }
     const int ntiles = (tm.count() + 15) / 16;
-    const bool pseudo = zt != nullptr && col < G;
+    const bool pseudo = stage && col < G;
     uint4 kreg[KS];
     uint4 vreg[4];
     bool vvalid[4];
@@ -157,18 +179,15 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
         }
     };
     issue(wave);
-    mid();
+    if (stage) {  // (the logits were requested first: this waits for them alone)
+        if (tid < tm.nblk) {
+#pragma unroll
+            for (int g = 0; g < G; ++g) zt[g][tid] = zv[g];
+        }
+        __syncthreads();
+    }
     for (int t = wave; t < ntiles; t += NW) {
         if (t != wave) issue(t);
-        // B operand of the logit product: query head `col` (zero for padding heads), requested after the
-        // tile's K/V loads
-        v8bf16 qb[KS];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            uint4 w = make_uint4(0, 0, 0, 0);
-            if (col < G) w = *reinterpret_cast<const uint4*>(qh + col * D + 32 * ks + 8 * grp);
-            qb[ks] = __builtin_bit_cast(v8bf16, w);
-        }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) kreg[ks] = kvalid ? kreg[ks] : make_uint4(0, 0, 0, 0);
 #pragma unroll

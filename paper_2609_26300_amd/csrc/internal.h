@@ -69,7 +69,8 @@ struct ScoreArgs {
     int score_kind;         // COMPKV_SCORE_*: CompKV score, mass only, or first-order mass estimate
     int chunks_only;        // chunked path: launch the chunk scoring without the selection
     int tail_first;         // set by the launcher: the last-block workgroups lead the grid (else trail)
-    uint32_t* arrive_zero;  // nullable: per-unit counters the last-block workgroups set to zero
+    uint32_t* arrive_zero;  // nullable: [2][units] words (arrivals, selection words), then [units][K]
+                            // (mailbox), that the last-block workgroups zero
 };
 
 struct DecodeArgs {
@@ -100,6 +101,9 @@ struct DecodeArgs {
     uint32_t* arrive;  // fused selection/exact launch: per-unit arrival counters (zeroed by the chunk
                        // launch); the unit's last workgroup merges its partials (null: a merge launch
                        // follows)
+    uint32_t* sel_word;  // one-selector fused launch: per-unit selection words (zeroed by the chunk launch)
+    uint32_t* mailbox;   // one-selector fused launch: [units][K] posted ids (zeroed by the chunk launch)
+    uint32_t* timeouts;  // per-unit words [units][4] at the start of the workspace (word 3 counts timeouts)
 };
 
 // ------------------------------------------------------------------ launchers (one per kernel family)
@@ -124,10 +128,15 @@ hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hi
 // d.cb blocks each (partials 0 .. n_comp - 1; the items' from d.part_base); hipErrorInvalidValue outside
 // its limits
 hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s);
+// the same step with one selector per unit and P - 1 workers (compensation share d.cb, then exact share
+// d.eb once the selection word is set): P workgroups per unit, all resident at once (checked by the
+// caller with select_exact_slots); partials: d.n_comp (= P - 1 under Mean, else 0) compensation, then P
+// exact; hipErrorInvalidValue outside its limits
+hipError_t launch_select_work(const Geom& g, ScoreArgs a, const DecodeArgs& d, int P, hipStream_t s);
 int select_exact_max_budget();
 int select_exact_waves();
 int select_exact_max_cb();  // blocks per compensation workgroup of the fused launch
-int select_exact_slots(const Geom& g, size_t dyn);  // its workgroups resident at once on the current device
+int select_exact_slots(const Geom& g, size_t dyn);  // one-selector launch: workgroups resident at once
 int select_exact_merge_terms();  // partials x heads limit of its in-launch merge
 hipError_t launch_decode_merge(const Geom& g, const DecodeArgs& a, int nitems, hipStream_t s);
 

@@ -95,7 +95,14 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     const int n = clamp_len(n_raw, geo.max_seq);
     const int X = (n + geo.B - 1) / geo.B;
     float* pp = a.ws_part + ((size_t)u * (nc + 1) + nc) * G * 2;
-    if (a.arrive_zero && tid == 0) a.arrive_zero[u] = 0u;  // for the launch that merges after this one
+    if (a.arrive_zero) {  // for the launch that merges after this one
+        if (tid == 0) {
+            a.arrive_zero[u] = 0u;
+            a.arrive_zero[geo.units() + u] = 0u;
+        }
+        uint32_t* mbox = a.arrive_zero + 2 * (size_t)geo.units() + (size_t)u * a.K;
+        for (int k = tid; k < a.K; k += kThreads) mbox[k] = 0u;
+    }
     // fused step with Mean compensation: this workgroup's compensation partial
     float* cp = (kStep && a.comp_part) ? a.comp_part + ((size_t)u * a.part_count + nc) * G * (D + 2) : nullptr;
     if (X == 0) {  // empty sequence: neutral partials
@@ -625,9 +632,55 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
 // chunk launch wrote, value vmean_b), reduced to one softmax partial per head (max, sum of weights,
 // weighted mean values). The exact items take their selected blocks' pseudo-tokens back out, so the
 // compensation needs no selection and the mean values stream while the HBM would otherwise idle.
-template <int D, int G>
-__global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int items) {
-    __shared__ SelExactLds<D, G> L;
+// threads of the fused selection/exact launch's workgroups and keys per thread
+constexpr int kSxThreads = 1024;
+constexpr int kSxKeys = 8192 / kSxThreads;
+// mean-value rows per thread and batch of a compensation workgroup (two batches in flight: 32 KB at
+// d = 128). While nearly every CU streams, that suffices for the HBM rate, and less data queued at the
+// memory keeps the latency of the selections' and the exact items' loads short.
+constexpr int kCompRows = 1;
+
+// Exact attention of unit u over nblk selected blocks whose ids are in LDS (ids; -1 or an id past the
+// unit's blocks contributes nothing) into decode partial `part` of the unit (device-coherent stores).
+// Under Mean compensation every token's weight is p_j - p'_j (the chunk launch's block logits).
+template <int D, int G, int NW, typename Lds>
+__device__ void sx_exact(const Geom& geo, const DecodeArgs& d, int u, int n, const int32_t* ids, int nblk,
+                         int part, Lds& L) {
+    constexpr int FT = NW * 64;
+    const int tid = threadIdx.x;
+    const int bseq = u / geo.hkv, h = u % geo.hkv;
+    const int X = (n + geo.B - 1) / geo.B;
+    TokenMap tm;
+    tm.dense = false;
+    tm.B = geo.B;
+    tm.invB = 1.0f / (float)geo.B;
+    tm.n = n;
+    tm.X = X;
+    tm.nblk = nblk;
+    tm.sel = ids;
+    tm.t0 = tm.t1 = 0;
+    tm.page = tm.pg0 = 0;
+    tm.invP = 0.0f;
+    tm.rowbase = L.rowbase;
+    for (int k = tid; k < nblk; k += FT) {
+        const int b = ids[k];
+        L.rowbase[k] = block_row0(geo, u, b >= 0 && b < X ? b : 0);
+    }
+    __syncthreads();
+    float m, l;
+    v4f32 acc[D / 16];
+    const uint16_t* qh = d.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
+    const bool pseudo = d.neg_pseudo != 0;  // Mean: the compensation added every block's pseudo-token
+    exact_tokens<D, G, NW>(tm, d.K, d.V, qh, pseudo ? d.blk_logit + (size_t)u * G * geo.xcap : nullptr, geo.xcap,
+                           L.u.ex.zb, d.scale, m, l, acc);
+    finish_exact<D, G, NW, true>(m, l, acc, L.u.ex, d.ws_part + ((size_t)u * d.part_count + part) * G * (D + 2));
+}
+
+template <int D, int G, int FT, int KPT>
+__global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int items) {
+    constexpr int NW = FT / 64;
+    using Lds = SelExactLdsT<D, G, kStepCbMax, NW>;
+    __shared__ Lds L;
     extern __shared__ float dyn[];
     const int tid = threadIdx.x;
     const int units = geo.units();
@@ -635,64 +688,111 @@ __global__ __launch_bounds__(kFinThreads) void select_exact_kernel(Geom geo, Sco
     if ((int)blockIdx.x >= items * units) {  // a compensation workgroup (workgroup-uniform)
         int c;
         xcd_unit_work((int)blockIdx.x - items * units, units, d.n_comp, u, c);
-        const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
-        const int X = (n + geo.B - 1) / geo.B;
-        const int c0 = min(c * d.cb, X), c1 = min(c0 + d.cb, X);
-        step_compensation<D, G, (G <= 4 ? 16 : 8), false>(geo, d, u, n, c0, c1, L,
+        const int xmax = geo.xmax();
+        const int c0 = min(c * d.cb, xmax), c1 = min(c0 + d.cb, xmax);
+        step_compensation<D, G, kCompRows, Lds, FT>(geo, d, u, d.seq_lens[u / geo.hkv], c0, c1, L,
                                                           d.ws_part + ((size_t)u * d.part_count + c) * G * (D + 2),
                                                           [] {});
-        if (d.arrive) arrive_and_merge<D, G>(geo, d, u, L);
+        if (d.arrive) arrive_and_merge<D, G, Lds, FT>(geo, d, u, L);
         return;
     }
     // the items of unit u all on XCD u % kXcds: the unit's selection inputs are fetched once into
     // that XCD's L2
     xcd_unit_work(blockIdx.x, units, items, u, item);
-    finalize_select<G>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
+    finalize_select<G, false, FT, KPT>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
     __syncthreads();
-    const int bseq = u / geo.hkv, h = u % geo.hkv;
-    const int n = clamp_len(d.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
+    const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
     const int nsel = L.nsel;
     if (item == 0) {  // the selection outputs (the ids past n_sel hold -1)
-        for (int k = tid; k < a.K; k += kFinThreads) a.sel[(size_t)u * a.K + k] = L.sel[k];
+        for (int k = tid; k < a.K; k += FT) a.sel[(size_t)u * a.K + k] = L.sel[k];
         if (tid == 0) a.n_sel[u] = nsel;
     }
-    TokenMap tm;
-    tm.dense = false;
-    tm.B = geo.B;
-    tm.invB = 1.0f / (float)geo.B;
-    tm.n = n;
-    tm.X = X;
     const int e0 = item * d.eb;
-    tm.nblk = max(0, min(d.eb, nsel - e0));
-    tm.sel = L.sel + e0;
-    tm.t0 = tm.t1 = 0;
-    tm.page = tm.pg0 = 0;
-    tm.invP = 0.0f;
-    tm.rowbase = L.rowbase;
-    for (int k = tid; k < tm.nblk; k += kFinThreads) {
-        const int b = tm.sel[k];
-        L.rowbase[k] = block_row0(geo, u, b >= 0 && b < X ? b : 0);
+    sx_exact<D, G, NW>(geo, d, u, n, L.sel + e0, max(0, min(d.eb, nsel - e0)), d.part_base + item, L);
+    if (d.arrive) arrive_and_merge<D, G, Lds, FT>(geo, d, u, L);
+}
+
+// ---------------------------------------------------------------- selection + exact, one selector
+// The same step when every workgroup of the launch is resident at once: per unit one selector and
+// P - 1 workers (grid units * P, the selectors first; xcd_unit_work keeps a unit's workgroups on one
+// XCD). The selector ranks the unit's blocks and posts every id slot k < K to the unit's mailbox
+// (id ^ kPosted, device-coherent; the chunk launch zeroed the mailbox, and no posted value is zero),
+// then attends exactly over the first eb ids. Worker w (1 .. P - 1) first streams its share of the
+// mean values (compensation blocks [(w - 1) cb, w cb), partial w - 1), requesting its slots
+// [w eb, (w + 1) eb) of the mailbox once the last mean values are in; a slot still zero is polled
+// until posted (a bounded wait: the selector started before any worker and never waits itself; past
+// the bound the unit's outputs become NaN and its timeout word counts it). Then it attends exactly
+// over those ids. Exact partials follow the P - 1 compensation partials (none under Drop); the unit's
+// last workgroup of P merges them all. The HBM streams from the start on every CU but the
+// selectors', and the selection runs once per unit.
+constexpr uint32_t kPosted = 0x80000000u;  // mailbox value of id b: b ^ kPosted (-1 gives 0x7FFFFFFF)
+constexpr uint32_t kSelFailed = 1u;        // selection word: a worker's wait timed out
+constexpr int kSelSpinLimit = 1 << 17;     // polls of a wait (each a memory round trip): well over 50 ms
+
+template <int D, int G>
+__global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int P) {
+    constexpr int FT = kSxThreads, NW = FT / 64;
+    using Lds = SelExactLdsT<D, G, kStepCbMax, NW>;
+    __shared__ Lds L;
+    extern __shared__ float dyn[];
+    const int tid = threadIdx.x;
+    const int units = geo.units();
+    int u, w;
+    if ((int)blockIdx.x < units) {
+        u = blockIdx.x;  // (XCD blockIdx % 8 = u % 8)
+        w = 0;
+    } else {
+        xcd_unit_work((int)blockIdx.x - units, units, P - 1, u, w);
+        ++w;
     }
-    __syncthreads();
-    float m, l;
-    v4f32 acc[D / 16];
-    const uint16_t* qh = d.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
-    const bool pseudo = d.neg_pseudo != 0;  // Mean: the chunks added every block's pseudo-token
-    exact_tokens<D, G, kSxWaves>(tm, d.K, d.V, qh,
-                                 pseudo ? L.u.ex.zb : nullptr, d.scale, m, l, acc, [&] {
-                                     if (!pseudo) return;  // workgroup-uniform
-                                     const float* lg = d.blk_logit + (size_t)u * G * geo.xcap;
-                                     for (int idx = tid; idx < G * tm.nblk; idx += kFinThreads) {
-                                         const int g = idx / tm.nblk, k = idx - g * tm.nblk;
-                                         const int b = tm.sel[k];
-                                         L.u.ex.zb[g][k] = lg[(size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0)];
-                                     }
-                                     __syncthreads();
-                                 });
-    float* part = d.ws_part + ((size_t)u * d.part_count + d.part_base + item) * G * (D + 2);
-    finish_exact<D, G, kSxWaves, true>(m, l, acc, L.u.ex, part);
-    if (d.arrive) arrive_and_merge<D, G>(geo, d, u, L);
+    uint32_t* word = d.sel_word + u;
+    uint32_t* mbox = d.mailbox + (size_t)u * a.K;
+    if (w == 0) {
+        finalize_select<G, false, FT, kSxKeys>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, true);
+        __syncthreads();
+        for (int k = tid; k < a.K; k += FT) {
+            const int32_t b = L.sel[k];
+            st_agent_u32(mbox + k, (uint32_t)b ^ kPosted);
+            a.sel[(size_t)u * a.K + k] = b;
+        }
+        if (tid == 0) a.n_sel[u] = L.nsel;
+        const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
+        sx_exact<D, G, NW>(geo, d, u, n, L.sel, max(0, min(d.eb, L.nsel)), d.part_base, L);
+    } else {
+        const int n_raw = d.seq_lens[u / geo.hkv];
+        const int e0 = w * d.eb;
+        const int nblk = max(0, min(d.eb, a.K - e0));  // (the ids past n_sel are -1)
+        uint32_t mv = 0u;
+        auto request = [&] { mv = ld_agent_u32(mbox + (tid < nblk ? e0 + tid : 0)); };
+        if (d.n_comp > 0) {
+            const int xmax = geo.xmax();
+            const int c0 = min((w - 1) * d.cb, xmax), c1 = min(c0 + d.cb, xmax);
+            step_compensation<D, G, kCompRows, Lds, FT>(
+                geo, d, u, n_raw, c0, c1, L, d.ws_part + ((size_t)u * d.part_count + w - 1) * G * (D + 2), request);
+        } else {
+            request();
+        }
+        const int n = clamp_len(n_raw, geo.max_seq);
+        bool ok = true;
+        if (tid < nblk) {
+            for (int spins = 0; mv == 0u && spins < kSelSpinLimit; ++spins) {
+                __builtin_amdgcn_s_sleep(2);
+                mv = ld_agent_u32(mbox + e0 + tid);
+            }
+            ok = mv != 0u;
+            L.sel[tid] = ok ? (int32_t)(mv ^ kPosted) : -1;
+        }
+        if (!ok) {
+            __hip_atomic_fetch_or(word, kSelFailed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (d.timeouts) __hip_atomic_fetch_add(d.timeouts + 4 * u + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __syncthreads();
+        sx_exact<D, G, NW>(geo, d, u, n, L.sel, nblk, d.part_base + w, L);
+    }
+    if (arrive_last(d.arrive + u, P, L.last)) {
+        const bool failed = (ld_agent_u32(word) & kSelFailed) != 0;  // (workgroup-uniform)
+        merge_unit<D, G, Lds, FT>(geo, d, u, L, failed);
+    }
 }
 
 template <int D, int G, bool kStep, int PMAX>
@@ -745,8 +845,25 @@ hipError_t dispatch_g(const Geom& g, const ScoreArgs& a, hipStream_t s) {
 template <int D, int G>
 hipError_t launch_sx(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int items, hipStream_t s) {
     const int grid = (items + d.n_comp) * g.units();
-    select_exact_kernel<D, G><<<dim3(grid), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a, d, items);
+    select_exact_kernel<D, G, kSxThreads, kSxKeys><<<dim3(grid), kSxThreads, finalize_dyn_lds(g, a), s>>>(g, a, d, items);
     return hipGetLastError();
+}
+
+template <int D, int G>
+hipError_t launch_work(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int P, hipStream_t s) {
+    select_work_kernel<D, G><<<dim3(P * g.units()), kSxThreads, finalize_dyn_lds(g, a), s>>>(g, a, d, P);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t work_g(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int P, hipStream_t s) {
+    switch (g.G) {
+        case 1: return launch_work<D, 1>(g, a, d, P, s);
+        case 2: return launch_work<D, 2>(g, a, d, P, s);
+        case 4: return launch_work<D, 4>(g, a, d, P, s);
+        case 8: return launch_work<D, 8>(g, a, d, P, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <int D>
@@ -764,17 +881,17 @@ hipError_t sx_g(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int item
 
 int select_max_bpc() { return kBpcMax; }
 int select_exact_max_budget() { return kSelLdsMax; }
-int select_exact_waves() { return kSxWaves; }
+int select_exact_waves() { return kSxThreads / 64; }
 int select_exact_max_cb() { return kStepCbMax; }
 int select_exact_merge_terms() { return kMergeMaxTerms; }
 
-// Resident workgroups of the fused selection/exact launch on the current device with `dyn` bytes of
+// Resident workgroups of the one-selector fused launch on the current device with `dyn` bytes of
 // dynamic LDS each.
 template <int D, int G>
 int sx_slots(size_t dyn) {
     int per_cu = 0, cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_exact_kernel<D, G>, kFinThreads, dyn) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_work_kernel<D, G>, kSxThreads, dyn) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
     return per_cu * cus;
@@ -799,6 +916,16 @@ hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, 
         (d.arrive && (d.part_count != d.n_comp + items || d.part_count * g.G > kMergeMaxTerms)))
         return hipErrorInvalidValue;
     return g.D == 128 ? sx_g<128>(g, a, d, items, s) : sx_g<64>(g, a, d, items, s);
+}
+hipError_t launch_select_work(const Geom& g, ScoreArgs a, const DecodeArgs& d, int P, hipStream_t s) {
+    a.keys_in_lds = 1;
+    const int keff = std::max(1, std::min(a.K, g.xmax()));
+    if (P < 2 || g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb < 1 || d.eb > kMaxEb ||
+        (long long)P * d.eb < keff || finalize_dyn_lds(g, a) > kDynBudget || !d.arrive || !d.sel_word || !d.mailbox ||
+        (d.n_comp != 0 && (d.n_comp != P - 1 || d.cb < 1 || d.cb > kStepCbMax || (long long)d.n_comp * d.cb < g.xmax())) ||
+        d.part_base != d.n_comp || d.part_count != d.n_comp + P || d.part_count * g.G > kMergeMaxTerms)
+        return hipErrorInvalidValue;
+    return g.D == 128 ? work_g<128>(g, a, d, P, s) : work_g<64>(g, a, d, P, s);
 }
 int select_one_group_terms() { return kUnitTerms; }
 int select_one_group_auto_blocks() { return kUnitBatch * kFinThreads / 8; }

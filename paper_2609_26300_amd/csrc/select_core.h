@@ -151,7 +151,7 @@ __device__ inline SelectCtx make_select_ctx(int X, int K, int n_sink, int n_rece
     return c;
 }
 
-// before the first barrier that precedes select_fast
+// before the first barrier that precedes select_fast (any workgroup of at least 256 threads)
 __device__ inline void select_init(FinalShared& sh) {
     const int tid = threadIdx.x;
     if (tid < kBitmapWords) sh.bitmap[tid] = 0u;
@@ -165,9 +165,10 @@ __device__ inline void select_init(FinalShared& sh) {
 // Fast path: the keys ck (each non-zero key held by exactly one thread; zero = no key) and this
 // thread's largest score bits mx. Returns false when too many keys tie around the cut: their bits are
 // then in c.keys and select_radix finishes.
-template <int KPT>
+template <int KPT, int FT = kFinThreads>
 __device__ bool select_fast(const SelectCtx& ctx, const unsigned long long (&ck)[KPT], uint32_t mx, FinalShared& sh) {
-    constexpr int FT = kFinThreads, NW = kFinWaves;
+    static_assert(FT >= kBitmapWords && FT <= kFinThreads && KPT * FT <= 32 * kBitmapWords, "selection shape");
+    constexpr int NW = FT / 64;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int X = ctx.X, K = ctx.K, kk = ctx.kk, sink = ctx.sink, rec_lo = ctx.rec_lo;
     const bool take_all = ctx.take_all, ranked = ctx.ranked;
@@ -230,8 +231,8 @@ __device__ bool select_fast(const SelectCtx& ctx, const unsigned long long (&ck)
             // exact rank among the candidates (order-independent); the kk best are selected. With
             // few candidates the four lanes of a quad share one.
             const int share = m <= FT / 4 ? 4 : 1;
-            const int i = tid / share, part = tid % share;
-            if (i < m) {  // quad-uniform
+            const int part = tid % share;
+            for (int i = tid / share; i < m; i += FT / share) {  // quad-uniform
                 const unsigned long long ci = sh.cand[i];
                 int r = 0;
                 int j = part;
@@ -288,8 +289,9 @@ __device__ bool select_fast(const SelectCtx& ctx, const unsigned long long (&ck)
 }
 
 // General path: radix select on the key bits of blocks [0, X), then ascending compaction.
+template <int FT = kFinThreads>
 __device__ void select_radix(const SelectCtx& c, FinalShared& sh) {
-    constexpr int FT = kFinThreads, NW = kFinWaves;
+    constexpr int NW = FT / 64;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int X = c.X, K = c.K, kk = c.kk;
     const bool take_all = c.take_all, ranked = c.ranked;
@@ -408,11 +410,13 @@ __device__ void select_radix(const SelectCtx& c, FinalShared& sh) {
 // scores (written to a.scores when write_scores) and the stable Top-K into sel_out / nsel_out (global
 // or LDS). dyn: [np][G] partial maxima, then factors; [np][G] sums; [xmax] key bits (keys_in_lds).
 // kCoh: the partials and terms were written by other workgroups of the same launch (device-coherent
-// loads, and none past the unit's blocks).
-template <int G, bool kCoh = false>
+// loads; the values of blocks past the unit's, loaded only to keep the loads in flight fixed, go unused).
+// FT threads holding up to KPT keys each (the terms of the first eight requested up front, the rest
+// once the normalizers are formed).
+template <int G, bool kCoh = false, int FT = kFinThreads, int KPT = kKeysPerThread>
 __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, FinalShared& sh, float* dyn,
                                 int32_t* sel_out, int32_t* nsel_out, bool write_scores) {
-    constexpr int FT = kFinThreads, KPT = kKeysPerThread;
+    constexpr int KB = KPT < 8 ? KPT : 8;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bseq = u / geo.hkv;
     const int xmax = geo.xmax();
@@ -420,34 +424,37 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
     const float* wu = a.ws_w + (size_t)u * xmax * G;
     const bool fast = xmax <= KPT * FT;
 
-    // ---- loads in the order of their use: the length, the partials, this thread's score terms
-    const int n = clamp_len(a.seq_lens[bseq], geo.max_seq);
-    const int X = (n + geo.B - 1) / geo.B;
+    // ---- loads in the order of their use: the length, the partials, this thread's score terms. Every
+    // load is issued, also where its value goes unused (a clamped address instead), so that the count
+    // of loads in flight is fixed and each wait below is for the loads it needs.
+    int n_raw = a.seq_lens[bseq];
     float* fac = dyn;
     float* sums = dyn + np * G;
-    const float2* pu = reinterpret_cast<const float2*>(a.ws_part + (size_t)u * np * G * 2);
     const bool one_pass = np * G <= FT;  // usual case: one partial per thread
     float2 pv = make_float2(0.0f, 0.0f);
-    if (one_pass && tid < np * G) pv = kCoh ? ld_agent2(a.ws_part + ((size_t)u * np * G + tid) * 2) : pu[tid];
-    __asm__ volatile("" ::: "memory");
-    float w[KPT][G];
-#pragma unroll
-    for (int k = 0; k < KPT; ++k) {  // branch-free: ids past xmax load block 0, unused
-        const int b = tid + k * FT;
-        if (kCoh && k * FT >= xmax) {
-#pragma unroll
-            for (int g = 0; g < G; ++g) w[k][g] = 0.0f;
-        } else {
-            load_terms<G, kCoh>(wu, b < xmax ? b : 0, w[k]);
-        }
+    if (one_pass) {  // (workgroup-uniform)
+        const float* pp = a.ws_part + ((size_t)u * np * G + (tid < np * G ? tid : 0)) * 2;
+        pv = kCoh ? ld_agent2(pp) : *reinterpret_cast<const float2*>(pp);
     }
+    __asm__ volatile("" ::: "memory");
+    float w[KB][G];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {  // ids past xmax load block 0, unused
+        const int b = tid + k * FT;
+        load_terms<G, kCoh>(wu, b < xmax ? b : 0, w[k]);
+    }
+    // the length is read only now (a value made uniform early would wait for every load above)
+    __asm__ volatile("" : "+v"(n_raw));
+    const int n = clamp_len(n_raw, geo.max_seq);
+    const int X = (n + geo.B - 1) / geo.B;
     if (one_pass && tid < np * G) {
         fac[tid] = pv.x;
         sums[tid] = pv.y;
     }
     if (!one_pass) {
         for (int idx = tid; idx < np * G; idx += FT) {
-            const float2 t = kCoh ? ld_agent2(a.ws_part + ((size_t)u * np * G + idx) * 2) : pu[idx];
+            const float* pp = a.ws_part + ((size_t)u * np * G + idx) * 2;
+            const float2 t = kCoh ? ld_agent2(pp) : *reinterpret_cast<const float2*>(pp);
             fac[idx] = t.x;
             sums[idx] = t.y;
         }
@@ -490,20 +497,36 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
     if (fast) {
         unsigned long long ck[KPT];
         uint32_t mx = 0u;
-#pragma unroll
-        for (int k = 0; k < KPT; ++k) {
+        auto key = [&](int k, const float (&wt)[G]) {
             const int b = tid + k * FT;
             ck[k] = 0ull;
             if (b < X) {
-                const float S = score_of(b, w[k]);
+                const float S = score_of(b, wt);
                 if (write_scores && a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
                 if (!mandatory(b, X, a.n_sink, a.n_recent)) {
                     ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);
                     mx = max(mx, __float_as_uint(S));
                 }
             }
+        };
+#pragma unroll
+        for (int k = 0; k < KB; ++k) key(k, w[k]);
+        if constexpr (KPT > KB) {
+            float w2[KPT - KB][G];
+#pragma unroll
+            for (int k = KB; k < KPT; ++k) {
+                if (k * FT >= xmax) {  // (workgroup-uniform)
+#pragma unroll
+                    for (int g = 0; g < G; ++g) w2[k - KB][g] = 0.0f;
+                } else {
+                    const int b = tid + k * FT;
+                    load_terms<G, kCoh>(wu, b < xmax ? b : 0, w2[k - KB]);
+                }
+            }
+#pragma unroll
+            for (int k = KB; k < KPT; ++k) key(k, w2[k - KB]);
         }
-        if (select_fast<KPT>(sc, ck, mx, sh)) return;
+        if (select_fast<KPT, FT>(sc, ck, mx, sh)) return;
     } else {
         // ---- general path (more than 8192 blocks): scores and their bits into the key array
         for (int b = tid; b < X; b += FT) {
@@ -515,19 +538,20 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
         }
     }
     __syncthreads();
-    select_radix(sc, sh);
+    select_radix<FT>(sc, sh);
 }
 
 constexpr int kSxWaves = kFinThreads / 64;
 constexpr int kSelLdsMax = 1024;  // budget limit of the fused kernel (ids held in LDS)
 constexpr int kStepCbMax = 1024;  // blocks per compensation workgroup of the fused launch
 
-// LDS of a workgroup that selects, attends exactly, streams mean values (at most CB blocks) or merges.
-template <int D, int G, int CB>
+// LDS of a workgroup of NW waves that selects, attends exactly, streams mean values (at most CB blocks)
+// or merges.
+template <int D, int G, int CB, int NW = kSxWaves>
 struct SelExactLdsT {
     union {
         FinalShared fin;
-        ExactLds<D, G, kSxWaves> ex;  // (compensation workgroups: their wave sums in ex.acc)
+        ExactLds<D, G, NW> ex;  // (compensation workgroups: their wave sums in ex.acc)
     } u;
     int32_t sel[kSelLdsMax];
     int32_t rowbase[kMaxEb];  // cache row of token 0 of each of the item's blocks
@@ -559,7 +583,7 @@ __device__ inline bool arrive_last(uint32_t* counter, int arrivals, int32_t& las
 // The merge of unit u's d.part_count partials in index order (so the result does not depend on which
 // workgroup runs it): per head the maximum M, the sum L of exp(m_p - M) l_p and of exp(m_p - M) acc_p,
 // then out = acc / L and lse = M + log L (NaN when `poison`).
-template <int D, int G, typename Lds>
+template <int D, int G, typename Lds, int FT = kFinThreads>
 __device__ void merge_unit(const Geom& geo, const DecodeArgs& d, int u, Lds& L, bool poison = false) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int np = d.part_count;
@@ -567,13 +591,15 @@ __device__ void merge_unit(const Geom& geo, const DecodeArgs& d, int u, Lds& L, 
     const float* pu = d.ws_part + (size_t)u * np * G * (D + 2);
     float* pm = reinterpret_cast<float*>(&L.u.fin);  // [np][G] maxima, then factors
     float* pl = pm + np * G;                         // [np][G] sums
-    const int g = tid / D, i = tid - g * D;
-    const bool mine = tid < G * D;
-    const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
+    // the first RB values of this thread's first coordinate, requested with the maxima and sums
     float x[RB];
+    {
+        const int g = tid / D, i = tid - g * D;
+        const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
 #pragma unroll
-    for (int k = 0; k < RB; ++k) x[k] = (mine && k < np) ? ld_agent(pi + (size_t)k * G * (D + 2)) : 0.0f;
-    for (int t = tid; t < np * G; t += kFinThreads) {
+        for (int k = 0; k < RB; ++k) x[k] = (tid < G * D && k < np) ? ld_agent(pi + (size_t)k * G * (D + 2)) : 0.0f;
+    }
+    for (int t = tid; t < np * G; t += FT) {
         const float* q = pu + (size_t)t * (D + 2);
         pm[t] = ld_agent(q);
         pl[t] = ld_agent(q + 1);
@@ -597,10 +623,13 @@ __device__ void merge_unit(const Geom& geo, const DecodeArgs& d, int u, Lds& L, 
         }
     }
     __syncthreads();
-    if (mine) {
+    // coordinate i of head g: the partials' values in index order, RB requested at a time
+    for (int idx = tid; idx < G * D; idx += FT) {
+        const int g = idx / D, i = idx - g * D;
+        const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
         float A = 0.0f;
         for (int p0 = 0; p0 < np; p0 += RB) {
-            if (p0 > 0) {
+            if (p0 > 0 || idx != tid) {
 #pragma unroll
                 for (int k = 0; k < RB; ++k) x[k] = p0 + k < np ? ld_agent(pi + (size_t)(p0 + k) * G * (D + 2)) : 0.0f;
             }
@@ -617,48 +646,78 @@ __device__ void merge_unit(const Geom& geo, const DecodeArgs& d, int u, Lds& L, 
 }
 
 // The fused selection/exact launch: count the arrival; the unit's last workgroup merges.
-template <int D, int G, typename Lds>
+template <int D, int G, typename Lds, int FT = kFinThreads>
 __device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, Lds& L) {
-    if (arrive_last(d.arrive + u, d.part_count, L.last)) merge_unit<D, G>(geo, d, u, L);
+    if (arrive_last(d.arrive + u, d.part_count, L.last)) merge_unit<D, G, Lds, FT>(geo, d, u, L);
 }
 
-// One compensation workgroup of a fused launch (see above): blocks [c0, c1) of unit u with n tokens,
-// ROWS mean-value rows in flight per thread. `ready` runs once the first rows are requested and before
-// the block logits are read (kCoh: device-coherent loads of block logits written in the same launch).
-template <int D, int G, int ROWS, bool kCoh, typename Lds, typename Ready>
-__device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, int n, int c0, int c1, Lds& L,
-                                  float* part, Ready&& ready) {
-    constexpr int NT = kFinThreads;
-    constexpr int LPB = D / 4;               // lanes per mean-value row (one float4 each)
-    constexpr int RPS = NT / LPB;            // rows per workgroup step
+// One compensation workgroup of a fused launch: blocks [c0, c1) (at most kStepCbMax, within the unit's
+// xmax; the blocks past the sequence's last contribute nothing) of unit u, whose sequence length n_raw
+// was requested before the call and is read only once the loads below are requested (a value made
+// uniform right away would wait for its load). The block logits zbar are requested first (loads return
+// in order, so they arrive ahead
+// of the mean values); then the mean-value rows in batches of NT / (D / 4) * ROWS rows, each batch
+// requested two batches ahead of its use (two register buffers of ROWS rows per thread), so that a
+// batch is in flight while another is weighed. While the first two batches are in flight: the pseudo-
+// logits log|b| + zbar and their per-head softmax weights (in LDS). `after` runs once the last mean
+// values have arrived, before the partial is reduced and stored (loads it issues are not queued behind
+// mean values).
+template <int D, int G, int ROWS, typename Lds, int NT = kFinThreads, typename After>
+__device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, int n_raw, int c0, int c1, Lds& L,
+                                  float* part, After&& after) {
+    constexpr int LPB = D / 4;     // lanes per mean-value row (one float4 each)
+    constexpr int RPS = NT / LPB;  // rows per workgroup step
+    constexpr int BATCH = RPS * ROWS;
+    constexpr int ZR = (kStepCbMax + NT - 1) / NT;  // block logits per thread and head
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nb = max(0, c1 - c0);
+    const int nb = max(0, min(c1 - c0, kStepCbMax));
     const int li = tid % LPB, slot = tid / LPB;
-    // this thread's first rows before anything else (branch-free: a slot past the range reloads the
-    // range's first row, weighted by zero)
-    const float4* vm = reinterpret_cast<const float4*>(d.vmean + ((size_t)u * geo.xcap + c0) * D) + li;
-    float4 v[ROWS];
+    const float* lg = d.blk_logit + (size_t)u * G * geo.xcap + c0;
+    float zl[G][ZR];
 #pragma unroll
-    for (int k = 0; k < ROWS; ++k) {
-        const int lb = slot + k * RPS;
-        v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
-    }
-    ready();
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int k = 0; k < ZR; ++k) {
+            const int lb = tid + k * NT;
+            zl[g][k] = lb < nb ? lg[(size_t)g * geo.xcap + lb] : 0.0f;
+        }
+    // (an empty range reads row 0 of the unit, unused)
+    const float4* vm = reinterpret_cast<const float4*>(d.vmean + ((size_t)u * geo.xcap + (nb > 0 ? c0 : 0)) * D) + li;
+    float4 va[ROWS], vb[ROWS];
+    // branch-free within a batch: a row past the range reloads the range's first row, weighted by zero
+    auto issue = [&](int base, float4 (&v)[ROWS]) {
+#pragma unroll
+        for (int k = 0; k < ROWS; ++k) {
+            const int lb = base + slot + k * RPS;
+            v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
+        }
+    };
+    // every wave's block logits are requested before any wave's mean values (a barrier that waits for
+    // no load): the returns of a CU come back in request order, so the logits then arrive first
+    __builtin_amdgcn_s_barrier();
+    // every batch is requested, also past the range (then row 0 again): the number of loads in flight
+    // stays fixed, so each wait below is for one batch, never for all of them
+    issue(0, va);
+    issue(BATCH, vb);
+    __asm__ volatile("" : "+v"(n_raw));
+    const int n = clamp_len(n_raw, geo.max_seq);
+    const int nv = max(0, min(nb, (n + geo.B - 1) / geo.B - c0));  // blocks of the range in the sequence
     // pseudo-logits log|b| + zbar, then per head (wave g) their max and the weights exp(. - max)
-    const float* lg = d.blk_logit + (size_t)u * G * geo.xcap;
-    for (int idx = tid; idx < G * nb; idx += NT) {
-        const int g = idx / nb, lb = idx - g * nb, b = c0 + lb;
-        const float z = kCoh ? ld_agent(lg + (size_t)g * geo.xcap + b) : lg[(size_t)g * geo.xcap + b];
-        L.cw[g][lb] = logf((float)min(geo.B, n - b * geo.B)) + z;
-    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int k = 0; k < ZR; ++k) {
+            const int lb = tid + k * NT, b = c0 + lb;
+            if (lb < nv) L.cw[g][lb] = logf((float)min(geo.B, n - b * geo.B)) + zl[g][k];
+        }
     __syncthreads();
     if (wave < G) {
         const int g = wave;
         float mx = -INFINITY;
-        for (int lb = lane; lb < nb; lb += 64) mx = fmaxf(mx, L.cw[g][lb]);
+        for (int lb = lane; lb < nv; lb += 64) mx = fmaxf(mx, L.cw[g][lb]);
         mx = wave_max(mx);
         float sum = 0.0f;
-        for (int lb = lane; lb < nb; lb += 64) {
+        for (int lb = lane; lb < nv; lb += 64) {
             const float wv = __expf(L.cw[g][lb] - mx);
             L.cw[g][lb] = wv;
             sum += wv;
@@ -674,18 +733,11 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
     float acc[G][4];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = acc[g][2] = acc[g][3] = 0.0f;
-    for (int lb0 = slot; lb0 < nb; lb0 += RPS * ROWS) {
-        if (lb0 != slot) {
-#pragma unroll
-            for (int k = 0; k < ROWS; ++k) {
-                const int lb = lb0 + k * RPS;
-                v[k] = vm[(size_t)(lb < nb ? lb : 0) * (D / 4)];
-            }
-        }
+    auto weigh = [&](int base, const float4 (&v)[ROWS]) {
 #pragma unroll
         for (int k = 0; k < ROWS; ++k) {
-            const int lb = lb0 + k * RPS;
-            if (lb < nb) {
+            const int lb = base + slot + k * RPS;
+            if (lb < nv) {
 #pragma unroll
                 for (int g = 0; g < G; ++g) {
                     const float wv = L.cw[g][lb];
@@ -696,7 +748,17 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
                 }
             }
         }
+    };
+    int base = 0;
+    for (; base + 2 * BATCH < nv; base += 2 * BATCH) {  // workgroup-uniform
+        weigh(base, va);
+        issue(base + 2 * BATCH, va);
+        weigh(base + BATCH, vb);
+        issue(base + 3 * BATCH, vb);
     }
+    weigh(base, va);
+    weigh(base + BATCH, vb);
+    after();
     // the row slots of a wave (lanes li, li + LPB, ...), then the waves in order
 #pragma unroll
     for (int off = LPB; off < 64; off <<= 1)
@@ -719,7 +781,7 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
         }
         float tot = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kSxWaves; ++w) tot += L.u.ex.acc[w][g][i];
+        for (int w = 0; w < NT / 64; ++w) tot += L.u.ex.acc[w][g][i];
         st_agent(p + 2 + i, tot);
     }
 }

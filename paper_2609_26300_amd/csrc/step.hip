@@ -520,16 +520,8 @@ __device__ void step_exact(const Geom& geo, const ScoreArgs& a, const DecodeArgs
     v4f32 acc[D / 16];
     const uint16_t* qh = d.q + ((size_t)bseq * geo.hq + (size_t)h * G) * D;
     const bool pseudo = d.neg_pseudo != 0;  // Mean: the compensation counted every block's pseudo-token
-    exact_tokens<D, G, kSxWaves>(tm, d.K, d.V, qh, pseudo ? L.u.ex.zb : nullptr, d.scale, m, l, acc, [&] {
-        if (!pseudo) return;  // workgroup-uniform
-        const float* lg = d.blk_logit + (size_t)u * G * geo.xcap;
-        for (int idx = tid; idx < G * tm.nblk; idx += kFinThreads) {
-            const int g = idx / tm.nblk, k = idx - g * tm.nblk;
-            const int b = tm.sel[k];
-            L.u.ex.zb[g][k] = ld_agent(lg + (size_t)g * geo.xcap + (b >= 0 && b < X ? b : 0));
-        }
-        __syncthreads();
-    });
+    exact_tokens<D, G, kSxWaves>(tm, d.K, d.V, qh, pseudo ? d.blk_logit + (size_t)u * G * geo.xcap : nullptr,
+                                 geo.xcap, L.u.ex.zb, d.scale, m, l, acc);
     float* part = d.ws_part + ((size_t)u * d.part_count + d.part_base + item) * G * (D + 2);
     finish_exact<D, G, kSxWaves, true>(m, l, acc, L.u.ex, part);
 }

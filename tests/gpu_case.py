@@ -289,6 +289,9 @@ CASES = {
     "wide_gqa_8k": lambda: Case(WORKLOADS["wide_gqa_64k"].with_(batch=2, context=8192, seed=18)),
     "long_16k_lognormal": lambda: Case(WORKLOADS["long_128k"].with_(batch=1, context=16384, budget_blocks=32,
                                                                     seed=19)),
+    # more mean-value rows than selected tokens per unit (the fused launch's form with compensation
+    # workgroups); the cases above with a budget of at least X / B blocks take its one-selector form
+    "long_16k_b8": lambda: Case(WORKLOADS["long_128k"].with_(batch=2, context=16384, budget_blocks=8, seed=31)),
     # selection paths: > 8192 blocks (keys outside registers), ~1000 candidates ranked by brute force,
     # and ~2000 candidates (radix select fallback)
     "block1_9000": lambda: Case(TINY.with_(context=9000, block_size=1, budget_blocks=40, seed=25)),
