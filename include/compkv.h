@@ -271,6 +271,19 @@ int compkv_decode_step_noalloc(const compkv_dims* dims, const compkv_select_para
 /* Bytes of the fixed scratch behind compkv_decode_step_noalloc. */
 size_t compkv_decode_step_noalloc_limit(void);
 
+/*
+ * Phase trace of compkv_decode_step (for measurement; a library built with -DCOMPKV_PHASE_TRACE, which
+ * paper_2609_26300_amd/build.py writes as libcompkv_trace.so): on the chunked-exact launch shape, thread 0
+ * of every workgroup of the chunk-scoring launch and of the fused selection/exact launch stores the GPU's
+ * 100 MHz real-time counter at its phase boundaries, and its role, into 16 64-bit words per workgroup
+ * (workgroup w at words 16 w .. 16 w + 15; the slot meanings are listed beside each kernel). chunk_records
+ * and fused_records are device arrays of at least 16 words per workgroup of the respective launch, written
+ * by every later compkv_decode_step until this is called again with null pointers (which stops the
+ * trace). The caller owns the arrays and keeps them alive while traced steps run. Returns COMPKV_OK, or
+ * COMPKV_EUNSUPPORTED from a library built without the trace (its kernels hold no marks).
+ */
+int compkv_phase_trace_set(void* chunk_records, void* fused_records);
+
 /* The launch shape compkv_decode_step takes for these dims and params on the current device:
  * COMPKV_SELECT_ONE_GROUP, COMPKV_SELECT_CHUNKED or COMPKV_SELECT_CHUNKED_EXACT (params->select_path
  * resolved), or a negative status (invalid dims or path). Enqueues nothing. */

@@ -35,6 +35,7 @@ from .binding import (  # noqa: F401
     compkv_decode_step,
     compkv_decode_step_noalloc,
     compkv_decode_step_noalloc_limit,
+    compkv_phase_trace_set,
     compkv_decode_step_path,
     compkv_dense_decode,
     compkv_score_select,

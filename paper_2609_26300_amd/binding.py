@@ -113,6 +113,8 @@ def library():
         L.compkv_decode_step_noalloc_limit.argtypes = []
         L.compkv_decode_step_noalloc_limit.restype = ctypes.c_size_t
         L.compkv_decode_step_path.argtypes = [dp, ctypes.POINTER(CompkvSelectParams)]
+        L.compkv_phase_trace_set.argtypes = [_vp, _vp]
+        L.compkv_phase_trace_set.restype = ctypes.c_int
         L.compkv_host_cache_pointer.argtypes = [_vp, ctypes.POINTER(ctypes.c_void_p)]
         L.compkv_host_cache_pointer.restype = ctypes.c_int
         L.compkv_workspace_bytes.argtypes = [dp, _i32, _i32]
@@ -356,6 +358,20 @@ def compkv_decode_step_noalloc(dims, params: CompkvSelectParams, q, k_cache, v_c
 
 def compkv_decode_step_noalloc_limit() -> int:
     return int(library().compkv_decode_step_noalloc_limit())
+
+
+def compkv_phase_trace_set(chunk_records=None, fused_records=None) -> None:
+    """Phase-trace records of the fused step's two launches (int64 device tensors of at least 16 words per
+    workgroup), or None for both to stop tracing. Raises on a library built without the trace."""
+    ptrs = []
+    for t_, name in ((chunk_records, "chunk_records"), (fused_records, "fused_records")):
+        if t_ is None:
+            ptrs.append(None)
+            continue
+        if t_.dtype != torch.int64 or not t_.is_cuda or not t_.is_contiguous():
+            raise CompkvError(f"{name} must be a contiguous int64 device tensor")
+        ptrs.append(ctypes.c_void_p(t_.data_ptr()))
+    _check(library().compkv_phase_trace_set(*ptrs), "compkv_phase_trace_set")
 
 
 def default_scale(head_dim: int) -> float:

@@ -38,21 +38,29 @@ def _run(cmd, verbose):
     return res
 
 
-def build(verbose: bool = False, jobs: int = 4) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+TRACE_LIB = os.path.join(PKG, "libcompkv_trace.so")
+
+
+def build(verbose: bool = False, jobs: int = 4, trace: bool = False) -> str:
+    """libcompkv.so, or with trace=True libcompkv_trace.so: the same library with the phase marks of the
+    fused step compiled in (-DCOMPKV_PHASE_TRACE; see compkv_phase_trace_set)."""
+    out_dir = os.path.join(BUILD, "trace") if trace else BUILD
+    lib = TRACE_LIB if trace else LIB
+    flags = FLAGS + (["-DCOMPKV_PHASE_TRACE"] if trace else [])
+    os.makedirs(out_dir, exist_ok=True)
 
     def compile_one(src):
-        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-        _run([HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        obj = os.path.join(out_dir, os.path.splitext(src)[0] + ".o")
+        _run([HIPCC, *flags, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
         return obj
 
     with ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB + f".tmp{os.getpid()}"
+    tmp = lib + f".tmp{os.getpid()}"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, trace="--trace" in sys.argv))

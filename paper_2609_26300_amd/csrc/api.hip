@@ -140,6 +140,10 @@ size_t dense_ws(const Geom& g) {
     return align_up((size_t)g.units() * sh.items * g.G * (g.D + 2) * sizeof(float));
 }
 
+// phase-trace build: the record arrays of the fused step's two launches (null: not traced)
+unsigned long long* g_trace_chunks = nullptr;
+unsigned long long* g_trace_fused = nullptr;
+
 struct SxShape {  // the fused step's selection + exact launch (sx_shape below)
     int eb, n_exact;
     int cb, n_comp;  // its compensation workgroups: blocks each, workgroups per unit
@@ -681,6 +685,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         if (step_part_bytes(g, nparts) > part_bytes || step_ws(g, K) > wsb_bytes)
             return COMPKV_EWORKSPACE;  // sizing invariant
         a.arrive_zero = arrive;
+        a.trace = g_trace_chunks;
         a.comp_part = nullptr;
         a.part_count = nparts;
         a.chunks_only = 1;
@@ -712,6 +717,8 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.sel_word = arrive + g.units();
         d.mailbox = arrive + 2 * (size_t)g.units();
         d.timeouts = state;
+        d.trace = g_trace_fused;
+        a.trace = g_trace_fused;  // (the selection's marks, in the fused launch's records)
         if (work) return launch_status(compkv::launch_select_work(g, a, d, sx.P, s));
         return launch_status(compkv::launch_select_exact(g, a, d, sx.n_exact, s));
     }
@@ -752,6 +759,18 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     e = compkv::launch_decode_items(g, d, n_ex, s);
     if (e != hipSuccess) return COMPKV_EHIP;
     return launch_status(compkv::launch_decode_merge(g, d, nparts, s));
+}
+
+int compkv_phase_trace_set(void* chunk_records, void* fused_records) {
+#ifdef COMPKV_PHASE_TRACE
+    g_trace_chunks = static_cast<unsigned long long*>(chunk_records);
+    g_trace_fused = static_cast<unsigned long long*>(fused_records);
+    return COMPKV_OK;
+#else
+    (void)chunk_records;
+    (void)fused_records;
+    return COMPKV_EUNSUPPORTED;
+#endif
 }
 
 size_t compkv_decode_step_noalloc_limit(void) { return kScratchBytes; }

@@ -38,6 +38,45 @@ struct StatsArgs {
     float* vmean;
 };
 
+// Phase trace (a library built with -DCOMPKV_PHASE_TRACE; the marks compile to nothing otherwise):
+// thread 0 of workgroup w of a traced launch stores the 100 MHz real-time counter at the phase
+// boundaries into trace[w * kTraceSlots + slot] (slots per kernel: the kernel's own comment), and a
+// role or count into the value slots. Only the fused step's two launches are traced.
+constexpr int kTraceSlots = 16;
+#ifdef COMPKV_PHASE_TRACE
+#define COMPKV_MARK(buf, slot)                                                                           \
+    do {                                                                                                 \
+        if ((buf) != nullptr && threadIdx.x == 0)                                                        \
+            (buf)[(size_t)blockIdx.x * ::compkv::kTraceSlots + (slot)] = __builtin_amdgcn_s_memrealtime(); \
+    } while (0)
+#define COMPKV_MARK_VALUE(buf, slot, v)                                                                  \
+    do {                                                                                                 \
+        if ((buf) != nullptr && threadIdx.x == 0)                                                        \
+            (buf)[(size_t)blockIdx.x * ::compkv::kTraceSlots + (slot)] = (unsigned long long)(v);        \
+    } while (0)
+// the start stamp is held (scalar registers) and stored with the end stamp: a store at the very start
+// would keep the first loads from being scheduled ahead of it
+#define COMPKV_TRACE_START() const unsigned long long compkv_trace_t0_ = __builtin_amdgcn_s_memrealtime()
+#define COMPKV_TRACE_END(buf)                   \
+    do {                                        \
+        COMPKV_MARK_VALUE(buf, 0, compkv_trace_t0_); \
+        COMPKV_MARK(buf, 15);                   \
+    } while (0)
+#else
+#define COMPKV_TRACE_START() \
+    do {                     \
+    } while (0)
+#define COMPKV_TRACE_END(buf) \
+    do {                      \
+    } while (0)
+#define COMPKV_MARK(buf, slot) \
+    do {                       \
+    } while (0)
+#define COMPKV_MARK_VALUE(buf, slot, v) \
+    do {                                \
+    } while (0)
+#endif
+
 struct ScoreArgs {
     const uint16_t* q;
     const float* kmean;
@@ -71,6 +110,7 @@ struct ScoreArgs {
     int tail_first;         // set by the launcher: the last-block workgroups lead the grid (else trail)
     uint32_t* arrive_zero;  // nullable: [2][units] words (arrivals, selection words), then [units][K]
                             // (mailbox), that the last-block workgroups zero
+    unsigned long long* trace;  // phase-trace build only: [grid][kTraceSlots] timestamps, or null
 };
 
 struct DecodeArgs {
@@ -104,6 +144,7 @@ struct DecodeArgs {
     uint32_t* sel_word;  // one-selector fused launch: per-unit selection words (zeroed by the chunk launch)
     uint32_t* mailbox;   // one-selector fused launch: [units][K] posted ids (zeroed by the chunk launch)
     uint32_t* timeouts;  // per-unit words [units][4] at the start of the workspace (word 3 counts timeouts)
+    unsigned long long* trace;  // phase-trace build only: [grid][kTraceSlots] timestamps, or null
 };
 
 // ------------------------------------------------------------------ launchers (one per kernel family)

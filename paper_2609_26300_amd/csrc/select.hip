@@ -179,18 +179,24 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     }
 }
 
-// PMAX = bpc / 32: block slots per thread (the chunk is 32 PMAX blocks).
+// PMAX = bpc / 32: block slots per thread (the chunk is 32 PMAX blocks). Phase-trace slots: 0 start,
+// 1 role (1 chunk, 2 last block), 2 query in LDS, 3 first slot computed, 4 every slot computed,
+// 6 stores begin, 15 end.
 template <int D, int G, bool kStep, int PMAX>
 __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreArgs a) {
     constexpr int NB = chunk_slots<PMAX>();
     static_assert(NB % 64 == 0 && NB >= 32 * PMAX, "per-block rows must cover the chunk and whole waves");
     __shared__ ChunkLds<D, G, kStep, NB> lds;
     const int units = geo.units();
+    COMPKV_TRACE_START();
     const int tail = a.tail_first ? (int)blockIdx.x : (int)blockIdx.x - units * a.nchunks;
     if (tail >= 0 && tail < units) {
+        COMPKV_MARK_VALUE(a.trace, 1, 2);
         score_tail<D, G, kStep>(geo, a, tail, lds.t);
+        COMPKV_TRACE_END(a.trace);
         return;
     }
+    COMPKV_MARK_VALUE(a.trace, 1, 1);
     const int ck = a.tail_first ? (int)blockIdx.x - units : (int)blockIdx.x;
     constexpr int NF4 = D / 32;           // float4 of the mean-key row per lane
     constexpr int LPB = D / 4;            // compensation: lanes per mean-value row (one float4 each)
@@ -229,6 +235,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     const int xs = X - 1;  // blocks [0, X - 1) are scored here (all full); the last one by the extra workgroup
     const float logB = logf((float)geo.B);
     __syncthreads();
+    COMPKV_MARK(a.trace, 2);  // the query in LDS
     // a rolling window of two slots: slot p + 2 is requested once slot p is computed
     float4 kv[2][NF4];
     float dv0[2];
@@ -297,7 +304,9 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             }
         }
         if (p + 2 < PMAX) issue(p + 2, w);
+        if (p == 0) COMPKV_MARK(a.trace, 3);  // the first slot computed
     }
+    COMPKV_MARK(a.trace, 4);  // every slot computed
     if (comp) {  // mean-value rows, requested once the mean keys are consumed
         const float4* vm = reinterpret_cast<const float4*>(a.vmean + (size_t)u * geo.xcap * D) + vli;
 #pragma unroll
@@ -361,6 +370,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
         }
     }
     __syncthreads();
+    COMPKV_MARK(a.trace, 6);  // the chunk's partials formed: stores
     // coalesced stores: block logits [g][b] (when requested) and score terms [b][g]
     for (int idx = tid; a.blk_logit && idx < G * nvalid; idx += kThreads) {
         const int g = idx / nvalid, lb = idx % nvalid;
@@ -414,6 +424,7 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
             p[2 + i] = st.acc[0][g][i] + st.acc[1][g][i] + st.acc[2][g][i] + st.acc[3][g][i];
         }
     }
+    COMPKV_TRACE_END(a.trace);
 }
 
 template <int G>
@@ -673,7 +684,9 @@ __device__ void sx_exact(const Geom& geo, const DecodeArgs& d, int u, int n, con
     const bool pseudo = d.neg_pseudo != 0;  // Mean: the compensation added every block's pseudo-token
     exact_tokens<D, G, NW>(tm, d.K, d.V, qh, pseudo ? d.blk_logit + (size_t)u * G * geo.xcap : nullptr, geo.xcap,
                            L.u.ex.zb, d.scale, m, l, acc);
+    COMPKV_MARK(d.trace, 8);  // this wave 0's tiles attended
     finish_exact<D, G, NW, true>(m, l, acc, L.u.ex, d.ws_part + ((size_t)u * d.part_count + part) * G * (D + 2));
+    COMPKV_MARK(d.trace, 9);  // partial stored
 }
 
 template <int D, int G, int FT, int KPT>
@@ -684,8 +697,10 @@ __global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a,
     extern __shared__ float dyn[];
     const int tid = threadIdx.x;
     const int units = geo.units();
+    COMPKV_TRACE_START();
     int u, item;
     if ((int)blockIdx.x >= items * units) {  // a compensation workgroup (workgroup-uniform)
+        COMPKV_MARK_VALUE(d.trace, 1, 2);
         int c;
         xcd_unit_work((int)blockIdx.x - items * units, units, d.n_comp, u, c);
         const int xmax = geo.xmax();
@@ -693,14 +708,18 @@ __global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a,
         step_compensation<D, G, kCompRows, Lds, FT>(geo, d, u, d.seq_lens[u / geo.hkv], c0, c1, L,
                                                           d.ws_part + ((size_t)u * d.part_count + c) * G * (D + 2),
                                                           [] {});
+        COMPKV_MARK(d.trace, 9);
         if (d.arrive) arrive_and_merge<D, G, Lds, FT>(geo, d, u, L);
+        COMPKV_TRACE_END(d.trace);
         return;
     }
+    COMPKV_MARK_VALUE(d.trace, 1, 1);
     // the items of unit u all on XCD u % kXcds: the unit's selection inputs are fetched once into
     // that XCD's L2
     xcd_unit_work(blockIdx.x, units, items, u, item);
     finalize_select<G, false, FT, KPT>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
     __syncthreads();
+    COMPKV_MARK(d.trace, 4);  // selected
     const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
     const int nsel = L.nsel;
     if (item == 0) {  // the selection outputs (the ids past n_sel hold -1)
@@ -710,6 +729,7 @@ __global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a,
     const int e0 = item * d.eb;
     sx_exact<D, G, NW>(geo, d, u, n, L.sel + e0, max(0, min(d.eb, nsel - e0)), d.part_base + item, L);
     if (d.arrive) arrive_and_merge<D, G, Lds, FT>(geo, d, u, L);
+    COMPKV_TRACE_END(d.trace);
 }
 
 // ---------------------------------------------------------------- selection + exact, one selector
@@ -725,6 +745,9 @@ __global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a,
 // over those ids. Exact partials follow the P - 1 compensation partials (none under Drop); the unit's
 // last workgroup of P merges them all. The HBM streams from the start on every CU but the
 // selectors', and the selection runs once per unit.
+// Phase-trace slots (both forms of the fused launch): 0 start, 1 role (1 selects, 2 streams mean values
+// first), 2 the selection's loads in, 3 keys formed, 4 selected, 5 compensation weights formed, 6 mean
+// values weighed, 7 ids in hand (worker), 8 wave 0's tiles attended, 9 partial stored, 10 merges, 15 end.
 constexpr uint32_t kPosted = 0x80000000u;  // mailbox value of id b: b ^ kPosted (-1 gives 0x7FFFFFFF)
 constexpr uint32_t kSelFailed = 1u;        // selection word: a worker's wait timed out
 constexpr int kSelSpinLimit = 1 << 17;     // polls of a wait (each a memory round trip): well over 50 ms
@@ -737,6 +760,7 @@ __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, Score
     extern __shared__ float dyn[];
     const int tid = threadIdx.x;
     const int units = geo.units();
+    COMPKV_TRACE_START();
     int u, w;
     if ((int)blockIdx.x < units) {
         u = blockIdx.x;  // (XCD blockIdx % 8 = u % 8)
@@ -747,9 +771,11 @@ __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, Score
     }
     uint32_t* word = d.sel_word + u;
     uint32_t* mbox = d.mailbox + (size_t)u * a.K;
+    COMPKV_MARK_VALUE(d.trace, 1, w == 0 ? 1 : 2);
     if (w == 0) {
         finalize_select<G, false, FT, kSxKeys>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, true);
         __syncthreads();
+        COMPKV_MARK(d.trace, 4);  // selected
         for (int k = tid; k < a.K; k += FT) {
             const int32_t b = L.sel[k];
             st_agent_u32(mbox + k, (uint32_t)b ^ kPosted);
@@ -787,12 +813,15 @@ __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, Score
             if (d.timeouts) __hip_atomic_fetch_add(d.timeouts + 4 * u + 3, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         __syncthreads();
+        COMPKV_MARK(d.trace, 7);  // the ids in hand
         sx_exact<D, G, NW>(geo, d, u, n, L.sel, nblk, d.part_base + w, L);
     }
     if (arrive_last(d.arrive + u, P, L.last)) {
+        COMPKV_MARK(d.trace, 10);  // this workgroup merges
         const bool failed = (ld_agent_u32(word) & kSelFailed) != 0;  // (workgroup-uniform)
         merge_unit<D, G, Lds, FT>(geo, d, u, L, failed);
     }
+    COMPKV_TRACE_END(d.trace);
 }
 
 template <int D, int G, bool kStep, int PMAX>

@@ -461,6 +461,7 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
     }
     select_init(sh);
     __syncthreads();
+    COMPKV_MARK(a.trace, 2);  // the selection's loads are in
     // ---- wave g: head g's log normalizer over every block, then each partial's factor exp(m_c - lse)
     if (wave < G) {
         const int g = wave;
@@ -526,6 +527,7 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
 #pragma unroll
             for (int k = KB; k < KPT; ++k) key(k, w2[k - KB]);
         }
+        COMPKV_MARK(a.trace, 3);  // normalizers and keys formed
         if (select_fast<KPT, FT>(sc, ck, mx, sh)) return;
     } else {
         // ---- general path (more than 8192 blocks): scores and their bits into the key array
@@ -648,7 +650,10 @@ __device__ void merge_unit(const Geom& geo, const DecodeArgs& d, int u, Lds& L, 
 // The fused selection/exact launch: count the arrival; the unit's last workgroup merges.
 template <int D, int G, typename Lds, int FT = kFinThreads>
 __device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, Lds& L) {
-    if (arrive_last(d.arrive + u, d.part_count, L.last)) merge_unit<D, G, Lds, FT>(geo, d, u, L);
+    if (arrive_last(d.arrive + u, d.part_count, L.last)) {
+        COMPKV_MARK(d.trace, 10);  // this workgroup merges
+        merge_unit<D, G, Lds, FT>(geo, d, u, L);
+    }
 }
 
 // One compensation workgroup of a fused launch: blocks [c0, c1) (at most kStepCbMax, within the unit's
@@ -729,6 +734,7 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
         }
     }
     __syncthreads();
+    COMPKV_MARK(d.trace, 5);  // weights formed
     // weighted mean values; lane li of a row slot holds coordinates 4 li .. 4 li + 3
     float acc[G][4];
 #pragma unroll
@@ -758,6 +764,7 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
     }
     weigh(base, va);
     weigh(base + BATCH, vb);
+    COMPKV_MARK(d.trace, 6);  // the last mean values weighed
     after();
     // the row slots of a wave (lanes li, li + LPB, ...), then the waves in order
 #pragma unroll
