@@ -57,10 +57,15 @@ constexpr int kTraceSlots = 16;
 // the start stamp is held (scalar registers) and stored with the end stamp: a store at the very start
 // would keep the first loads from being scheduled ahead of it
 #define COMPKV_TRACE_START() const unsigned long long compkv_trace_t0_ = __builtin_amdgcn_s_memrealtime()
-#define COMPKV_TRACE_END(buf)                   \
-    do {                                        \
-        COMPKV_MARK_VALUE(buf, 0, compkv_trace_t0_); \
-        COMPKV_MARK(buf, 15);                   \
+// slot 14: where the workgroup ran (XCC id << 32 | the HW_ID register: CU, SIMD, wave slot)
+#define COMPKV_TRACE_END(buf)                                                          \
+    do {                                                                               \
+        unsigned compkv_hw_ = 0, compkv_xcc_ = 0;                                      \
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(compkv_hw_));        \
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(compkv_xcc_));      \
+        COMPKV_MARK_VALUE(buf, 14, ((unsigned long long)compkv_xcc_ << 32) | compkv_hw_); \
+        COMPKV_MARK_VALUE(buf, 0, compkv_trace_t0_);                                   \
+        COMPKV_MARK(buf, 15);                                                          \
     } while (0)
 #else
 #define COMPKV_TRACE_START() \

@@ -582,24 +582,36 @@ __device__ inline bool arrive_last(uint32_t* counter, int arrivals, int32_t& las
     return last != 0;
 }
 
-// The merge of unit u's d.part_count partials in index order (so the result does not depend on which
-// workgroup runs it): per head the maximum M, the sum L of exp(m_p - M) l_p and of exp(m_p - M) acc_p,
-// then out = acc / L and lse = M + log L (NaN when `poison`).
+// The merge of unit u's d.part_count partials (the result does not depend on which workgroup runs it):
+// per head the maximum M, the sum L of exp(m_p - M) l_p and of exp(m_p - M) acc_p, then out = acc / L
+// and lse = M + log L (NaN when `poison`). SPLIT = FT / (G d) threads share a coordinate: thread h of
+// a coordinate adds partials h, h + SPLIT, ... in that order (RB of them requested per round, the first
+// round with the maxima and sums), then the SPLIT sums are added in h order (in the compensation
+// weights' LDS, free by then), so a unit of up to SPLIT RB partials costs one memory round trip.
 template <int D, int G, typename Lds, int FT = kFinThreads>
 __device__ void merge_unit(const Geom& geo, const DecodeArgs& d, int u, Lds& L, bool poison = false) {
+    constexpr int GD = G * D;
+    constexpr int SPLIT = GD >= FT ? 1 : FT / GD;
+    static_assert(SPLIT == 1 || SPLIT * GD <= (int)(sizeof(L.cw) / sizeof(float)), "split sums fit in LDS");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int np = d.part_count;
-    constexpr int RB = 16;  // partial values requested per round
+    constexpr int RB = 16;  // partial values requested per round and thread
     const float* pu = d.ws_part + (size_t)u * np * G * (D + 2);
     float* pm = reinterpret_cast<float*>(&L.u.fin);  // [np][G] maxima, then factors
     float* pl = pm + np * G;                         // [np][G] sums
-    // the first RB values of this thread's first coordinate, requested with the maxima and sums
+    float* part_sum = &L.cw[0][0];                   // [SPLIT][G d]
+    const int h = SPLIT > 1 ? tid / GD : 0;          // this thread's share of a coordinate's partials
+    const int idx0 = SPLIT > 1 ? tid - h * GD : tid;
+    // the first round of this thread's first coordinate, requested with the maxima and sums
     float x[RB];
     {
-        const int g = tid / D, i = tid - g * D;
+        const int g = idx0 / D, i = idx0 - g * D;
         const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
 #pragma unroll
-        for (int k = 0; k < RB; ++k) x[k] = (tid < G * D && k < np) ? ld_agent(pi + (size_t)k * G * (D + 2)) : 0.0f;
+        for (int k = 0; k < RB; ++k) {
+            const int p = h + SPLIT * k;
+            x[k] = (idx0 < GD && p < np) ? ld_agent(pi + (size_t)p * G * (D + 2)) : 0.0f;
+        }
     }
     for (int t = tid; t < np * G; t += FT) {
         const float* q = pu + (size_t)t * (D + 2);
@@ -625,25 +637,46 @@ __device__ void merge_unit(const Geom& geo, const DecodeArgs& d, int u, Lds& L, 
         }
     }
     __syncthreads();
-    // coordinate i of head g: the partials' values in index order, RB requested at a time
-    for (int idx = tid; idx < G * D; idx += FT) {
+    const int bseq = u / geo.hkv, hk = u - bseq * geo.hkv;
+    auto emit = [&](int idx, float A) {  // coordinate idx of the unit's output
         const int g = idx / D, i = idx - g * D;
-        const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
-        float A = 0.0f;
-        for (int p0 = 0; p0 < np; p0 += RB) {
-            if (p0 > 0 || idx != tid) {
-#pragma unroll
-                for (int k = 0; k < RB; ++k) x[k] = p0 + k < np ? ld_agent(pi + (size_t)(p0 + k) * G * (D + 2)) : 0.0f;
-            }
-#pragma unroll
-            for (int k = 0; k < RB; ++k)
-                if (p0 + k < np) A += pm[(p0 + k) * G + g] * x[k];
-        }
-        const int bseq = u / geo.hkv, h = u - bseq * geo.hkv;
-        const size_t o = (size_t)bseq * geo.hq + (size_t)h * G + g;
+        const size_t o = (size_t)bseq * geo.hq + (size_t)hk * G + g;
         const float S = L.cl[g];
         d.out[o * D + i] = poison ? __int_as_float(0x7FC00000) : (S > 0.0f ? A / S : 0.0f);
         if (i == 0 && d.lse) d.lse[o] = poison ? __int_as_float(0x7FC00000) : (S > 0.0f ? L.cm[g] + logf(S) : -INFINITY);
+    };
+    // coordinate idx of head g: this thread's partials in order, RB requested at a time
+    for (int idx = idx0; idx < GD; idx += SPLIT > 1 ? GD : FT) {
+        const int g = idx / D, i = idx - g * D;
+        const float* pi = pu + (size_t)g * (D + 2) + 2 + i;
+        float A = 0.0f;
+        for (int p0 = 0; p0 < np; p0 += SPLIT * RB) {
+            if (p0 > 0 || idx != idx0) {
+#pragma unroll
+                for (int k = 0; k < RB; ++k) {
+                    const int p = p0 + h + SPLIT * k;
+                    x[k] = p < np ? ld_agent(pi + (size_t)p * G * (D + 2)) : 0.0f;
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < RB; ++k) {
+                const int p = p0 + h + SPLIT * k;
+                if (p < np) A += pm[p * G + g] * x[k];
+            }
+        }
+        if constexpr (SPLIT > 1)
+            part_sum[h * GD + idx] = A;
+        else
+            emit(idx, A);
+    }
+    if constexpr (SPLIT > 1) {
+        __syncthreads();
+        for (int idx = tid; idx < GD; idx += FT) {
+            float A = 0.0f;
+#pragma unroll
+            for (int s = 0; s < SPLIT; ++s) A += part_sum[s * GD + idx];
+            emit(idx, A);
+        }
     }
 }
 

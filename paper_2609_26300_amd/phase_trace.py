@@ -172,8 +172,24 @@ def main(argv=None):
             en = np.concatenate([rel(r[r[:, 1] == role][:, 15]) for r, rel in recs])
             lines.extend([f"| start (from step start) | {_pct(st)} |", f"| end (from step start) | {_pct(en)} |", ""])
 
+    def by_xcd(title, recs):
+        # end times of each XCD's workgroups (slot 14 holds the XCC id in its high word)
+        ends = {}
+        for r, rel in recs:
+            x = (r[:, 14] >> np.uint64(32)).astype(np.int64)
+            for xcd in np.unique(x):
+                ends.setdefault(int(xcd), []).append(rel(r[x == xcd][:, 15]))
+        lines.extend([f"{title}: workgroup end times per XCD", "", "| XCD | workgroups per step | p10 | p50 | p90 | max |",
+                      "|---|---|---|---|---|---|"])
+        for xcd in sorted(ends):
+            e = np.concatenate(ends[xcd])
+            lines.append(f"| {xcd} | {len(e) // len(recs)} | {_pct(e)} |")
+        lines.append("")
+
     table("Chunk-scoring launch", chunks, CHUNK_PHASES)
+    by_xcd("Chunk-scoring launch", chunks)
     table("Fused selection/exact launch", fused, FUSED_PHASES)
+    by_xcd("Fused selection/exact launch", fused)
     # the step's critical path, median over steps
     k1_end = np.median([rel(r[:, 15]).max() for r, rel in chunks])
     k2_start = np.median([rel(r[:, 0]).min() for r, rel in fused])
