@@ -1,38 +1,47 @@
-// select.hip -- block scoring and Top-K selection (Sections 4.1, 4.2; Appendix E.1). Two launches.
+// select.hip -- block scoring and Top-K selection (Sections 4.1, 4.2; Appendix E.1), and the decode
+// step's fused selection/exact launch.
 //
-// Launch 1, grid = units * (nchunks + 1). Chunk workgroups stream the fp32 summaries (mean key, grouped
-// variances) of `bpc` consecutive blocks of one unit. Eight lanes share a block: lane i of the eight
-// reads float4 i, i+8, ... of the mean-key row (the eight lanes read 128 contiguous bytes per load) and
-// the variance groups t = i, i+8, .... Every load is issued first, before the sequence length is even
-// read (block ids are clamped to the allocated range and masked afterwards). For each of the unit's G
-// query heads a workgroup forms the block-mean logit zbar = s q.kmean, the projected variance
-// sig2 = s^2 sum_t Q_t dvar_t and the log weight estimate a = log|b| + zbar + sig2/2 (the log of the
-// numerator of Eq. compkv-mass-estimate). It writes zbar (block logits, reused by the decode), the
-// chunk's per-head (max m_c of a, sum of exp(a - m_c)), and per block the G terms
-// w_g = exp(a_g - m_c) sig2_g, stored contiguously so one vector load fetches a block's terms.
-// The last block of each unit (the one a decode step appends to) is scored by one extra workgroup per
-// unit, which writes its own partial; the chunks skip it. The grid is one-dimensional. When every
-// workgroup is resident at once these lead it (ids 0 .. units-1: dispatched first, they are no longer
-// the last to finish); otherwise they trail it, so that the chunks (the long pole) all start at once and
-// the short extra workgroups take the first slots that free up.
+// Launch 1, grid = units * (nchunks + 1), one-dimensional. Chunk workgroups stream the fp32 summaries
+// (mean key, grouped variances) of `bpc` consecutive blocks of one unit. Eight lanes share a block: lane
+// i of the eight reads float4 i, i+8, ... of the mean-key row (the eight lanes read 128 contiguous bytes
+// per load) and the variance groups t = i, i+8, .... The sequence length and the query are requested
+// first and the query is in LDS before any mean key is requested (a CU returns loads in request order,
+// so a query requested after the other workgroups' mean keys would wait behind them); then two slots of
+// 32 blocks are in flight, slot p + 2 requested once slot p is computed (block ids are clamped to the
+// allocated range and masked afterwards). For each of the unit's G query heads a workgroup forms the
+// block-mean logit zbar = s q.kmean, the projected variance sig2 = s^2 sum_t Q_t dvar_t and the log
+// weight estimate a = log|b| + zbar + sig2/2 (the log of the numerator of Eq. compkv-mass-estimate). It
+// writes zbar (block logits, reused by the decode), the chunk's per-head (max m_c of a, sum of
+// exp(a - m_c)), and per block the G terms w_g = exp(a_g - m_c) sig2_g, stored contiguously so one
+// vector load fetches a block's terms. The last block of each unit (the one a decode step appends to) is
+// scored by one extra workgroup per unit, which writes its own partial; the chunks skip it. When every
+// workgroup is resident at once these lead the grid (dispatched first, they are no longer the last to
+// finish); otherwise they trail it, so that the chunks (the long pole) all start at once.
 //
 // Fused decode step (kStep): the extra workgroup first stores the new row and recomputes the last
-// block's summary with the append's routine (bit-identical), so no chunk waits for it; every workgroup
-// also forms the compensation partial of its blocks: pseudo-logits log|b| + zbar, weights
-// exp(. - max) and the weighted mean values (streamed alongside the mean keys).
+// block's summary with the append's routine (bit-identical), so no chunk waits for it, and zeroes the
+// unit's words for the fused selection/exact launch. On the chunked shape every workgroup also forms the
+// compensation partial of its blocks (pseudo-logits log|b| + zbar, weights exp(. - max), weighted mean
+// values); on the chunked-exact shape the fused launch streams the mean values instead.
 //
-// Launch 2, grid = (units): the kernel boundary makes every partial visible (no cross-workgroup fences
-// or atomics). One workgroup per unit merges the partials into each head's log normalizer lse_g and
-// forms S_b = sum_g exp(m_c - lse_g) w_g (= Eq. compkv-score). Block b is ranked by the 64-bit key
+// Launch 2 (chunked shape), grid = units: the kernel boundary makes every partial visible. One
+// workgroup per unit merges the partials into each head's log normalizer lse_g and forms
+// S_b = sum_g exp(m_c - lse_g) w_g (= Eq. compkv-score). Block b is ranked by the 64-bit key
 // (bits of S_b) << 32 | ~b: scores are >= 0, so their IEEE bit patterns order like the values, and the
 // keys are unique and order exactly like (S_b descending, b ascending), the stable Top-K of the paper.
-// Up to 8192 blocks the keys stay in registers (32 per thread). One histogram of each key's distance
-// below the largest score (bins of 1/16 octave on the float bits; keys farther than 255 bins are not
-// counted) locates the bin that holds the (K-|F|)-th largest key; only the keys in that bin or above
-// are ranked exactly, by brute force, and a bitmap of the selected and mandatory blocks is compacted
-// into ascending ids. Larger inputs, or ties that leave too many keys at or above the cut's bin, go
-// through a three-pass radix select on the score bits instead. Wave-level reductions and prefix sums
-// use DPP lane moves.
+// Up to 8192 blocks the keys stay in registers (eight per thread of 1024). One histogram of each key's
+// distance below the largest score (bins of 1/16 octave on the float bits; keys farther than 255 bins
+// are not counted) locates the bin that holds the (K-|F|)-th largest key; only the keys in that bin or
+// above are ranked exactly, by brute force, and a bitmap of the selected and mandatory blocks is
+// compacted into ascending ids. Larger inputs, or ties that leave too many keys at or above the cut's
+// bin, go through a three-pass radix select on the score bits instead. Wave-level reductions and prefix
+// sums use DPP lane moves. (select_core.h holds this selection, shared with the fused launches.)
+//
+// The chunked-exact shape replaces launch 2 and the decode's launches by one fused selection/exact
+// launch in one of two forms (below): item workgroups that each select and attend, beside compensation
+// workgroups that stream the mean values; or one selector per unit whose ids the unit's other
+// workgroups take from a mailbox after streaming their share of the mean values. Either form merges the
+// unit's partials in the launch (its last workgroup).
 #include "select_core.h"
 
 namespace compkv {
@@ -627,14 +636,14 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
 }
 
 // ---------------------------------------------------------------- selection + exact items, fused
-// The fused step's selection and exact items as one launch: a one-dimensional grid of items * units
-// workgroups of kFinThreads threads, mapped by xcd_unit_work so that (when the units fill whole rounds
-// of eight) all items of unit u run on XCD u % 8. Every workgroup of a unit repeats the unit's selection from the chunk partials (the
-// same computation as select_finalize_kernel, so all of them hold the same ids) into LDS; item 0 also
-// writes the selection outputs. Then the sixteen waves attend exactly over the item's blocks (exact.h,
-// one 16-token tile per wave and round) and write the item's partial. This saves the launch between
-// selection and exact attention and the round trip of the selected ids through memory; it pays off
-// while the items fit one resident round (one workgroup per CU).
+// Form 1 of the fused step's selection/exact launch: a one-dimensional grid of (items + n_comp) * units
+// workgroups of kSxThreads threads, mapped by xcd_unit_work so that (when the units fill whole rounds
+// of eight) all workgroups of unit u run on XCD u % 8. Every item workgroup of a unit repeats the unit's
+// selection from the chunk partials (the same computation as select_finalize_kernel, so all of them
+// hold the same ids) into LDS; item 0 also writes the selection outputs. Then the sixteen waves attend
+// exactly over the item's blocks (exact.h, one 16-token tile per wave and round) and write the item's
+// partial. The unit's last workgroup to arrive merges its partials (merge_unit), so the step needs no
+// further launch. The launch pays off while every workgroup is resident at once (one per CU).
 //
 // Compensation workgroups (the fused step with Mean compensation and the chunk launch scoring only):
 // the same launch also holds n_comp workgroups per unit, after the item workgroups in the grid, that
