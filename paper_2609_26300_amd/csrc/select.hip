@@ -948,7 +948,8 @@ int select_exact_slots(const Geom& g, size_t dyn) { return g.D == 128 ? sx_slots
 hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s) {
     // the keys of the fast path's tie fallback stay in LDS: no workgroup writes global scratch
     a.keys_in_lds = 1;
-    if (g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb > kMaxEb ||
+    if (a.bpc < 1 || (a.bpc & (a.bpc - 1)) != 0 || g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax ||
+        d.eb > kMaxEb ||
         finalize_dyn_lds(g, a) > kDynBudget || (d.n_comp > 0 && (d.cb < 1 || d.cb > kStepCbMax)) ||
         (long long)d.n_comp * d.cb < (d.n_comp > 0 ? g.xmax() : 0) || d.part_base + items > d.part_count ||
         (d.arrive && (d.part_count != d.n_comp + items || d.part_count * g.G > kMergeMaxTerms)))
@@ -958,7 +959,7 @@ hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, 
 hipError_t launch_select_work(const Geom& g, ScoreArgs a, const DecodeArgs& d, int P, hipStream_t s) {
     a.keys_in_lds = 1;
     const int keff = std::max(1, std::min(a.K, g.xmax()));
-    if (P < 2 || g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb < 1 || d.eb > kMaxEb ||
+    if (P < 2 || a.bpc < 1 || (a.bpc & (a.bpc - 1)) != 0 || g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb < 1 || d.eb > kMaxEb ||
         (long long)P * d.eb < keff || finalize_dyn_lds(g, a) > kDynBudget || !d.arrive || !d.sel_word || !d.mailbox ||
         (d.n_comp != 0 && (d.n_comp != P - 1 || d.cb < 1 || d.cb > kStepCbMax || (long long)d.n_comp * d.cb < g.xmax())) ||
         d.part_base != d.n_comp || d.part_count != d.n_comp + P || d.part_count * g.G > kMergeMaxTerms)

@@ -192,8 +192,10 @@ __device__ bool select_fast(const SelectCtx& ctx, const unsigned long long (&ck)
             if (bin[k] < (uint32_t)kHistTail) atomicAdd(&sh.hist[bin[k]], 1);
         }
         __syncthreads();
-        // wave 0: prefix over the counted bins (four per lane); the bin reaching kk holds the cut
-        if (wave == 0) {
+        // every wave: prefix over the counted bins (four per lane); the bin reaching kk holds the cut (at
+        // most one lane finds it; none: the cut lies below the counted range, beta = kHistTail)
+        uint32_t beta;
+        {
             int c[4], tot = 0;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -202,14 +204,15 @@ __device__ bool select_fast(const SelectCtx& ctx, const unsigned long long (&ck)
                 tot += c[e];
             }
             int run = wave_incl_scan(tot) - tot;
+            int cut = kHistTail;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                if (run < kk && run + c[e] >= kk) sh.beta = 4 * lane + e;
+                if (run < kk && run + c[e] >= kk) cut = 4 * lane + e;
                 run += c[e];
             }
+            const unsigned long long found = __ballot(cut != kHistTail);
+            beta = found ? (uint32_t)__builtin_amdgcn_readlane(cut, (int)__builtin_ctzll(found)) : (uint32_t)kHistTail;
         }
-        __syncthreads();
-        const uint32_t beta = (uint32_t)sh.beta;  // kHistTail: the cut lies below the counted range
         // candidates: keys in the cut's bin or above; each wave reserves its slots with one atomic
         int mine = 0;
 #pragma unroll
@@ -485,8 +488,9 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
     const SelectCtx sc = make_select_ctx(X, a.K, a.n_sink, a.n_recent, sel_out, nsel_out,
                                          a.keys_in_lds ? reinterpret_cast<uint32_t*>(dyn + 2 * np * G)
                                                        : a.ws_key + (size_t)u * xmax);
+    const int bpc_log2 = __builtin_ctz((unsigned)a.bpc);  // the chunk size is a power of two (32, 64, 128)
     auto score_of = [&](int b, const float (&wt)[G]) {
-        const float* f = fac + (b == X - 1 ? nc : b / a.bpc) * G;
+        const float* f = fac + (b == X - 1 ? nc : b >> bpc_log2) * G;
         float S = 0.0f;
 #pragma unroll
         for (int g = 0; g < G; ++g) S += f[g] * wt[g];
