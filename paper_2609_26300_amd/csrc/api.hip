@@ -174,7 +174,7 @@ int step_partials(const Geom& g, int K) {
     const int nchunks = score_shape(g).nchunks;
     const SxShape sx = sx_shape(g, nchunks, K);
     return std::max(std::max(nchunks + 1 + sparse_shape(g, K).n_exact, sx.fits ? sx.n_comp + sx.n_exact : 0),
-                    sx.work ? 2 * sx.P - 1 : 0);
+                    sx.work ? sx.P : 0);
 }
 
 // fused step: the arrival counters of the fused selection/exact launch's in-launch merge and the
@@ -255,7 +255,7 @@ SxShape sx_shape(const Geom& g, int nchunks, int K) {
     const bool work_fits = cus > 0 && P >= 2 && (long long)g.units() * P <= resident &&
                            K <= compkv::select_exact_max_budget() && xmax <= 8192 && dyn <= 32768 &&
                            web <= compkv::decode_max_eb() && wcb <= cbmax &&
-                           (2 * P - 1) * g.G <= compkv::select_exact_merge_terms();
+                           P * g.G <= compkv::select_exact_merge_terms();
     const bool items_round = fits && cus > 0 && (long long)g.units() * (n_exact + n_comp) <= resident;
     // the one-selector form where a unit's selected tokens are at least its mean-value rows (both 4 d
     // bytes each): spread over all of the unit's workgroups, the exact share then outweighs the repeated
@@ -679,7 +679,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         float* dpart = reinterpret_cast<float*>(static_cast<char*>(wsb) + score_ws(g));
         const bool work = sx.work;
         const int n_comp = drop ? 0 : (work ? sx.P - 1 : sx.n_comp);
-        const int nparts = n_comp + (work ? sx.P : sx.n_exact);
+        const int nparts = work ? sx.P : n_comp + sx.n_exact;
         const size_t part_bytes = step_part_bytes(g, step_partials(g, K));
         uint32_t* arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(wsb) + score_ws(g) + part_bytes);
         if (step_part_bytes(g, nparts) > part_bytes || step_ws(g, K) > wsb_bytes)
@@ -710,7 +710,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.dense = 0;
         d.scale = params->scale;
         d.part_count = nparts;
-        d.part_base = n_comp;
+        d.part_base = work ? 0 : n_comp;
         d.neg_pseudo = drop ? 0 : 1;
         d.sel_padded = 1;
         d.arrive = arrive;

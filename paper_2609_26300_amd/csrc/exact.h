@@ -35,6 +35,7 @@ template <int D, int G, int NW>
 struct ExactLds {
     float m[NW][G], l[NW][G];
     float f[NW][G];  // each wave's rescale factor exp(m_w - M) per head
+    float fx[G];     // the same for an absorbed partial (finish_exact's xm, xl, xacc)
     float M[G], L[G];
     alignas(16) float acc[NW][G][D];
     float zb[G][kMaxEb];  // fused step: the block logits of the item's selected blocks
@@ -267,9 +268,12 @@ __device__ void exact_tokens(const TokenMap& tm, const uint16_t* __restrict__ Ku
 // Combine the NW waves' exact states in LDS and write the item's partial: the per-head maximum M
 // over the waves and each wave's factor exp(m_w - M) first, then every coordinate as a plain sum of
 // the waves' scaled accumulators in wave order. kCoherent: the partial is stored with device-coherent
-// stores (merged by another workgroup of the same launch).
+// stores (merged by another workgroup of the same launch). With xm non-null, one more partial in LDS
+// (per head: max xm[g], sum xl[g], weighted sums xacc[g * xstride + i]) is absorbed after the waves.
 template <int D, int G, int NW, bool kCoherent = false>
-__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], ExactLds<D, G, NW>& sh, float* part) {
+__device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], ExactLds<D, G, NW>& sh, float* part,
+                             const float* xm = nullptr, const float* xl = nullptr, const float* xacc = nullptr,
+                             int xstride = 0) {
     constexpr int CPL = D / 16;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -293,12 +297,18 @@ __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], Exact
         float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < NW; ++w) M = fmaxf(M, sh.m[w][g]);
+        if (xm) M = fmaxf(M, xm[g]);
         float L = 0.0f;
 #pragma unroll
         for (int w = 0; w < NW; ++w) {
             const float fw = sh.m[w][g] == -INFINITY ? 0.0f : __expf(sh.m[w][g] - M);
             sh.f[w][g] = fw;
             L += fw * sh.l[w][g];
+        }
+        if (xm) {
+            const float fx = xm[g] == -INFINITY ? 0.0f : __expf(xm[g] - M);
+            sh.fx[g] = fx;
+            L += fx * xl[g];
         }
         sh.M[g] = M;
         sh.L[g] = L;
@@ -309,6 +319,7 @@ __device__ void finish_exact(float m, float l, const v4f32 (&acc)[D / 16], Exact
         float aa = 0.0f;
 #pragma unroll
         for (int w = 0; w < NW; ++w) aa += sh.f[w][g] * sh.acc[w][g][i];
+        if (xm) aa += sh.fx[g] * xacc[(size_t)g * xstride + i];
         float* p = part + (size_t)g * (D + 2);
         if constexpr (kCoherent) {
             if (i == 0) {

@@ -176,8 +176,8 @@ hipError_t launch_decode_items(const Geom& g, const DecodeArgs& a, int items, hi
 hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s);
 // the same step with one selector per unit and P - 1 workers (compensation share d.cb, then exact share
 // d.eb once the selection word is set): P workgroups per unit, all resident at once (checked by the
-// caller with select_exact_slots); partials: d.n_comp (= P - 1 under Mean, else 0) compensation, then P
-// exact; hipErrorInvalidValue outside its limits
+// caller with select_exact_slots); one partial per workgroup (d.part_count = P, d.part_base = 0: a
+// worker's compensation partial joins its exact one); hipErrorInvalidValue outside its limits
 hipError_t launch_select_work(const Geom& g, ScoreArgs a, const DecodeArgs& d, int P, hipStream_t s);
 int select_exact_max_budget();
 int select_exact_waves();

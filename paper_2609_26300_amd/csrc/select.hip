@@ -663,9 +663,10 @@ constexpr int kCompRows = 1;
 // Exact attention of unit u over nblk selected blocks whose ids are in LDS (ids; -1 or an id past the
 // unit's blocks contributes nothing) into decode partial `part` of the unit (device-coherent stores).
 // Under Mean compensation every token's weight is p_j - p'_j (the chunk launch's block logits).
+// absorb: the workgroup's compensation partial (step_compensation with kKeep) joins the stored partial.
 template <int D, int G, int NW, typename Lds>
 __device__ void sx_exact(const Geom& geo, const DecodeArgs& d, int u, int n, const int32_t* ids, int nblk,
-                         int part, Lds& L) {
+                         int part, Lds& L, bool absorb = false) {
     constexpr int FT = NW * 64;
     const int tid = threadIdx.x;
     const int bseq = u / geo.hkv, h = u % geo.hkv;
@@ -694,7 +695,9 @@ __device__ void sx_exact(const Geom& geo, const DecodeArgs& d, int u, int n, con
     exact_tokens<D, G, NW>(tm, d.K, d.V, qh, pseudo ? d.blk_logit + (size_t)u * G * geo.xcap : nullptr, geo.xcap,
                            L.u.ex.zb, d.scale, m, l, acc);
     COMPKV_MARK(d.trace, 8);  // this wave 0's tiles attended
-    finish_exact<D, G, NW, true>(m, l, acc, L.u.ex, d.ws_part + ((size_t)u * d.part_count + part) * G * (D + 2));
+    constexpr int kCwStride = (int)(sizeof(L.cw[0]) / sizeof(float));
+    finish_exact<D, G, NW, true>(m, l, acc, L.u.ex, d.ws_part + ((size_t)u * d.part_count + part) * G * (D + 2),
+                                 absorb ? L.cm : nullptr, L.cl, &L.cw[0][0], kCwStride);
     COMPKV_MARK(d.trace, 9);  // partial stored
 }
 
@@ -747,12 +750,12 @@ __global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a,
 // XCD). The selector ranks the unit's blocks and posts every id slot k < K to the unit's mailbox
 // (id ^ kPosted, device-coherent; the chunk launch zeroed the mailbox, and no posted value is zero),
 // then attends exactly over the first eb ids. Worker w (1 .. P - 1) first streams its share of the
-// mean values (compensation blocks [(w - 1) cb, w cb), partial w - 1), requesting its slots
-// [w eb, (w + 1) eb) of the mailbox once the last mean values are in; a slot still zero is polled
-// until posted (a bounded wait: the selector started before any worker and never waits itself; past
-// the bound the unit's outputs become NaN and its timeout word counts it). Then it attends exactly
-// over those ids. Exact partials follow the P - 1 compensation partials (none under Drop); the unit's
-// last workgroup of P merges them all. The HBM streams from the start on every CU but the
+// mean values (compensation blocks [(w - 1) cb, w cb)), requesting its slots [w eb, (w + 1) eb) of the
+// mailbox once the last mean values are in; a slot still zero is polled until posted (a bounded wait:
+// the selector started before any worker and never waits itself; past the bound the unit's outputs
+// become NaN and its timeout word counts it). Then it attends exactly over those ids, and its
+// compensation partial (kept in LDS) joins its exact partial: workgroup w stores partial w, and the
+// unit's last workgroup of P merges the P partials. The HBM streams from the start on every CU but the
 // selectors', and the selection runs once per unit.
 // Phase-trace slots (both forms of the fused launch): 0 start, 1 role (1 selects, 2 streams mean values
 // first), 2 the selection's loads in, 3 keys formed, 4 selected, 5 compensation weights formed, 6 mean
@@ -761,7 +764,7 @@ constexpr uint32_t kPosted = 0x80000000u;  // mailbox value of id b: b ^ kPosted
 constexpr uint32_t kSelFailed = 1u;        // selection word: a worker's wait timed out
 constexpr int kSelSpinLimit = 1 << 17;     // polls of a wait (each a memory round trip): well over 50 ms
 
-template <int D, int G>
+template <int D, int G, int KPT>  // KPT: keys per thread of the selection (xmax <= KPT kSxThreads)
 __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int P) {
     constexpr int FT = kSxThreads, NW = FT / 64;
     using Lds = SelExactLdsT<D, G, kStepCbMax, NW>;
@@ -782,7 +785,7 @@ __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, Score
     uint32_t* mbox = d.mailbox + (size_t)u * a.K;
     COMPKV_MARK_VALUE(d.trace, 1, w == 0 ? 1 : 2);
     if (w == 0) {
-        finalize_select<G, false, FT, kSxKeys>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, true);
+        finalize_select<G, false, FT, KPT>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, true);
         __syncthreads();
         COMPKV_MARK(d.trace, 4);  // selected
         for (int k = tid; k < a.K; k += FT) {
@@ -792,18 +795,21 @@ __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, Score
         }
         if (tid == 0) a.n_sel[u] = L.nsel;
         const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
-        sx_exact<D, G, NW>(geo, d, u, n, L.sel, max(0, min(d.eb, L.nsel)), d.part_base, L);
+        sx_exact<D, G, NW>(geo, d, u, n, L.sel, max(0, min(d.eb, L.nsel)), 0, L);
     } else {
         const int n_raw = d.seq_lens[u / geo.hkv];
         const int e0 = w * d.eb;
         const int nblk = max(0, min(d.eb, a.K - e0));  // (the ids past n_sel are -1)
         uint32_t mv = 0u;
         auto request = [&] { mv = ld_agent_u32(mbox + (tid < nblk ? e0 + tid : 0)); };
-        if (d.n_comp > 0) {
+        const bool comp = d.n_comp > 0;  // (workgroup-uniform)
+        if (comp) {  // its compensation partial stays in LDS for the exact partial to absorb
             const int xmax = geo.xmax();
             const int c0 = min((w - 1) * d.cb, xmax), c1 = min(c0 + d.cb, xmax);
-            step_compensation<D, G, kCompRows, Lds, FT>(
-                geo, d, u, n_raw, c0, c1, L, d.ws_part + ((size_t)u * d.part_count + w - 1) * G * (D + 2), request);
+            // the slots are polled once the last mean values are requested: if the selector has posted
+            // them by then, they return with those values; else they are requested once more after them
+            step_compensation<D, G, kCompRows, Lds, FT, true>(
+                geo, d, u, n_raw, c0, c1, L, nullptr, [&] { if (__any(mv == 0u)) request(); }, request);
         } else {
             request();
         }
@@ -823,7 +829,7 @@ __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, Score
         }
         __syncthreads();
         COMPKV_MARK(d.trace, 7);  // the ids in hand
-        sx_exact<D, G, NW>(geo, d, u, n, L.sel, nblk, d.part_base + w, L);
+        sx_exact<D, G, NW>(geo, d, u, n, L.sel, nblk, w, L, comp);
     }
     if (arrive_last(d.arrive + u, P, L.last)) {
         COMPKV_MARK(d.trace, 10);  // this workgroup merges
@@ -889,7 +895,15 @@ hipError_t launch_sx(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int
 
 template <int D, int G>
 hipError_t launch_work(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int P, hipStream_t s) {
-    select_work_kernel<D, G><<<dim3(P * g.units()), kSxThreads, finalize_dyn_lds(g, a), s>>>(g, a, d, P);
+    const dim3 grid(P * g.units());
+    const size_t dyn = finalize_dyn_lds(g, a);
+    // keys per thread for the unit's blocks: fewer loads and keys where the blocks are few
+    if (g.xmax() <= kSxThreads)
+        select_work_kernel<D, G, 1><<<grid, kSxThreads, dyn, s>>>(g, a, d, P);
+    else if (g.xmax() <= 4 * kSxThreads)
+        select_work_kernel<D, G, 4><<<grid, kSxThreads, dyn, s>>>(g, a, d, P);
+    else
+        select_work_kernel<D, G, kSxKeys><<<grid, kSxThreads, dyn, s>>>(g, a, d, P);
     return hipGetLastError();
 }
 
@@ -929,7 +943,7 @@ template <int D, int G>
 int sx_slots(size_t dyn) {
     int per_cu = 0, cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_work_kernel<D, G>, kSxThreads, dyn) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, select_work_kernel<D, G, kSxKeys>, kSxThreads, dyn) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
     return per_cu * cus;
@@ -962,7 +976,7 @@ hipError_t launch_select_work(const Geom& g, ScoreArgs a, const DecodeArgs& d, i
     if (P < 2 || a.bpc < 1 || (a.bpc & (a.bpc - 1)) != 0 || g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb < 1 || d.eb > kMaxEb ||
         (long long)P * d.eb < keff || finalize_dyn_lds(g, a) > kDynBudget || !d.arrive || !d.sel_word || !d.mailbox ||
         (d.n_comp != 0 && (d.n_comp != P - 1 || d.cb < 1 || d.cb > kStepCbMax || (long long)d.n_comp * d.cb < g.xmax())) ||
-        d.part_base != d.n_comp || d.part_count != d.n_comp + P || d.part_count * g.G > kMergeMaxTerms)
+        d.part_base != 0 || d.part_count != P || d.part_count * g.G > kMergeMaxTerms)
         return hipErrorInvalidValue;
     return g.D == 128 ? work_g<128>(g, a, d, P, s) : work_g<64>(g, a, d, P, s);
 }

@@ -693,6 +693,19 @@ __device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, Ld
     }
 }
 
+// The mean-value stream of one compensation range of unit u: blocks [c0, c1) (at most kStepCbMax, within
+// the unit's xmax; blocks past the sequence's last contribute nothing), each a pseudo-token with logit
+// log|b| + zbar_b (the block logits the chunk launch wrote) and value vmean_b, reduced to one softmax
+// partial per head. In steps, so that a caller can place the requests:
+//   request_logits()  the block logits of the range (ZR per thread and head);
+//   request_rows()    the first two batches of mean-value rows (NT / (D / 4) * ROWS rows each, two
+//                     register buffers of ROWS rows per thread);
+//   weigh(...)        the pseudo-logits and their per-head weights (in LDS), then every batch, each
+//                     requested two batches ahead of its use so that one batch is in flight while
+//                     another is weighed; the per-wave sums are left in L.u.ex.acc;
+//   store(...) / keep(...)  the partial to memory (device-coherent) / to LDS (L.cm, L.cl, L.cw[g][0, D)).
+// Every batch is requested, also past the range (then the range's first row again, weighted by zero):
+// the number of loads in flight stays fixed, so each wait is for one batch, never for all of them.
 // One compensation workgroup of a fused launch: blocks [c0, c1) (at most kStepCbMax, within the unit's
 // xmax; the blocks past the sequence's last contribute nothing) of unit u, whose sequence length n_raw
 // was requested before the call and is read only once the loads below are requested (a value made
@@ -702,11 +715,19 @@ __device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, Ld
 // requested two batches ahead of its use (two register buffers of ROWS rows per thread), so that a
 // batch is in flight while another is weighed. While the first two batches are in flight: the pseudo-
 // logits log|b| + zbar and their per-head softmax weights (in LDS). `after` runs once the last mean
-// values have arrived, before the partial is reduced and stored (loads it issues are not queued behind
-// mean values).
-template <int D, int G, int ROWS, typename Lds, int NT = kFinThreads, typename After>
+// values have arrived, before the partial is reduced (loads it issues are not queued behind mean values);
+// `poll` runs once, right after the last batch is requested (a load whose value the caller uses after the
+// call: it returns with the last mean values instead of a round trip after them). The partial is stored
+// to `part` (device-coherent), or with kKeep left in LDS for the workgroup's exact partial to absorb:
+// per head its max in L.cm, its sum in L.cl and its weighted sums in L.cw[g][0, D) (the weights are
+// no longer needed by then).
+struct NoPoll {
+    __device__ void operator()() const {}
+};
+template <int D, int G, int ROWS, typename Lds, int NT = kFinThreads, bool kKeep = false, typename After,
+          typename Poll = NoPoll>
 __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, int n_raw, int c0, int c1, Lds& L,
-                                  float* part, After&& after) {
+                                  float* part, After&& after, Poll&& poll = Poll()) {
     constexpr int LPB = D / 4;     // lanes per mean-value row (one float4 each)
     constexpr int RPS = NT / LPB;  // rows per workgroup step
     constexpr int BATCH = RPS * ROWS;
@@ -799,6 +820,7 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
         weigh(base + BATCH, vb);
         issue(base + 3 * BATCH, vb);
     }
+    poll();  // (after the last requests)
     weigh(base, va);
     weigh(base + BATCH, vb);
     COMPKV_MARK(d.trace, 6);  // the last mean values weighed
@@ -816,17 +838,39 @@ __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, i
             *reinterpret_cast<float4*>(&L.u.ex.acc[wave][g][4 * li]) = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
     }
     __syncthreads();
-    for (int idx = tid; idx < G * D; idx += NT) {
-        const int g = idx / D, i = idx - g * D;
-        float* p = part + (size_t)g * (D + 2);
-        if (i == 0) {
-            st_agent(p, L.cm[g]);
-            st_agent(p + 1, L.cl[g]);
-        }
-        float tot = 0.0f;
+    if constexpr (kKeep) {
+        static_assert(D <= (int)(sizeof(L.cw[0]) / sizeof(float)), "the sums fit the weights' rows");
+        constexpr int PT = (G * D + NT - 1) / NT;
+        float tot[PT];
 #pragma unroll
-        for (int w = 0; w < NT / 64; ++w) tot += L.u.ex.acc[w][g][i];
-        st_agent(p + 2 + i, tot);
+        for (int k = 0; k < PT; ++k) {
+            const int idx = tid + k * NT;
+            tot[k] = 0.0f;
+            if (idx < G * D) {
+                const int g = idx / D, i = idx - g * D;
+#pragma unroll
+                for (int w = 0; w < NT / 64; ++w) tot[k] += L.u.ex.acc[w][g][i];
+            }
+        }
+        __syncthreads();  // (every wave sum read: the exact path reuses L.u.ex)
+#pragma unroll
+        for (int k = 0; k < PT; ++k) {
+            const int idx = tid + k * NT;
+            if (idx < G * D) L.cw[idx / D][idx % D] = tot[k];
+        }
+    } else {
+        for (int idx = tid; idx < G * D; idx += NT) {
+            const int g = idx / D, i = idx - g * D;
+            float* p = part + (size_t)g * (D + 2);
+            if (i == 0) {
+                st_agent(p, L.cm[g]);
+                st_agent(p + 1, L.cl[g]);
+            }
+            float tot = 0.0f;
+#pragma unroll
+            for (int w = 0; w < NT / 64; ++w) tot += L.u.ex.acc[w][g][i];
+            st_agent(p + 2 + i, tot);
+        }
     }
 }
 
