@@ -888,8 +888,15 @@ hipError_t dispatch_g(const Geom& g, const ScoreArgs& a, hipStream_t s) {
 
 template <int D, int G>
 hipError_t launch_sx(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int items, hipStream_t s) {
-    const int grid = (items + d.n_comp) * g.units();
-    select_exact_kernel<D, G, kSxThreads, kSxKeys><<<dim3(grid), kSxThreads, finalize_dyn_lds(g, a), s>>>(g, a, d, items);
+    const dim3 grid((items + d.n_comp) * g.units());
+    const size_t dyn = finalize_dyn_lds(g, a);
+    // keys per thread for the unit's blocks (as in launch_work)
+    if (g.xmax() <= kSxThreads)
+        select_exact_kernel<D, G, kSxThreads, 1><<<grid, kSxThreads, dyn, s>>>(g, a, d, items);
+    else if (g.xmax() <= 4 * kSxThreads)
+        select_exact_kernel<D, G, kSxThreads, 4><<<grid, kSxThreads, dyn, s>>>(g, a, d, items);
+    else
+        select_exact_kernel<D, G, kSxThreads, kSxKeys><<<grid, kSxThreads, dyn, s>>>(g, a, d, items);
     return hipGetLastError();
 }
 
