@@ -34,9 +34,10 @@ def step_kernels(path: int) -> str:
     """The dispatches of one compkv_decode_step call on the given launch shape."""
     return {1: "compkv_decode_step: chunk scoring (append, compensation stream), selection, exact items, merge",
             2: "compkv_decode_step: one-group scoring and selection (append), exact and compensation items, merge",
-            3: "compkv_decode_step: chunk scoring (append, compensation stream), selection + exact items, merge",
-            4: "compkv_decode_step: one launch (append, chunk scoring, selection, compensation stream, exact "
-               "items, merge)",
+            3: "compkv_decode_step: chunk scoring (append), then one launch of selection, compensation stream, "
+               "exact items and merge",
+            4: "compkv_decode_step: group scoring (append), then one launch of selector, compensation stream, "
+               "exact items and merge",
             }[path]
 
 
