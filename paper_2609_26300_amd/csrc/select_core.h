@@ -706,12 +706,16 @@ __device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, Ld
 //   store(...) / keep(...)  the partial to memory (device-coherent) / to LDS (L.cm, L.cl, L.cw[g][0, D)).
 // Every batch is requested, also past the range (then the range's first row again, weighted by zero):
 // the number of loads in flight stays fixed, so each wait is for one batch, never for all of them.
+struct NoPoll {
+    __device__ void operator()() const {}
+};
+
 // One compensation workgroup of a fused launch: blocks [c0, c1) (at most kStepCbMax, within the unit's
 // xmax; the blocks past the sequence's last contribute nothing) of unit u, whose sequence length n_raw
 // was requested before the call and is read only once the loads below are requested (a value made
 // uniform right away would wait for its load). The block logits zbar are requested first (loads return
-// in order, so they arrive ahead
-// of the mean values); then the mean-value rows in batches of NT / (D / 4) * ROWS rows, each batch
+// in order, so they arrive ahead of the mean values); then the mean-value rows in batches of
+// NT / (D / 4) * ROWS rows, each batch
 // requested two batches ahead of its use (two register buffers of ROWS rows per thread), so that a
 // batch is in flight while another is weighed. While the first two batches are in flight: the pseudo-
 // logits log|b| + zbar and their per-head softmax weights (in LDS). `after` runs once the last mean
@@ -721,9 +725,6 @@ __device__ void arrive_and_merge(const Geom& geo, const DecodeArgs& d, int u, Ld
 // to `part` (device-coherent), or with kKeep left in LDS for the workgroup's exact partial to absorb:
 // per head its max in L.cm, its sum in L.cl and its weighted sums in L.cw[g][0, D) (the weights are
 // no longer needed by then).
-struct NoPoll {
-    __device__ void operator()() const {}
-};
 template <int D, int G, int ROWS, typename Lds, int NT = kFinThreads, bool kKeep = false, typename After,
           typename Poll = NoPoll>
 __device__ void step_compensation(const Geom& geo, const DecodeArgs& d, int u, int n_raw, int c0, int c1, Lds& L,
