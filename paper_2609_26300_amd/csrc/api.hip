@@ -169,7 +169,7 @@ size_t step_part_bytes(const Geom& g, int parts) {
 // fused step: the score region, then [units][parts][G][D + 2] decode partials. Chunked path: the
 // compensation of each chunk and of the last block, then each exact item's (nchunks + 1 + n_exact);
 // fused selection/exact launch: each compensation workgroup's, then each exact item's (n_comp +
-// n_exact). Sized for the larger of the two.
+// n_exact), or in its one-selector form one per workgroup (P). Sized for the largest.
 int step_partials(const Geom& g, int K) {
     const int nchunks = score_shape(g).nchunks;
     const SxShape sx = sx_shape(g, nchunks, K);
