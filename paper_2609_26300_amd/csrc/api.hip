@@ -127,7 +127,8 @@ size_t score_ws(const Geom& g) {
     const ScoreShape sh = score_shape(g);
     const size_t units = g.units(), xmax = g.xmax();
     return align_up(units * (sh.nchunks + 1) * g.G * 2 * sizeof(float)) +
-           align_up(units * xmax * g.G * sizeof(float)) + align_up(units * xmax * sizeof(uint32_t));
+           align_up(units * xmax * g.G * sizeof(float)) + align_up(units * xmax * sizeof(uint32_t)) +
+           align_up(units * g.G * 4 * sizeof(float));
 }
 
 size_t sparse_ws(const Geom& g, int K) {
@@ -351,6 +352,10 @@ compkv::ScoreArgs score_args(const Geom& g, const compkv_select_params* params, 
     a.ws_w = reinterpret_cast<float*>(p);
     p += align_up(units * xmax * g.G * sizeof(float));
     a.ws_key = reinterpret_cast<uint32_t*>(p);
+    p += align_up(units * xmax * sizeof(uint32_t));
+    a.ws_qv = reinterpret_cast<float*>(p);
+    a.zlog = blk_logit;
+    a.zstride = g.xcap;
     a.q = static_cast<const uint16_t*>(q);
     a.kmean = kmean;
     a.dvar = dvar;
@@ -367,6 +372,20 @@ compkv::ScoreArgs score_args(const Geom& g, const compkv_select_params* params, 
     a.scale = params->scale;
     a.score_kind = params->score_kind;
     return a;
+}
+
+// The selection forms its score terms from zbar and the variances where these are fewer than the
+// terms (r = 4 variances against G = 8 terms per block) and the keys fit the four-per-thread selection:
+// the scoring launch then writes zbar alone (to blk_logit, or without it to the terms' region,
+// [units][G][xmax]) and the query's group sums. (At G = 4 the reads would not shrink, and forming the
+// terms in the selection lengthens it: measured 128K +1.8 us, 32K +1.1 us.)
+void use_logit_terms(const Geom& g, compkv::ScoreArgs& a) {
+    if (a.one_group || g.r != 4 || g.G != 8 || g.xmax() > 4096) return;
+    a.logit_terms = 1;
+    if (!a.zlog) {
+        a.zlog = a.ws_w;
+        a.zstride = g.xmax();
+    }
 }
 
 constexpr int kMaxDevices = 64;
@@ -473,6 +492,7 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     void* body = static_cast<char*>(workspace) + state_bytes(g);
     compkv::ScoreArgs a = score_args(g, params, q, kmean, dvar, seq_lens, sel, n_sel, blk_logit, scores, body);
     a.one_group = one;
+    use_logit_terms(g, a);
     return launch_status(compkv::launch_score_select(g, a, static_cast<hipStream_t>(stream)));
 }
 
@@ -638,6 +658,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         d.part_count = sh.parts;
         d.part_base = drop ? 0 : 1 + sh.n_comp;
         d.neg_pseudo = drop ? 0 : 1;
+        use_logit_terms(g, a);
         return launch_status(compkv::launch_step_stream(g, a, d, state, s));
     }
     if (one) {
@@ -668,6 +689,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
     }
     // chunked scoring; then either the selection and the exact items as two launches, or
     // (CHUNKED_EXACT, or AUTO when every item workgroup is resident at once) one fused launch
+    use_logit_terms(g, a);
     const SxShape sx = sx_shape(g, sc.nchunks, K);
     const bool use_sx = use_select_exact(params->select_path, sx);
     if (use_sx) {

@@ -92,7 +92,13 @@ struct ScoreArgs {
     float* blk_logit;
     float* scores;     // nullable
     float* ws_part;    // [units][nchunks][G][2]  (chunk max m_c, chunk sum of exp(a - m_c))
-    float* ws_w;       // [units][xmax][G]       exp(a - m_c) * projected variance
+    float* ws_w;       // [units][xmax][G]       exp(a - m_c) * projected variance (unless logit_terms)
+    float* zlog;       // where the chunk launch stores zbar, [units][G][zstride] (blk_logit, or with
+    int zstride;       // logit_terms and no blk_logit the ws_w region with stride xmax); null: nowhere
+    float* ws_qv;      // [units][G][4]: s^2 Q_{g,t} of the step's query (logit_terms)
+    int logit_terms;   // set by the host (r = 4, G >= 4, chunked selection of up to 4096 blocks): the
+                       // selection forms each block's terms from zbar (zlog) and its variances (dvar)
+                       // instead of reading score terms the chunk launch wrote
     uint32_t* ws_key;  // [units][xmax]          score bits (when they do not fit in LDS)
     int bpc;          // blocks per chunk (multiple of 32)
     int nchunks;      // grid.x
@@ -157,6 +163,8 @@ struct DecodeArgs {
 hipError_t launch_build_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
 hipError_t launch_append_stats(const Geom& g, const StatsArgs& a, hipStream_t s);
 hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s);
+// ScoreArgs::logit_terms within its limits (r = 4, 4 <= G <= 8, at most 4096 blocks, zlog and ws_qv set)
+bool logit_terms_ok(const Geom& g, const ScoreArgs& a);
 int select_max_bpc();
 int select_max_chunk_heads();  // nchunks * G limit of the selection's partial merge
 int select_one_group_terms();  // G * xmax limit of the one-workgroup-per-unit selection

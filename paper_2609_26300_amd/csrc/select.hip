@@ -161,11 +161,13 @@ __device__ void score_tail(const Geom& geo, const ScoreArgs& a, int u, TailShare
     const float lnb = logf((float)nb);
     for (int g = tid; g < G; g += kThreads) {
         const float z = ts.z[g], v = ts.v[g];
-        if (a.blk_logit) a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
+        if (a.zlog) a.zlog[((size_t)u * G + g) * a.zstride + b] = z;
         pp[2 * g] = lnb + z + kind_half(a.score_kind) * v;  // the partial of one block: max a, sum exp(a - a) = 1
         pp[2 * g + 1] = 1.0f;
-        a.ws_w[((size_t)u * geo.xmax() + b) * G + g] = kind_term(a.score_kind, v);
+        if (!a.logit_terms) a.ws_w[((size_t)u * geo.xmax() + b) * G + g] = kind_term(a.score_kind, v);
     }
+    if (a.logit_terms)  // the query's group sums for the selection (r = 4)
+        for (int idx = tid; idx < G * 4; idx += kThreads) a.ws_qv[(size_t)u * G * 4 + idx] = ts.Qv[idx / 4][idx % 4];
     if (cp) {
         for (int idx = tid; idx < G * D; idx += kThreads) {
             const int g = idx / D, i = idx % D;
@@ -381,11 +383,11 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     __syncthreads();
     COMPKV_MARK(a.trace, 6);  // the chunk's partials formed: stores
     // coalesced stores: block logits [g][b] (when requested) and score terms [b][g]
-    for (int idx = tid; a.blk_logit && idx < G * nvalid; idx += kThreads) {
+    for (int idx = tid; a.zlog && idx < G * nvalid; idx += kThreads) {
         const int g = idx / nvalid, lb = idx % nvalid;
-        a.blk_logit[((size_t)u * G + g) * geo.xcap + chunk0 + lb] = sh.z[g][lb];
+        a.zlog[((size_t)u * G + g) * a.zstride + chunk0 + lb] = sh.z[g][lb];
     }
-    for (int idx = tid; idx < G * nvalid; idx += kThreads) {
+    for (int idx = tid; !a.logit_terms && idx < G * nvalid; idx += kThreads) {
         const int lb = idx / G, g = idx % G;
         a.ws_w[((size_t)u * xmax + chunk0 + lb) * G + g] =
             expf(logw(g, lb) - sh.m[g]) * kind_term(a.score_kind, sh.v[g][lb]);
@@ -436,12 +438,13 @@ __global__ __launch_bounds__(kThreads) void score_chunks_kernel(Geom geo, ScoreA
     COMPKV_TRACE_END(a.trace);
 }
 
-template <int G>
+template <int G, bool kLogits = false>
 __global__ __launch_bounds__(kFinThreads) void select_finalize_kernel(Geom geo, ScoreArgs a) {
     __shared__ FinalShared sh;
     extern __shared__ float dyn[];
     const int u = blockIdx.x;
-    finalize_select<G>(geo, a, u, sh, dyn, a.sel + (size_t)u * a.K, a.n_sel + u, true);
+    finalize_select<G, false, kFinThreads, kLogits ? 4 : kKeysPerThread, kLogits>(
+        geo, a, u, sh, dyn, a.sel + (size_t)u * a.K, a.n_sel + u, true);
 }
 
 
@@ -581,7 +584,7 @@ __global__ __launch_bounds__(kFinThreads) void unit_select_kernel(Geom geo, Scor
                         const int g = g0 + gb;
                         const float lnb = logf((float)min(geo.B, n - b * geo.B));
                         A[b * G + g] = lnb + z + kind_half(a.score_kind) * Vp[b * G + g];
-                        if (a.blk_logit) a.blk_logit[((size_t)u * G + g) * geo.xcap + b] = z;
+                        if (a.zlog) a.zlog[((size_t)u * G + g) * a.zstride + b] = z;
                     }
                 }
             }
@@ -701,7 +704,7 @@ __device__ void sx_exact(const Geom& geo, const DecodeArgs& d, int u, int n, con
     COMPKV_MARK(d.trace, 9);  // partial stored
 }
 
-template <int D, int G, int FT, int KPT>
+template <int D, int G, int FT, int KPT, bool kLogits = false>
 __global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int items) {
     constexpr int NW = FT / 64;
     using Lds = SelExactLdsT<D, G, kStepCbMax, NW>;
@@ -729,7 +732,7 @@ __global__ __launch_bounds__(FT) void select_exact_kernel(Geom geo, ScoreArgs a,
     // the items of unit u all on XCD u % kXcds: the unit's selection inputs are fetched once into
     // that XCD's L2
     xcd_unit_work(blockIdx.x, units, items, u, item);
-    finalize_select<G, false, FT, KPT>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
+    finalize_select<G, false, FT, KPT, kLogits>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, item == 0);
     __syncthreads();
     COMPKV_MARK(d.trace, 4);  // selected
     const int n = clamp_len(d.seq_lens[u / geo.hkv], geo.max_seq);
@@ -764,7 +767,8 @@ constexpr uint32_t kPosted = 0x80000000u;  // mailbox value of id b: b ^ kPosted
 constexpr uint32_t kSelFailed = 1u;        // selection word: a worker's wait timed out
 constexpr int kSelSpinLimit = 1 << 17;     // polls of a wait (each a memory round trip): well over 50 ms
 
-template <int D, int G, int KPT>  // KPT: keys per thread of the selection (xmax <= KPT kSxThreads)
+// KPT: keys per thread of the selection (xmax <= KPT kSxThreads); kLogits: a.logit_terms
+template <int D, int G, int KPT, bool kLogits = false>
 __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, ScoreArgs a, DecodeArgs d, int P) {
     constexpr int FT = kSxThreads, NW = FT / 64;
     using Lds = SelExactLdsT<D, G, kStepCbMax, NW>;
@@ -785,7 +789,7 @@ __global__ __launch_bounds__(kSxThreads) void select_work_kernel(Geom geo, Score
     uint32_t* mbox = d.mailbox + (size_t)u * a.K;
     COMPKV_MARK_VALUE(d.trace, 1, w == 0 ? 1 : 2);
     if (w == 0) {
-        finalize_select<G, false, FT, KPT>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, true);
+        finalize_select<G, false, FT, KPT, kLogits>(geo, a, u, L.u.fin, dyn, L.sel, &L.nsel, true);
         __syncthreads();
         COMPKV_MARK(d.trace, 4);  // selected
         for (int k = tid; k < a.K; k += FT) {
@@ -871,6 +875,12 @@ hipError_t launch_pair(const Geom& g, const ScoreArgs& a, hipStream_t s) {
         launch_chunks<D, G, false>(g, a, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.chunks_only) return e;
+    if constexpr (G >= 4) {
+        if (a.logit_terms) {
+            select_finalize_kernel<G, true><<<dim3(g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a);
+            return hipGetLastError();
+        }
+    }
     select_finalize_kernel<G><<<dim3(g.units()), kFinThreads, finalize_dyn_lds(g, a), s>>>(g, a);
     return hipGetLastError();
 }
@@ -890,6 +900,15 @@ template <int D, int G>
 hipError_t launch_sx(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int items, hipStream_t s) {
     const dim3 grid((items + d.n_comp) * g.units());
     const size_t dyn = finalize_dyn_lds(g, a);
+    if constexpr (G >= 4) {
+        if (a.logit_terms) {  // (at most 4096 blocks: checked by the launcher)
+            if (g.xmax() <= kSxThreads)
+                select_exact_kernel<D, G, kSxThreads, 1, true><<<grid, kSxThreads, dyn, s>>>(g, a, d, items);
+            else
+                select_exact_kernel<D, G, kSxThreads, 4, true><<<grid, kSxThreads, dyn, s>>>(g, a, d, items);
+            return hipGetLastError();
+        }
+    }
     // keys per thread for the unit's blocks (as in launch_work)
     if (g.xmax() <= kSxThreads)
         select_exact_kernel<D, G, kSxThreads, 1><<<grid, kSxThreads, dyn, s>>>(g, a, d, items);
@@ -904,6 +923,15 @@ template <int D, int G>
 hipError_t launch_work(const Geom& g, const ScoreArgs& a, const DecodeArgs& d, int P, hipStream_t s) {
     const dim3 grid(P * g.units());
     const size_t dyn = finalize_dyn_lds(g, a);
+    if constexpr (G >= 4) {
+        if (a.logit_terms) {  // (at most 4096 blocks: checked by the launcher)
+            if (g.xmax() <= kSxThreads)
+                select_work_kernel<D, G, 1, true><<<grid, kSxThreads, dyn, s>>>(g, a, d, P);
+            else
+                select_work_kernel<D, G, 4, true><<<grid, kSxThreads, dyn, s>>>(g, a, d, P);
+            return hipGetLastError();
+        }
+    }
     // keys per thread for the unit's blocks: fewer loads and keys where the blocks are few
     if (g.xmax() <= kSxThreads)
         select_work_kernel<D, G, 1><<<grid, kSxThreads, dyn, s>>>(g, a, d, P);
@@ -966,9 +994,15 @@ int sx_slots_d(const Geom& g, size_t dyn) {
 }
 int select_exact_slots(const Geom& g, size_t dyn) { return g.D == 128 ? sx_slots_d<128>(g, dyn) : sx_slots_d<64>(g, dyn); }
 
+// the selection's logit-terms input (ScoreArgs::logit_terms) within its limits
+bool logit_terms_ok(const Geom& g, const ScoreArgs& a) {
+    return !a.logit_terms || (g.r == 4 && g.G >= 4 && g.G <= 8 && g.xmax() <= 4 * kFinThreads && a.zlog && a.ws_qv);
+}
+
 hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, int items, hipStream_t s) {
     // the keys of the fast path's tie fallback stay in LDS: no workgroup writes global scratch
     a.keys_in_lds = 1;
+    if (!logit_terms_ok(g, a)) return hipErrorInvalidValue;
     if (a.bpc < 1 || (a.bpc & (a.bpc - 1)) != 0 || g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax ||
         d.eb > kMaxEb ||
         finalize_dyn_lds(g, a) > kDynBudget || (d.n_comp > 0 && (d.cb < 1 || d.cb > kStepCbMax)) ||
@@ -979,6 +1013,7 @@ hipError_t launch_select_exact(const Geom& g, ScoreArgs a, const DecodeArgs& d, 
 }
 hipError_t launch_select_work(const Geom& g, ScoreArgs a, const DecodeArgs& d, int P, hipStream_t s) {
     a.keys_in_lds = 1;
+    if (!logit_terms_ok(g, a)) return hipErrorInvalidValue;
     const int keff = std::max(1, std::min(a.K, g.xmax()));
     if (P < 2 || a.bpc < 1 || (a.bpc & (a.bpc - 1)) != 0 || g.xmax() > kFinThreads * kKeysPerThread || a.K > kSelLdsMax || d.eb < 1 || d.eb > kMaxEb ||
         (long long)P * d.eb < keff || finalize_dyn_lds(g, a) > kDynBudget || !d.arrive || !d.sel_word || !d.mailbox ||
@@ -992,6 +1027,7 @@ int select_one_group_auto_blocks() { return kUnitBatch * kFinThreads / 8; }
 int select_max_chunk_heads() { return (int)(kDynBudget / (2 * sizeof(float))); }
 
 hipError_t launch_score_select(const Geom& g, ScoreArgs a, hipStream_t s) {
+    if (!logit_terms_ok(g, a) || (a.logit_terms && a.one_group)) return hipErrorInvalidValue;
     if (a.one_group) {
         if (g.G * g.xmax() > kUnitTerms) return hipErrorInvalidValue;
         return g.D == 128 ? dispatch_g<128>(g, a, s) : dispatch_g<64>(g, a, s);

@@ -86,6 +86,8 @@ constexpr int kCandCap = 1024;     // candidates ranked by brute force on the fa
 constexpr int kHistTail = 255;     // distance bins counted on the fast path (bin 255 = everything farther)
 
 struct FinalShared {
+    float qv[8 * 4];  // logit terms: s^2 Q_{g,t} (G <= 8 heads, r = 4 groups)
+    float lse[8];     // logit terms: each head's log normalizer
     int hist[kHistBins];
     uint32_t wmax[kFinWaves];
     int cnt[kFinWaves], cnt2[kFinWaves];
@@ -416,9 +418,15 @@ __device__ void select_radix(const SelectCtx& c, FinalShared& sh) {
 // loads; the values of blocks past the unit's, loaded only to keep the loads in flight fixed, go unused).
 // FT threads holding up to KPT keys each (the terms of the first eight requested up front, the rest
 // once the normalizers are formed).
-template <int G, bool kCoh = false, int FT = kFinThreads, int KPT = kKeysPerThread>
+// kLogits (a.logit_terms, G >= 4, r = 4, at most 4096 blocks): block b's terms are formed here from
+// zbar (a.zlog), its variances (dvar) and the query's group sums (a.ws_qv): sig2_{g,b} = sum_t
+// s^2 Q_{g,t} D_{b,t}, a_{g,b} = log|b| + zbar_{g,b} + half * sig2_{g,b}, and S_b = sum_g
+// exp(a_{g,b} - lse_g) * term(sig2_{g,b}), with lse_g from the chunk partials as above.
+template <int G, bool kCoh = false, int FT = kFinThreads, int KPT = kKeysPerThread, bool kLogits = false>
 __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, FinalShared& sh, float* dyn,
                                 int32_t* sel_out, int32_t* nsel_out, bool write_scores) {
+    static_assert(!kLogits || (G >= 4 && G <= 8 && !kCoh && KPT <= 4), "logit terms: four to eight heads, one "
+                                                                         "launch apart, at most 4096 blocks");
     constexpr int KB = KPT < 8 ? KPT : 8;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bseq = u / geo.hkv;
@@ -439,12 +447,24 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
         const float* pp = a.ws_part + ((size_t)u * np * G + (tid < np * G ? tid : 0)) * 2;
         pv = kCoh ? ld_agent2(pp) : *reinterpret_cast<const float2*>(pp);
     }
+    float qv = 0.0f;
+    if constexpr (kLogits) qv = a.ws_qv[(size_t)u * G * 4 + (tid < G * 4 ? tid : 0)];
     __asm__ volatile("" ::: "memory");
+    // score terms (or, kLogits, zbar of each head and the block's four variances)
     float w[KB][G];
+    float4 dvk[kLogits ? KB : 1];
 #pragma unroll
     for (int k = 0; k < KB; ++k) {  // ids past xmax load block 0, unused
         const int b = tid + k * FT;
-        load_terms<G, kCoh>(wu, b < xmax ? b : 0, w[k]);
+        const int bb = b < xmax ? b : 0;
+        if constexpr (kLogits) {
+            const float* zu = a.zlog + (size_t)u * G * a.zstride + bb;
+#pragma unroll
+            for (int g = 0; g < G; ++g) w[k][g] = zu[(size_t)g * a.zstride];
+            dvk[k] = *reinterpret_cast<const float4*>(a.dvar + ((size_t)u * geo.xcap + bb) * 4);
+        } else {
+            load_terms<G, kCoh>(wu, bb, w[k]);
+        }
     }
     // the length is read only now (a value made uniform early would wait for every load above)
     __asm__ volatile("" : "+v"(n_raw));
@@ -454,6 +474,7 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
         fac[tid] = pv.x;
         sums[tid] = pv.y;
     }
+    if (kLogits && tid < G * 4) sh.qv[tid] = qv;
     if (!one_pass) {
         for (int idx = tid; idx < np * G; idx += FT) {
             const float* pp = a.ws_part + ((size_t)u * np * G + idx) * 2;
@@ -478,6 +499,7 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
         }
         l = wave_sum(l);  // (every lane's reads above are complete)
         const float lse = m + logf(l);
+        if (kLogits && lane == 0) sh.lse[g] = lse;
         for (int c = lane; c < np; c += 64) {
             const float pm = fac[c * G + g];
             fac[c * G + g] = pm == -INFINITY ? 0.0f : expf(pm - lse);
@@ -502,11 +524,26 @@ __device__ void finalize_select(const Geom& geo, const ScoreArgs& a, int u, Fina
     if (fast) {
         unsigned long long ck[KPT];
         uint32_t mx = 0u;
+        const float half = kind_half(a.score_kind);
+        const float logB = logf((float)geo.B), lnlast = logf((float)max(1, n - (X - 1) * geo.B));
         auto key = [&](int k, const float (&wt)[G]) {
             const int b = tid + k * FT;
             ck[k] = 0ull;
             if (b < X) {
-                const float S = score_of(b, wt);
+                float S;
+                if constexpr (kLogits) {  // wt: zbar of each head
+                    const float4 dv = dvk[k];
+                    const float lnb = b == X - 1 ? lnlast : logB;
+                    S = 0.0f;
+#pragma unroll
+                    for (int g = 0; g < G; ++g) {
+                        const float v = sh.qv[4 * g] * dv.x + sh.qv[4 * g + 1] * dv.y + sh.qv[4 * g + 2] * dv.z +
+                                        sh.qv[4 * g + 3] * dv.w;
+                        S += __expf(lnb + wt[g] + half * v - sh.lse[g]) * kind_term(a.score_kind, v);
+                    }
+                } else {
+                    S = score_of(b, wt);
+                }
                 if (write_scores && a.scores) a.scores[(size_t)u * geo.xcap + b] = S;
                 if (!mandatory(b, X, a.n_sink, a.n_recent)) {
                     ck[k] = ((unsigned long long)__float_as_uint(S) << 32) | (0xFFFFFFFFu - (uint32_t)b);

@@ -215,7 +215,7 @@ __device__ void score_group(const Geom& geo, const ScoreArgs& a, int gpu, int gi
         const int g = idx / nval, j = idx - g * nval;
         a.blk_logit[((size_t)u * G + g) * geo.xcap + grp0 + j] = sh.z[g][j];
     }
-    for (int idx = tid; idx < G * nval; idx += kScoreThreads) {
+    for (int idx = tid; !a.logit_terms && idx < G * nval; idx += kScoreThreads) {
         const int j = idx / G, g = idx - j * G;
         a.ws_w[((size_t)u * geo.xmax() + grp0 + j) * G + g] =
             expf(logw(g, j) - sh.m[j / bpc][g]) * kind_term(a.score_kind, sh.v[g][j]);
@@ -291,8 +291,10 @@ __device__ void step_score_tail(const Geom& geo, const ScoreArgs& a, const Decod
         st_agent(a.blk_logit + ((size_t)u * G + g) * geo.xcap + b, z);
         st_agent(pp + 2 * g, lnb + z + kind_half(a.score_kind) * v);  // one block: max a, sum 1
         st_agent(pp + 2 * g + 1, 1.0f);
-        st_agent(a.ws_w + ((size_t)u * geo.xmax() + b) * G + g, kind_term(a.score_kind, v));
+        if (!a.logit_terms) st_agent(a.ws_w + ((size_t)u * geo.xmax() + b) * G + g, kind_term(a.score_kind, v));
     }
+    if (a.logit_terms)  // the query's group sums for the selection (r = 4)
+        for (int idx = tid; idx < G * 4; idx += NT) a.ws_qv[(size_t)u * G * 4 + idx] = ts.Qv[idx / 4][idx % 4];
     if (cp) {
         for (int idx = tid; idx < G * D; idx += NT) {
             const int g = idx / D, i = idx - g * D;
@@ -369,7 +371,14 @@ __device__ void step_select(const Geom& geo, const ScoreArgs& a, const DecodeArg
                             StepLds<D, G>& L, float* dyn) {
     const int tid = threadIdx.x;
     SelExactLdsT<D, G, kStepCbMax>& S = L.u.sx;
-    finalize_select<G>(geo, a, u, S.u.fin, dyn, S.sel, &S.nsel, true);
+    bool done = false;
+    if constexpr (G >= 4) {
+        if (a.logit_terms) {  // (workgroup-uniform)
+            finalize_select<G, false, kFinThreads, 4, true>(geo, a, u, S.u.fin, dyn, S.sel, &S.nsel, true);
+            done = true;
+        }
+    }
+    if (!done) finalize_select<G>(geo, a, u, S.u.fin, dyn, S.sel, &S.nsel, true);
     __syncthreads();
     for (int k = tid; k < a.K; k += kFinThreads) st_agent_i32(a.sel + (size_t)u * a.K + k, S.sel[k]);
     if (tid == 0) st_agent_i32(a.n_sel + u, S.nsel);
@@ -618,7 +627,8 @@ hipError_t launch_step_stream(const Geom& g, ScoreArgs a, const DecodeArgs& d, u
         (d.neg_pseudo && (d.n_comp < 1 || d.cb < 1 || d.cb > kStepCbMax || (long long)d.n_comp * d.cb < g.xmax() ||
                           d.part_base != 1 + d.n_comp)) ||
         (!d.neg_pseudo && (d.n_comp != 0 || d.part_base != 0)) || np != d.part_base + d.n_exact ||
-        np * g.G > kMergeMaxTerms || step_stream_dyn_lds(g, a.nchunks) > kDynBudget || !state || !a.blk_logit)
+        np * g.G > kMergeMaxTerms || step_stream_dyn_lds(g, a.nchunks) > kDynBudget || !state || !a.blk_logit ||
+        !logit_terms_ok(g, a) || (a.logit_terms && a.zlog != a.blk_logit))
         return hipErrorInvalidValue;
     return g.D == 128 ? stream_g<128>(g, a, d, state, s) : stream_g<64>(g, a, d, state, s);
 }
