@@ -28,6 +28,8 @@
  *      scores            fp32 [batch][n_kv_heads][Xcap]
  *      out               fp32 [batch][n_q_heads][d]; lse fp32 [batch][n_q_heads] (natural log)
  *  - bf16 values are passed as their 16-bit patterns. Inputs must be finite.
+ *  - q, k_cache, v_cache, k_new, v_new, kmean, dvar and vmean are read with 16-byte vector loads: each
+ *    must be 16-byte aligned (any device allocation is); a misaligned one is COMPKV_EINVAL.
  *  - workspace: device scratch of at least compkv_workspace_bytes(...) bytes, 256-byte aligned. Its
  *    first 16 * batch * n_kv_heads bytes, rounded up to 256, are per-unit words of the STREAM step
  *    (below): they must be zero before a workspace's first compkv_decode_step on that path (zero the

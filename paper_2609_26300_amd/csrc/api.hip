@@ -4,6 +4,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <initializer_list>
 #include <mutex>
 
 using compkv::Geom;
@@ -331,6 +332,13 @@ int step_path(const Geom& g, const compkv_select_params* params, int* st) {
                : COMPKV_SELECT_CHUNKED;
 }
 
+// arrays the kernels read with 16-byte vector loads: null (checked separately) or 16-byte aligned
+bool vec_aligned(std::initializer_list<const void*> ps) {
+    for (const void* p : ps)
+        if ((reinterpret_cast<uintptr_t>(p) & 15u) != 0) return false;
+    return true;
+}
+
 int check_ws(const Geom& g, void* ws, size_t bytes, size_t need) {
     if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0 || bytes < need) return COMPKV_EWORKSPACE;
     (void)g;
@@ -441,6 +449,7 @@ int compkv_build_stats(const compkv_dims* dims, const void* k_cache, const void*
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!k_cache || !v_cache || !seq_lens || !kmean || !dvar || !vmean) return COMPKV_EINVAL;
+    if (!vec_aligned({k_cache, v_cache, kmean, dvar, vmean})) return COMPKV_EINVAL;
     compkv::StatsArgs a{};
     a.K = static_cast<const uint16_t*>(k_cache);
     a.V = static_cast<const uint16_t*>(v_cache);
@@ -458,6 +467,7 @@ int compkv_append_stats(const compkv_dims* dims, void* k_cache, void* v_cache, c
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!k_cache || !v_cache || !k_new || !v_new || !seq_lens || !kmean || !dvar || !vmean) return COMPKV_EINVAL;
+    if (!vec_aligned({k_cache, v_cache, k_new, v_new, kmean, dvar, vmean})) return COMPKV_EINVAL;
     compkv::StatsArgs a{};
     a.K = static_cast<const uint16_t*>(k_cache);
     a.V = static_cast<const uint16_t*>(v_cache);
@@ -480,6 +490,7 @@ int compkv_score_select(const compkv_dims* dims, const compkv_select_params* par
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!params || !q || !kmean || !dvar || !seq_lens || !sel || !n_sel) return COMPKV_EINVAL;
+    if (!vec_aligned({q, kmean, dvar})) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
     if (params->score_kind < COMPKV_SCORE_COMPKV || params->score_kind > COMPKV_SCORE_FIRST_ORDER) return COMPKV_EINVAL;
@@ -505,6 +516,7 @@ int compkv_sparse_decode(const compkv_dims* dims, float scale, const void* q, co
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!q || !k_cache || !v_cache || !seq_lens || !sel || !n_sel || !out) return COMPKV_EINVAL;
+    if (!vec_aligned({q, k_cache, v_cache, kmean, vmean})) return COMPKV_EINVAL;
     // Mean: vmean with blk_logit or kmean (zbar recomputed); Drop: vmean and blk_logit both null
     if (vmean ? (!blk_logit && !kmean) : blk_logit != nullptr) return COMPKV_EINVAL;
     if (sel_stride < 1) return COMPKV_EINVAL;
@@ -544,6 +556,7 @@ int compkv_dense_decode(const compkv_dims* dims, float scale, const void* q, con
     int st = check_dims(dims, &g);
     if (st != COMPKV_OK) return st;
     if (!q || !k_cache || !v_cache || !seq_lens || !out) return COMPKV_EINVAL;
+    if (!vec_aligned({q, k_cache, v_cache})) return COMPKV_EINVAL;
     const size_t need = ws_bytes(g, 1, COMPKV_WS_DENSE_DECODE);
     st = check_ws(g, workspace, workspace_bytes, need);
     if (st != COMPKV_OK) return st;
@@ -597,6 +610,7 @@ int compkv_decode_step(const compkv_dims* dims, const compkv_select_params* para
         !blk_logit || !out)
         return COMPKV_EINVAL;
     if ((k_new == nullptr) != (v_new == nullptr)) return COMPKV_EINVAL;
+    if (!vec_aligned({q, k_cache, v_cache, k_new, v_new, kmean, dvar, vmean})) return COMPKV_EINVAL;
     if (params->budget_blocks < 1 || params->n_sink < 0 || params->n_recent < 0) return COMPKV_EINVAL;
     if (params->budget_blocks < params->n_sink + params->n_recent) return COMPKV_EBUDGET;
     if (params->score_kind < COMPKV_SCORE_COMPKV || params->score_kind > COMPKV_SCORE_FIRST_ORDER) return COMPKV_EINVAL;

@@ -90,6 +90,26 @@ def test_null_pointers_rejected():
                                   16, FAKE, None, FAKE, 1 << 30, None) == EINVAL  # q required
 
 
+def test_misaligned_vector_arrays_rejected():
+    """Arrays read with 16-byte vector loads must be 16-byte aligned: a pointer 4 bytes off is EINVAL
+    on the host for every call that reads it (the rest of each call's arguments are valid)."""
+    d = dims()
+    L = P.library()
+    OFF = ctypes.c_void_p(4100)
+    assert L.compkv_build_stats(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, OFF, FAKE, None) == EINVAL  # dvar
+    assert L.compkv_build_stats(ctypes.byref(d), OFF, FAKE, FAKE, FAKE, FAKE, FAKE, None) == EINVAL  # k_cache
+    assert L.compkv_append_stats(ctypes.byref(d), FAKE, FAKE, OFF, FAKE, FAKE, FAKE, FAKE, FAKE, None) == EINVAL
+    p = P.CompkvSelectParams(16, 1, 2, 0.088)
+    assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), OFF, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                 None, FAKE, 1 << 30, None) == EINVAL  # q
+    assert L.compkv_score_select(ctypes.byref(d), ctypes.byref(p), FAKE, FAKE, OFF, FAKE, FAKE, FAKE, None,
+                                 None, FAKE, 1 << 30, None) == EINVAL  # dvar
+    assert L.compkv_sparse_decode(ctypes.byref(d), 0.1, FAKE, FAKE, FAKE, FAKE, OFF, FAKE, FAKE, FAKE, FAKE,
+                                  16, FAKE, None, FAKE, 1 << 30, None) == EINVAL  # vmean
+    for name in ("q", "k_cache", "v_cache", "k_new", "v_new", "kmean", "dvar", "vmean"):
+        assert _step(L, d, p, **{name: OFF}) == EINVAL, name
+
+
 def test_budget_below_mandatory_set_rejected():
     """Section 4.2: the sink and recent blocks count inside the budget, so K < n_sink + n_recent
     cannot be honoured."""
